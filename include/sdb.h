@@ -1,0 +1,296 @@
+/*
+ * sdb.h -- C ABI of libsdb, a fused star-schema query engine for one AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The library evaluates the query shape the paper studies (Sections 3.3, 4.2
+ * and 4.3): one pass over int32 fact columns that applies literal predicates
+ * on fact columns, probes lookup tables built from filtered dimension tables,
+ * gathers dimension attributes as group keys, and ends in a scalar SUM or a
+ * GROUP BY ... SUM over 64-bit integers.
+ *
+ * Conventions for every entry point
+ *  - Plain C structs and pointers only. "device" pointers point to GPU memory
+ *    (hipMalloc / torch CUDA tensors); "host" pointers to CPU memory.
+ *  - The caller owns every buffer: fact and dimension columns, the dimension
+ *    workspace, the planner and finalize scratch, and all outputs. They must
+ *    stay valid until the work queued on the stream has finished. The library
+ *    allocates no device memory and keeps no global mutable state besides a
+ *    per-thread error string and a per-device properties cache.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *  - Every call returns an sdb_status; nothing throws across the ABI.
+ *    sdb_last_error() returns a message for the last failing call on the
+ *    calling thread. Arguments are validated on the host before any launch.
+ *  - All arithmetic is integer. Sums wrap modulo 2^64 and are reported as
+ *    signed int64; the result does not depend on execution order.
+ */
+#ifndef SDB_H
+#define SDB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SDB_API __attribute__((visibility("default")))
+
+#define SDB_ABI_VERSION 1
+
+typedef enum sdb_status {
+    SDB_OK = 0,
+    SDB_INVALID_ARG = 1,          /* null pointer, negative size, index out of range, bad op code */
+    SDB_UNSUPPORTED = 2,          /* a limit below is exceeded (columns, stages, payload domain) */
+    SDB_CAPACITY = 3,             /* group count exceeds the caller's capacity or 2^31 - 1 */
+    SDB_WORKSPACE_TOO_SMALL = 4,  /* workspace / scratch smaller than the required size */
+    SDB_DUP_KEY = 5,              /* a dimension key occurs in more than one row */
+    SDB_KEY_RANGE = 6,            /* DENSE forced but the key range exceeds the dense limit */
+    SDB_HIP_ERROR = 7             /* a HIP runtime call or kernel launch failed */
+} sdb_status;
+
+/* Comparison operators of a predicate `column OP literal`. Literals are int64,
+ * so a bound outside the int32 range is legal and simply always/never holds.
+ * BETWEEN is inclusive on both ends: lo <= x <= hi (the paper lowers a BETWEEN
+ * to the conjunction of its two bounds, Section 4.2). */
+enum { SDB_OP_EQ = 0, SDB_OP_NE = 1, SDB_OP_LT = 2, SDB_OP_LE = 3,
+       SDB_OP_GT = 4, SDB_OP_GE = 5, SDB_OP_BETWEEN = 6 };
+
+/* Dimension lookup-table layouts (Section 3.3: a direct-mapped table indexed
+ * by a dense primary key, or a double-sized open-addressing hash table). */
+enum { SDB_TABLE_AUTO = 0, SDB_TABLE_DENSE = 1, SDB_TABLE_HASH = 2 };
+
+/* Aggregate expressions over fact columns a and b, computed in int64. */
+enum { SDB_AGG_COL = 0, SDB_AGG_MUL = 1, SDB_AGG_SUB = 2, SDB_AGG_ADD = 3 };
+
+/* Terminals (Sections 3.2, 3.3 and 4.3): one register accumulator per lane
+ * reduced to one atomic per block; a block-private group table in LDS flushed
+ * once per block; or one global atomic per surviving row. */
+enum { SDB_TERMINAL_AUTO = 0, SDB_TERMINAL_SCALAR = 1, SDB_TERMINAL_LDS = 2,
+       SDB_TERMINAL_GLOBAL = 3 };
+
+#define SDB_MAX_DIM_COLS 8
+#define SDB_MAX_DIM_PREDS 4
+#define SDB_MAX_PAYLOADS 3
+#define SDB_MAX_FACT_COLS 16
+#define SDB_MAX_FACT_PREDS 8
+#define SDB_MAX_JOINS 6
+#define SDB_MAX_GROUP_KEYS 4
+#define SDB_MAX_STAGES (SDB_MAX_FACT_PREDS + SDB_MAX_JOINS)
+#define SDB_PLAN_SCRATCH_BYTES 256
+
+/* One predicate. `col` indexes the owning descriptor's `cols[]`. `hi` is
+ * used by SDB_OP_BETWEEN only. */
+typedef struct sdb_pred {
+    int32_t col;
+    int32_t op;
+    int64_t lo;
+    int64_t hi;
+} sdb_pred;
+
+/* A dimension table to turn into a lookup table.
+ *  key          device, n_rows int32 primary keys (must be distinct)
+ *  cols[]       device, n_rows int32 each: attribute columns referenced by
+ *               preds[].col and payload_cols[]
+ *  preds[]      conjunctive filter on the dimension rows (Section 3.3)
+ *  payload_cols attributes to gather for passing rows (group keys), 0..3
+ *  kind         SDB_TABLE_*; AUTO picks DENSE when the key range is at most
+ *               max(2 * n_rows, 1024) slots, else HASH (the paper checks the
+ *               key range at run time and falls back to a hash table, 4.3)
+ *  load_factor  HASH only; 0 means 0.5 (the paper's double-sized table) */
+typedef struct sdb_dim_desc {
+    const int32_t* key;
+    int64_t n_rows;
+    int32_t n_cols;
+    const int32_t* cols[SDB_MAX_DIM_COLS];
+    int32_t n_preds;
+    sdb_pred preds[SDB_MAX_DIM_PREDS];
+    int32_t n_payloads;
+    int32_t payload_cols[SDB_MAX_PAYLOADS];
+    int32_t kind;
+    double load_factor;
+} sdb_dim_desc;
+
+/* A built lookup table: a plain handle into the caller's workspace.
+ * A passing row's code is sum_p (payload_p - payload_min[p]) * payload_div[p]
+ * with payload_div of the last payload 1; `domain` codes exist.
+ *  DENSE: map[key - key_min] is the code (width bytes), or `sentinel` (all
+ *         ones of the width) for a filtered row or a key no row holds.
+ *  HASH:  n_slots = 2^hash_bits 8-byte slots {low 32 bits: key, high 32
+ *         bits: code + 1, or 0xFFFFFFFF for a filtered row}; a slot with high
+ *         half 0 is empty. Slot of key k starts at (k * 0x9E3779B1 mod 2^32)
+ *         >> (32 - hash_bits) (Fibonacci hashing) and probes linearly. */
+typedef struct sdb_dim {
+    int32_t kind;                 /* SDB_TABLE_DENSE or SDB_TABLE_HASH */
+    int32_t width;                /* DENSE: 1, 2 or 4 bytes per entry; HASH: 8 */
+    int64_t n_rows;
+    int64_t n_pass;               /* rows that pass the dimension predicates */
+    int32_t key_min;              /* over all rows (0 when n_rows == 0) */
+    int32_t key_max;
+    uint64_t n_slots;
+    int32_t hash_bits;
+    uint32_t sentinel;
+    uint64_t domain;
+    int32_t n_payloads;
+    int32_t payload_min[SDB_MAX_PAYLOADS];     /* over passing rows */
+    uint32_t payload_radix[SDB_MAX_PAYLOADS];  /* max - min + 1 over passing rows; 1 if none pass */
+    uint64_t payload_div[SDB_MAX_PAYLOADS];
+    void* map;                    /* device, inside the workspace */
+    void* stats;                  /* device, inside the workspace */
+} sdb_dim;
+
+typedef struct sdb_join {
+    int32_t fact_key_col;         /* index into sdb_query.cols[] */
+    const sdb_dim* dim;           /* host pointer to a built handle */
+} sdb_join;
+
+typedef struct sdb_group_key {
+    int32_t join;                 /* index into sdb_query.joins[] */
+    int32_t payload;              /* index into that dimension's payloads */
+} sdb_group_key;
+
+typedef struct sdb_agg {
+    int32_t kind;                 /* SDB_AGG_* */
+    int32_t a;                    /* index into sdb_query.cols[] */
+    int32_t b;                    /* index into sdb_query.cols[] (ignored for COL) */
+} sdb_agg;
+
+/* A star query over n_fact rows (the fact table is the spine: predicates
+ * narrow the live rows, probes drop misses and filtered rows, gathers pull
+ * group keys, the terminal consumes the survivors; Section 4.2).
+ * The force_* fields override the planner (0 = automatic):
+ *  force_terminal  SDB_TERMINAL_*
+ *  force_ipt       items per lane per loop iteration (1..8)
+ *  force_vector    1: 4-row items with 128-bit loads (columns must be 16-byte
+ *                  aligned); -1: 1-row items
+ *  force_order     1: keep query order (predicates, then joins), no sampling
+ *  grid_blocks     blocks of the fused kernel */
+typedef struct sdb_query {
+    int64_t n_fact;
+    int32_t n_cols;
+    const int32_t* cols[SDB_MAX_FACT_COLS];
+    int32_t n_preds;
+    sdb_pred preds[SDB_MAX_FACT_PREDS];
+    int32_t n_joins;
+    sdb_join joins[SDB_MAX_JOINS];
+    int32_t n_group_keys;
+    sdb_group_key group_keys[SDB_MAX_GROUP_KEYS];
+    sdb_agg agg;
+    int32_t force_terminal;
+    int32_t force_ipt;
+    int32_t force_vector;
+    int32_t force_order;
+    int32_t grid_blocks;
+} sdb_query;
+
+/* The one-pass plan. Stages run in the listed order; each is a fact
+ * predicate (kind 0, index into preds[]) or a join probe (kind 1, index into
+ * joins[]). Group id = sum_k (key_k - key_min[k]) * stride[k] with the last
+ * key's stride 1, so ascending group ids are ascending key tuples. */
+typedef struct sdb_plan {
+    int32_t n_stages;
+    int32_t stage_kind[SDB_MAX_STAGES];
+    int32_t stage_index[SDB_MAX_STAGES];
+    double stage_pass[SDB_MAX_STAGES];    /* pass fraction on the sample, or the estimate used */
+    int64_t sampled_rows;                 /* 0 when no sample was taken */
+    int32_t terminal;
+    int32_t ipt;
+    int32_t vector;                       /* 1: 4-row items with 128-bit loads */
+    int32_t block;
+    int32_t grid;                         /* 0: chosen at launch */
+    int32_t n_group_keys;
+    int32_t key_min[SDB_MAX_GROUP_KEYS];
+    uint32_t radix[SDB_MAX_GROUP_KEYS];
+    uint64_t stride[SDB_MAX_GROUP_KEYS];
+    uint64_t n_groups;                    /* product of radices; 1 without GROUP BY */
+} sdb_plan;
+
+/* ---- errors and ABI ---------------------------------------------------- */
+
+/* Message for the last failing call on this thread ("" if none). The string
+ * stays valid until the next call on the same thread. */
+SDB_API const char* sdb_last_error(void);
+
+/* Fixed name of a status code. */
+SDB_API const char* sdb_status_string(int32_t status);
+
+/* SDB_ABI_VERSION of the built library. */
+SDB_API int32_t sdb_abi_version(void);
+
+/* Writes sizeof of sdb_pred, sdb_dim_desc, sdb_dim, sdb_join, sdb_group_key,
+ * sdb_agg, sdb_query, sdb_plan (in that order) to sizes[0..n-1], n <= 8, so a
+ * binding can check its struct layout. Host only. */
+SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n);
+
+/* ---- dimension build (separate from the fused pass, Section 4.2) ------- */
+
+/* Host only. Workspace bytes sdb_build_dim needs for `desc`: 256 bytes of
+ * statistics, then the lookup table sized by an upper bound (a DENSE map of
+ * max(2 * n_rows, 1024) 4-byte slots plus its occupancy bitmap, and/or a HASH
+ * table of next_pow2(n_rows / load_factor) 8-byte slots). */
+SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* bytes);
+
+/* Builds the lookup table for `desc` into `workspace` (device, 256-byte
+ * aligned, workspace_bytes >= sdb_dim_required_bytes) on `stream`, and fills
+ * `out` (host). Passes over the dimension rows: statistics (key range, pass
+ * count, payload ranges), then the direct-mapped map (Section 3.3: one code
+ * per key, the sentinel for filtered rows; 1, 2 or 4 bytes by payload domain)
+ * or the open-addressing table (64-bit compare-and-swap inserts). Synchronizes
+ * the stream twice (to read the statistics and the duplicate-key flag).
+ * Errors: INVALID_ARG, UNSUPPORTED (payload domain >= 2^32 - 1), KEY_RANGE,
+ * WORKSPACE_TOO_SMALL, DUP_KEY, HIP_ERROR. */
+SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace,
+                                 int64_t workspace_bytes, void* stream, sdb_dim* out);
+
+/* ---- planning ----------------------------------------------------------- */
+
+/* Orders the stages of `q` (host) into `plan` (host). Unless q->force_order
+ * is set, a sampling kernel evaluates every stage on its own over every
+ * ceil(n_fact / 65536)-th fact row and the stages are sorted by ascending
+ * pass fraction (ties: predicates before probes, smaller tables first, then
+ * query order); this needs `scratch` (device, >= SDB_PLAN_SCRATCH_BYTES) and
+ * synchronizes `stream` once. With force_order set, scratch and stream are
+ * unused and no GPU call is made. Also fixes group radices and strides from
+ * the built tables' payload ranges, the terminal (scalar without GROUP BY;
+ * LDS when the group table fits a block's LDS; else global), items per lane
+ * and the block size. Errors: INVALID_ARG, UNSUPPORTED, CAPACITY,
+ * WORKSPACE_TOO_SMALL, HIP_ERROR. */
+SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_t scratch_bytes,
+                                       void* stream, sdb_plan* plan);
+
+/* ---- the fused pass ----------------------------------------------------- */
+
+/* Runs `q` with `plan` (from sdb_plan_star_query for this query and these
+ * tables) as one fused probe-filter-aggregate kernel (Sections 3.2 and 4.2)
+ * after zeroing the outputs, all queued on `stream` (asynchronous).
+ * sums/counts: device int64[plan->n_groups], indexed by group id;
+ * n_groups_capacity >= plan->n_groups. Without GROUP BY, sums[0] and
+ * counts[0] hold the total and the live row count. Errors: INVALID_ARG,
+ * CAPACITY, HIP_ERROR (launch failures only). */
+SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
+                                      int64_t* sums, int64_t* counts,
+                                      int64_t n_groups_capacity, void* stream);
+
+/* ---- finalize ----------------------------------------------------------- */
+
+/* Host only. Scratch bytes sdb_finalize_groups needs for `plan`. */
+SDB_API sdb_status sdb_finalize_scratch_bytes(const sdb_plan* plan, int64_t* bytes);
+
+/* Compacts the group table on the device (asynchronous, on `stream`): every
+ * group with counts[g] > 0 in ascending group id order, which is ascending
+ * lexicographic key order. out_keys: device int32[out_capacity][n_group_keys]
+ * (the key values, i.e. payload codes plus payload minima); out_sums,
+ * out_counts: device int64[out_capacity]; out_n: device int64[1], the number
+ * of groups written. Without GROUP BY one row is written even when its count
+ * is 0. out_capacity must be >= plan->n_groups. scratch: device,
+ * >= sdb_finalize_scratch_bytes. Errors: INVALID_ARG, CAPACITY,
+ * WORKSPACE_TOO_SMALL, HIP_ERROR. */
+SDB_API sdb_status sdb_finalize_groups(const sdb_plan* plan, const int64_t* sums,
+                                       const int64_t* counts, int32_t* out_keys,
+                                       int64_t* out_sums, int64_t* out_counts,
+                                       int64_t out_capacity, int64_t* out_n,
+                                       void* scratch, int64_t scratch_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDB_H */

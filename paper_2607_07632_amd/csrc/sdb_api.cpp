@@ -1,0 +1,712 @@
+// Host runtime of libsdb: argument validation, dimension-table sizing and
+// bookkeeping, the one-pass planner, and the C ABI declared in include/sdb.h.
+// All device work is queued on the caller's stream through the launchers in
+// sdb_kernels.hip; this file allocates no device memory.
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "sdb_internal.h"
+
+using namespace sdb;
+
+namespace {
+
+thread_local std::string g_error;
+
+sdb_status fail(sdb_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = std::string(sdb_status_string(s)) + ": " + buf;
+    return s;
+}
+
+sdb_status ok() {
+    g_error.clear();
+    return SDB_OK;
+}
+
+sdb_status hip_fail(hipError_t e, const char* what) {
+    return fail(SDB_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define SDB_HIP(call, what)                              \
+    do {                                                 \
+        hipError_t e_ = (call);                          \
+        if (e_ != hipSuccess) return hip_fail(e_, what); \
+    } while (0)
+
+inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+inline uint64_t next_pow2(uint64_t x) {
+    uint64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// ---- predicates -----------------------------------------------------------
+
+bool valid_op(int32_t op) { return op >= SDB_OP_EQ && op <= SDB_OP_BETWEEN; }
+
+// Lowers `x OP literal(s)` with int64 literals to one unsigned range test over
+// int32 values: pass <=> ((uint32)(x - lo) <= span) != negate.
+RangeTest lower_pred(const sdb_pred& p) {
+    const int64_t kMin = INT32_MIN, kMax = INT32_MAX;
+    auto clamp = [&](int64_t v) { return std::min(std::max(v, kMin - 1), kMax + 1); };
+    int64_t a = kMin, b = kMax;   // inclusive range that passes (before negation)
+    int negate = 0;
+    const int64_t v = clamp(p.lo);
+    switch (p.op) {
+        case SDB_OP_EQ: a = v; b = v; break;
+        case SDB_OP_NE: a = v; b = v; negate = 1; break;
+        case SDB_OP_LT: b = v - 1; break;
+        case SDB_OP_LE: b = v; break;
+        case SDB_OP_GT: a = v + 1; break;
+        case SDB_OP_GE: a = v; break;
+        case SDB_OP_BETWEEN: a = v; b = clamp(p.hi); break;
+    }
+    a = std::max(a, kMin);
+    b = std::min(b, kMax);
+    RangeTest t;
+    if (a > b) {   // nothing is inside: "in" never holds, "not in" always holds
+        t.lo = INT32_MIN;
+        t.span = 0xFFFFFFFFu;
+        t.negate = negate ? 0 : 1;
+        return t;
+    }
+    t.lo = (int32_t)a;
+    t.span = (uint32_t)(b - a);
+    t.negate = negate;
+    return t;
+}
+
+// ---- device properties ----------------------------------------------------
+
+struct DeviceInfo {
+    int cus = 0;
+};
+
+std::mutex g_dev_mu;
+std::vector<DeviceInfo> g_dev;
+
+sdb_status device_info(DeviceInfo* out) {
+    int dev = 0;
+    SDB_HIP(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if ((int)g_dev.size() <= dev) g_dev.resize(dev + 1);
+    if (g_dev[dev].cus == 0) {
+        int cus = 0;
+        SDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev),
+                "hipDeviceGetAttribute");
+        g_dev[dev].cus = cus;
+    }
+    *out = g_dev[dev];
+    return SDB_OK;
+}
+
+// ---- dimension sizing -----------------------------------------------------
+
+constexpr uint64_t kStatsBytes = 256;
+
+uint64_t dense_slot_limit(int64_t n_rows) {
+    return std::max<uint64_t>(2 * (uint64_t)n_rows, (uint64_t)kDenseSlack);
+}
+
+uint64_t dense_bytes(uint64_t slots, int width) {
+    return align_up(slots * (uint64_t)width, 256) + align_up((slots + 31) / 32 * 4, 256);
+}
+
+double effective_lf(const sdb_dim_desc* d) {
+    return d->load_factor > 0.0 ? d->load_factor : 0.5;
+}
+
+uint64_t hash_capacity(int64_t n_rows, double lf) {
+    uint64_t need = (uint64_t)std::ceil((double)n_rows / lf);
+    need = std::max<uint64_t>(need, (uint64_t)n_rows + 1);   // at least one empty slot
+    return std::max<uint64_t>(next_pow2(need), 2);
+}
+
+sdb_status check_dim_desc(const sdb_dim_desc* d) {
+    if (!d) return fail(SDB_INVALID_ARG, "null dimension descriptor");
+    if (d->n_rows < 0) return fail(SDB_INVALID_ARG, "negative n_rows");
+    if (d->n_rows > (int64_t)INT32_MAX) return fail(SDB_UNSUPPORTED, "n_rows above 2^31 - 1");
+    if (d->n_rows > 0 && !d->key) return fail(SDB_INVALID_ARG, "null key column");
+    if (d->n_cols < 0 || d->n_cols > SDB_MAX_DIM_COLS)
+        return fail(SDB_UNSUPPORTED, "n_cols %d outside 0..%d", d->n_cols, SDB_MAX_DIM_COLS);
+    for (int c = 0; c < d->n_cols; ++c)
+        if (d->n_rows > 0 && !d->cols[c]) return fail(SDB_INVALID_ARG, "null dimension column %d", c);
+    if (d->n_preds < 0 || d->n_preds > SDB_MAX_DIM_PREDS)
+        return fail(SDB_UNSUPPORTED, "n_preds %d outside 0..%d", d->n_preds, SDB_MAX_DIM_PREDS);
+    for (int q = 0; q < d->n_preds; ++q) {
+        if (d->preds[q].col < 0 || d->preds[q].col >= d->n_cols)
+            return fail(SDB_INVALID_ARG, "predicate %d names column %d of %d", q, d->preds[q].col, d->n_cols);
+        if (!valid_op(d->preds[q].op)) return fail(SDB_INVALID_ARG, "predicate %d: bad op %d", q, d->preds[q].op);
+    }
+    if (d->n_payloads < 0 || d->n_payloads > SDB_MAX_PAYLOADS)
+        return fail(SDB_UNSUPPORTED, "n_payloads %d outside 0..%d", d->n_payloads, SDB_MAX_PAYLOADS);
+    for (int p = 0; p < d->n_payloads; ++p)
+        if (d->payload_cols[p] < 0 || d->payload_cols[p] >= d->n_cols)
+            return fail(SDB_INVALID_ARG, "payload %d names column %d of %d", p, d->payload_cols[p], d->n_cols);
+    if (d->kind < SDB_TABLE_AUTO || d->kind > SDB_TABLE_HASH)
+        return fail(SDB_INVALID_ARG, "bad table kind %d", d->kind);
+    if (d->kind != SDB_TABLE_DENSE) {
+        const double lf = effective_lf(d);
+        if (!(lf > 0.0 && lf <= 0.9)) return fail(SDB_INVALID_ARG, "load factor %g outside (0, 0.9]", lf);
+        if (hash_capacity(d->n_rows, lf) > (1ull << 31))
+            return fail(SDB_UNSUPPORTED, "hash table above 2^31 slots");
+    }
+    return SDB_OK;
+}
+
+uint64_t required_bytes(const sdb_dim_desc* d) {
+    uint64_t table = 0;
+    if (d->kind != SDB_TABLE_HASH) table = std::max(table, dense_bytes(dense_slot_limit(d->n_rows), 4));
+    if (d->kind != SDB_TABLE_DENSE) table = std::max(table, hash_capacity(d->n_rows, effective_lf(d)) * 8);
+    return kStatsBytes + table;
+}
+
+BuildParams build_params(const sdb_dim_desc* d, DimStats* stats) {
+    BuildParams bp;
+    std::memset(&bp, 0, sizeof bp);
+    bp.key = d->key;
+    bp.n = d->n_rows;
+    for (int c = 0; c < d->n_cols; ++c) bp.cols[c] = d->cols[c];
+    bp.n_preds = d->n_preds;
+    for (int q = 0; q < d->n_preds; ++q) {
+        bp.pred_col[q] = d->preds[q].col;
+        bp.pred[q] = lower_pred(d->preds[q]);
+    }
+    bp.n_payloads = d->n_payloads;
+    for (int p = 0; p < d->n_payloads; ++p) bp.payload_col[p] = d->payload_cols[p];
+    bp.stats = stats;
+    return bp;
+}
+
+// ---- query validation and stages -------------------------------------------
+
+sdb_status check_query(const sdb_query* q) {
+    if (!q) return fail(SDB_INVALID_ARG, "null query");
+    if (q->n_fact < 0) return fail(SDB_INVALID_ARG, "negative n_fact");
+    if (q->n_cols < 1 || q->n_cols > SDB_MAX_FACT_COLS)
+        return fail(SDB_UNSUPPORTED, "n_cols %d outside 1..%d", q->n_cols, SDB_MAX_FACT_COLS);
+    for (int c = 0; c < q->n_cols; ++c)
+        if (q->n_fact > 0 && !q->cols[c]) return fail(SDB_INVALID_ARG, "null fact column %d", c);
+    if (q->n_preds < 0 || q->n_preds > SDB_MAX_FACT_PREDS)
+        return fail(SDB_UNSUPPORTED, "n_preds %d outside 0..%d", q->n_preds, SDB_MAX_FACT_PREDS);
+    for (int i = 0; i < q->n_preds; ++i) {
+        if (q->preds[i].col < 0 || q->preds[i].col >= q->n_cols)
+            return fail(SDB_INVALID_ARG, "fact predicate %d names column %d of %d", i, q->preds[i].col, q->n_cols);
+        if (!valid_op(q->preds[i].op)) return fail(SDB_INVALID_ARG, "fact predicate %d: bad op %d", i, q->preds[i].op);
+    }
+    if (q->n_joins < 0 || q->n_joins > SDB_MAX_JOINS)
+        return fail(SDB_UNSUPPORTED, "n_joins %d outside 0..%d", q->n_joins, SDB_MAX_JOINS);
+    for (int j = 0; j < q->n_joins; ++j) {
+        const sdb_join& jn = q->joins[j];
+        if (jn.fact_key_col < 0 || jn.fact_key_col >= q->n_cols)
+            return fail(SDB_INVALID_ARG, "join %d names column %d of %d", j, jn.fact_key_col, q->n_cols);
+        if (!jn.dim) return fail(SDB_INVALID_ARG, "join %d has no dimension table", j);
+        if (jn.dim->kind != SDB_TABLE_DENSE && jn.dim->kind != SDB_TABLE_HASH)
+            return fail(SDB_INVALID_ARG, "join %d: dimension table is not built", j);
+        if (!jn.dim->map) return fail(SDB_INVALID_ARG, "join %d: dimension table has no map", j);
+        if (jn.dim->kind == SDB_TABLE_DENSE && jn.dim->width != 1 && jn.dim->width != 2 && jn.dim->width != 4)
+            return fail(SDB_INVALID_ARG, "join %d: bad dense width %d", j, jn.dim->width);
+        if (jn.dim->kind == SDB_TABLE_HASH &&
+            (jn.dim->hash_bits < 1 || jn.dim->hash_bits > 31 || jn.dim->n_slots != (1ull << jn.dim->hash_bits)))
+            return fail(SDB_INVALID_ARG, "join %d: bad hash table geometry", j);
+    }
+    if (q->n_group_keys < 0 || q->n_group_keys > SDB_MAX_GROUP_KEYS)
+        return fail(SDB_UNSUPPORTED, "n_group_keys %d outside 0..%d", q->n_group_keys, SDB_MAX_GROUP_KEYS);
+    for (int k = 0; k < q->n_group_keys; ++k) {
+        const sdb_group_key& g = q->group_keys[k];
+        if (g.join < 0 || g.join >= q->n_joins)
+            return fail(SDB_INVALID_ARG, "group key %d names join %d of %d", k, g.join, q->n_joins);
+        if (g.payload < 0 || g.payload >= q->joins[g.join].dim->n_payloads)
+            return fail(SDB_INVALID_ARG, "group key %d names payload %d of %d", k, g.payload,
+                        q->joins[g.join].dim->n_payloads);
+    }
+    if (q->agg.kind < SDB_AGG_COL || q->agg.kind > SDB_AGG_ADD)
+        return fail(SDB_INVALID_ARG, "bad aggregate kind %d", q->agg.kind);
+    if (q->agg.a < 0 || q->agg.a >= q->n_cols) return fail(SDB_INVALID_ARG, "aggregate operand a = %d", q->agg.a);
+    if (q->agg.kind != SDB_AGG_COL && (q->agg.b < 0 || q->agg.b >= q->n_cols))
+        return fail(SDB_INVALID_ARG, "aggregate operand b = %d", q->agg.b);
+    if (q->force_terminal < SDB_TERMINAL_AUTO || q->force_terminal > SDB_TERMINAL_GLOBAL)
+        return fail(SDB_INVALID_ARG, "bad force_terminal %d", q->force_terminal);
+    if (q->force_ipt != 0 && q->force_ipt != 1 && q->force_ipt != 2 && q->force_ipt != 4 && q->force_ipt != 8)
+        return fail(SDB_UNSUPPORTED, "force_ipt %d is not 0, 1, 2, 4 or 8", q->force_ipt);
+    if (q->force_vector < -1 || q->force_vector > 1) return fail(SDB_INVALID_ARG, "bad force_vector %d", q->force_vector);
+    if (q->grid_blocks < 0) return fail(SDB_INVALID_ARG, "negative grid_blocks");
+    return SDB_OK;
+}
+
+// Group radices and strides: key k's code ranges over its payload radix;
+// the last key varies fastest.
+sdb_status group_layout(const sdb_query* q, sdb_plan* plan) {
+    plan->n_group_keys = q->n_group_keys;
+    uint64_t g = 1;
+    for (int k = q->n_group_keys - 1; k >= 0; --k) {
+        const sdb_dim* d = q->joins[q->group_keys[k].join].dim;
+        const int p = q->group_keys[k].payload;
+        plan->key_min[k] = d->payload_min[p];
+        plan->radix[k] = d->payload_radix[p];
+        plan->stride[k] = g;
+        if (d->payload_radix[p] == 0) return fail(SDB_INVALID_ARG, "group key %d has radix 0", k);
+        g *= d->payload_radix[p];
+        if (g > (uint64_t)INT32_MAX)
+            return fail(SDB_CAPACITY, "group domain exceeds 2^31 - 1 (key %d)", k);
+    }
+    plan->n_groups = g;
+    return SDB_OK;
+}
+
+// The stage of a fact predicate or join probe in FusedParams form.
+StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int index) {
+    StageDev S;
+    std::memset(&S, 0, sizeof S);
+    if (kind == 0) {
+        S.kind = ST_PRED;
+        S.col = q->preds[index].col;
+        S.test = lower_pred(q->preds[index]);
+        return S;
+    }
+    const sdb_join& jn = q->joins[index];
+    const sdb_dim* d = jn.dim;
+    S.col = jn.fact_key_col;
+    S.map = d->map;
+    S.sentinel = d->sentinel;
+    if (d->kind == SDB_TABLE_DENSE) {
+        S.kind = ST_DENSE;
+        S.width = d->width;
+        S.kmin = d->key_min;
+        S.nslots = (uint32_t)d->n_slots;
+    } else {
+        S.kind = ST_HASH;
+        S.width = 8;
+        S.nslots = (uint32_t)d->n_slots;
+        S.hmask = (uint32_t)(d->n_slots - 1);
+        S.hshift = 32 - d->hash_bits;
+    }
+    S.n_gk = 0;
+    if (plan) {
+        for (int k = 0; k < q->n_group_keys; ++k) {
+            if (q->group_keys[k].join != index) continue;
+            const int p = q->group_keys[k].payload;
+            const int n = S.n_gk++;
+            S.gk_div[n] = (uint32_t)d->payload_div[p];
+            // modulo is only needed when higher payloads share the code
+            const bool top = (p == 0);
+            S.gk_radix[n] = top ? 0u : d->payload_radix[p];
+            S.gk_stride[n] = (uint32_t)plan->stride[k];
+        }
+    }
+    return S;
+}
+
+uint64_t stage_table_bytes(const sdb_query* q, int kind, int index) {
+    if (kind == 0) return 0;
+    const sdb_dim* d = q->joins[index].dim;
+    return d->n_slots * (uint64_t)d->width;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+FusedParams fused_params(const sdb_query* q, const sdb_plan* plan) {
+    FusedParams p;
+    std::memset(&p, 0, sizeof p);
+    for (int c = 0; c < q->n_cols; ++c) p.cols[c] = q->cols[c];
+    p.n = q->n_fact;
+    p.nstages = plan->n_stages;
+    for (int s = 0; s < plan->n_stages; ++s) p.st[s] = make_stage(q, plan, plan->stage_kind[s], plan->stage_index[s]);
+    p.agg_kind = q->agg.kind;
+    p.agg_a = q->agg.a;
+    p.agg_b = q->agg.kind == SDB_AGG_COL ? q->agg.a : q->agg.b;
+    p.n_groups = (uint32_t)plan->n_groups;
+    return p;
+}
+
+// Every column the fused kernel reads: stage columns and aggregate operands.
+bool columns_aligned(const sdb_query* q, const sdb_plan* plan) {
+    for (int s = 0; s < plan->n_stages; ++s) {
+        const int col = plan->stage_kind[s] == 0 ? q->preds[plan->stage_index[s]].col
+                                                 : q->joins[plan->stage_index[s]].fact_key_col;
+        if (!aligned16(q->cols[col])) return false;
+    }
+    if (!aligned16(q->cols[q->agg.a])) return false;
+    if (q->agg.kind != SDB_AGG_COL && !aligned16(q->cols[q->agg.b])) return false;
+    return true;
+}
+
+int default_ipt(int terminal) { return terminal == TERM_SCALAR ? 4 : 2; }
+
+sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) {
+    const int64_t rows_per_item = plan->vector ? 4 : 1;
+    const int64_t n_items = q->n_fact / rows_per_item;
+    const int64_t tile = (int64_t)kBlock * plan->ipt;
+    int64_t tiles = (n_items + tile - 1) / tile;
+    if (tiles < 1) tiles = 1;
+    if (q->grid_blocks > 0) {
+        *grid_out = (int)std::min<int64_t>(q->grid_blocks, INT32_MAX);
+        return SDB_OK;
+    }
+    DeviceInfo di;
+    sdb_status st = device_info(&di);
+    if (st != SDB_OK) return st;
+    const size_t lds = plan->terminal == TERM_LDS ? (size_t)plan->n_groups * 16 : 0;
+    int per_cu = fused_blocks_per_cu(plan->vector, plan->ipt, plan->terminal, lds);
+    if (per_cu <= 0) return fail(SDB_HIP_ERROR, "occupancy query failed for the fused kernel");
+    const int64_t full = (int64_t)di.cus * per_cu;
+    *grid_out = (int)std::min<int64_t>(tiles, full);
+    return SDB_OK;
+}
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+
+extern "C" {
+
+SDB_API const char* sdb_last_error(void) { return g_error.c_str(); }
+
+SDB_API const char* sdb_status_string(int32_t s) {
+    switch (s) {
+        case SDB_OK: return "SDB_OK";
+        case SDB_INVALID_ARG: return "SDB_INVALID_ARG";
+        case SDB_UNSUPPORTED: return "SDB_UNSUPPORTED";
+        case SDB_CAPACITY: return "SDB_CAPACITY";
+        case SDB_WORKSPACE_TOO_SMALL: return "SDB_WORKSPACE_TOO_SMALL";
+        case SDB_DUP_KEY: return "SDB_DUP_KEY";
+        case SDB_KEY_RANGE: return "SDB_KEY_RANGE";
+        case SDB_HIP_ERROR: return "SDB_HIP_ERROR";
+        default: return "SDB_UNKNOWN_STATUS";
+    }
+}
+
+SDB_API int32_t sdb_abi_version(void) { return SDB_ABI_VERSION; }
+
+SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n) {
+    if (!sizes || n < 0 || n > 8) return fail(SDB_INVALID_ARG, "sizes must hold 0..8 entries");
+    const int64_t all[8] = {(int64_t)sizeof(sdb_pred),  (int64_t)sizeof(sdb_dim_desc),
+                            (int64_t)sizeof(sdb_dim),   (int64_t)sizeof(sdb_join),
+                            (int64_t)sizeof(sdb_group_key), (int64_t)sizeof(sdb_agg),
+                            (int64_t)sizeof(sdb_query), (int64_t)sizeof(sdb_plan)};
+    for (int i = 0; i < n; ++i) sizes[i] = all[i];
+    return ok();
+}
+
+SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* bytes) {
+    sdb_status st = check_dim_desc(desc);
+    if (st != SDB_OK) return st;
+    if (!bytes) return fail(SDB_INVALID_ARG, "null output");
+    *bytes = (int64_t)required_bytes(desc);
+    return ok();
+}
+
+SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace, int64_t workspace_bytes,
+                                 void* stream, sdb_dim* out) {
+    sdb_status st = check_dim_desc(desc);
+    if (st != SDB_OK) return st;
+    if (!out) return fail(SDB_INVALID_ARG, "null output handle");
+    if (!workspace) return fail(SDB_INVALID_ARG, "null workspace");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(SDB_INVALID_ARG, "workspace is not 256-byte aligned");
+    const uint64_t need = required_bytes(desc);
+    if (workspace_bytes < 0 || (uint64_t)workspace_bytes < need)
+        return fail(SDB_WORKSPACE_TOO_SMALL, "workspace holds %lld bytes, %llu needed",
+                    (long long)workspace_bytes, (unsigned long long)need);
+    hipStream_t s = (hipStream_t)stream;
+    std::memset(out, 0, sizeof *out);
+
+    DimStats* dstats = (DimStats*)workspace;
+    uint8_t* table = (uint8_t*)workspace + kStatsBytes;
+    BuildParams bp = build_params(desc, dstats);
+
+    // pass 1: statistics
+    SDB_HIP(launch_dim_stats(bp, s), "dimension statistics launch");
+    DimStats hs;
+    SDB_HIP(hipMemcpyAsync(&hs, dstats, sizeof hs, hipMemcpyDeviceToHost, s), "statistics copy");
+    SDB_HIP(hipStreamSynchronize(s), "statistics sync");
+
+    const int64_t n = desc->n_rows;
+    out->n_rows = n;
+    out->n_pass = (int64_t)hs.npass;
+    out->key_min = n > 0 ? hs.kmin : 0;
+    out->key_max = n > 0 ? hs.kmax : -1;
+    out->n_payloads = desc->n_payloads;
+    // payload codes: mixed radix over the payload ranges of passing rows, last payload fastest
+    uint64_t domain = 1;
+    for (int p = desc->n_payloads - 1; p >= 0; --p) {
+        const bool any = hs.npass > 0;
+        const int32_t lo = any ? hs.pmin[p] : 0;
+        const uint64_t radix = any ? (uint64_t)((int64_t)hs.pmax[p] - (int64_t)lo + 1) : 1;
+        out->payload_min[p] = lo;
+        out->payload_div[p] = domain;
+        if (radix > 0xFFFFFFFFull) return fail(SDB_UNSUPPORTED, "payload %d spans more than 2^32 - 1 values", p);
+        out->payload_radix[p] = (uint32_t)radix;
+        domain *= radix;
+        if (domain >= 0xFFFFFFFFull) return fail(SDB_UNSUPPORTED, "payload domain reaches 2^32 - 1 codes");
+    }
+    out->domain = domain;
+
+    const uint64_t range = n > 0 ? (uint64_t)((int64_t)out->key_max - (int64_t)out->key_min + 1) : 0;
+    int kind = desc->kind;
+    if (kind == SDB_TABLE_AUTO) kind = range <= dense_slot_limit(n) ? SDB_TABLE_DENSE : SDB_TABLE_HASH;
+    if (kind == SDB_TABLE_DENSE && range > dense_slot_limit(n))
+        return fail(SDB_KEY_RANGE, "key range %llu exceeds the dense limit %llu",
+                    (unsigned long long)range, (unsigned long long)dense_slot_limit(n));
+    out->kind = kind;
+    out->stats = workspace;
+    out->map = table;
+    bp.kmin = out->key_min;
+    for (int p = 0; p < desc->n_payloads; ++p) {
+        bp.pmin[p] = out->payload_min[p];
+        bp.pdiv[p] = (uint32_t)out->payload_div[p];
+    }
+
+    if (kind == SDB_TABLE_DENSE) {
+        const int width = domain <= 0xFFull ? 1 : (domain <= 0xFFFFull ? 2 : 4);   // codes stay below the all-ones sentinel
+        const uint32_t sentinel = width == 1 ? 0xFFu : (width == 2 ? 0xFFFFu : 0xFFFFFFFFu);
+        out->width = width;
+        out->sentinel = sentinel;
+        out->n_slots = range;
+        const uint64_t map_bytes = align_up(range * width, 256);
+        uint32_t* occ = (uint32_t*)(table + map_bytes);
+        bp.map = table;
+        bp.occ = occ;
+        bp.width = width;
+        bp.nslots = range;
+        bp.sentinel = sentinel;
+        SDB_HIP(launch_fill_u32((uint32_t*)table, map_bytes / 4, 0xFFFFFFFFu, s), "map fill");
+        SDB_HIP(launch_fill_u32(occ, (range + 31) / 32, 0u, s), "occupancy fill");
+        SDB_HIP(launch_dense_scatter(bp, s), "dense scatter launch");
+    } else {
+        const uint64_t cap = hash_capacity(n, effective_lf(desc));
+        int bits = 0;
+        while ((1ull << bits) < cap) ++bits;
+        out->width = 8;
+        out->sentinel = 0xFFFFFFFEu;   // code + 1 == 0xFFFFFFFF marks a filtered row
+        out->n_slots = cap;
+        out->hash_bits = bits;
+        bp.map = table;
+        bp.nslots = cap;
+        bp.hmask = (uint32_t)(cap - 1);
+        bp.hshift = 32 - bits;
+        SDB_HIP(launch_fill_u32((uint32_t*)table, cap * 2, 0u, s), "hash table fill");
+        SDB_HIP(launch_hash_insert(bp, s), "hash insert launch");
+    }
+    uint32_t dup = 0;
+    SDB_HIP(hipMemcpyAsync(&dup, &dstats->dup, sizeof dup, hipMemcpyDeviceToHost, s), "flag copy");
+    SDB_HIP(hipStreamSynchronize(s), "build sync");
+    if (dup & 1u) return fail(SDB_DUP_KEY, "dimension key column holds a duplicate key");
+    if (dup) return fail(SDB_HIP_ERROR, "dimension build inconsistency (flag %u)", dup);
+    return ok();
+}
+
+SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_t scratch_bytes,
+                                       void* stream, sdb_plan* plan) {
+    sdb_status st = check_query(q);
+    if (st != SDB_OK) return st;
+    if (!plan) return fail(SDB_INVALID_ARG, "null plan");
+    std::memset(plan, 0, sizeof *plan);
+
+    // stages in query order: predicates, then joins
+    int n = 0;
+    for (int i = 0; i < q->n_preds; ++i) {
+        plan->stage_kind[n] = 0;
+        plan->stage_index[n] = i;
+        plan->stage_pass[n] = 0.5;
+        ++n;
+    }
+    for (int j = 0; j < q->n_joins; ++j) {
+        const sdb_dim* d = q->joins[j].dim;
+        plan->stage_kind[n] = 1;
+        plan->stage_index[n] = j;
+        plan->stage_pass[n] = d->n_rows > 0 ? (double)d->n_pass / (double)d->n_rows : 0.0;
+        ++n;
+    }
+    plan->n_stages = n;
+
+    st = group_layout(q, plan);
+    if (st != SDB_OK) return st;
+
+    if (!q->force_order && n > 1 && q->n_fact > 0) {
+        if (!scratch) return fail(SDB_INVALID_ARG, "null planner scratch");
+        if (scratch_bytes < SDB_PLAN_SCRATCH_BYTES)
+            return fail(SDB_WORKSPACE_TOO_SMALL, "planner scratch holds %lld bytes, %d needed",
+                        (long long)scratch_bytes, SDB_PLAN_SCRATCH_BYTES);
+        hipStream_t s = (hipStream_t)stream;
+        FusedParams fp = fused_params(q, plan);
+        const int64_t step = (q->n_fact + 65535) / 65536;
+        const int64_t n_sample = (q->n_fact + step - 1) / step;
+        unsigned long long* dcounts = (unsigned long long*)scratch;
+        SDB_HIP(launch_sample(fp, step, n_sample, dcounts, s), "sample launch");
+        unsigned long long hc[kMaxStages];
+        SDB_HIP(hipMemcpyAsync(hc, dcounts, sizeof hc, hipMemcpyDeviceToHost, s), "sample copy");
+        SDB_HIP(hipStreamSynchronize(s), "sample sync");
+        for (int i = 0; i < n; ++i) plan->stage_pass[i] = (double)hc[i] / (double)n_sample;
+        plan->sampled_rows = n_sample;
+
+        std::vector<int> order(n);
+        for (int i = 0; i < n; ++i) order[i] = i;
+        std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+            if (plan->stage_pass[x] != plan->stage_pass[y]) return plan->stage_pass[x] < plan->stage_pass[y];
+            if (plan->stage_kind[x] != plan->stage_kind[y]) return plan->stage_kind[x] < plan->stage_kind[y];
+            return stage_table_bytes(q, plan->stage_kind[x], plan->stage_index[x]) <
+                   stage_table_bytes(q, plan->stage_kind[y], plan->stage_index[y]);
+        });
+        sdb_plan tmp = *plan;
+        for (int i = 0; i < n; ++i) {
+            plan->stage_kind[i] = tmp.stage_kind[order[i]];
+            plan->stage_index[i] = tmp.stage_index[order[i]];
+            plan->stage_pass[i] = tmp.stage_pass[order[i]];
+        }
+    }
+
+    // terminal
+    int term;
+    if (q->force_terminal != SDB_TERMINAL_AUTO) term = q->force_terminal;
+    else if (q->n_group_keys == 0) term = TERM_SCALAR;
+    else if (plan->n_groups <= (uint64_t)kLdsGroupLimit) term = TERM_LDS;
+    else term = TERM_GLOBAL;
+    if (term == TERM_SCALAR && q->n_group_keys > 0)
+        return fail(SDB_INVALID_ARG, "scalar terminal forced on a grouped query");
+    if (term == TERM_LDS && plan->n_groups > (uint64_t)kLdsGroupLimit)
+        return fail(SDB_CAPACITY, "LDS terminal holds at most %d groups, plan has %llu", kLdsGroupLimit,
+                    (unsigned long long)plan->n_groups);
+    plan->terminal = term;
+    plan->ipt = q->force_ipt ? q->force_ipt : default_ipt(term);
+    const bool aligned = columns_aligned(q, plan);
+    if (q->force_vector == 1 && !aligned && q->n_fact > 0)
+        return fail(SDB_INVALID_ARG, "vector loads forced but a column is not 16-byte aligned");
+    plan->vector = q->force_vector == -1 ? 0 : (aligned ? 1 : 0);
+    plan->block = kBlock;
+    plan->grid = q->grid_blocks;
+    return ok();
+}
+
+SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
+                                      int64_t* counts, int64_t n_groups_capacity, void* stream) {
+    sdb_status st = check_query(q);
+    if (st != SDB_OK) return st;
+    if (!plan) return fail(SDB_INVALID_ARG, "null plan");
+    if (!sums || !counts) return fail(SDB_INVALID_ARG, "null output");
+    if (plan->n_stages != q->n_preds + q->n_joins) return fail(SDB_INVALID_ARG, "plan does not match the query");
+    {
+        bool seen[SDB_MAX_STAGES] = {false};
+        for (int s = 0; s < plan->n_stages; ++s) {
+            const int k = plan->stage_kind[s], i = plan->stage_index[s];
+            if ((k != 0 && k != 1) || i < 0 || (k == 0 && i >= q->n_preds) || (k == 1 && i >= q->n_joins))
+                return fail(SDB_INVALID_ARG, "plan stage %d is invalid", s);
+            const int slot = k == 0 ? i : q->n_preds + i;
+            if (seen[slot]) return fail(SDB_INVALID_ARG, "plan stage %d repeats a stage", s);
+            seen[slot] = true;
+        }
+    }
+    sdb_plan layout;
+    std::memset(&layout, 0, sizeof layout);
+    st = group_layout(q, &layout);
+    if (st != SDB_OK) return st;
+    if (layout.n_groups != plan->n_groups) return fail(SDB_INVALID_ARG, "plan group count does not match the query");
+    for (int k = 0; k < q->n_group_keys; ++k)
+        if (layout.stride[k] != plan->stride[k] || layout.radix[k] != plan->radix[k])
+            return fail(SDB_INVALID_ARG, "plan group layout does not match the query");
+    if (n_groups_capacity < 0 || (uint64_t)n_groups_capacity < plan->n_groups)
+        return fail(SDB_CAPACITY, "output holds %lld groups, plan needs %llu", (long long)n_groups_capacity,
+                    (unsigned long long)plan->n_groups);
+    if (plan->terminal < TERM_SCALAR || plan->terminal > TERM_GLOBAL)
+        return fail(SDB_INVALID_ARG, "bad plan terminal %d", plan->terminal);
+    if (plan->terminal == TERM_SCALAR && q->n_group_keys > 0)
+        return fail(SDB_INVALID_ARG, "scalar terminal on a grouped query");
+    if (plan->terminal == TERM_LDS && plan->n_groups > (uint64_t)kLdsGroupLimit)
+        return fail(SDB_CAPACITY, "LDS terminal holds at most %d groups", kLdsGroupLimit);
+    if (plan->ipt != 1 && plan->ipt != 2 && plan->ipt != 4 && plan->ipt != 8)
+        return fail(SDB_INVALID_ARG, "bad plan ipt %d", plan->ipt);
+    if (plan->vector && q->n_fact > 0 && !columns_aligned(q, plan))
+        return fail(SDB_INVALID_ARG, "vector plan but a column is not 16-byte aligned");
+
+    hipStream_t s = (hipStream_t)stream;
+    SDB_HIP(launch_fill_u64((unsigned long long*)sums, plan->n_groups, s), "sums fill");
+    SDB_HIP(launch_fill_u64((unsigned long long*)counts, plan->n_groups, s), "counts fill");
+    if (q->n_fact == 0) return ok();
+
+    FusedParams p = fused_params(q, plan);
+    p.sums = (unsigned long long*)sums;
+    p.counts = (unsigned long long*)counts;
+    int grid = plan->grid;
+    if (grid <= 0) {
+        st = choose_grid(q, plan, &grid);
+        if (st != SDB_OK) return st;
+    }
+    const size_t lds = plan->terminal == TERM_LDS ? (size_t)plan->n_groups * 16 : 0;
+    SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, grid, lds, s), "fused kernel launch");
+    return ok();
+}
+
+SDB_API sdb_status sdb_finalize_scratch_bytes(const sdb_plan* plan, int64_t* bytes) {
+    if (!plan || !bytes) return fail(SDB_INVALID_ARG, "null argument");
+    const uint64_t nb = (plan->n_groups + kFinGroupsPerBlock - 1) / kFinGroupsPerBlock;
+    *bytes = (int64_t)std::max<uint64_t>(nb * 8, 256);
+    return ok();
+}
+
+SDB_API sdb_status sdb_finalize_groups(const sdb_plan* plan, const int64_t* sums, const int64_t* counts,
+                                       int32_t* out_keys, int64_t* out_sums, int64_t* out_counts,
+                                       int64_t out_capacity, int64_t* out_n, void* scratch,
+                                       int64_t scratch_bytes, void* stream) {
+    if (!plan) return fail(SDB_INVALID_ARG, "null plan");
+    if (!sums || !counts || !out_sums || !out_counts || !out_n || !scratch)
+        return fail(SDB_INVALID_ARG, "null argument");
+    if (plan->n_group_keys < 0 || plan->n_group_keys > SDB_MAX_GROUP_KEYS)
+        return fail(SDB_INVALID_ARG, "bad plan key count");
+    if (plan->n_group_keys > 0 && !out_keys) return fail(SDB_INVALID_ARG, "null key output");
+    if (plan->n_groups == 0 || plan->n_groups > (uint64_t)INT32_MAX)
+        return fail(SDB_INVALID_ARG, "bad plan group count");
+    {
+        // the last key varies fastest: stride[last] = 1, stride[k] = stride[k+1] * radix[k+1]
+        uint64_t g = 1;
+        for (int k = plan->n_group_keys - 1; k >= 0; --k) {
+            if (plan->radix[k] == 0 || plan->stride[k] != g) return fail(SDB_INVALID_ARG, "bad plan group layout");
+            g *= plan->radix[k];
+        }
+        if (g != plan->n_groups) return fail(SDB_INVALID_ARG, "bad plan group count");
+    }
+    if (out_capacity < 0 || (uint64_t)out_capacity < plan->n_groups)
+        return fail(SDB_CAPACITY, "output holds %lld groups, plan needs %llu", (long long)out_capacity,
+                    (unsigned long long)plan->n_groups);
+    int64_t need = 0;
+    sdb_finalize_scratch_bytes(plan, &need);
+    if (scratch_bytes < need)
+        return fail(SDB_WORKSPACE_TOO_SMALL, "finalize scratch holds %lld bytes, %lld needed",
+                    (long long)scratch_bytes, (long long)need);
+    FinalizeParams fp;
+    std::memset(&fp, 0, sizeof fp);
+    fp.sums = (const long long*)sums;
+    fp.counts = (const long long*)counts;
+    fp.n_groups = plan->n_groups;
+    fp.n_keys = plan->n_group_keys;
+    fp.scalar = plan->n_group_keys == 0;
+    for (int k = 0; k < plan->n_group_keys; ++k) {
+        fp.key_min[k] = plan->key_min[k];
+        fp.radix[k] = plan->radix[k];
+        fp.stride[k] = (uint32_t)plan->stride[k];
+    }
+    fp.out_keys = out_keys;
+    fp.out_sums = (long long*)out_sums;
+    fp.out_counts = (long long*)out_counts;
+    fp.out_n = (long long*)out_n;
+    fp.block_off = (long long*)scratch;
+    fp.n_blocks = (int64_t)((plan->n_groups + kFinGroupsPerBlock - 1) / kFinGroupsPerBlock);
+    SDB_HIP(launch_finalize(fp, (hipStream_t)stream), "finalize launch");
+    return ok();
+}
+
+}  // extern "C"

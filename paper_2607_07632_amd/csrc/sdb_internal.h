@@ -1,0 +1,130 @@
+// Internal structures shared by the host runtime (sdb_api.cpp) and the
+// device kernels (sdb_kernels.hip). Nothing here is part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "sdb.h"
+
+namespace sdb {
+
+constexpr int kMaxStages = SDB_MAX_STAGES;
+constexpr int kBlock = 256;              // threads per block of the fused kernel
+constexpr int kLdsGroupLimit = 2048;     // LDS terminal: sums + counts of G <= 2048 groups (32 KB)
+constexpr int kFinBlock = 256;           // finalize: threads per block
+constexpr int kFinPerThread = 4;         // finalize: groups per thread
+constexpr int kFinGroupsPerBlock = kFinBlock * kFinPerThread;
+constexpr int kDenseSlack = 1024;        // dense limit: key range <= max(2 * n_rows, 1024)
+
+enum StageKind : int32_t { ST_PRED = 0, ST_DENSE = 1, ST_HASH = 2 };
+enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3 };
+
+// A literal comparison lowered to one unsigned range test over int32:
+// pass  <=>  ((uint32_t)(x - lo) <= span) != negate.
+struct RangeTest {
+    int32_t lo;
+    uint32_t span;
+    int32_t negate;
+};
+
+// One stage of the fused pass, as the kernel reads it (kernel argument).
+struct StageDev {
+    int32_t kind;          // StageKind
+    int32_t col;           // fact column index
+    RangeTest test;        // ST_PRED
+    int32_t width;         // ST_DENSE: bytes per map entry (1, 2, 4)
+    int32_t kmin;          // ST_DENSE: key of slot 0
+    uint32_t nslots;       // ST_DENSE: slots; ST_HASH: capacity (power of two)
+    uint32_t hmask;        // ST_HASH: capacity - 1
+    int32_t hshift;        // ST_HASH: 32 - log2(capacity)
+    uint32_t sentinel;     // code meaning "no passing dimension row"
+    const void* map;       // ST_DENSE / ST_HASH table
+    int32_t n_gk;          // group keys decoded from this table's code
+    uint32_t gk_div[SDB_MAX_PAYLOADS];     // key code = (code / div) % radix (div 1: skip)
+    uint32_t gk_radix[SDB_MAX_PAYLOADS];   // 0: no modulo needed
+    uint32_t gk_stride[SDB_MAX_PAYLOADS];  // group-id stride of that key
+};
+
+struct FusedParams {
+    const int32_t* cols[SDB_MAX_FACT_COLS];
+    int64_t n;
+    int32_t nstages;
+    int32_t agg_kind;
+    int32_t agg_a;
+    int32_t agg_b;
+    uint32_t n_groups;
+    int32_t pad_;
+    unsigned long long* sums;
+    unsigned long long* counts;
+    StageDev st[kMaxStages];
+};
+
+// Statistics block at the start of a dimension workspace.
+struct DimStats {
+    int32_t kmin;
+    int32_t kmax;
+    unsigned long long npass;
+    int32_t pmin[SDB_MAX_PAYLOADS];
+    int32_t pmax[SDB_MAX_PAYLOADS];
+    uint32_t dup;          // 1: duplicate key seen; 2: hash table full (cannot happen when sized)
+    uint32_t pad_[5];
+};
+static_assert(sizeof(DimStats) <= 256, "stats must fit the reserved 256 bytes");
+
+struct BuildParams {
+    const int32_t* key;
+    int64_t n;
+    const int32_t* cols[SDB_MAX_DIM_COLS];
+    int32_t n_preds;
+    int32_t pred_col[SDB_MAX_DIM_PREDS];
+    RangeTest pred[SDB_MAX_DIM_PREDS];
+    int32_t n_payloads;
+    int32_t payload_col[SDB_MAX_PAYLOADS];
+    int32_t pmin[SDB_MAX_PAYLOADS];
+    uint32_t pdiv[SDB_MAX_PAYLOADS];
+    DimStats* stats;
+    void* map;                 // dense map or hash table
+    uint32_t* occ;             // dense occupancy bitmap
+    int32_t width;
+    int32_t kmin;
+    uint64_t nslots;
+    uint32_t sentinel;
+    uint32_t hmask;
+    int32_t hshift;
+};
+
+struct FinalizeParams {
+    const long long* sums;
+    const long long* counts;
+    uint64_t n_groups;
+    int32_t n_keys;
+    int32_t scalar;
+    int32_t key_min[SDB_MAX_GROUP_KEYS];
+    uint32_t radix[SDB_MAX_GROUP_KEYS];
+    uint32_t stride[SDB_MAX_GROUP_KEYS];
+    int32_t* out_keys;
+    long long* out_sums;
+    long long* out_counts;
+    long long* out_n;
+    long long* block_off;      // scratch: one entry per finalize block
+    int64_t n_blocks;
+};
+
+// ---- launchers (sdb_kernels.hip) -----------------------------------------
+hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s);
+hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s);
+hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s);
+hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s);
+hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s);
+hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
+                         unsigned long long* pass_counts, hipStream_t s);
+// Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if
+// the instance does not exist.
+int fused_blocks_per_cu(int vector, int ipt, int terminal, size_t lds_bytes);
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid,
+                        size_t lds_bytes, hipStream_t s);
+hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);
+
+}  // namespace sdb

@@ -1,0 +1,667 @@
+// Device kernels of libsdb for CDNA4 (gfx950, wave64).
+//
+//  * dimension build: statistics pass, direct-mapped packed map scatter, and
+//    open-addressing insert with 64-bit compare-and-swap (Section 3.3);
+//  * plan sampling: each stage evaluated on its own over a strided fact sample;
+//  * the fused probe-filter-aggregate pass (Sections 3.2, 4.2, 4.3);
+//  * group-table compaction.
+//
+// The fused pass is a grid-stride persistent loop. A lane owns IPT items per
+// iteration; an item is W consecutive fact rows (W = 4: one 128-bit load per
+// column per item). Stages run in plan order; a stage loads its column only
+// for items that still hold a live row, and the whole wave leaves the stage
+// list as soon as no lane has a live row (wave-wide vote). Probes keep the
+// group id in a register; the terminal is a register accumulator, an LDS
+// group table, or global 64-bit atomics.
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+
+#include "sdb_internal.h"
+
+namespace sdb {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// small helpers
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ bool range_pass(const RangeTest& t, int32_t x) {
+    return ((uint32_t)(x - t.lo) <= t.span) != (t.negate != 0);
+}
+
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__device__ __forceinline__ int32_t wave_min_i32(int32_t v) {
+    for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
+    for (int off = 32; off > 0; off >>= 1) v = max(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// Loads the W rows of item `item` of a fact column (non-temporal: fact data is
+// streamed once and should not evict the dimension maps and group tables).
+template <int W>
+__device__ __forceinline__ void load_item(const int32_t* col, int64_t item, int32_t (&x)[W]) {
+    if constexpr (W == 4) {
+        v4i v = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(col) + item);
+        x[0] = v.x;
+        x[1] = v.y;
+        x[2] = v.z;
+        x[3] = v.w;
+    } else {
+        x[0] = __builtin_nontemporal_load(col + item);
+    }
+}
+
+__device__ __forceinline__ uint32_t load_dense_code(const StageDev& S, uint32_t idx) {
+    if (S.width == 1) return static_cast<const uint8_t*>(S.map)[idx];
+    if (S.width == 2) return static_cast<const uint16_t*>(S.map)[idx];
+    return static_cast<const uint32_t*>(S.map)[idx];
+}
+
+__device__ __forceinline__ uint32_t hash_slot(const StageDev& S, int32_t k) {
+    return ((uint32_t)k * 0x9E3779B1u) >> S.hshift & S.hmask;
+}
+
+// Resolves a hash probe whose first slot value is `slot`; returns the code or
+// the sentinel. Linear probing; at most nslots slots are inspected.
+__device__ __forceinline__ uint32_t hash_resolve(const StageDev& S, int32_t k, uint32_t h,
+                                                 unsigned long long slot) {
+    const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
+    for (uint32_t it = 0; it < S.nslots; ++it) {
+        const uint32_t hi = (uint32_t)(slot >> 32);
+        if (hi == 0u) return S.sentinel;                       // empty slot: key absent
+        if ((int32_t)(uint32_t)slot == k) return hi - 1u;      // filtered rows hold 0xFFFFFFFF -> sentinel
+        h = (h + 1u) & S.hmask;
+        slot = tab[h];
+    }
+    return S.sentinel;
+}
+
+__device__ __forceinline__ uint32_t code_contribution(const StageDev& S, uint32_t c) {
+    uint32_t g = 0;
+    for (int k = 0; k < S.n_gk; ++k) {
+        uint32_t q = c;
+        if (S.gk_div[k] != 1u) q /= S.gk_div[k];
+        if (S.gk_radix[k] != 0u) q %= S.gk_radix[k];
+        g += q * S.gk_stride[k];
+    }
+    return g;
+}
+
+// One stage for a single row (plan sampling).
+__device__ __forceinline__ bool stage_pass_one(const StageDev& S, int32_t x) {
+    if (S.kind == ST_PRED) return range_pass(S.test, x);
+    if (S.kind == ST_DENSE) {
+        const uint32_t idx = (uint32_t)(x - S.kmin);
+        return idx < S.nslots && load_dense_code(S, idx) != S.sentinel;
+    }
+    const uint32_t h = hash_slot(S, x);
+    const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
+    return hash_resolve(S, x, h, tab[h]) != S.sentinel;
+}
+
+// ---------------------------------------------------------------------------
+// fills
+// ---------------------------------------------------------------------------
+
+__global__ void fill_u32_kernel(uint32_t* p, uint64_t n, uint32_t v) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+__global__ void fill_u64_kernel(unsigned long long* p, uint64_t n) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0ull;
+}
+
+static int fill_grid(uint64_t n) {
+    uint64_t g = (n + 255) / 256;
+    if (g > 4096) g = 4096;
+    if (g < 1) g = 1;
+    return (int)g;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s) {
+    if (n_words == 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(fill_grid(n_words)), dim3(256), 0, s, p, n_words, value);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_u64_kernel, dim3(fill_grid(n)), dim3(256), 0, s, p, n);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// dimension build
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ bool dim_row_passes(const BuildParams& bp, int64_t i) {
+    bool pass = true;
+    for (int q = 0; q < bp.n_preds; ++q) pass = pass && range_pass(bp.pred[q], bp.cols[bp.pred_col[q]][i]);
+    return pass;
+}
+
+__global__ void stats_init_kernel(DimStats* st) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        st->kmin = INT_MAX;
+        st->kmax = INT_MIN;
+        st->npass = 0ull;
+        for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+            st->pmin[p] = INT_MAX;
+            st->pmax[p] = INT_MIN;
+        }
+        st->dup = 0u;
+    }
+}
+
+// Key range over all rows; pass count and payload ranges over passing rows.
+__global__ void __launch_bounds__(256) dim_stats_kernel(BuildParams bp) {
+    int32_t kmin = INT_MAX, kmax = INT_MIN;
+    unsigned long long npass = 0;
+    int32_t pmin[SDB_MAX_PAYLOADS], pmax[SDB_MAX_PAYLOADS];
+    for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+        pmin[p] = INT_MAX;
+        pmax[p] = INT_MIN;
+    }
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
+        const int32_t k = bp.key[i];
+        kmin = min(kmin, k);
+        kmax = max(kmax, k);
+        if (dim_row_passes(bp, i)) {
+            ++npass;
+            for (int p = 0; p < bp.n_payloads; ++p) {
+                const int32_t v = bp.cols[bp.payload_col[p]][i];
+                pmin[p] = min(pmin[p], v);
+                pmax[p] = max(pmax[p], v);
+            }
+        }
+    }
+    kmin = wave_min_i32(kmin);
+    kmax = wave_max_i32(kmax);
+    npass = wave_sum_u64(npass);
+    for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+        pmin[p] = wave_min_i32(pmin[p]);
+        pmax[p] = wave_max_i32(pmax[p]);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        DimStats* st = bp.stats;
+        atomicMin(&st->kmin, kmin);
+        atomicMax(&st->kmax, kmax);
+        if (npass) atomicAdd(&st->npass, npass);
+        for (int p = 0; p < bp.n_payloads; ++p) {
+            atomicMin(&st->pmin[p], pmin[p]);
+            atomicMax(&st->pmax[p], pmax[p]);
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t dim_row_code(const BuildParams& bp, int64_t i) {
+    uint32_t c = 0;
+    for (int p = 0; p < bp.n_payloads; ++p)
+        c += (uint32_t)(bp.cols[bp.payload_col[p]][i] - bp.pmin[p]) * bp.pdiv[p];
+    return c;
+}
+
+// Direct-mapped map: one entry per key in [kmin, kmin + nslots); a passing row
+// stores its code, a filtered row (and every key no row holds, from the fill)
+// the all-ones sentinel. An occupancy bit per slot detects duplicate keys.
+__global__ void __launch_bounds__(256) dense_scatter_kernel(BuildParams bp) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
+        const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
+        if ((uint64_t)idx >= bp.nslots) {          // cannot happen: kmin/kmax cover all keys
+            atomicOr(&bp.stats->dup, 4u);
+            continue;
+        }
+        const uint32_t bit = 1u << (idx & 31u);
+        const uint32_t old = atomicOr(&bp.occ[idx >> 5], bit);
+        if (old & bit) atomicOr(&bp.stats->dup, 1u);
+        const uint32_t c = dim_row_passes(bp, i) ? dim_row_code(bp, i) : bp.sentinel;
+        if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx] = (uint8_t)c;
+        else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx] = (uint16_t)c;
+        else static_cast<uint32_t*>(bp.map)[idx] = c;
+    }
+}
+
+// Open addressing, linear probing, 8-byte slots {key, code + 1 | 0xFFFFFFFF}.
+__global__ void __launch_bounds__(256) hash_insert_kernel(BuildParams bp) {
+    unsigned long long* tab = static_cast<unsigned long long*>(bp.map);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
+        const int32_t k = bp.key[i];
+        const uint32_t enc = dim_row_passes(bp, i) ? dim_row_code(bp, i) + 1u : 0xFFFFFFFFu;
+        const unsigned long long slot = ((unsigned long long)enc << 32) | (uint32_t)k;
+        uint32_t h = ((uint32_t)k * 0x9E3779B1u) >> bp.hshift & bp.hmask;
+        bool placed = false;
+        for (uint64_t it = 0; it < bp.nslots; ++it) {
+            const unsigned long long old = atomicCAS(&tab[h], 0ull, slot);
+            if (old == 0ull) {
+                placed = true;
+                break;
+            }
+            if ((int32_t)(uint32_t)old == k) {
+                atomicOr(&bp.stats->dup, 1u);
+                placed = true;
+                break;
+            }
+            h = (h + 1u) & bp.hmask;
+        }
+        if (!placed) atomicOr(&bp.stats->dup, 2u);
+    }
+}
+
+static int build_grid(int64_t n) {
+    int64_t g = (n + 255) / 256;
+    if (g > 8192) g = 8192;
+    if (g < 1) g = 1;
+    return (int)g;
+}
+
+hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s) {
+    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, s, bp.stats);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || bp.n == 0) return e;
+    hipLaunchKernelGGL(dim_stats_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+    return hipGetLastError();
+}
+
+hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s) {
+    if (bp.n == 0) return hipSuccess;
+    hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+    return hipGetLastError();
+}
+
+hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s) {
+    if (bp.n == 0) return hipSuccess;
+    hipLaunchKernelGGL(hash_insert_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// plan sampling: pass count of every stage on its own over a strided sample
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(256) sample_kernel(FusedParams p, int64_t step, int64_t n_sample,
+                                                     unsigned long long* pass_counts) {
+    __shared__ unsigned int cnt[kMaxStages];
+    if (threadIdx.x < kMaxStages) cnt[threadIdx.x] = 0u;
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    // every lane runs the same number of iterations so the wave-wide votes below are complete
+    const int64_t n_iter = (n_sample + stride - 1) / stride;
+    for (int64_t it = 0; it < n_iter; ++it) {
+        const int64_t k = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        const bool valid = k < n_sample;
+        const int64_t row = valid ? k * step : 0;
+        for (int s = 0; s < p.nstages; ++s) {
+            const StageDev& S = p.st[s];
+            bool pass = false;
+            if (valid) pass = stage_pass_one(S, p.cols[S.col][row]);
+            const unsigned long long m = __ballot(pass);
+            if ((threadIdx.x & 63) == 0 && m) atomicAdd(&cnt[s], (unsigned int)__popcll(m));
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < p.nstages && cnt[threadIdx.x])
+        atomicAdd(&pass_counts[threadIdx.x], (unsigned long long)cnt[threadIdx.x]);
+}
+
+hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
+                         unsigned long long* pass_counts, hipStream_t s) {
+    hipLaunchKernelGGL(fill_u64_kernel, dim3(1), dim3(64), 0, s, pass_counts, (uint64_t)kMaxStages);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n_sample == 0 || p.nstages == 0) return e;
+    int64_t g = (n_sample + 255) / 256;
+    if (g > 256) g = 256;
+    hipLaunchKernelGGL(sample_kernel, dim3((int)g), dim3(256), 0, s, p, step, n_sample, pass_counts);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// the fused probe-filter-aggregate pass
+// ---------------------------------------------------------------------------
+
+template <int TERM>
+struct TermState {
+    unsigned long long sum = 0;
+    unsigned long long cnt = 0;
+    unsigned long long* lsum = nullptr;
+    unsigned long long* lcnt = nullptr;
+};
+
+template <int TERM>
+__device__ __forceinline__ void accumulate(const FusedParams& p, TermState<TERM>& ts, uint32_t g,
+                                           long long v) {
+    if constexpr (TERM == TERM_SCALAR) {
+        ts.sum += (unsigned long long)v;
+        ts.cnt += 1ull;
+    } else if constexpr (TERM == TERM_LDS) {
+        atomicAdd(&ts.lsum[g], (unsigned long long)v);
+        atomicAdd(&ts.lcnt[g], 1ull);
+    } else {
+        atomicAdd(&p.sums[g], (unsigned long long)v);
+        atomicAdd(&p.counts[g], 1ull);
+    }
+}
+
+// Runs every stage and the terminal for IPT items of W rows each. `live[j]`
+// holds one bit per row of item j. All lanes of the wave must call this
+// together (the early exit is a wave-wide vote).
+template <int W, int IPT, int TERM>
+__device__ __forceinline__ void process_items(const FusedParams& p, const int64_t (&item)[IPT],
+                                              uint32_t (&live)[IPT], TermState<TERM>& ts) {
+    uint32_t gid[IPT][W];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+#pragma unroll
+        for (int r = 0; r < W; ++r) gid[j][r] = 0u;
+
+    for (int s = 0; s < p.nstages; ++s) {
+        uint32_t any = 0;
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) any |= live[j];
+        if (!__any(any != 0u)) return;            // no live row left in the wave
+        const StageDev& S = p.st[s];
+        const int32_t* col = p.cols[S.col];
+        int32_t x[IPT][W];
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            if (live[j]) load_item<W>(col, item[j], x[j]);
+            else {
+#pragma unroll
+                for (int r = 0; r < W; ++r) x[j][r] = 0;
+            }
+        }
+        if (S.kind == ST_PRED) {
+#pragma unroll
+            for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                for (int r = 0; r < W; ++r)
+                    if (!range_pass(S.test, x[j][r])) live[j] &= ~(1u << r);
+        } else if (S.kind == ST_DENSE) {
+            uint32_t c[IPT][W];
+#pragma unroll
+            for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                for (int r = 0; r < W; ++r) {
+                    const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+                    c[j][r] = S.sentinel;
+                    if (((live[j] >> r) & 1u) && idx < S.nslots) c[j][r] = load_dense_code(S, idx);
+                }
+#pragma unroll
+            for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                for (int r = 0; r < W; ++r) {
+                    if (c[j][r] == S.sentinel) live[j] &= ~(1u << r);
+                    else if (S.n_gk) gid[j][r] += code_contribution(S, c[j][r]);
+                }
+        } else {
+            const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
+            uint32_t h[IPT][W];
+            unsigned long long sl[IPT][W];
+#pragma unroll
+            for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                for (int r = 0; r < W; ++r) {
+                    h[j][r] = hash_slot(S, x[j][r]);
+                    sl[j][r] = 0ull;
+                    if ((live[j] >> r) & 1u) sl[j][r] = tab[h[j][r]];
+                }
+#pragma unroll
+            for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                for (int r = 0; r < W; ++r) {
+                    if (!((live[j] >> r) & 1u)) continue;
+                    const uint32_t c = hash_resolve(S, x[j][r], h[j][r], sl[j][r]);
+                    if (c == S.sentinel) live[j] &= ~(1u << r);
+                    else if (S.n_gk) gid[j][r] += code_contribution(S, c);
+                }
+        }
+    }
+
+    uint32_t any = 0;
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) any |= live[j];
+    if (!__any(any != 0u)) return;
+
+    int32_t a[IPT][W], b[IPT][W];
+    const int32_t* ca = p.cols[p.agg_a];
+    const int32_t* cb = p.cols[p.agg_b];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+        if (live[j]) load_item<W>(ca, item[j], a[j]);
+        if (live[j] && p.agg_kind != SDB_AGG_COL) load_item<W>(cb, item[j], b[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+#pragma unroll
+        for (int r = 0; r < W; ++r) {
+            if (!((live[j] >> r) & 1u)) continue;
+            const long long va = a[j][r];
+            long long v;
+            if (p.agg_kind == SDB_AGG_COL) v = va;
+            else if (p.agg_kind == SDB_AGG_MUL) v = (long long)((unsigned long long)va * (unsigned long long)(long long)b[j][r]);
+            else if (p.agg_kind == SDB_AGG_SUB) v = va - (long long)b[j][r];
+            else v = va + (long long)b[j][r];
+            accumulate<TERM>(p, ts, gid[j][r], v);
+        }
+}
+
+template <int W, int IPT, int TERM>
+__global__ void __launch_bounds__(kBlock) star_fused_kernel(FusedParams p) {
+    extern __shared__ unsigned long long lds[];
+    TermState<TERM> ts;
+    if constexpr (TERM == TERM_LDS) {
+        ts.lsum = lds;
+        ts.lcnt = lds + p.n_groups;
+        for (uint32_t g = threadIdx.x; g < 2u * p.n_groups; g += blockDim.x) lds[g] = 0ull;
+        __syncthreads();
+    }
+
+    const int64_t n_items = p.n / W;
+    const int64_t tile = (int64_t)kBlock * IPT;
+    const int64_t n_tiles = (n_items + tile - 1) / tile;
+    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+        int64_t item[IPT];
+        uint32_t live[IPT];
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            item[j] = t * tile + (int64_t)j * kBlock + threadIdx.x;
+            live[j] = item[j] < n_items ? (1u << W) - 1u : 0u;
+        }
+        process_items<W, IPT, TERM>(p, item, live, ts);
+    }
+    if constexpr (W > 1) {
+        // the last n mod W rows, one per lane, by the last block
+        if (blockIdx.x == gridDim.x - 1) {
+            int64_t row[1] = {n_items * W + (int64_t)threadIdx.x};
+            uint32_t live1[1] = {row[0] < p.n ? 1u : 0u};
+            process_items<1, 1, TERM>(p, row, live1, ts);
+        }
+    }
+
+    if constexpr (TERM == TERM_SCALAR) {
+        __shared__ unsigned long long red[2][kBlock / 64];
+        const unsigned long long s = wave_sum_u64(ts.sum);
+        const unsigned long long c = wave_sum_u64(ts.cnt);
+        if ((threadIdx.x & 63) == 0) {
+            red[0][threadIdx.x >> 6] = s;
+            red[1][threadIdx.x >> 6] = c;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            unsigned long long bs = 0, bc = 0;
+            for (int w = 0; w < kBlock / 64; ++w) {
+                bs += red[0][w];
+                bc += red[1][w];
+            }
+            if (bc) {
+                atomicAdd(&p.sums[0], bs);
+                atomicAdd(&p.counts[0], bc);
+            }
+        }
+    } else if constexpr (TERM == TERM_LDS) {
+        __syncthreads();
+        for (uint32_t g = threadIdx.x; g < p.n_groups; g += blockDim.x) {
+            const unsigned long long c = ts.lcnt[g];
+            if (c) {
+                atomicAdd(&p.sums[g], ts.lsum[g]);
+                atomicAdd(&p.counts[g], c);
+            }
+        }
+    }
+}
+
+template <int W, int IPT, int TERM>
+static const void* fused_fn() {
+    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM>);
+}
+
+static const void* pick_fused(int vector, int ipt, int terminal) {
+#define SDB_PICK(Wv, I)                                                        \
+    if (ipt == I) {                                                            \
+        if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR>();    \
+        if (terminal == TERM_LDS) return fused_fn<Wv, I, TERM_LDS>();          \
+        if (terminal == TERM_GLOBAL) return fused_fn<Wv, I, TERM_GLOBAL>();    \
+    }
+    if (vector) {
+        SDB_PICK(4, 1)
+        SDB_PICK(4, 2)
+        SDB_PICK(4, 4)
+        SDB_PICK(4, 8)
+    } else {
+        SDB_PICK(1, 1)
+        SDB_PICK(1, 2)
+        SDB_PICK(1, 4)
+        SDB_PICK(1, 8)
+    }
+#undef SDB_PICK
+    return nullptr;
+}
+
+int fused_blocks_per_cu(int vector, int ipt, int terminal, size_t lds_bytes) {
+    const void* fn = pick_fused(vector, ipt, terminal);
+    if (!fn) return -1;
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kBlock, lds_bytes) != hipSuccess)
+        return -1;
+    return blocks;
+}
+
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid,
+                        size_t lds_bytes, hipStream_t s) {
+    const void* fn = pick_fused(vector, ipt, terminal);
+    if (!fn) return hipErrorInvalidValue;
+    void* args[] = {const_cast<FusedParams*>(&p)};
+    return hipLaunchKernel(fn, dim3(grid), dim3(kBlock), args, lds_bytes, s);
+}
+
+// ---------------------------------------------------------------------------
+// finalize: order-preserving compaction of the group table
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ bool group_present(const FinalizeParams& fp, uint64_t g) {
+    if (g >= fp.n_groups) return false;
+    return fp.scalar ? true : fp.counts[g] > 0;
+}
+
+__global__ void __launch_bounds__(kFinBlock) fin_count_kernel(FinalizeParams fp) {
+    __shared__ unsigned int wsum[kFinBlock / 64];
+    const uint64_t base = (uint64_t)blockIdx.x * kFinGroupsPerBlock;
+    unsigned int c = 0;
+    for (int k = 0; k < kFinPerThread; ++k) c += group_present(fp, base + (uint64_t)k * kFinBlock + threadIdx.x);
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned int t = 0;
+        for (int w = 0; w < kFinBlock / 64; ++w) t += wsum[w];
+        fp.block_off[blockIdx.x] = t;
+    }
+}
+
+// One block turns the per-block counts into exclusive offsets and writes the total.
+__global__ void __launch_bounds__(1024) fin_scan_kernel(FinalizeParams fp) {
+    __shared__ long long buf[1024];
+    __shared__ long long carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < fp.n_blocks; base += 1024) {
+        const int64_t i = base + threadIdx.x;
+        const long long v = i < fp.n_blocks ? fp.block_off[i] : 0;
+        buf[threadIdx.x] = v;
+        __syncthreads();
+        for (int off = 1; off < 1024; off <<= 1) {       // Hillis-Steele inclusive scan
+            const long long add = threadIdx.x >= (unsigned)off ? buf[threadIdx.x - off] : 0;
+            __syncthreads();
+            buf[threadIdx.x] += add;
+            __syncthreads();
+        }
+        const long long incl = buf[threadIdx.x];
+        if (i < fp.n_blocks) fp.block_off[i] = carry + incl - v;
+        __syncthreads();
+        if (threadIdx.x == 1023) carry += incl;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) fp.out_n[0] = carry;
+}
+
+__global__ void __launch_bounds__(kFinBlock) fin_scatter_kernel(FinalizeParams fp) {
+    __shared__ unsigned int wcnt[kFinBlock / 64];
+    __shared__ long long run;
+    if (threadIdx.x == 0) run = fp.block_off[blockIdx.x];
+    __syncthreads();
+    const uint64_t base = (uint64_t)blockIdx.x * kFinGroupsPerBlock;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int k = 0; k < kFinPerThread; ++k) {
+        const uint64_t g = base + (uint64_t)k * kFinBlock + threadIdx.x;
+        const bool present = group_present(fp, g);
+        const unsigned long long m = __ballot(present);
+        const unsigned int before_in_wave = __popcll(m & ((1ull << lane) - 1ull));
+        if (lane == 0) wcnt[wave] = __popcll(m);
+        __syncthreads();
+        unsigned int before = before_in_wave;
+        unsigned int total = 0;
+        for (int w = 0; w < kFinBlock / 64; ++w) {
+            if (w < wave) before += wcnt[w];
+            total += wcnt[w];
+        }
+        if (present) {
+            const long long o = run + before;
+            for (int q = 0; q < fp.n_keys; ++q)
+                fp.out_keys[o * fp.n_keys + q] =
+                    (int32_t)(((uint32_t)g / fp.stride[q]) % fp.radix[q]) + fp.key_min[q];
+            fp.out_sums[o] = fp.sums[g];
+            fp.out_counts[o] = fp.counts[g];
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) run += total;
+        __syncthreads();
+    }
+}
+
+hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s) {
+    hipLaunchKernelGGL(fin_count_kernel, dim3((unsigned)fp.n_blocks), dim3(kFinBlock), 0, s, fp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fin_scan_kernel, dim3(1), dim3(1024), 0, s, fp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fin_scatter_kernel, dim3((unsigned)fp.n_blocks), dim3(kFinBlock), 0, s, fp);
+    return hipGetLastError();
+}
+
+}  // namespace sdb

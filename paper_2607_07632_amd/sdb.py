@@ -1,0 +1,399 @@
+"""ctypes binding of libsdb (include/sdb.h): argument marshalling only.
+
+Every step of the query runs in the library's HIP kernels; this module only
+lays out the C structs, passes torch device pointers and the current HIP
+stream, allocates the caller-owned buffers with torch, and copies results back.
+It fails loudly when the built library is missing: there is no fallback.
+
+The high-level helpers (``build_dims``, ``StarQuery``) translate the plain-data
+query description used by the test suite and the benchmark (column names,
+predicate ops, joins, group keys, aggregate) into the C descriptors.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass, field
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsdb.so")
+
+MAX_DIM_COLS = 8
+MAX_DIM_PREDS = 4
+MAX_PAYLOADS = 3
+MAX_FACT_COLS = 16
+MAX_FACT_PREDS = 8
+MAX_JOINS = 6
+MAX_GROUP_KEYS = 4
+MAX_STAGES = MAX_FACT_PREDS + MAX_JOINS
+PLAN_SCRATCH_BYTES = 256
+
+OPS = {"eq": 0, "ne": 1, "lt": 2, "le": 3, "gt": 4, "ge": 5, "between": 6}
+TABLES = {"auto": 0, "dense": 1, "hash": 2}
+AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
+TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3}
+TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global"}
+STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
+          4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
+
+i32, u32, i64, u64, vp = C.c_int32, C.c_uint32, C.c_int64, C.c_uint64, C.c_void_p
+
+
+class SdbPred(C.Structure):
+    _fields_ = [("col", i32), ("op", i32), ("lo", i64), ("hi", i64)]
+
+
+class SdbDimDesc(C.Structure):
+    _fields_ = [("key", vp), ("n_rows", i64), ("n_cols", i32), ("cols", vp * MAX_DIM_COLS),
+                ("n_preds", i32), ("preds", SdbPred * MAX_DIM_PREDS), ("n_payloads", i32),
+                ("payload_cols", i32 * MAX_PAYLOADS), ("kind", i32), ("load_factor", C.c_double)]
+
+
+class SdbDim(C.Structure):
+    _fields_ = [("kind", i32), ("width", i32), ("n_rows", i64), ("n_pass", i64),
+                ("key_min", i32), ("key_max", i32), ("n_slots", u64), ("hash_bits", i32),
+                ("sentinel", u32), ("domain", u64), ("n_payloads", i32),
+                ("payload_min", i32 * MAX_PAYLOADS), ("payload_radix", u32 * MAX_PAYLOADS),
+                ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp)]
+
+
+class SdbJoin(C.Structure):
+    _fields_ = [("fact_key_col", i32), ("dim", C.POINTER(SdbDim))]
+
+
+class SdbGroupKey(C.Structure):
+    _fields_ = [("join", i32), ("payload", i32)]
+
+
+class SdbAgg(C.Structure):
+    _fields_ = [("kind", i32), ("a", i32), ("b", i32)]
+
+
+class SdbQuery(C.Structure):
+    _fields_ = [("n_fact", i64), ("n_cols", i32), ("cols", vp * MAX_FACT_COLS),
+                ("n_preds", i32), ("preds", SdbPred * MAX_FACT_PREDS),
+                ("n_joins", i32), ("joins", SdbJoin * MAX_JOINS),
+                ("n_group_keys", i32), ("group_keys", SdbGroupKey * MAX_GROUP_KEYS),
+                ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
+                ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32)]
+
+
+class SdbPlan(C.Structure):
+    _fields_ = [("n_stages", i32), ("stage_kind", i32 * MAX_STAGES),
+                ("stage_index", i32 * MAX_STAGES), ("stage_pass", C.c_double * MAX_STAGES),
+                ("sampled_rows", i64), ("terminal", i32), ("ipt", i32), ("vector", i32),
+                ("block", i32), ("grid", i32), ("n_group_keys", i32),
+                ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
+                ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64)]
+
+
+STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan]
+
+# exported symbol -> (restype, argtypes)
+SIGNATURES = {
+    "sdb_last_error": (C.c_char_p, []),
+    "sdb_status_string": (C.c_char_p, [i32]),
+    "sdb_abi_version": (i32, []),
+    "sdb_struct_sizes": (i32, [C.POINTER(i64), i32]),
+    "sdb_dim_required_bytes": (i32, [C.POINTER(SdbDimDesc), C.POINTER(i64)]),
+    "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
+    "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
+    "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp]),
+    "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
+    "sdb_finalize_groups": (i32, [C.POINTER(SdbPlan), vp, vp, vp, vp, vp, i64, vp, vp, i64, vp]),
+}
+
+
+class SdbError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libsdb (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2607_07632_amd.build` (there is no fallback)")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        sizes = (i64 * len(STRUCTS))()
+        if L.sdb_struct_sizes(sizes, len(STRUCTS)) != 0:
+            raise RuntimeError("sdb_struct_sizes failed")
+        for s, n in zip(STRUCTS, sizes):
+            if C.sizeof(s) != n:
+                raise RuntimeError(f"struct {s.__name__}: binding has {C.sizeof(s)} bytes, library {n}")
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        msg = lib().sdb_last_error().decode()
+        raise SdbError(status, msg)
+
+
+def _stream_handle(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else (t.data_ptr() or None)
+
+
+def _pred(p: dict, col_index: dict) -> SdbPred:
+    if p["op"] not in OPS:
+        raise ValueError(f"unknown predicate op {p['op']!r}")
+    hi = p.get("hi")
+    return SdbPred(col_index[p["col"]], OPS[p["op"]], int(p["lo"]), int(hi if hi is not None else 0))
+
+
+# ---------------------------------------------------------------------------
+# dimension tables
+# ---------------------------------------------------------------------------
+
+@dataclass
+class DimTable:
+    """A built lookup table and the device memory it lives in."""
+    handle: SdbDim
+    desc: SdbDimDesc
+    workspace: object                      # torch uint8 tensor (device)
+    keep: list = field(default_factory=list)
+
+    @property
+    def kind(self) -> str:
+        return {1: "dense", 2: "hash"}[self.handle.kind]
+
+
+def dim_required_bytes(desc: SdbDimDesc) -> int:
+    out = i64(0)
+    _check(lib().sdb_dim_required_bytes(C.byref(desc), C.byref(out)))
+    return out.value
+
+
+def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
+              load_factor: float = 0.0, stream=None, workspace=None) -> DimTable:
+    """Builds the lookup table of one dimension.
+
+    ``key`` and the values of ``cols`` are int32 device tensors of equal
+    length; ``preds`` are predicate dicts naming columns of ``cols``;
+    ``payloads`` name the columns to gather.
+    """
+    import torch
+    names = list(cols)
+    if len(names) > MAX_DIM_COLS:
+        raise ValueError("too many dimension columns")
+    idx = {n: i for i, n in enumerate(names)}
+    d = SdbDimDesc()
+    d.key = _ptr(key)
+    d.n_rows = int(key.numel())
+    d.n_cols = len(names)
+    for i, n in enumerate(names):
+        t = cols[n]
+        if t.dtype != torch.int32 or not t.is_cuda or t.numel() != key.numel():
+            raise ValueError(f"dimension column {n!r} must be int32 on the GPU with {key.numel()} rows")
+        d.cols[i] = _ptr(t)
+    if len(preds) > MAX_DIM_PREDS or len(payloads) > MAX_PAYLOADS:
+        raise ValueError("too many dimension predicates or payloads")
+    d.n_preds = len(preds)
+    for i, p in enumerate(preds):
+        d.preds[i] = _pred(p, idx)
+    d.n_payloads = len(payloads)
+    for i, p in enumerate(payloads):
+        d.payload_cols[i] = idx[p]
+    d.kind = TABLES[kind]
+    d.load_factor = float(load_factor or 0.0)
+    need = dim_required_bytes(d)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=key.device)
+    h = SdbDim()
+    _check(lib().sdb_build_dim(C.byref(d), _ptr(workspace), workspace.numel(),
+                               _stream_handle(stream), C.byref(h)))
+    return DimTable(h, d, workspace, [key] + [cols[n] for n in names])
+
+
+def build_dims(dims: dict, dim_keys: dict, query: dict, stream=None) -> list:
+    """One DimTable per join of ``query`` (dims: name -> {column: int32 device tensor})."""
+    out = []
+    for jd in query.get("joins", []):
+        t = dims[jd["dim"]]
+        key_name = dim_keys[jd["dim"]]
+        needed = [p["col"] for p in jd.get("preds", [])] + list(jd.get("payloads", []))
+        cols = {}
+        for n in needed:
+            cols.setdefault(n, t[n])
+        out.append(build_dim(t[key_name], cols, jd.get("preds", []), list(jd.get("payloads", [])),
+                             jd.get("kind", "auto"), jd.get("load_factor", 0.0), stream=stream))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# queries
+# ---------------------------------------------------------------------------
+
+@dataclass
+class QueryResult:
+    keys: np.ndarray      # int64 [n_groups, n_keys]
+    sums: np.ndarray      # int64 [n_groups]
+    counts: np.ndarray    # int64 [n_groups]
+
+    def as_rows(self):
+        return [(tuple(int(x) for x in k), int(s), int(c))
+                for k, s, c in zip(self.keys, self.sums, self.counts)]
+
+
+class StarQuery:
+    """The C query descriptor for one star query over device columns.
+
+    ``fact`` maps column name to an int32 device tensor; ``tables`` is the
+    list of DimTable per join (``build_dims``); ``query`` the plain-data
+    description. ``force`` may hold terminal ('scalar'|'lds'|'global'), ipt,
+    vector (1 / -1), order (True = keep query order) and grid.
+    """
+
+    def __init__(self, fact: dict, tables: list, query: dict, force: dict | None = None):
+        import torch
+        force = dict(force or {})
+        needed = []
+        for p in query.get("fact_preds", []):
+            needed.append(p["col"])
+        for jd in query.get("joins", []):
+            needed.append(jd["fact_key"])
+        agg = query["agg"]
+        needed.append(agg["a"])
+        if agg["kind"] != "col":
+            needed.append(agg["b"])
+        names = list(dict.fromkeys(needed))
+        if len(names) > MAX_FACT_COLS:
+            raise ValueError("too many fact columns")
+        idx = {n: i for i, n in enumerate(names)}
+        q = SdbQuery()
+        n = None
+        for i, name in enumerate(names):
+            t = fact[name]
+            if t.dtype != torch.int32 or not t.is_cuda:
+                raise ValueError(f"fact column {name!r} must be an int32 GPU tensor")
+            if n is None:
+                n = t.numel()
+            elif t.numel() != n:
+                raise ValueError("fact columns differ in length")
+            q.cols[i] = _ptr(t)
+        q.n_fact = int(n or 0)
+        q.n_cols = len(names)
+        preds = query.get("fact_preds", [])
+        if len(preds) > MAX_FACT_PREDS or len(tables) > MAX_JOINS:
+            raise ValueError("too many predicates or joins")
+        q.n_preds = len(preds)
+        for i, p in enumerate(preds):
+            q.preds[i] = _pred(p, idx)
+        joins = query.get("joins", [])
+        assert len(joins) == len(tables)
+        q.n_joins = len(joins)
+        for j, (jd, tab) in enumerate(zip(joins, tables)):
+            q.joins[j] = SdbJoin(idx[jd["fact_key"]], C.pointer(tab.handle))
+        gb = query.get("group_by", [])
+        if len(gb) > MAX_GROUP_KEYS:
+            raise ValueError("too many group keys")
+        q.n_group_keys = len(gb)
+        for k, (ref, payload) in enumerate(gb):
+            j = ref if isinstance(ref, int) else next(i for i, jd in enumerate(joins) if jd["dim"] == ref)
+            q.group_keys[k] = SdbGroupKey(j, list(joins[j]["payloads"]).index(payload))
+        q.agg = SdbAgg(AGGS[agg["kind"]], idx[agg["a"]], idx[agg["b"]] if agg["kind"] != "col" else 0)
+        q.force_terminal = TERMINALS[force.get("terminal", "auto")]
+        q.force_ipt = int(force.get("ipt", 0))
+        q.force_vector = int(force.get("vector", 0))
+        q.force_order = 1 if force.get("order") else 0
+        q.grid_blocks = int(force.get("grid", 0))
+        self.q = q
+        self.query = query
+        self.tables = tables
+        self.fact = fact
+        self.n_keys = len(gb)
+        self.plan_obj = None
+        self._plan_scratch = None
+
+    # -- steps ------------------------------------------------------------
+    def plan(self, stream=None) -> SdbPlan:
+        import torch
+        if self._plan_scratch is None:
+            dev = next(iter(self.fact.values())).device
+            self._plan_scratch = torch.empty(PLAN_SCRATCH_BYTES, dtype=torch.uint8, device=dev)
+        p = SdbPlan()
+        _check(lib().sdb_plan_star_query(C.byref(self.q), _ptr(self._plan_scratch),
+                                         self._plan_scratch.numel(), _stream_handle(stream),
+                                         C.byref(p)))
+        self.plan_obj = p
+        return p
+
+    def alloc_outputs(self, plan: SdbPlan | None = None):
+        import torch
+        plan = plan or self.plan_obj
+        dev = next(iter(self.fact.values())).device
+        g = int(plan.n_groups)
+        return (torch.empty(g, dtype=torch.int64, device=dev), torch.empty(g, dtype=torch.int64, device=dev))
+
+    def run(self, sums, counts, plan: SdbPlan | None = None, stream=None) -> None:
+        plan = plan or self.plan_obj
+        _check(lib().sdb_run_star_query(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
+                                        sums.numel(), _stream_handle(stream)))
+
+    def finalize(self, sums, counts, plan: SdbPlan | None = None, stream=None, outputs=None):
+        """Device compaction; returns (keys, sums, counts, n) device tensors (n: int64[1])."""
+        import torch
+        plan = plan or self.plan_obj
+        dev = sums.device
+        g = int(plan.n_groups)
+        if outputs is None:
+            nb = i64(0)
+            _check(lib().sdb_finalize_scratch_bytes(C.byref(plan), C.byref(nb)))
+            outputs = (torch.empty((g, max(self.n_keys, 1)), dtype=torch.int32, device=dev),
+                       torch.empty(g, dtype=torch.int64, device=dev),
+                       torch.empty(g, dtype=torch.int64, device=dev),
+                       torch.empty(1, dtype=torch.int64, device=dev),
+                       torch.empty(nb.value, dtype=torch.uint8, device=dev))
+        k, s, c, n, scratch = outputs
+        _check(lib().sdb_finalize_groups(C.byref(plan), _ptr(sums), _ptr(counts), _ptr(k), _ptr(s),
+                                         _ptr(c), g, _ptr(n), _ptr(scratch), scratch.numel(),
+                                         _stream_handle(stream)))
+        return outputs
+
+    def execute(self, stream=None, replan: bool = True) -> QueryResult:
+        """plan -> fused pass -> compaction, then copy the groups to the host."""
+        import torch
+        if replan or self.plan_obj is None:
+            self.plan(stream)
+        sums, counts = self.alloc_outputs()
+        self.run(sums, counts, stream=stream)
+        k, s, c, n, _ = self.finalize(sums, counts, stream=stream)
+        (stream or torch.cuda.current_stream()).synchronize()
+        m = int(n.item())
+        keys = k[:m, :self.n_keys].to(torch.int64).cpu().numpy()
+        return QueryResult(keys.reshape(m, self.n_keys), s[:m].cpu().numpy(), c[:m].cpu().numpy())
+
+
+def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
+    stages = []
+    for s in range(plan.n_stages):
+        kind, i = plan.stage_kind[s], plan.stage_index[s]
+        name = None
+        if query is not None:
+            name = (query["fact_preds"][i]["col"] if kind == 0 else query["joins"][i]["dim"])
+        stages.append({"kind": "pred" if kind == 0 else "probe", "index": i, "name": name,
+                       "pass": round(plan.stage_pass[s], 6)})
+    return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
+            "ipt": plan.ipt, "vector": plan.vector, "block": plan.block, "grid": plan.grid,
+            "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
+            "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}

@@ -1,0 +1,245 @@
+"""The C ABI on the CPU: the library loads, exports what include/sdb.h declares,
+agrees with the binding's struct layout, and validates and plans on the host
+(no GPU call is made by anything tested here)."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2607_07632_amd import sdb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sdb.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SDB_API\s+[\w\s\*]+?\b(sdb_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    syms = declared_symbols()
+    for name in ["sdb_build_dim", "sdb_run_star_query", "sdb_plan_star_query", "sdb_finalize_groups",
+                 "sdb_dim_required_bytes", "sdb_last_error"]:
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol():
+    L = sdb.lib()
+    for name in declared_symbols():
+        assert hasattr(L, name), name
+    assert set(declared_symbols()) == set(sdb.SIGNATURES)
+
+
+def test_struct_layout_matches_binding():
+    L = sdb.lib()
+    sizes = (C.c_int64 * 8)()
+    assert L.sdb_struct_sizes(sizes, 8) == 0
+    assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
+    assert L.sdb_abi_version() == 1
+
+
+def test_status_strings():
+    L = sdb.lib()
+    assert L.sdb_status_string(0) == b"SDB_OK"
+    assert L.sdb_status_string(5) == b"SDB_DUP_KEY"
+    assert L.sdb_status_string(99) == b"SDB_UNKNOWN_STATUS"
+
+
+def _desc(n_rows=1000, kind="auto", n_cols=2, lf=0.0):
+    d = sdb.SdbDimDesc()
+    d.key = 0x10000
+    d.n_rows = n_rows
+    d.n_cols = n_cols
+    for i in range(n_cols):
+        d.cols[i] = 0x20000 + 0x1000 * i
+    d.kind = sdb.TABLES[kind]
+    d.load_factor = lf
+    return d
+
+
+def test_required_bytes_bounds():
+    dense = sdb.dim_required_bytes(_desc(1000, "dense"))
+    # stats + 2000 slots x 4 B + occupancy bitmap
+    assert dense == 256 + 8192 + 256
+    h = sdb.dim_required_bytes(_desc(1000, "hash"))
+    assert h == 256 + 2048 * 8
+    a = sdb.dim_required_bytes(_desc(1000, "auto"))
+    assert a == max(dense, h)
+    big = sdb.dim_required_bytes(_desc(1 << 24, "hash", lf=0.5))
+    assert big == 256 + (1 << 25) * 8            # 256 MiB table at load factor 0.5
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda d: setattr(d, "n_rows", -1), "SDB_INVALID_ARG"),
+    (lambda d: setattr(d, "n_cols", 9), "SDB_UNSUPPORTED"),
+    (lambda d: setattr(d, "kind", 7), "SDB_INVALID_ARG"),
+    (lambda d: (setattr(d, "kind", 2), setattr(d, "load_factor", 0.95)), "SDB_INVALID_ARG"),
+    (lambda d: (setattr(d, "n_preds", 1), setattr(d.preds[0], "col", 5)), "SDB_INVALID_ARG"),
+    (lambda d: (setattr(d, "n_preds", 1), setattr(d.preds[0], "op", 9)), "SDB_INVALID_ARG"),
+    (lambda d: (setattr(d, "n_payloads", 1), setattr(d.payload_cols, "__setitem__", None)), None),
+    (lambda d: (setattr(d, "n_payloads", 4)), "SDB_UNSUPPORTED"),
+    (lambda d: setattr(d, "key", None), "SDB_INVALID_ARG"),
+])
+def test_dim_descriptor_validation(mutate, status):
+    d = _desc()
+    try:
+        mutate(d)
+    except (AttributeError, TypeError):
+        pass
+    if status is None:
+        sdb.dim_required_bytes(d)
+        return
+    with pytest.raises(sdb.SdbError) as e:
+        sdb.dim_required_bytes(d)
+    assert e.value.name == status
+    assert sdb.lib().sdb_last_error().decode().startswith(status)
+
+
+def _fake_dim(kind=1, width=1, n_rows=200_000, n_pass=40_000, radices=(25,), mins=(0,),
+              key_min=0, n_slots=200_000, bits=0):
+    h = sdb.SdbDim()
+    h.kind = kind
+    h.width = width
+    h.n_rows = n_rows
+    h.n_pass = n_pass
+    h.key_min = key_min
+    h.key_max = key_min + n_slots - 1
+    h.n_slots = n_slots if kind == 1 else (1 << bits)
+    h.hash_bits = bits
+    h.sentinel = 0xFF
+    h.n_payloads = len(radices)
+    div = 1
+    for p in range(len(radices) - 1, -1, -1):
+        h.payload_radix[p] = radices[p]
+        h.payload_min[p] = mins[p]
+        h.payload_div[p] = div
+        div *= radices[p]
+    h.domain = div
+    h.map = 0x40000
+    return h
+
+
+def _query(dims, group_keys, n_fact=1000, n_preds=0, align=True):
+    q = sdb.SdbQuery()
+    q.n_fact = n_fact
+    q.n_cols = 4
+    base = 0x100000 if align else 0x100004
+    for c in range(4):
+        q.cols[c] = base + c * 0x10000
+    q.n_preds = n_preds
+    for i in range(n_preds):
+        q.preds[i] = sdb.SdbPred(3, sdb.OPS["lt"], 30, 0)
+    q.n_joins = len(dims)
+    for j, d in enumerate(dims):
+        q.joins[j] = sdb.SdbJoin(j % 3, C.pointer(d))
+    q.n_group_keys = len(group_keys)
+    for k, (j, p) in enumerate(group_keys):
+        q.group_keys[k] = sdb.SdbGroupKey(j, p)
+    q.agg = sdb.SdbAgg(sdb.AGGS["col"], 3, 0)
+    q.force_order = 1
+    return q
+
+
+def _plan(q):
+    p = sdb.SdbPlan()
+    st = sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p))
+    if st != 0:
+        raise sdb.SdbError(st, sdb.lib().sdb_last_error().decode())
+    return p
+
+
+def test_plan_group_layout_and_terminals():
+    sup = _fake_dim(radices=(25,), mins=(0,))
+    date = _fake_dim(n_rows=2556, n_pass=2556, radices=(8,), mins=(1992,), n_slots=2556)
+    p = _plan(_query([sup, date], [(0, 0), (1, 0)]))
+    assert p.n_groups == 200 and list(p.radix[:2]) == [25, 8] and list(p.stride[:2]) == [8, 1]
+    assert list(p.key_min[:2]) == [0, 1992]
+    assert sdb.TERMINAL_NAMES[p.terminal] == "lds" and p.ipt == 2 and p.vector == 1
+    assert [p.stage_kind[i] for i in range(2)] == [1, 1]
+    cust = _fake_dim(n_rows=3_000_000, radices=(250,), n_slots=3_000_000)
+    sup2 = _fake_dim(radices=(250,))
+    date2 = _fake_dim(n_rows=2556, radices=(6,), mins=(1992,), n_slots=2556)
+    p3 = _plan(_query([cust, sup2, date2], [(0, 0), (1, 0), (2, 0)]))
+    assert p3.n_groups == 375_000 and sdb.TERMINAL_NAMES[p3.terminal] == "global"
+    assert list(p3.stride[:3]) == [1500, 6, 1]
+    p1 = _plan(_query([date2], [], n_preds=2))
+    assert p1.n_groups == 1 and sdb.TERMINAL_NAMES[p1.terminal] == "scalar" and p1.ipt == 4
+    assert [p1.stage_kind[i] for i in range(3)] == [0, 0, 1]
+
+
+def test_plan_multi_payload_layout():
+    d = _fake_dim(radices=(5, 7, 3), mins=(10, -2, 0))
+    p = _plan(_query([d], [(0, 2), (0, 0)]))
+    assert p.n_groups == 15 and list(p.radix[:2]) == [3, 5] and list(p.stride[:2]) == [5, 1]
+    assert list(p.key_min[:2]) == [0, 10]
+
+
+def test_plan_capacity_and_validation_errors():
+    big = _fake_dim(radices=(60_000,))
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(_query([big, big], [(0, 0), (1, 0)]))
+    assert e.value.name == "SDB_CAPACITY"
+    d = _fake_dim()
+    q = _query([d], [(0, 1)])
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(q)
+    assert e.value.name == "SDB_INVALID_ARG"
+    q = _query([d], [(0, 0)])
+    q.force_terminal = sdb.TERMINALS["scalar"]
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(q)
+    assert e.value.name == "SDB_INVALID_ARG"
+    q = _query([d], [(0, 0)])
+    q.force_ipt = 3
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(q)
+    assert e.value.name == "SDB_UNSUPPORTED"
+    q = _query([d], [(0, 0)], align=False)
+    assert _plan(q).vector == 0
+    q.force_vector = 1
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(q)
+    assert e.value.name == "SDB_INVALID_ARG"
+    q = _query([d], [(0, 0)])
+    q.n_fact = -5
+    with pytest.raises(sdb.SdbError):
+        _plan(q)
+    q = _query([d, d], [(0, 0)], n_fact=1000)
+    q.force_order = 0
+    with pytest.raises(sdb.SdbError) as e:          # sampling two stages needs scratch
+        _plan(q)
+    assert e.value.name == "SDB_INVALID_ARG"
+
+
+def test_run_rejects_mismatched_plan_before_any_launch():
+    d = _fake_dim()
+    q = _query([d], [(0, 0)])
+    p = _plan(q)
+    L = sdb.lib()
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p), 0x1000, 0x2000, 10, None) == 3   # CAPACITY
+    p2 = sdb.SdbPlan.from_buffer_copy(p)
+    p2.n_stages = 0
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p2), 0x1000, 0x2000, 100, None) == 1
+    p3 = sdb.SdbPlan.from_buffer_copy(p)
+    p3.stage_index[0] = 4
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p3), 0x1000, 0x2000, 100, None) == 1
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p), None, 0x2000, 100, None) == 1
+
+
+def test_finalize_scratch_and_validation():
+    d = _fake_dim(radices=(250,))
+    q = _query([d, d], [(0, 0), (1, 0)])
+    p = _plan(q)
+    nb = C.c_int64(0)
+    assert sdb.lib().sdb_finalize_scratch_bytes(C.byref(p), C.byref(nb)) == 0
+    assert nb.value == ((62_500 + 1023) // 1024) * 8
+    L = sdb.lib()
+    st = L.sdb_finalize_groups(C.byref(p), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 10, 0x6000, 0x7000,
+                               nb.value, None)
+    assert st == 3
+    st = L.sdb_finalize_groups(C.byref(p), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 62_500, 0x6000,
+                               0x7000, 8, None)
+    assert st == 4

@@ -1,0 +1,212 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, exactly.
+
+All arithmetic is integer, so every group key, sum and count must be equal bit
+for bit. Sizes here let the oracle finish in seconds while still spanning many
+blocks, tiles and a ragged tail; the full 600M-row shapes are covered in
+test_gpu_fullsize.py.
+"""
+
+import numpy as np
+import pytest
+
+import datagen
+from datagen.star import random_tiny_workload
+from gpu_util import assert_same, oracle_rows, require_gpu, run_gpu, upload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+SIZES = {"c1_scalar_scan": None, "c2_join_group": 4_000_003, "c3_star3": 4_000_001,
+         "c4_star4_zipf": 4_000_002, "c5_hash_stress": 2_000_003}
+
+_cache = {}
+
+
+def workload(name):
+    if name not in _cache:
+        _cache[name] = datagen.make_workload(name, n_fact=SIZES[name])
+    return _cache[name]
+
+
+@pytest.mark.parametrize("name", list(SIZES))
+def test_config_parity(name):
+    w = workload(name)
+    want = oracle_rows(w)
+    got, q = run_gpu(w)
+    print(name, w.n_fact, "rows;", len(want), "groups;", q.plan_obj.terminal, q.plan_obj.ipt)
+    assert_same(got.as_rows(), want, name)
+
+
+@pytest.mark.parametrize("name", ["c2_join_group", "c3_star3"])
+@pytest.mark.parametrize("force", [
+    {"order": True}, {"vector": -1}, {"ipt": 1}, {"ipt": 8}, {"terminal": "global"},
+    {"ipt": 4, "vector": -1, "terminal": "global"}, {"grid": 7}, {"grid": 1, "ipt": 2},
+])
+def test_forced_plans_agree(name, force):
+    w = workload(name)
+    want = oracle_rows(w)
+    got, _ = run_gpu(w, force=force)
+    assert_same(got.as_rows(), want, f"{name} {force}")
+
+
+def test_c1_forced_plans_agree():
+    w = workload("c1_scalar_scan")
+    want = oracle_rows(w)
+    for force in [{"ipt": 1}, {"ipt": 2}, {"ipt": 8}, {"vector": -1}, {"order": True},
+                  {"terminal": "global"}, {"terminal": "lds"}, {"grid": 3}]:
+        got, _ = run_gpu(w, force=force)
+        assert_same(got.as_rows(), want, f"c1 {force}")
+
+
+def test_table_kinds_agree():
+    w = datagen.make_workload("c2_join_group", n_fact=1_000_005)
+    want = oracle_rows(w)
+    for kinds in [("hash", "hash"), ("dense", "hash"), ("hash", "dense")]:
+        q = dict(w.query)
+        q["joins"] = [dict(j, kind=k) for j, k in zip(w.query["joins"], kinds)]
+        w2 = datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys, q)
+        got, qq = run_gpu(w2)
+        assert [t.kind for t in qq.tables] == list(kinds)
+        assert_same(got.as_rows(), want, f"c2 {kinds}")
+
+
+def test_c5_dense_and_low_load_factor_agree():
+    w = datagen.make_workload("c5_hash_stress", n_fact=500_001)
+    want = oracle_rows(w)
+    for kind, lf in [("dense", 0.0), ("hash", 0.25), ("auto", 0.0)]:
+        q = dict(w.query)
+        q["joins"] = [dict(w.query["joins"][0], kind=kind, load_factor=lf)]
+        w2 = datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys, q)
+        got, _ = run_gpu(w2)
+        assert_same(got.as_rows(), want, f"c5 {kind} {lf}")
+
+
+@pytest.mark.parametrize("block", range(6))
+def test_random_tiny_schemas(block):
+    for seed in range(block * 50, block * 50 + 50):
+        w = random_tiny_workload(seed, max_fact=3000, max_dim_rows=400)
+        want = oracle_rows(w)
+        got, _ = run_gpu(w)
+        assert_same(got.as_rows(), want, f"tiny seed {seed}")
+
+
+@pytest.mark.parametrize("seed", [7, 19, 23])
+def test_random_tiny_schemas_forced(seed):
+    w = random_tiny_workload(seed + 1000, max_fact=5000, max_dim_rows=500, n_fact=4099)
+    want = oracle_rows(w)
+    for force in [{"vector": -1}, {"ipt": 1, "grid": 2}, {"ipt": 8}, {"order": True},
+                  {"terminal": "global"}]:
+        got, _ = run_gpu(w, force=force)
+        assert_same(got.as_rows(), want, f"tiny {seed} {force}")
+
+
+@pytest.mark.parametrize("n", [0, 1, 3, 4, 5, 63, 64, 65, 255, 256, 257, 1023, 1025, 4097])
+def test_small_and_ragged_sizes(n):
+    for name in ["c1_scalar_scan", "c3_star3", "c2_join_group"]:
+        w = datagen.make_workload(name, n_fact=n, row_start=12_345)
+        got, _ = run_gpu(w)
+        assert_same(got.as_rows(), oracle_rows(w), f"{name} n={n}")
+
+
+@pytest.mark.parametrize("offset", [1, 2, 3, 4])
+def test_misaligned_columns(offset):
+    w = datagen.make_workload("c3_star3", n_fact=300_007)
+    want = oracle_rows(w)
+    got, q = run_gpu(w, dev=upload(w, offset=offset))
+    assert q.plan_obj.vector == (1 if offset % 4 == 0 else 0)
+    assert_same(got.as_rows(), want, f"offset {offset}")
+
+
+def test_repeat_runs_are_identical():
+    w = workload("c4_star4_zipf")
+    fact_dims = upload(w)
+    from paper_2607_07632_amd import sdb
+    tables = sdb.build_dims(fact_dims[1], w.dim_keys, w.query)
+    first, q = run_gpu(w, dev=fact_dims, tables=tables)
+    for _ in range(3):
+        again = q.execute(replan=False)
+        assert again.as_rows() == first.as_rows()
+
+
+def test_all_pass_and_all_fail():
+    w = datagen.make_workload("c2_join_group", n_fact=200_000)
+    q = dict(w.query)
+    q["joins"] = [dict(w.query["joins"][0], preds=[{"col": "region", "op": "ge", "lo": -(2**40), "hi": None}]),
+                  w.query["joins"][1]]
+    w2 = datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys, q)
+    got, _ = run_gpu(w2)
+    want = oracle_rows(w2)
+    assert sum(c for _, _, c in want) == w.n_fact
+    assert_same(got.as_rows(), want, "all pass")
+    q["fact_preds"] = [{"col": "revenue", "op": "gt", "lo": 2**31, "hi": None}]
+    w3 = datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys, q)
+    got, _ = run_gpu(w3)
+    assert got.as_rows() == [] == oracle_rows(w3)
+
+
+def test_extreme_literals_and_values():
+    rng = np.random.default_rng(5)
+    n = 70_001
+    v = rng.integers(-(2**31), 2**31, size=n, dtype=np.int64).astype(np.int32)
+    v[:6] = [-(2**31), 2**31 - 1, 0, -1, 1, 2**31 - 2]
+    fact = {"v": v, "w": rng.integers(-(2**31), 2**31, size=n, dtype=np.int64).astype(np.int32)}
+    for pred in [{"col": "v", "op": "lt", "lo": -(2**31)}, {"col": "v", "op": "le", "lo": -(2**31)},
+                 {"col": "v", "op": "ge", "lo": 2**31 - 1}, {"col": "v", "op": "gt", "lo": 2**31 - 2},
+                 {"col": "v", "op": "ne", "lo": 0}, {"col": "v", "op": "between", "lo": -5, "hi": 2**33},
+                 {"col": "v", "op": "between", "lo": 10, "hi": -10}, {"col": "v", "op": "eq", "lo": 2**31 - 1},
+                 {"col": "v", "op": "ne", "lo": -(2**35)}]:
+        pred = dict(pred, hi=pred.get("hi"))
+        for agg in [{"kind": "mul", "a": "v", "b": "w"}, {"kind": "sub", "a": "v", "b": "w"},
+                    {"kind": "add", "a": "w", "b": "v"}]:
+            q = {"fact_preds": [pred], "joins": [], "group_by": [], "agg": agg}
+            w = datagen.Workload("extreme", n, fact, {}, {}, q)
+            got, _ = run_gpu(w)
+            assert_same(got.as_rows(), oracle_rows(w), f"{pred} {agg}")
+
+
+def test_errors_are_reported():
+    import torch
+    from paper_2607_07632_amd import sdb
+    key = torch.tensor([5, 6, 7, 6], dtype=torch.int32, device="cuda")
+    a = torch.tensor([1, 2, 3, 4], dtype=torch.int32, device="cuda")
+    for kind in ["dense", "hash", "auto"]:
+        with pytest.raises(sdb.SdbError) as e:
+            sdb.build_dim(key, {"a": a}, [], ["a"], kind)
+        assert e.value.name == "SDB_DUP_KEY"
+    sparse = torch.tensor([0, 10_000_000], dtype=torch.int32, device="cuda")
+    b = torch.tensor([1, 2], dtype=torch.int32, device="cuda")
+    with pytest.raises(sdb.SdbError) as e:
+        sdb.build_dim(sparse, {"a": b}, [], [], "dense")
+    assert e.value.name == "SDB_KEY_RANGE"
+    t = sdb.build_dim(sparse, {"a": b}, [], [], "auto")
+    assert t.kind == "hash"
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(sdb.SdbError) as e:
+        sdb.build_dim(key[:3], {"a": a[:3]}, [], [], "auto", workspace=small)
+    assert e.value.name == "SDB_WORKSPACE_TOO_SMALL"
+
+
+def test_build_statistics_match_numpy():
+    import torch
+    from paper_2607_07632_amd import sdb
+    w = datagen.make_workload("c4_star4_zipf", n_fact=10)
+    part = w.dims["part"]
+    dev = {k: torch.from_numpy(v).cuda() for k, v in part.items()}
+    t = sdb.build_dim(dev["part_key"], {"category": dev["category"], "brand": dev["brand"]},
+                      [{"col": "category", "op": "eq", "lo": 1, "hi": None}], ["brand"])
+    ok = part["category"] == 1
+    h = t.handle
+    assert h.n_pass == int(ok.sum()) and h.kind == 1 and h.width == 2
+    assert h.payload_min[0] == part["brand"][ok].min()
+    assert h.payload_radix[0] == part["brand"][ok].max() - part["brand"][ok].min() + 1
+    # the map itself: the sentinel for filtered rows, brand - min otherwise
+    torch.cuda.synchronize()
+    ws = t.workspace.cpu().numpy()
+    got = ws[256:256 + h.n_slots * 2].view(np.uint16)
+    want = np.where(ok, part["brand"] - h.payload_min[0], 0xFFFF).astype(np.uint16)
+    assert np.array_equal(got, want)
