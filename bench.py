@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused star-schema query on one MI355X.
+
+One step is one pass of the whole hot path over the resident fact table:
+build every dimension lookup table, plan (a sampling kernel orders the
+stages), the fused probe-filter-aggregate kernel, and the device compaction of
+the group table (its size read back to the host). Fact columns are generated
+once, uploaded, and stay in HBM; the timed region starts with them resident.
+
+Default workload: c3_star3, 600M fact rows (int32 cust_key, supp_key,
+date_key, revenue), customer 3M / supplier 200k / date 2556 rows, SUM(revenue)
+GROUP BY (customer city, supplier city, year).
+
+Prints one JSON line. `value` = fact rows per second of the whole step.
+`roofline` rates the fused kernel: fact-column bytes (4 bytes x distinct fact
+columns x rows) over its mean duration, timed with HIP events on the stream it
+runs on. `cpu_baseline` times the CPU oracle (numpy, one thread) on the first
+rows of the same workload; the GPU result on those rows is compared with it.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_07632_amd", "csrc", "sdb_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def traffic_from_profile(workload: str):
+    """HBM bytes per fused-kernel launch from a committed counter summary, or None
+    when the summary is missing or was taken from a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"star_fused_{workload}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def upload_fact(cfg_name: str, n: int, device) -> dict:
+    """Generate each fact column into one pinned host buffer and copy it to HBM."""
+    import torch
+    import datagen
+    from datagen.star import CONFIGS
+    cfg = CONFIGS[cfg_name]
+    staging = torch.empty(n, dtype=torch.int32, pin_memory=True)
+    out = {}
+    for col in cfg.fact_cols:
+        t0 = time.perf_counter()
+        datagen.fact_column(cfg_name, col.name, 0, n, out=staging.numpy())
+        d = torch.empty(n, dtype=torch.int32, device=device)
+        d.copy_(staging, non_blocking=True)
+        torch.cuda.synchronize()
+        out[col.name] = d
+        log(f"  fact column {col.name}: {n} rows in {time.perf_counter() - t0:.1f} s")
+    del staging
+    return out
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c3_star3")
+    ap.add_argument("--rows", type=int, default=None, help="fact rows (default: the workload's size)")
+    ap.add_argument("--cpu-rows", type=int, default=12_000_000, help="oracle sample rows")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (scale for HBM byte counters)")
+    ap.add_argument("--force", default="", help="planner overrides, e.g. ipt=4,vector=1,terminal=global")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the path needs no collective, and --gpus {args.gpus} "
+              "is not supported (see the sharding plan in the design notes)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import datagen
+    from datagen.star import CONFIGS
+    from paper_2607_07632_amd import sdb
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        return 1
+    sdb.lib()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.config]
+    n = cfg.n_fact if args.rows is None else int(args.rows)
+    force = {}
+    for kv in filter(None, args.force.split(",")):
+        k, v = kv.split("=")
+        force[k] = v if k == "terminal" else (v == "1" if k == "order" else int(v))
+
+    log(f"[bench] {args.config}: {n} fact rows; generating and uploading")
+    t0 = time.perf_counter()
+    fact = upload_fact(args.config, n, dev)
+    wdims = datagen.make_workload(args.config, n_fact=0)
+    dims = {d: {c: torch.from_numpy(a).to(dev) for c, a in t.items()} for d, t in wdims.dims.items()}
+    query = wdims.query
+    log(f"[bench] data resident after {time.perf_counter() - t0:.1f} s")
+
+    # workspaces reused by every step (the library allocates nothing itself)
+    tables = sdb.build_dims(dims, wdims.dim_keys, query)
+    workspaces = [t.workspace for t in tables]
+    q0 = sdb.StarQuery(fact, tables, query, force)
+    plan0 = q0.plan()
+    sums, counts = q0.alloc_outputs(plan0)
+    fin_out = q0.finalize(sums, counts, plan=plan0)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def build_tables():
+        out = []
+        for jd, ws in zip(query["joins"], workspaces):
+            t = dims[jd["dim"]]
+            cols = {}
+            for c in [p["col"] for p in jd.get("preds", [])] + list(jd.get("payloads", [])):
+                cols.setdefault(c, t[c])
+            out.append(sdb.build_dim(t[wdims.dim_keys[jd["dim"]]], cols, jd.get("preds", []),
+                                     list(jd.get("payloads", [])), jd.get("kind", "auto"),
+                                     jd.get("load_factor", 0.0), workspace=ws))
+        return out
+
+    def step(ev_pair=None):
+        tabs = build_tables()
+        q = sdb.StarQuery(fact, tabs, query, force)
+        plan = q.plan()
+        if ev_pair is not None:
+            ev_pair[0].record(stream)
+        q.run(sums, counts, plan=plan)
+        if ev_pair is not None:
+            ev_pair[1].record(stream)
+        k, s, c, nout, _ = q.finalize(sums, counts, plan=plan, outputs=fin_out)
+        return int(nout.item()), plan
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    n_groups_out = 0
+    plan = plan0
+    for i in range(args.steps):
+        n_groups_out, plan = step(events[i])
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    kernel_ms = [a.elapsed_time(b) for a, b in events]
+    kernel_ms_mean = float(np.mean(kernel_ms))
+
+    ms_per_step = 1000.0 * t_total / max(args.steps, 1)
+    rows_per_s = n / (t_total / max(args.steps, 1))
+    fact_cols = int(q0.q.n_cols)
+    b_dense_per_row = 4 * fact_cols
+    achieved = n * b_dense_per_row / (kernel_ms_mean * 1e-3) / 1e9
+    traffic = traffic_from_profile(args.config)
+    plan_info = sdb.plan_summary(plan, query)
+    log(f"[bench] plan {json.dumps(plan_info)}")
+    log(f"[bench] fused kernel mean {kernel_ms_mean:.4f} ms (min {min(kernel_ms):.4f}, "
+        f"max {max(kernel_ms):.4f}); step {ms_per_step:.4f} ms; groups {n_groups_out}")
+
+    result = {
+        "metric": "fact rows/sec and effective GB/s per star query; % of HBM peak (1 GPU)",
+        "value": rows_per_s,
+        "unit": "fact rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.config}: {cfg.describe}",
+            "fact_rows": n,
+            "fact_columns": fact_cols,
+            "dimensions": {d: int(next(iter(t.values())).numel()) for d, t in dims.items()},
+            "n_groups_domain": int(plan.n_groups),
+            "n_groups_nonempty": n_groups_out,
+            "plan": plan_info,
+            "step": "build dims + sampled plan + fused kernel + device compaction",
+        },
+        "effective_GBps_step": rows_per_s * b_dense_per_row / 1e9,
+        "fused_kernel_ms": kernel_ms_mean,
+        "fused_kernel_rows_per_s": n / (kernel_ms_mean * 1e-3),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "bytes_basis": f"{b_dense_per_row} B/row fact-column bytes x {n} rows per launch",
+        },
+        "cpu_baseline": None,
+    }
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 3 x 1 GiB device-to-device copies done")
+
+    if not args.no_cpu:
+        import oracle
+        m = min(args.cpu_rows, n)
+        sample = {k: v[:m].cpu().numpy() for k, v in fact.items()}
+        t0 = time.perf_counter()
+        ref = oracle.star_query(sample, wdims.dims, wdims.dim_keys, query)
+        t_oracle = time.perf_counter() - t0
+        # GPU on the same rows (column views), compared bit for bit
+        qs = sdb.StarQuery({k: v[:m] for k, v in fact.items()}, build_tables(), query, force)
+        got = qs.execute()
+        parity = got.as_rows() == ref.as_rows()
+        result["cpu_baseline"] = {
+            "value": m / t_oracle,
+            "unit": "fact rows/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": f"first {m} of {n} fact rows of {args.config}, full dimension tables; "
+                      f"numpy oracle, one thread, {t_oracle:.1f} s",
+        }
+        result["parity_on_cpu_sample"] = parity
+        log(f"[bench] oracle {m} rows in {t_oracle:.1f} s; GPU result on the sample "
+            f"{'equals' if parity else 'DIFFERS FROM'} the oracle")
+
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -34,7 +34,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 1
+#define SDB_ABI_VERSION 2
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -113,7 +113,9 @@ typedef struct sdb_dim_desc {
  * A passing row's code is sum_p (payload_p - payload_min[p]) * payload_div[p]
  * with payload_div of the last payload 1; `domain` codes exist.
  *  DENSE: map[key - key_min] is the code (width bytes), or `sentinel` (all
- *         ones of the width) for a filtered row or a key no row holds.
+ *         ones of the width) for a filtered row or a key no row holds; bit
+ *         (key - key_min) of the bitmap `bits` (32-bit words) is set iff a
+ *         passing row holds that key.
  *  HASH:  n_slots = 2^hash_bits 8-byte slots {low 32 bits: key, high 32
  *         bits: code + 1, or 0xFFFFFFFF for a filtered row}; a slot with high
  *         half 0 is empty. Slot of key k starts at (k * 0x9E3779B1 mod 2^32)
@@ -135,6 +137,7 @@ typedef struct sdb_dim {
     uint64_t payload_div[SDB_MAX_PAYLOADS];
     void* map;                    /* device, inside the workspace */
     void* stats;                  /* device, inside the workspace */
+    void* bits;                   /* DENSE: device pass bitmap inside the workspace; HASH: NULL */
 } sdb_dim;
 
 typedef struct sdb_join {
@@ -158,11 +161,13 @@ typedef struct sdb_agg {
  * group keys, the terminal consumes the survivors; Section 4.2).
  * The force_* fields override the planner (0 = automatic):
  *  force_terminal  SDB_TERMINAL_*
- *  force_ipt       items per lane per loop iteration (1..8)
+ *  force_ipt       items per lane per loop iteration (1, 2 or 4)
  *  force_vector    1: 4-row items with 128-bit loads (columns must be 16-byte
  *                  aligned); -1: 1-row items
  *  force_order     1: keep query order (predicates, then joins), no sampling
- *  grid_blocks     blocks of the fused kernel */
+ *  grid_blocks     blocks of the fused kernel
+ *  force_lds       -1: every probe uses the device table (no LDS staging)
+ *  force_xcd       -1: no per-XCD group-table copies; 1: use them */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -179,28 +184,47 @@ typedef struct sdb_query {
     int32_t force_vector;
     int32_t force_order;
     int32_t grid_blocks;
+    int32_t force_lds;
+    int32_t force_xcd;
 } sdb_query;
+
+/* Where a probe looks its table up (sdb_plan.stage_lds):
+ *  GLOBAL  the map or hash table in device memory, one gather per live row;
+ *  MAP     the whole dense map copied into each block's LDS;
+ *  BITS    the dense table's pass bitmap copied into LDS; the group-key code,
+ *          if any, is gathered from the device map for the rows that survive
+ *          every stage (stage_defer >= 0) or right after the bit test. */
+enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2 };
 
 /* The one-pass plan. Stages run in the listed order; each is a fact
  * predicate (kind 0, index into preds[]) or a join probe (kind 1, index into
  * joins[]). Group id = sum_k (key_k - key_min[k]) * stride[k] with the last
- * key's stride 1, so ascending group ids are ascending key tuples. */
+ * key's stride 1, so ascending group ids are ascending key tuples.
+ * With xcd_copies > 0 the global terminal accumulates into that many private
+ * copies of the group table (one per XCD, in the run scratch) that a second
+ * kernel adds into the outputs. */
 typedef struct sdb_plan {
     int32_t n_stages;
     int32_t stage_kind[SDB_MAX_STAGES];
     int32_t stage_index[SDB_MAX_STAGES];
     double stage_pass[SDB_MAX_STAGES];    /* pass fraction on the sample, or the estimate used */
+    int32_t stage_lds[SDB_MAX_STAGES];    /* SDB_LDS_* */
+    int32_t stage_defer[SDB_MAX_STAGES];  /* deferred-gather slot (0 or 1), or -1 */
     int64_t sampled_rows;                 /* 0 when no sample was taken */
+    double est_cost;                      /* cost model value of the chosen order */
     int32_t terminal;
     int32_t ipt;
     int32_t vector;                       /* 1: 4-row items with 128-bit loads */
     int32_t block;
     int32_t grid;                         /* 0: chosen at launch */
+    int32_t xcd_copies;
+    int32_t lds_bytes;                    /* dynamic LDS per block */
     int32_t n_group_keys;
     int32_t key_min[SDB_MAX_GROUP_KEYS];
     uint32_t radix[SDB_MAX_GROUP_KEYS];
     uint64_t stride[SDB_MAX_GROUP_KEYS];
     uint64_t n_groups;                    /* product of radices; 1 without GROUP BY */
+    int64_t run_scratch_bytes;            /* device scratch sdb_run_star_query needs */
 } sdb_plan;
 
 /* ---- errors and ABI ---------------------------------------------------- */
@@ -224,8 +248,8 @@ SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n);
 
 /* Host only. Workspace bytes sdb_build_dim needs for `desc`: 256 bytes of
  * statistics, then the lookup table sized by an upper bound (a DENSE map of
- * max(2 * n_rows, 1024) 4-byte slots plus its occupancy bitmap, and/or a HASH
- * table of next_pow2(n_rows / load_factor) 8-byte slots). */
+ * max(2 * n_rows, 1024) 4-byte slots plus its occupancy and pass bitmaps,
+ * and/or a HASH table of next_pow2(n_rows / load_factor) 8-byte slots). */
 SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* bytes);
 
 /* Builds the lookup table for `desc` into `workspace` (device, 256-byte
@@ -259,15 +283,19 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
 /* ---- the fused pass ----------------------------------------------------- */
 
 /* Runs `q` with `plan` (from sdb_plan_star_query for this query and these
- * tables) as one fused probe-filter-aggregate kernel (Sections 3.2 and 4.2)
- * after zeroing the outputs, all queued on `stream` (asynchronous).
+ * tables) as one fused probe-filter-aggregate kernel (Sections 3.2 and 4.2),
+ * all queued on `stream` (asynchronous). The outputs are zeroed first (or,
+ * with per-XCD copies, the copies are zeroed and then added into them).
  * sums/counts: device int64[plan->n_groups], indexed by group id;
  * n_groups_capacity >= plan->n_groups. Without GROUP BY, sums[0] and
- * counts[0] hold the total and the live row count. Errors: INVALID_ARG,
- * CAPACITY, HIP_ERROR (launch failures only). */
+ * counts[0] hold the total and the live row count. scratch: device,
+ * 256-byte aligned, >= plan->run_scratch_bytes (may be NULL when that is 0).
+ * Errors: INVALID_ARG, CAPACITY, WORKSPACE_TOO_SMALL, HIP_ERROR (launch
+ * failures only). */
 SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
                                       int64_t* sums, int64_t* counts,
-                                      int64_t n_groups_capacity, void* stream);
+                                      int64_t n_groups_capacity, void* scratch,
+                                      int64_t scratch_bytes, void* stream);
 
 /* ---- finalize ----------------------------------------------------------- */
 

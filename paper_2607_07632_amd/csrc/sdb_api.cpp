@@ -122,8 +122,9 @@ uint64_t dense_slot_limit(int64_t n_rows) {
     return std::max<uint64_t>(2 * (uint64_t)n_rows, (uint64_t)kDenseSlack);
 }
 
+// map, occupancy bitmap, pass bitmap (each region 256-byte aligned)
 uint64_t dense_bytes(uint64_t slots, int width) {
-    return align_up(slots * (uint64_t)width, 256) + align_up((slots + 31) / 32 * 4, 256);
+    return align_up(slots * (uint64_t)width, 256) + 2 * align_up((slots + 31) / 32 * 4, 256);
 }
 
 double effective_lf(const sdb_dim_desc* d) {
@@ -241,8 +242,8 @@ sdb_status check_query(const sdb_query* q) {
         return fail(SDB_INVALID_ARG, "aggregate operand b = %d", q->agg.b);
     if (q->force_terminal < SDB_TERMINAL_AUTO || q->force_terminal > SDB_TERMINAL_GLOBAL)
         return fail(SDB_INVALID_ARG, "bad force_terminal %d", q->force_terminal);
-    if (q->force_ipt != 0 && q->force_ipt != 1 && q->force_ipt != 2 && q->force_ipt != 4 && q->force_ipt != 8)
-        return fail(SDB_UNSUPPORTED, "force_ipt %d is not 0, 1, 2, 4 or 8", q->force_ipt);
+    if (q->force_ipt != 0 && q->force_ipt != 1 && q->force_ipt != 2 && q->force_ipt != 4)
+        return fail(SDB_UNSUPPORTED, "force_ipt %d is not 0, 1, 2 or 4", q->force_ipt);
     if (q->force_vector < -1 || q->force_vector > 1) return fail(SDB_INVALID_ARG, "bad force_vector %d", q->force_vector);
     if (q->grid_blocks < 0) return fail(SDB_INVALID_ARG, "negative grid_blocks");
     return SDB_OK;
@@ -268,10 +269,13 @@ sdb_status group_layout(const sdb_query* q, sdb_plan* plan) {
     return SDB_OK;
 }
 
-// The stage of a fact predicate or join probe in FusedParams form.
-StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int index) {
+// The stage of a fact predicate or join probe in FusedParams form, with the
+// LDS placement and deferred-gather slot the plan chose for position `pos`
+// (pos < 0: no placement, used by the sampling kernel).
+StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int index, int pos) {
     StageDev S;
     std::memset(&S, 0, sizeof S);
+    S.defer = -1;
     if (kind == 0) {
         S.kind = ST_PRED;
         S.col = q->preds[index].col;
@@ -282,6 +286,7 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
     const sdb_dim* d = jn.dim;
     S.col = jn.fact_key_col;
     S.map = d->map;
+    S.bits = d->bits;
     S.sentinel = d->sentinel;
     if (d->kind == SDB_TABLE_DENSE) {
         S.kind = ST_DENSE;
@@ -307,6 +312,10 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
             S.gk_radix[n] = top ? 0u : d->payload_radix[p];
             S.gk_stride[n] = (uint32_t)plan->stride[k];
         }
+        if (pos >= 0) {
+            S.lds_mode = plan->stage_lds[pos];
+            S.defer = plan->stage_defer[pos];
+        }
     }
     return S;
 }
@@ -317,19 +326,146 @@ uint64_t stage_table_bytes(const sdb_query* q, int kind, int index) {
     return d->n_slots * (uint64_t)d->width;
 }
 
+// Bytes a dense table occupies in LDS as its whole map or as its pass bitmap.
+uint64_t lds_map_bytes(const sdb_dim* d) { return align_up(d->n_slots * (uint64_t)d->width, 16); }
+uint64_t lds_bits_bytes(const sdb_dim* d) { return align_up((d->n_slots + 31) / 32 * 4, 16); }
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-FusedParams fused_params(const sdb_query* q, const sdb_plan* plan) {
+// Per-row cost of a stage's lookup relative to streaming one int32 column
+// (measured on MI355X: a device-memory gather costs about 3 column streams
+// when the table stays in L2, about 6 when it is several MB, and a probe into
+// a table larger than the MALL is latency bound).
+double probe_cost(const sdb_query* q, int kind, int index, int lds_mode) {
+    if (kind == 0) return 0.05;
+    if (lds_mode != LDS_GLOBAL) return 0.3;
+    const sdb_dim* d = q->joins[index].dim;
+    const uint64_t bytes = d->n_slots * (uint64_t)d->width;
+    if (d->kind == SDB_TABLE_HASH) return bytes > (64ull << 20) ? 60.0 : 10.0;
+    return bytes > (2ull << 20) ? 6.0 : 3.0;
+}
+
+// Fraction of 128-byte lines (32 int32 rows) holding at least one live row.
+double line_fraction(double f) { return 1.0 - std::pow(1.0 - std::min(std::max(f, 0.0), 1.0), 32.0); }
+
+// Modeled cost of running the stages in `order`: column streaming at line
+// granularity plus lookups for the rows that reach each stage, then the
+// aggregate columns and deferred gathers for the survivors.
+double order_cost(const sdb_query* q, const sdb_plan* plan, const int* order, int n) {
+    double f = 1.0, cost = 0.0;
+    for (int i = 0; i < n; ++i) {
+        const int s = order[i];
+        cost += line_fraction(f) + f * probe_cost(q, plan->stage_kind[s], plan->stage_index[s], plan->stage_lds[s]);
+        f *= plan->stage_pass[s];
+    }
+    const int agg_cols = q->agg.kind == SDB_AGG_COL ? 1 : 2;
+    cost += agg_cols * line_fraction(f);
+    for (int s = 0; s < n; ++s)
+        if (plan->stage_lds[s] == LDS_BITS && plan->stage_kind[s] == 1) {
+            const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
+            bool gathers = false;
+            for (int k = 0; k < q->n_group_keys; ++k) gathers |= q->group_keys[k].join == plan->stage_index[s];
+            if (gathers) cost += f * (d->n_slots * (uint64_t)d->width > (2ull << 20) ? 6.0 : 3.0);
+        }
+    return cost;
+}
+
+// Cheapest order under order_cost: exhaustive up to 7 stages, else greedy by
+// the rank (1 - pass) / cost of each stage taken alone.
+void choose_order(const sdb_query* q, sdb_plan* plan) {
+    const int n = plan->n_stages;
+    std::vector<int> order(n), best;
+    for (int i = 0; i < n; ++i) order[i] = i;
+    double best_cost = 0.0;
+    if (n <= 7) {
+        best_cost = order_cost(q, plan, order.data(), n);
+        best = order;
+        while (std::next_permutation(order.begin(), order.end())) {
+            const double c = order_cost(q, plan, order.data(), n);
+            if (c < best_cost - 1e-12) {
+                best_cost = c;
+                best = order;
+            }
+        }
+    } else {
+        std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+            const double cx = 1.0 + probe_cost(q, plan->stage_kind[x], plan->stage_index[x], plan->stage_lds[x]);
+            const double cy = 1.0 + probe_cost(q, plan->stage_kind[y], plan->stage_index[y], plan->stage_lds[y]);
+            return (1.0 - plan->stage_pass[x]) / cx > (1.0 - plan->stage_pass[y]) / cy;
+        });
+        best = order;
+        best_cost = order_cost(q, plan, best.data(), n);
+    }
+    const sdb_plan tmp = *plan;
+    for (int i = 0; i < n; ++i) {
+        plan->stage_kind[i] = tmp.stage_kind[best[i]];
+        plan->stage_index[i] = tmp.stage_index[best[i]];
+        plan->stage_pass[i] = tmp.stage_pass[best[i]];
+        plan->stage_lds[i] = tmp.stage_lds[best[i]];
+    }
+    plan->est_cost = best_cost;
+}
+
+// LDS placement: dense tables, smallest first, as the whole map when it fits
+// the remaining budget, else as the pass bitmap, else left in device memory.
+void place_lds(const sdb_query* q, sdb_plan* plan, uint64_t budget) {
+    std::vector<int> cand;
+    for (int s = 0; s < plan->n_stages; ++s) {
+        plan->stage_lds[s] = LDS_GLOBAL;
+        if (plan->stage_kind[s] == 1 && q->joins[plan->stage_index[s]].dim->kind == SDB_TABLE_DENSE &&
+            q->joins[plan->stage_index[s]].dim->n_slots > 0)
+            cand.push_back(s);
+    }
+    std::stable_sort(cand.begin(), cand.end(), [&](int x, int y) {
+        return lds_bits_bytes(q->joins[plan->stage_index[x]].dim) < lds_bits_bytes(q->joins[plan->stage_index[y]].dim);
+    });
+    uint64_t left = budget;
+    for (int s : cand) {
+        const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
+        if (lds_map_bytes(d) <= left) {
+            plan->stage_lds[s] = LDS_MAP;
+            left -= lds_map_bytes(d);
+        } else if (d->bits && lds_bits_bytes(d) <= left) {
+            plan->stage_lds[s] = LDS_BITS;
+            left -= lds_bits_bytes(d);
+        }
+    }
+}
+
+// Dynamic LDS layout of the fused kernel: the LDS group table, then each
+// staged table at a 16-byte aligned offset. Returns the total bytes.
+uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
+    uint64_t off = plan->terminal == TERM_LDS ? plan->n_groups * 16 : 0;
+    if (p) p->term_lds_bytes = (uint32_t)off;
+    for (int s = 0; s < plan->n_stages; ++s) {
+        if (plan->stage_lds[s] == LDS_GLOBAL) continue;
+        const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
+        const uint64_t bytes = plan->stage_lds[s] == LDS_MAP ? lds_map_bytes(d) : lds_bits_bytes(d);
+        if (p) {
+            p->st[s].lds_off = (uint32_t)off;
+            p->st[s].lds_bytes = (uint32_t)bytes;
+        }
+        off += bytes;
+    }
+    return (uint32_t)off;
+}
+
+FusedParams fused_params(const sdb_query* q, const sdb_plan* plan, bool placed) {
     FusedParams p;
     std::memset(&p, 0, sizeof p);
     for (int c = 0; c < q->n_cols; ++c) p.cols[c] = q->cols[c];
     p.n = q->n_fact;
     p.nstages = plan->n_stages;
-    for (int s = 0; s < plan->n_stages; ++s) p.st[s] = make_stage(q, plan, plan->stage_kind[s], plan->stage_index[s]);
+    p.defer_stage = -1;
+    for (int s = 0; s < plan->n_stages; ++s) {
+        p.st[s] = make_stage(q, plan, plan->stage_kind[s], plan->stage_index[s], placed ? s : -1);
+        if (placed && p.st[s].defer == 0) p.defer_stage = s;
+    }
     p.agg_kind = q->agg.kind;
     p.agg_a = q->agg.a;
     p.agg_b = q->agg.kind == SDB_AGG_COL ? q->agg.a : q->agg.b;
     p.n_groups = (uint32_t)plan->n_groups;
+    if (placed) lds_layout(q, plan, &p);
     return p;
 }
 
@@ -345,12 +481,12 @@ bool columns_aligned(const sdb_query* q, const sdb_plan* plan) {
     return true;
 }
 
-int default_ipt(int terminal) { return terminal == TERM_SCALAR ? 4 : 2; }
+constexpr int kDefaultIpt = 4;
 
 sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) {
     const int64_t rows_per_item = plan->vector ? 4 : 1;
     const int64_t n_items = q->n_fact / rows_per_item;
-    const int64_t tile = (int64_t)kBlock * plan->ipt;
+    const int64_t tile = (int64_t)plan->block * plan->ipt;
     int64_t tiles = (n_items + tile - 1) / tile;
     if (tiles < 1) tiles = 1;
     if (q->grid_blocks > 0) {
@@ -360,8 +496,7 @@ sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) 
     DeviceInfo di;
     sdb_status st = device_info(&di);
     if (st != SDB_OK) return st;
-    const size_t lds = plan->terminal == TERM_LDS ? (size_t)plan->n_groups * 16 : 0;
-    int per_cu = fused_blocks_per_cu(plan->vector, plan->ipt, plan->terminal, lds);
+    int per_cu = fused_blocks_per_cu(plan->vector, plan->ipt, plan->terminal, plan->block, (size_t)plan->lds_bytes);
     if (per_cu <= 0) return fail(SDB_HIP_ERROR, "occupancy query failed for the fused kernel");
     const int64_t full = (int64_t)di.cus * per_cu;
     *grid_out = (int)std::min<int64_t>(tiles, full);
@@ -479,14 +614,18 @@ SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace, int6
         out->sentinel = sentinel;
         out->n_slots = range;
         const uint64_t map_bytes = align_up(range * width, 256);
+        const uint64_t bits_bytes = align_up((range + 31) / 32 * 4, 256);
         uint32_t* occ = (uint32_t*)(table + map_bytes);
+        uint32_t* pass_bits = (uint32_t*)(table + map_bytes + bits_bytes);
+        out->bits = pass_bits;
         bp.map = table;
         bp.occ = occ;
+        bp.pass_bits = pass_bits;
         bp.width = width;
         bp.nslots = range;
         bp.sentinel = sentinel;
         SDB_HIP(launch_fill_u32((uint32_t*)table, map_bytes / 4, 0xFFFFFFFFu, s), "map fill");
-        SDB_HIP(launch_fill_u32(occ, (range + 31) / 32, 0u, s), "occupancy fill");
+        SDB_HIP(launch_fill_u32(occ, 2 * bits_bytes / 4, 0u, s), "bitmap fill");
         SDB_HIP(launch_dense_scatter(bp, s), "dense scatter launch");
     } else {
         const uint64_t cap = hash_capacity(n, effective_lf(desc));
@@ -534,42 +673,10 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         ++n;
     }
     plan->n_stages = n;
+    for (int s = 0; s < SDB_MAX_STAGES; ++s) plan->stage_defer[s] = -1;
 
     st = group_layout(q, plan);
     if (st != SDB_OK) return st;
-
-    if (!q->force_order && n > 1 && q->n_fact > 0) {
-        if (!scratch) return fail(SDB_INVALID_ARG, "null planner scratch");
-        if (scratch_bytes < SDB_PLAN_SCRATCH_BYTES)
-            return fail(SDB_WORKSPACE_TOO_SMALL, "planner scratch holds %lld bytes, %d needed",
-                        (long long)scratch_bytes, SDB_PLAN_SCRATCH_BYTES);
-        hipStream_t s = (hipStream_t)stream;
-        FusedParams fp = fused_params(q, plan);
-        const int64_t step = (q->n_fact + 65535) / 65536;
-        const int64_t n_sample = (q->n_fact + step - 1) / step;
-        unsigned long long* dcounts = (unsigned long long*)scratch;
-        SDB_HIP(launch_sample(fp, step, n_sample, dcounts, s), "sample launch");
-        unsigned long long hc[kMaxStages];
-        SDB_HIP(hipMemcpyAsync(hc, dcounts, sizeof hc, hipMemcpyDeviceToHost, s), "sample copy");
-        SDB_HIP(hipStreamSynchronize(s), "sample sync");
-        for (int i = 0; i < n; ++i) plan->stage_pass[i] = (double)hc[i] / (double)n_sample;
-        plan->sampled_rows = n_sample;
-
-        std::vector<int> order(n);
-        for (int i = 0; i < n; ++i) order[i] = i;
-        std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-            if (plan->stage_pass[x] != plan->stage_pass[y]) return plan->stage_pass[x] < plan->stage_pass[y];
-            if (plan->stage_kind[x] != plan->stage_kind[y]) return plan->stage_kind[x] < plan->stage_kind[y];
-            return stage_table_bytes(q, plan->stage_kind[x], plan->stage_index[x]) <
-                   stage_table_bytes(q, plan->stage_kind[y], plan->stage_index[y]);
-        });
-        sdb_plan tmp = *plan;
-        for (int i = 0; i < n; ++i) {
-            plan->stage_kind[i] = tmp.stage_kind[order[i]];
-            plan->stage_index[i] = tmp.stage_index[order[i]];
-            plan->stage_pass[i] = tmp.stage_pass[order[i]];
-        }
-    }
 
     // terminal
     int term;
@@ -583,23 +690,76 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         return fail(SDB_CAPACITY, "LDS terminal holds at most %d groups, plan has %llu", kLdsGroupLimit,
                     (unsigned long long)plan->n_groups);
     plan->terminal = term;
-    plan->ipt = q->force_ipt ? q->force_ipt : default_ipt(term);
+
+    // pass fraction of every stage on a strided sample of the fact rows
+    if (!q->force_order && n > 1 && q->n_fact > 0) {
+        if (!scratch) return fail(SDB_INVALID_ARG, "null planner scratch");
+        if (scratch_bytes < SDB_PLAN_SCRATCH_BYTES)
+            return fail(SDB_WORKSPACE_TOO_SMALL, "planner scratch holds %lld bytes, %d needed",
+                        (long long)scratch_bytes, SDB_PLAN_SCRATCH_BYTES);
+        hipStream_t s = (hipStream_t)stream;
+        FusedParams fp = fused_params(q, plan, false);
+        const int64_t step = (q->n_fact + 65535) / 65536;
+        const int64_t n_sample = (q->n_fact + step - 1) / step;
+        unsigned long long* dcounts = (unsigned long long*)scratch;
+        SDB_HIP(launch_sample(fp, step, n_sample, dcounts, s), "sample launch");
+        unsigned long long hc[kMaxStages];
+        SDB_HIP(hipMemcpyAsync(hc, dcounts, sizeof hc, hipMemcpyDeviceToHost, s), "sample copy");
+        SDB_HIP(hipStreamSynchronize(s), "sample sync");
+        for (int i = 0; i < n; ++i) plan->stage_pass[i] = (double)hc[i] / (double)n_sample;
+        plan->sampled_rows = n_sample;
+    }
+
+    // LDS placement of small dense tables, then the cheapest stage order
+    if (q->force_lds != -1) place_lds(q, plan, (uint64_t)kLdsStageBudget);
+    if (!q->force_order && n > 1) choose_order(q, plan);
+    else {
+        int order[SDB_MAX_STAGES];
+        for (int i = 0; i < n; ++i) order[i] = i;
+        plan->est_cost = order_cost(q, plan, order, n);
+    }
+    // the first LDS-bitmap stage that carries group keys gathers its code after all stages
+    for (int s = 0; s < n; ++s) {
+        if (plan->stage_kind[s] != 1 || plan->stage_lds[s] != LDS_BITS) continue;
+        bool gathers = false;
+        for (int k = 0; k < q->n_group_keys; ++k) gathers |= q->group_keys[k].join == plan->stage_index[s];
+        if (gathers) {
+            plan->stage_defer[s] = 0;
+            break;
+        }
+    }
+    plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
+
+    plan->ipt = q->force_ipt ? q->force_ipt : kDefaultIpt;
     const bool aligned = columns_aligned(q, plan);
     if (q->force_vector == 1 && !aligned && q->n_fact > 0)
         return fail(SDB_INVALID_ARG, "vector loads forced but a column is not 16-byte aligned");
     plan->vector = q->force_vector == -1 ? 0 : (aligned ? 1 : 0);
     plan->block = kBlock;
     plan->grid = q->grid_blocks;
+
+    // per-XCD private group tables for the global terminal when enough rows survive
+    double f = 1.0;
+    for (int s = 0; s < n; ++s) f *= plan->stage_pass[s];
+    const double survivors = f * (double)q->n_fact;
+    const uint64_t copy_bytes = (uint64_t)kXcdCopies * plan->n_groups * 16;
+    bool xcd = term == TERM_GLOBAL && survivors >= 2.0 * (double)plan->n_groups && copy_bytes <= (1ull << 30);
+    if (q->force_xcd == 1) xcd = term == TERM_GLOBAL;
+    if (q->force_xcd == -1) xcd = false;
+    plan->xcd_copies = xcd ? kXcdCopies : 0;
+    plan->run_scratch_bytes = xcd ? (int64_t)copy_bytes : 0;
     return ok();
 }
 
 SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
-                                      int64_t* counts, int64_t n_groups_capacity, void* stream) {
+                                      int64_t* counts, int64_t n_groups_capacity, void* scratch,
+                                      int64_t scratch_bytes, void* stream) {
     sdb_status st = check_query(q);
     if (st != SDB_OK) return st;
     if (!plan) return fail(SDB_INVALID_ARG, "null plan");
     if (!sums || !counts) return fail(SDB_INVALID_ARG, "null output");
     if (plan->n_stages != q->n_preds + q->n_joins) return fail(SDB_INVALID_ARG, "plan does not match the query");
+    int n_defer = 0;
     {
         bool seen[SDB_MAX_STAGES] = {false};
         for (int s = 0; s < plan->n_stages; ++s) {
@@ -609,8 +769,22 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
             const int slot = k == 0 ? i : q->n_preds + i;
             if (seen[slot]) return fail(SDB_INVALID_ARG, "plan stage %d repeats a stage", s);
             seen[slot] = true;
+            const int lm = plan->stage_lds[s];
+            if (lm != LDS_GLOBAL) {
+                if (k != 1 || q->joins[i].dim->kind != SDB_TABLE_DENSE)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: LDS placement needs a dense table", s);
+                if (lm != LDS_MAP && lm != LDS_BITS) return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
+                if (lm == LDS_BITS && !q->joins[i].dim->bits)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: table has no bitmap", s);
+            }
+            if (plan->stage_defer[s] != -1) {
+                if (plan->stage_defer[s] != 0 || lm != LDS_BITS)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: bad deferred gather", s);
+                ++n_defer;
+            }
         }
     }
+    if (n_defer > 1) return fail(SDB_INVALID_ARG, "plan defers more than one gather");
     sdb_plan layout;
     std::memset(&layout, 0, sizeof layout);
     st = group_layout(q, &layout);
@@ -628,26 +802,53 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         return fail(SDB_INVALID_ARG, "scalar terminal on a grouped query");
     if (plan->terminal == TERM_LDS && plan->n_groups > (uint64_t)kLdsGroupLimit)
         return fail(SDB_CAPACITY, "LDS terminal holds at most %d groups", kLdsGroupLimit);
-    if (plan->ipt != 1 && plan->ipt != 2 && plan->ipt != 4 && plan->ipt != 8)
+    if (plan->ipt != 1 && plan->ipt != 2 && plan->ipt != 4)
         return fail(SDB_INVALID_ARG, "bad plan ipt %d", plan->ipt);
+    if (plan->block != 64 && plan->block != 128 && plan->block != 256 && plan->block != kMaxBlock)
+        return fail(SDB_INVALID_ARG, "bad plan block %d", plan->block);
     if (plan->vector && q->n_fact > 0 && !columns_aligned(q, plan))
         return fail(SDB_INVALID_ARG, "vector plan but a column is not 16-byte aligned");
+    if (plan->xcd_copies != 0 && (plan->xcd_copies != kXcdCopies || plan->terminal != TERM_GLOBAL))
+        return fail(SDB_INVALID_ARG, "bad plan xcd_copies %d", plan->xcd_copies);
+    const uint64_t need_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
+    if (need_scratch) {
+        if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
+        if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
+        if (scratch_bytes < 0 || (uint64_t)scratch_bytes < need_scratch)
+            return fail(SDB_WORKSPACE_TOO_SMALL, "run scratch holds %lld bytes, %llu needed",
+                        (long long)scratch_bytes, (unsigned long long)need_scratch);
+    }
+
+    FusedParams p = fused_params(q, plan, true);
+    const uint32_t lds_bytes = lds_layout(q, plan, nullptr);
+    if ((int64_t)lds_bytes != (int64_t)plan->lds_bytes)
+        return fail(SDB_INVALID_ARG, "plan LDS size does not match the tables");
+    if (lds_bytes > 160u * 1024u) return fail(SDB_UNSUPPORTED, "plan needs %u bytes of LDS", lds_bytes);
 
     hipStream_t s = (hipStream_t)stream;
-    SDB_HIP(launch_fill_u64((unsigned long long*)sums, plan->n_groups, s), "sums fill");
-    SDB_HIP(launch_fill_u64((unsigned long long*)counts, plan->n_groups, s), "counts fill");
-    if (q->n_fact == 0) return ok();
-
-    FusedParams p = fused_params(q, plan);
+    if (plan->xcd_copies) {
+        SDB_HIP(launch_fill_u64((unsigned long long*)scratch, need_scratch / 8, s), "copy fill");
+    } else {
+        SDB_HIP(launch_zero_pair((unsigned long long*)sums, (unsigned long long*)counts, plan->n_groups, s),
+                "output fill");
+    }
     p.sums = (unsigned long long*)sums;
     p.counts = (unsigned long long*)counts;
-    int grid = plan->grid;
-    if (grid <= 0) {
-        st = choose_grid(q, plan, &grid);
-        if (st != SDB_OK) return st;
+    p.xcd_copies = plan->xcd_copies;
+    p.xtab = plan->xcd_copies ? (unsigned long long*)scratch : nullptr;
+    if (q->n_fact > 0) {
+        int grid = plan->grid;
+        if (grid <= 0) {
+            st = choose_grid(q, plan, &grid);
+            if (st != SDB_OK) return st;
+        }
+        SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, grid, plan->block, lds_bytes, s),
+                "fused kernel launch");
     }
-    const size_t lds = plan->terminal == TERM_LDS ? (size_t)plan->n_groups * 16 : 0;
-    SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, grid, lds, s), "fused kernel launch");
+    if (plan->xcd_copies)
+        SDB_HIP(launch_xcd_merge((const unsigned long long*)scratch, plan->xcd_copies, plan->n_groups,
+                                 (unsigned long long*)sums, (unsigned long long*)counts, s),
+                "copy merge launch");
     return ok();
 }
 

@@ -11,14 +11,18 @@
 namespace sdb {
 
 constexpr int kMaxStages = SDB_MAX_STAGES;
-constexpr int kBlock = 256;              // threads per block of the fused kernel
+constexpr int kBlock = 256;              // default threads per block of the fused kernel
+constexpr int kMaxBlock = 512;           // launch bound of the fused kernel
 constexpr int kLdsGroupLimit = 2048;     // LDS terminal: sums + counts of G <= 2048 groups (32 KB)
+constexpr int kLdsStageBudget = 32768;   // LDS bytes per block for staged dimension tables
+constexpr int kXcdCopies = 8;            // XCDs of an MI355X: private group-table copies
 constexpr int kFinBlock = 256;           // finalize: threads per block
 constexpr int kFinPerThread = 4;         // finalize: groups per thread
 constexpr int kFinGroupsPerBlock = kFinBlock * kFinPerThread;
 constexpr int kDenseSlack = 1024;        // dense limit: key range <= max(2 * n_rows, 1024)
 
 enum StageKind : int32_t { ST_PRED = 0, ST_DENSE = 1, ST_HASH = 2 };
+enum LdsMode : int32_t { LDS_GLOBAL = SDB_LDS_GLOBAL, LDS_MAP = SDB_LDS_MAP, LDS_BITS = SDB_LDS_BITS };
 enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3 };
 
 // A literal comparison lowered to one unsigned range test over int32:
@@ -41,6 +45,11 @@ struct StageDev {
     int32_t hshift;        // ST_HASH: 32 - log2(capacity)
     uint32_t sentinel;     // code meaning "no passing dimension row"
     const void* map;       // ST_DENSE / ST_HASH table
+    const void* bits;      // ST_DENSE: pass bitmap (32-bit words)
+    int32_t lds_mode;      // LdsMode: where the probe looks the key up
+    uint32_t lds_off;      // byte offset of the staged table in dynamic LDS
+    uint32_t lds_bytes;    // staged bytes (a multiple of 16)
+    int32_t defer;         // LDS_BITS with group keys: 0 = gather the code after all stages
     int32_t n_gk;          // group keys decoded from this table's code
     uint32_t gk_div[SDB_MAX_PAYLOADS];     // key code = (code / div) % radix (div 1: skip)
     uint32_t gk_radix[SDB_MAX_PAYLOADS];   // 0: no modulo needed
@@ -55,9 +64,12 @@ struct FusedParams {
     int32_t agg_a;
     int32_t agg_b;
     uint32_t n_groups;
-    int32_t pad_;
+    uint32_t term_lds_bytes;   // LDS group table at the start of dynamic LDS (LDS terminal)
+    int32_t defer_stage;       // stage whose code is gathered after all stages, or -1
+    int32_t xcd_copies;        // > 0: global terminal adds into xtab copy (XCC id mod copies)
     unsigned long long* sums;
     unsigned long long* counts;
+    unsigned long long* xtab;  // interleaved {sum, count} x n_groups x xcd_copies
     StageDev st[kMaxStages];
 };
 
@@ -87,6 +99,7 @@ struct BuildParams {
     DimStats* stats;
     void* map;                 // dense map or hash table
     uint32_t* occ;             // dense occupancy bitmap
+    uint32_t* pass_bits;       // dense pass bitmap
     int32_t width;
     int32_t kmin;
     uint64_t nslots;
@@ -115,6 +128,7 @@ struct FinalizeParams {
 // ---- launchers (sdb_kernels.hip) -----------------------------------------
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s);
+hipError_t launch_zero_pair(unsigned long long* a, unsigned long long* b, uint64_t n, hipStream_t s);
 hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s);
 hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s);
 hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s);
@@ -122,9 +136,11 @@ hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
                          unsigned long long* pass_counts, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if
 // the instance does not exist.
-int fused_blocks_per_cu(int vector, int ipt, int terminal, size_t lds_bytes);
-hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid,
+int fused_blocks_per_cu(int vector, int ipt, int terminal, int block, size_t lds_bytes);
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid, int block,
                         size_t lds_bytes, hipStream_t s);
+hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
+                            unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);
 
 }  // namespace sdb

@@ -124,6 +124,14 @@ __global__ void fill_u64_kernel(unsigned long long* p, uint64_t n) {
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0ull;
 }
 
+__global__ void zero_pair_kernel(unsigned long long* a, unsigned long long* b, uint64_t n) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        a[i] = 0ull;
+        b[i] = 0ull;
+    }
+}
+
 static int fill_grid(uint64_t n) {
     uint64_t g = (n + 255) / 256;
     if (g > 4096) g = 4096;
@@ -140,6 +148,12 @@ hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStr
 hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s) {
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(fill_u64_kernel, dim3(fill_grid(n)), dim3(256), 0, s, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_pair(unsigned long long* a, unsigned long long* b, uint64_t n, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_pair_kernel, dim3(fill_grid(n)), dim3(256), 0, s, a, b, n);
     return hipGetLastError();
 }
 
@@ -167,7 +181,13 @@ __global__ void stats_init_kernel(DimStats* st) {
 }
 
 // Key range over all rows; pass count and payload ranges over passing rows.
+// Each block reduces in registers and LDS and then adds its result with one
+// set of atomics, so the atomics stay few however large the dimension.
 __global__ void __launch_bounds__(256) dim_stats_kernel(BuildParams bp) {
+    constexpr int kWaves = 256 / 64;
+    __shared__ int32_t s_kmin[kWaves], s_kmax[kWaves];
+    __shared__ unsigned long long s_np[kWaves];
+    __shared__ int32_t s_pmin[SDB_MAX_PAYLOADS][kWaves], s_pmax[SDB_MAX_PAYLOADS][kWaves];
     int32_t kmin = INT_MAX, kmax = INT_MIN;
     unsigned long long npass = 0;
     int32_t pmin[SDB_MAX_PAYLOADS], pmax[SDB_MAX_PAYLOADS];
@@ -196,14 +216,36 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildParams bp) {
         pmin[p] = wave_min_i32(pmin[p]);
         pmax[p] = wave_max_i32(pmax[p]);
     }
+    const int wave = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) {
+        s_kmin[wave] = kmin;
+        s_kmax[wave] = kmax;
+        s_np[wave] = npass;
+        for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+            s_pmin[p][wave] = pmin[p];
+            s_pmax[p][wave] = pmax[p];
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kWaves; ++w) {
+            kmin = min(kmin, s_kmin[w]);
+            kmax = max(kmax, s_kmax[w]);
+            npass += s_np[w];
+            for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+                pmin[p] = min(pmin[p], s_pmin[p][w]);
+                pmax[p] = max(pmax[p], s_pmax[p][w]);
+            }
+        }
         DimStats* st = bp.stats;
-        atomicMin(&st->kmin, kmin);
-        atomicMax(&st->kmax, kmax);
-        if (npass) atomicAdd(&st->npass, npass);
-        for (int p = 0; p < bp.n_payloads; ++p) {
-            atomicMin(&st->pmin[p], pmin[p]);
-            atomicMax(&st->pmax[p], pmax[p]);
+        if (kmin != INT_MAX) atomicMin(&st->kmin, kmin);
+        if (kmax != INT_MIN) atomicMax(&st->kmax, kmax);
+        if (npass) {
+            atomicAdd(&st->npass, npass);
+            for (int p = 0; p < bp.n_payloads; ++p) {
+                atomicMin(&st->pmin[p], pmin[p]);
+                atomicMax(&st->pmax[p], pmax[p]);
+            }
         }
     }
 }
@@ -215,24 +257,54 @@ __device__ __forceinline__ uint32_t dim_row_code(const BuildParams& bp, int64_t 
     return c;
 }
 
+constexpr int kScatterRun = 32;   // consecutive dimension rows per thread in the dense scatter
+
+__device__ __forceinline__ void flush_bits(const BuildParams& bp, uint32_t word, uint32_t occ,
+                                           uint32_t pass) {
+    if (!occ) return;
+    const uint32_t old = atomicOr(&bp.occ[word], occ);
+    if (old & occ) atomicOr(&bp.stats->dup, 1u);
+    if (pass) atomicOr(&bp.pass_bits[word], pass);
+}
+
 // Direct-mapped map: one entry per key in [kmin, kmin + nslots); a passing row
 // stores its code, a filtered row (and every key no row holds, from the fill)
-// the all-ones sentinel. An occupancy bit per slot detects duplicate keys.
+// the all-ones sentinel. One occupancy bit per slot detects duplicate keys and
+// one pass bit per slot forms the filter bitmap. A thread walks a run of
+// consecutive rows and merges their bits per 32-bit word before one atomic OR,
+// so dense keys stored in key order cost one atomic per 32 rows.
 __global__ void __launch_bounds__(256) dense_scatter_kernel(BuildParams bp) {
+    const int64_t n_runs = (bp.n + kScatterRun - 1) / kScatterRun;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
-        const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
-        if ((uint64_t)idx >= bp.nslots) {          // cannot happen: kmin/kmax cover all keys
-            atomicOr(&bp.stats->dup, 4u);
-            continue;
+    for (int64_t run = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; run < n_runs; run += stride) {
+        const int64_t r0 = run * kScatterRun;
+        const int64_t r1 = min(r0 + kScatterRun, bp.n);
+        uint32_t cur = 0xFFFFFFFFu, occ = 0u, pass = 0u;
+        for (int64_t i = r0; i < r1; ++i) {
+            const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
+            if ((uint64_t)idx >= bp.nslots) {      // cannot happen: kmin/kmax cover all keys
+                atomicOr(&bp.stats->dup, 4u);
+                continue;
+            }
+            const uint32_t word = idx >> 5, bit = 1u << (idx & 31u);
+            if (word != cur) {
+                flush_bits(bp, cur, occ, pass);
+                cur = word;
+                occ = 0u;
+                pass = 0u;
+            }
+            if (occ & bit) atomicOr(&bp.stats->dup, 1u);
+            occ |= bit;
+            uint32_t c = bp.sentinel;
+            if (dim_row_passes(bp, i)) {
+                c = dim_row_code(bp, i);
+                pass |= bit;
+            }
+            if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx] = (uint8_t)c;
+            else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx] = (uint16_t)c;
+            else static_cast<uint32_t*>(bp.map)[idx] = c;
         }
-        const uint32_t bit = 1u << (idx & 31u);
-        const uint32_t old = atomicOr(&bp.occ[idx >> 5], bit);
-        if (old & bit) atomicOr(&bp.stats->dup, 1u);
-        const uint32_t c = dim_row_passes(bp, i) ? dim_row_code(bp, i) : bp.sentinel;
-        if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx] = (uint8_t)c;
-        else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx] = (uint16_t)c;
-        else static_cast<uint32_t*>(bp.map)[idx] = c;
+        flush_bits(bp, cur, occ, pass);
     }
 }
 
@@ -265,7 +337,7 @@ __global__ void __launch_bounds__(256) hash_insert_kernel(BuildParams bp) {
 
 static int build_grid(int64_t n) {
     int64_t g = (n + 255) / 256;
-    if (g > 8192) g = 8192;
+    if (g > 1024) g = 1024;
     if (g < 1) g = 1;
     return (int)g;
 }
@@ -280,7 +352,8 @@ hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s) {
 
 hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s) {
     if (bp.n == 0) return hipSuccess;
-    hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+    hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid((bp.n + kScatterRun - 1) / kScatterRun)),
+                       dim3(256), 0, s, bp);
     return hipGetLastError();
 }
 
@@ -294,8 +367,10 @@ hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s) {
 // plan sampling: pass count of every stage on its own over a strided sample
 // ---------------------------------------------------------------------------
 
-__global__ void __launch_bounds__(256) sample_kernel(FusedParams p, int64_t step, int64_t n_sample,
+__global__ void __launch_bounds__(256) sample_kernel(FusedParams kernel_args, int64_t step, int64_t n_sample,
                                                      unsigned long long* pass_counts) {
+    (void)kernel_args;
+    const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
     __shared__ unsigned int cnt[kMaxStages];
     if (threadIdx.x < kMaxStages) cnt[threadIdx.x] = 0u;
     __syncthreads();
@@ -334,12 +409,21 @@ hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
 // the fused probe-filter-aggregate pass
 // ---------------------------------------------------------------------------
 
+// Hardware register XCC_ID (register id 20, bits [3:0]): the XCD the wave runs
+// on. Only used to pick a private group-table copy, so a wrong value would
+// cost speed, never correctness (every copy is updated with device-scope
+// atomics and all copies are added up afterwards).
+__device__ __forceinline__ uint32_t xcc_id() {
+    return __builtin_amdgcn_s_getreg((3 << 11) | 20) & 0xFu;
+}
+
 template <int TERM>
 struct TermState {
     unsigned long long sum = 0;
     unsigned long long cnt = 0;
-    unsigned long long* lsum = nullptr;
+    unsigned long long* lsum = nullptr;   // LDS terminal
     unsigned long long* lcnt = nullptr;
+    unsigned long long* xt = nullptr;     // global terminal: this XCD's interleaved copy, or null
 };
 
 template <int TERM>
@@ -352,22 +436,44 @@ __device__ __forceinline__ void accumulate(const FusedParams& p, TermState<TERM>
         atomicAdd(&ts.lsum[g], (unsigned long long)v);
         atomicAdd(&ts.lcnt[g], 1ull);
     } else {
-        atomicAdd(&p.sums[g], (unsigned long long)v);
-        atomicAdd(&p.counts[g], 1ull);
+        if (ts.xt) {   // sum and count of a group share a cache line
+            atomicAdd(&ts.xt[2u * g], (unsigned long long)v);
+            atomicAdd(&ts.xt[2u * g + 1u], 1ull);
+        } else {
+            atomicAdd(&p.sums[g], (unsigned long long)v);
+            atomicAdd(&p.counts[g], 1ull);
+        }
     }
+}
+
+__device__ __forceinline__ uint32_t lds_code(const StageDev& S, const unsigned char* lds, uint32_t idx) {
+    const unsigned char* base = lds + S.lds_off;
+    if (S.width == 1) return base[idx];
+    if (S.width == 2) return reinterpret_cast<const uint16_t*>(base)[idx];
+    return reinterpret_cast<const uint32_t*>(base)[idx];
+}
+
+__device__ __forceinline__ bool lds_bit(const StageDev& S, const unsigned char* lds, uint32_t idx) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(lds + S.lds_off);
+    return (words[idx >> 5] >> (idx & 31u)) & 1u;
 }
 
 // Runs every stage and the terminal for IPT items of W rows each. `live[j]`
 // holds one bit per row of item j. All lanes of the wave must call this
 // together (the early exit is a wave-wide vote).
 template <int W, int IPT, int TERM>
-__device__ __forceinline__ void process_items(const FusedParams& p, const int64_t (&item)[IPT],
-                                              uint32_t (&live)[IPT], TermState<TERM>& ts) {
+__device__ __forceinline__ void process_items(const FusedParams& p, const unsigned char* lds,
+                                              const int64_t (&item)[IPT], uint32_t (&live)[IPT],
+                                              TermState<TERM>& ts) {
     uint32_t gid[IPT][W];
+    uint32_t didx[IPT][W];   // deferred gather: slot index in the deferred stage's map
 #pragma unroll
     for (int j = 0; j < IPT; ++j)
 #pragma unroll
-        for (int r = 0; r < W; ++r) gid[j][r] = 0u;
+        for (int r = 0; r < W; ++r) {
+            gid[j][r] = 0u;
+            didx[j][r] = 0u;
+        }
 
     for (int s = 0; s < p.nstages; ++s) {
         uint32_t any = 0;
@@ -391,16 +497,53 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const int64_
 #pragma unroll
                 for (int r = 0; r < W; ++r)
                     if (!range_pass(S.test, x[j][r])) live[j] &= ~(1u << r);
-        } else if (S.kind == ST_DENSE) {
-            uint32_t c[IPT][W];
+        } else if (S.kind == ST_DENSE && S.lds_mode == LDS_BITS) {
+            // filter from the LDS bitmap; the code (if any) comes from the device map later
 #pragma unroll
             for (int j = 0; j < IPT; ++j)
 #pragma unroll
                 for (int r = 0; r < W; ++r) {
                     const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
-                    c[j][r] = S.sentinel;
-                    if (((live[j] >> r) & 1u) && idx < S.nslots) c[j][r] = load_dense_code(S, idx);
+                    const bool ok = ((live[j] >> r) & 1u) && idx < S.nslots && lds_bit(S, lds, idx);
+                    if (!ok) live[j] &= ~(1u << r);
+                    didx[j][r] = S.defer == 0 ? idx : didx[j][r];
                 }
+            if (S.n_gk && S.defer != 0) {
+                uint32_t c[IPT][W];
+#pragma unroll
+                for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                    for (int r = 0; r < W; ++r) {
+                        c[j][r] = 0u;
+                        if ((live[j] >> r) & 1u) c[j][r] = load_dense_code(S, (uint32_t)(x[j][r] - S.kmin));
+                    }
+#pragma unroll
+                for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                    for (int r = 0; r < W; ++r)
+                        if ((live[j] >> r) & 1u) gid[j][r] += code_contribution(S, c[j][r]);
+            }
+        } else if (S.kind == ST_DENSE) {
+            uint32_t c[IPT][W];
+            if (S.lds_mode == LDS_MAP) {
+#pragma unroll
+                for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                    for (int r = 0; r < W; ++r) {
+                        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+                        c[j][r] = S.sentinel;
+                        if (((live[j] >> r) & 1u) && idx < S.nslots) c[j][r] = lds_code(S, lds, idx);
+                    }
+            } else {
+#pragma unroll
+                for (int j = 0; j < IPT; ++j)
+#pragma unroll
+                    for (int r = 0; r < W; ++r) {
+                        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+                        c[j][r] = S.sentinel;
+                        if (((live[j] >> r) & 1u) && idx < S.nslots) c[j][r] = load_dense_code(S, idx);
+                    }
+            }
 #pragma unroll
             for (int j = 0; j < IPT; ++j)
 #pragma unroll
@@ -409,26 +552,31 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const int64_
                     else if (S.n_gk) gid[j][r] += code_contribution(S, c[j][r]);
                 }
         } else {
+            // open addressing: first slots of two items in flight, then resolve
             const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
-            uint32_t h[IPT][W];
-            unsigned long long sl[IPT][W];
+            constexpr int HJ = IPT < 2 ? IPT : 2;
 #pragma unroll
-            for (int j = 0; j < IPT; ++j)
+            for (int j0 = 0; j0 < IPT; j0 += HJ) {
+                uint32_t h[HJ][W];
+                unsigned long long sl[HJ][W];
 #pragma unroll
-                for (int r = 0; r < W; ++r) {
-                    h[j][r] = hash_slot(S, x[j][r]);
-                    sl[j][r] = 0ull;
-                    if ((live[j] >> r) & 1u) sl[j][r] = tab[h[j][r]];
-                }
+                for (int jj = 0; jj < HJ; ++jj)
 #pragma unroll
-            for (int j = 0; j < IPT; ++j)
+                    for (int r = 0; r < W; ++r) {
+                        h[jj][r] = hash_slot(S, x[j0 + jj][r]);
+                        sl[jj][r] = 0ull;
+                        if ((live[j0 + jj] >> r) & 1u) sl[jj][r] = tab[h[jj][r]];
+                    }
 #pragma unroll
-                for (int r = 0; r < W; ++r) {
-                    if (!((live[j] >> r) & 1u)) continue;
-                    const uint32_t c = hash_resolve(S, x[j][r], h[j][r], sl[j][r]);
-                    if (c == S.sentinel) live[j] &= ~(1u << r);
-                    else if (S.n_gk) gid[j][r] += code_contribution(S, c);
-                }
+                for (int jj = 0; jj < HJ; ++jj)
+#pragma unroll
+                    for (int r = 0; r < W; ++r) {
+                        if (!((live[j0 + jj] >> r) & 1u)) continue;
+                        const uint32_t c = hash_resolve(S, x[j0 + jj][r], h[jj][r], sl[jj][r]);
+                        if (c == S.sentinel) live[j0 + jj] &= ~(1u << r);
+                        else if (S.n_gk) gid[j0 + jj][r] += code_contribution(S, c);
+                    }
+            }
         }
     }
 
@@ -436,6 +584,24 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const int64_
 #pragma unroll
     for (int j = 0; j < IPT; ++j) any |= live[j];
     if (!__any(any != 0u)) return;
+
+    if (p.defer_stage >= 0) {
+        // group-key code of the LDS-bitmap stage, gathered only for the survivors
+        const StageDev& S = p.st[p.defer_stage];
+        uint32_t c[IPT][W];
+#pragma unroll
+        for (int j = 0; j < IPT; ++j)
+#pragma unroll
+            for (int r = 0; r < W; ++r) {
+                c[j][r] = 0u;
+                if ((live[j] >> r) & 1u) c[j][r] = load_dense_code(S, didx[j][r]);
+            }
+#pragma unroll
+        for (int j = 0; j < IPT; ++j)
+#pragma unroll
+            for (int r = 0; r < W; ++r)
+                if ((live[j] >> r) & 1u) gid[j][r] += code_contribution(S, c[j][r]);
+    }
 
     int32_t a[IPT][W], b[IPT][W];
     const int32_t* ca = p.cols[p.agg_a];
@@ -460,41 +626,58 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const int64_
         }
 }
 
+// The kernel reads its parameters in place from the kernel-argument segment
+// (constant memory, scalar loads); indexing the by-value copy with a runtime
+// stage number could otherwise make the compiler copy it to scratch.
 template <int W, int IPT, int TERM>
-__global__ void __launch_bounds__(kBlock) star_fused_kernel(FusedParams p) {
-    extern __shared__ unsigned long long lds[];
+__global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kernel_args) {
+    (void)kernel_args;
+    const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     TermState<TERM> ts;
     if constexpr (TERM == TERM_LDS) {
-        ts.lsum = lds;
-        ts.lcnt = lds + p.n_groups;
-        for (uint32_t g = threadIdx.x; g < 2u * p.n_groups; g += blockDim.x) lds[g] = 0ull;
-        __syncthreads();
+        ts.lsum = reinterpret_cast<unsigned long long*>(lds);
+        ts.lcnt = ts.lsum + p.n_groups;
+        for (uint32_t g = threadIdx.x; g < 2u * p.n_groups; g += blockDim.x) ts.lsum[g] = 0ull;
     }
+    if constexpr (TERM == TERM_GLOBAL) {
+        if (p.xcd_copies > 0)
+            ts.xt = p.xtab + 2ull * p.n_groups * (xcc_id() & (uint32_t)(p.xcd_copies - 1));
+    }
+    // stage the LDS-resident dimension tables (16-byte copies; sources are padded)
+    for (int s = 0; s < p.nstages; ++s) {
+        const StageDev& S = p.st[s];
+        if (S.lds_mode == LDS_GLOBAL) continue;
+        const v4i* src = reinterpret_cast<const v4i*>(S.lds_mode == LDS_MAP ? S.map : S.bits);
+        v4i* dst = reinterpret_cast<v4i*>(lds + S.lds_off);
+        for (uint32_t i = threadIdx.x; i < S.lds_bytes / 16u; i += blockDim.x) dst[i] = src[i];
+    }
+    __syncthreads();
 
     const int64_t n_items = p.n / W;
-    const int64_t tile = (int64_t)kBlock * IPT;
+    const int64_t tile = (int64_t)blockDim.x * IPT;
     const int64_t n_tiles = (n_items + tile - 1) / tile;
     for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
         int64_t item[IPT];
         uint32_t live[IPT];
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
-            item[j] = t * tile + (int64_t)j * kBlock + threadIdx.x;
+            item[j] = t * tile + (int64_t)j * blockDim.x + threadIdx.x;
             live[j] = item[j] < n_items ? (1u << W) - 1u : 0u;
         }
-        process_items<W, IPT, TERM>(p, item, live, ts);
+        process_items<W, IPT, TERM>(p, lds, item, live, ts);
     }
     if constexpr (W > 1) {
         // the last n mod W rows, one per lane, by the last block
         if (blockIdx.x == gridDim.x - 1) {
             int64_t row[1] = {n_items * W + (int64_t)threadIdx.x};
             uint32_t live1[1] = {row[0] < p.n ? 1u : 0u};
-            process_items<1, 1, TERM>(p, row, live1, ts);
+            process_items<1, 1, TERM>(p, lds, row, live1, ts);
         }
     }
 
     if constexpr (TERM == TERM_SCALAR) {
-        __shared__ unsigned long long red[2][kBlock / 64];
+        __shared__ unsigned long long red[2][kMaxBlock / 64];
         const unsigned long long s = wave_sum_u64(ts.sum);
         const unsigned long long c = wave_sum_u64(ts.cnt);
         if ((threadIdx.x & 63) == 0) {
@@ -504,7 +687,7 @@ __global__ void __launch_bounds__(kBlock) star_fused_kernel(FusedParams p) {
         __syncthreads();
         if (threadIdx.x == 0) {
             unsigned long long bs = 0, bc = 0;
-            for (int w = 0; w < kBlock / 64; ++w) {
+            for (uint32_t w = 0; w < blockDim.x / 64u; ++w) {
                 bs += red[0][w];
                 bc += red[1][w];
             }
@@ -525,6 +708,31 @@ __global__ void __launch_bounds__(kBlock) star_fused_kernel(FusedParams p) {
     }
 }
 
+// Adds the per-XCD copies into the outputs (which it overwrites).
+__global__ void __launch_bounds__(256) xcd_merge_kernel(const unsigned long long* xtab, int copies,
+                                                        uint64_t n_groups, unsigned long long* sums,
+                                                        unsigned long long* counts) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; g < n_groups; g += stride) {
+        unsigned long long s = 0, c = 0;
+        for (int x = 0; x < copies; ++x) {
+            const unsigned long long* e = xtab + 2ull * (n_groups * (uint64_t)x + g);
+            s += e[0];
+            c += e[1];
+        }
+        sums[g] = s;
+        counts[g] = c;
+    }
+}
+
+hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
+                            unsigned long long* sums, unsigned long long* counts, hipStream_t s) {
+    if (n_groups == 0) return hipSuccess;
+    hipLaunchKernelGGL(xcd_merge_kernel, dim3(fill_grid(n_groups)), dim3(256), 0, s, xtab, copies, n_groups,
+                       sums, counts);
+    return hipGetLastError();
+}
+
 template <int W, int IPT, int TERM>
 static const void* fused_fn() {
     return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM>);
@@ -541,32 +749,30 @@ static const void* pick_fused(int vector, int ipt, int terminal) {
         SDB_PICK(4, 1)
         SDB_PICK(4, 2)
         SDB_PICK(4, 4)
-        SDB_PICK(4, 8)
     } else {
         SDB_PICK(1, 1)
         SDB_PICK(1, 2)
         SDB_PICK(1, 4)
-        SDB_PICK(1, 8)
     }
 #undef SDB_PICK
     return nullptr;
 }
 
-int fused_blocks_per_cu(int vector, int ipt, int terminal, size_t lds_bytes) {
+int fused_blocks_per_cu(int vector, int ipt, int terminal, int block, size_t lds_bytes) {
     const void* fn = pick_fused(vector, ipt, terminal);
     if (!fn) return -1;
     int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kBlock, lds_bytes) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, block, lds_bytes) != hipSuccess)
         return -1;
     return blocks;
 }
 
-hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid,
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid, int block,
                         size_t lds_bytes, hipStream_t s) {
     const void* fn = pick_fused(vector, ipt, terminal);
     if (!fn) return hipErrorInvalidValue;
     void* args[] = {const_cast<FusedParams*>(&p)};
-    return hipLaunchKernel(fn, dim3(grid), dim3(kBlock), args, lds_bytes, s);
+    return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);
 }
 
 // ---------------------------------------------------------------------------

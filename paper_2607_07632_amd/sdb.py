@@ -35,6 +35,7 @@ TABLES = {"auto": 0, "dense": 1, "hash": 2}
 AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
 TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3}
 TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global"}
+LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits"}
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
           4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
 
@@ -56,7 +57,7 @@ class SdbDim(C.Structure):
                 ("key_min", i32), ("key_max", i32), ("n_slots", u64), ("hash_bits", i32),
                 ("sentinel", u32), ("domain", u64), ("n_payloads", i32),
                 ("payload_min", i32 * MAX_PAYLOADS), ("payload_radix", u32 * MAX_PAYLOADS),
-                ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp)]
+                ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp), ("bits", vp)]
 
 
 class SdbJoin(C.Structure):
@@ -77,16 +78,19 @@ class SdbQuery(C.Structure):
                 ("n_joins", i32), ("joins", SdbJoin * MAX_JOINS),
                 ("n_group_keys", i32), ("group_keys", SdbGroupKey * MAX_GROUP_KEYS),
                 ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
-                ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32)]
+                ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
+                ("force_lds", i32), ("force_xcd", i32)]
 
 
 class SdbPlan(C.Structure):
     _fields_ = [("n_stages", i32), ("stage_kind", i32 * MAX_STAGES),
                 ("stage_index", i32 * MAX_STAGES), ("stage_pass", C.c_double * MAX_STAGES),
-                ("sampled_rows", i64), ("terminal", i32), ("ipt", i32), ("vector", i32),
-                ("block", i32), ("grid", i32), ("n_group_keys", i32),
+                ("stage_lds", i32 * MAX_STAGES), ("stage_defer", i32 * MAX_STAGES),
+                ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
+                ("vector", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
+                ("lds_bytes", i32), ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
-                ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64)]
+                ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64)]
 
 
 STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan]
@@ -100,7 +104,7 @@ SIGNATURES = {
     "sdb_dim_required_bytes": (i32, [C.POINTER(SdbDimDesc), C.POINTER(i64)]),
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
     "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
-    "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp]),
+    "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
     "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
     "sdb_finalize_groups": (i32, [C.POINTER(SdbPlan), vp, vp, vp, vp, vp, i64, vp, vp, i64, vp]),
 }
@@ -317,6 +321,8 @@ class StarQuery:
         q.force_vector = int(force.get("vector", 0))
         q.force_order = 1 if force.get("order") else 0
         q.grid_blocks = int(force.get("grid", 0))
+        q.force_lds = int(force.get("lds", 0))
+        q.force_xcd = int(force.get("xcd", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -324,6 +330,7 @@ class StarQuery:
         self.n_keys = len(gb)
         self.plan_obj = None
         self._plan_scratch = None
+        self._run_scratch = None
 
     # -- steps ------------------------------------------------------------
     def plan(self, stream=None) -> SdbPlan:
@@ -345,10 +352,25 @@ class StarQuery:
         g = int(plan.n_groups)
         return (torch.empty(g, dtype=torch.int64, device=dev), torch.empty(g, dtype=torch.int64, device=dev))
 
-    def run(self, sums, counts, plan: SdbPlan | None = None, stream=None) -> None:
+    def run_scratch(self, plan: SdbPlan | None = None):
+        """Device scratch for sdb_run_star_query (None when the plan needs none)."""
+        import torch
         plan = plan or self.plan_obj
+        need = int(plan.run_scratch_bytes)
+        if need == 0:
+            return None
+        if self._run_scratch is None or self._run_scratch.numel() < need:
+            dev = next(iter(self.fact.values())).device
+            self._run_scratch = torch.empty(need, dtype=torch.uint8, device=dev)
+        return self._run_scratch
+
+    def run(self, sums, counts, plan: SdbPlan | None = None, stream=None, scratch=None) -> None:
+        plan = plan or self.plan_obj
+        if scratch is None:
+            scratch = self.run_scratch(plan)
+        nbytes = 0 if scratch is None else scratch.numel()
         _check(lib().sdb_run_star_query(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
-                                        sums.numel(), _stream_handle(stream)))
+                                        sums.numel(), _ptr(scratch), nbytes, _stream_handle(stream)))
 
     def finalize(self, sums, counts, plan: SdbPlan | None = None, stream=None, outputs=None):
         """Device compaction; returns (keys, sums, counts, n) device tensors (n: int64[1])."""
@@ -391,9 +413,16 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
         name = None
         if query is not None:
             name = (query["fact_preds"][i]["col"] if kind == 0 else query["joins"][i]["dim"])
-        stages.append({"kind": "pred" if kind == 0 else "probe", "index": i, "name": name,
-                       "pass": round(plan.stage_pass[s], 6)})
+        st = {"kind": "pred" if kind == 0 else "probe", "index": i, "name": name,
+              "pass": round(plan.stage_pass[s], 6)}
+        if kind == 1:
+            st["table"] = LDS_NAMES.get(plan.stage_lds[s], plan.stage_lds[s])
+            if plan.stage_defer[s] >= 0:
+                st["deferred_gather"] = True
+        stages.append(st)
     return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
             "ipt": plan.ipt, "vector": plan.vector, "block": plan.block, "grid": plan.grid,
+            "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
+            "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}

@@ -38,7 +38,7 @@ def test_struct_layout_matches_binding():
     sizes = (C.c_int64 * 8)()
     assert L.sdb_struct_sizes(sizes, 8) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
-    assert L.sdb_abi_version() == 1
+    assert L.sdb_abi_version() == 2
 
 
 def test_status_strings():
@@ -62,8 +62,8 @@ def _desc(n_rows=1000, kind="auto", n_cols=2, lf=0.0):
 
 def test_required_bytes_bounds():
     dense = sdb.dim_required_bytes(_desc(1000, "dense"))
-    # stats + 2000 slots x 4 B + occupancy bitmap
-    assert dense == 256 + 8192 + 256
+    # stats + 2000 slots x 4 B + occupancy and pass bitmaps
+    assert dense == 256 + 8192 + 2 * 256
     h = sdb.dim_required_bytes(_desc(1000, "hash"))
     assert h == 256 + 2048 * 8
     a = sdb.dim_required_bytes(_desc(1000, "auto"))
@@ -157,7 +157,7 @@ def test_plan_group_layout_and_terminals():
     p = _plan(_query([sup, date], [(0, 0), (1, 0)]))
     assert p.n_groups == 200 and list(p.radix[:2]) == [25, 8] and list(p.stride[:2]) == [8, 1]
     assert list(p.key_min[:2]) == [0, 1992]
-    assert sdb.TERMINAL_NAMES[p.terminal] == "lds" and p.ipt == 2 and p.vector == 1
+    assert sdb.TERMINAL_NAMES[p.terminal] == "lds" and p.ipt == 4 and p.vector == 1
     assert [p.stage_kind[i] for i in range(2)] == [1, 1]
     cust = _fake_dim(n_rows=3_000_000, radices=(250,), n_slots=3_000_000)
     sup2 = _fake_dim(radices=(250,))
@@ -193,7 +193,7 @@ def test_plan_capacity_and_validation_errors():
         _plan(q)
     assert e.value.name == "SDB_INVALID_ARG"
     q = _query([d], [(0, 0)])
-    q.force_ipt = 3
+    q.force_ipt = 8
     with pytest.raises(sdb.SdbError) as e:
         _plan(q)
     assert e.value.name == "SDB_UNSUPPORTED"
@@ -219,14 +219,21 @@ def test_run_rejects_mismatched_plan_before_any_launch():
     q = _query([d], [(0, 0)])
     p = _plan(q)
     L = sdb.lib()
-    assert L.sdb_run_star_query(C.byref(q), C.byref(p), 0x1000, 0x2000, 10, None) == 3   # CAPACITY
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p), 0x1000, 0x2000, 10, None, 0, None) == 3   # CAPACITY
     p2 = sdb.SdbPlan.from_buffer_copy(p)
     p2.n_stages = 0
-    assert L.sdb_run_star_query(C.byref(q), C.byref(p2), 0x1000, 0x2000, 100, None) == 1
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p2), 0x1000, 0x2000, 100, None, 0, None) == 1
     p3 = sdb.SdbPlan.from_buffer_copy(p)
     p3.stage_index[0] = 4
-    assert L.sdb_run_star_query(C.byref(q), C.byref(p3), 0x1000, 0x2000, 100, None) == 1
-    assert L.sdb_run_star_query(C.byref(q), C.byref(p), None, 0x2000, 100, None) == 1
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p3), 0x1000, 0x2000, 100, None, 0, None) == 1
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p), None, 0x2000, 100, None, 0, None) == 1
+    p4 = sdb.SdbPlan.from_buffer_copy(p)
+    p4.stage_lds[0] = 1                                   # LDS map on a table with width 1: allowed
+    p4.stage_defer[0] = 0                                 # but a deferred gather needs the bitmap mode
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p4), 0x1000, 0x2000, 100, None, 0, None) == 1
+    p5 = sdb.SdbPlan.from_buffer_copy(p)
+    p5.xcd_copies = 8                                     # copies need the global terminal
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p5), 0x1000, 0x2000, 100, None, 0, None) == 1
 
 
 def test_finalize_scratch_and_validation():

@@ -44,7 +44,7 @@ def test_config_parity(name):
 
 @pytest.mark.parametrize("name", ["c2_join_group", "c3_star3"])
 @pytest.mark.parametrize("force", [
-    {"order": True}, {"vector": -1}, {"ipt": 1}, {"ipt": 8}, {"terminal": "global"},
+    {"order": True}, {"vector": -1}, {"ipt": 1}, {"ipt": 4}, {"terminal": "global"},
     {"ipt": 4, "vector": -1, "terminal": "global"}, {"grid": 7}, {"grid": 1, "ipt": 2},
 ])
 def test_forced_plans_agree(name, force):
@@ -57,7 +57,7 @@ def test_forced_plans_agree(name, force):
 def test_c1_forced_plans_agree():
     w = workload("c1_scalar_scan")
     want = oracle_rows(w)
-    for force in [{"ipt": 1}, {"ipt": 2}, {"ipt": 8}, {"vector": -1}, {"order": True},
+    for force in [{"ipt": 1}, {"ipt": 2}, {"ipt": 4}, {"vector": -1}, {"order": True},
                   {"terminal": "global"}, {"terminal": "lds"}, {"grid": 3}]:
         got, _ = run_gpu(w, force=force)
         assert_same(got.as_rows(), want, f"c1 {force}")
@@ -99,7 +99,7 @@ def test_random_tiny_schemas(block):
 def test_random_tiny_schemas_forced(seed):
     w = random_tiny_workload(seed + 1000, max_fact=5000, max_dim_rows=500, n_fact=4099)
     want = oracle_rows(w)
-    for force in [{"vector": -1}, {"ipt": 1, "grid": 2}, {"ipt": 8}, {"order": True},
+    for force in [{"vector": -1}, {"ipt": 1, "grid": 2}, {"ipt": 4}, {"order": True},
                   {"terminal": "global"}]:
         got, _ = run_gpu(w, force=force)
         assert_same(got.as_rows(), want, f"tiny {seed} {force}")
