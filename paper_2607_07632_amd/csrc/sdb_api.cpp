@@ -278,6 +278,7 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
     S.defer = -1;
     if (kind == 0) {
         S.kind = ST_PRED;
+        S.op = OP_PRED;
         S.col = q->preds[index].col;
         S.test = lower_pred(q->preds[index]);
         return S;
@@ -317,6 +318,14 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
             S.defer = plan->stage_defer[pos];
         }
     }
+    S.gk_mode = S.n_gk == 0 ? GK_NONE
+              : (S.n_gk == 1 && S.gk_div[0] == 1u && S.gk_radix[0] == 0u ? GK_ONE : GK_GENERAL);
+    const int wsel = S.width == 1 ? 0 : (S.width == 2 ? 1 : 2);
+    if (S.kind == ST_HASH) S.op = OP_HASH;
+    else if (S.nslots == 0) S.op = OP_NEVER;
+    else if (S.lds_mode == LDS_BITS) S.op = OP_LDS_BITS;
+    else if (S.lds_mode == LDS_MAP) S.op = OP_LDS_MAP1 + wsel;
+    else S.op = OP_MAP1 + wsel;
     return S;
 }
 
@@ -481,7 +490,7 @@ bool columns_aligned(const sdb_query* q, const sdb_plan* plan) {
     return true;
 }
 
-constexpr int kDefaultIpt = 4;
+constexpr int kDefaultIpt = 2;
 
 sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) {
     const int64_t rows_per_item = plan->vector ? 4 : 1;

@@ -22,6 +22,23 @@ constexpr int kFinGroupsPerBlock = kFinBlock * kFinPerThread;
 constexpr int kDenseSlack = 1024;        // dense limit: key range <= max(2 * n_rows, 1024)
 
 enum StageKind : int32_t { ST_PRED = 0, ST_DENSE = 1, ST_HASH = 2 };
+
+// What the fused kernel does for a stage, fixed by the host so the kernel
+// branches once per stage and tile instead of once per row.
+enum StageOp : int32_t {
+    OP_PRED = 0,      // literal range test
+    OP_NEVER = 1,     // lookup in an empty table: every row misses
+    OP_LDS_BITS = 2,  // pass bitmap in LDS
+    OP_LDS_MAP1 = 3,  // whole map in LDS, 1/2/4-byte codes
+    OP_LDS_MAP2 = 4,
+    OP_LDS_MAP4 = 5,
+    OP_MAP1 = 6,      // map in device memory, 1/2/4-byte codes
+    OP_MAP2 = 7,
+    OP_MAP4 = 8,
+    OP_HASH = 9       // open-addressing table in device memory
+};
+// How a table's code becomes part of the group id.
+enum GroupMode : int32_t { GK_NONE = 0, GK_ONE = 1, GK_GENERAL = 2 };
 enum LdsMode : int32_t { LDS_GLOBAL = SDB_LDS_GLOBAL, LDS_MAP = SDB_LDS_MAP, LDS_BITS = SDB_LDS_BITS };
 enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3 };
 
@@ -36,6 +53,8 @@ struct RangeTest {
 // One stage of the fused pass, as the kernel reads it (kernel argument).
 struct StageDev {
     int32_t kind;          // StageKind
+    int32_t op;            // StageOp
+    int32_t gk_mode;       // GroupMode: GK_ONE adds code * gk_stride[0]
     int32_t col;           // fact column index
     RangeTest test;        // ST_PRED
     int32_t width;         // ST_DENSE: bytes per map entry (1, 2, 4)

@@ -446,184 +446,203 @@ __device__ __forceinline__ void accumulate(const FusedParams& p, TermState<TERM>
     }
 }
 
-__device__ __forceinline__ uint32_t lds_code(const StageDev& S, const unsigned char* lds, uint32_t idx) {
-    const unsigned char* base = lds + S.lds_off;
-    if (S.width == 1) return base[idx];
-    if (S.width == 2) return reinterpret_cast<const uint16_t*>(base)[idx];
-    return reinterpret_cast<const uint32_t*>(base)[idx];
+template <int WB>
+__device__ __forceinline__ uint32_t ld_code(const void* base, uint32_t idx) {
+    if constexpr (WB == 1) return static_cast<const uint8_t*>(base)[idx];
+    else if constexpr (WB == 2) return static_cast<const uint16_t*>(base)[idx];
+    else return static_cast<const uint32_t*>(base)[idx];
 }
 
-__device__ __forceinline__ bool lds_bit(const StageDev& S, const unsigned char* lds, uint32_t idx) {
-    const uint32_t* words = reinterpret_cast<const uint32_t*>(lds + S.lds_off);
-    return (words[idx >> 5] >> (idx & 31u)) & 1u;
-}
+// Row loops over the IPT items of W rows a lane owns. Liveness is one bool
+// per row; rows that are no longer live still execute the (branch-free) code
+// but read a fixed, valid slot so they cost no extra memory lines.
+#define SDB_ROWS(j, r)                        \
+    _Pragma("unroll") for (int j = 0; j < IPT; ++j) \
+    _Pragma("unroll") for (int r = 0; r < W; ++r)
 
-// Runs every stage and the terminal for IPT items of W rows each. `live[j]`
-// holds one bit per row of item j. All lanes of the wave must call this
-// together (the early exit is a wave-wide vote).
-template <int W, int IPT, int TERM>
-__device__ __forceinline__ void process_items(const FusedParams& p, const unsigned char* lds,
-                                              const int64_t (&item)[IPT], uint32_t (&live)[IPT],
-                                              TermState<TERM>& ts) {
-    uint32_t gid[IPT][W];
-    uint32_t didx[IPT][W];   // deferred gather: slot index in the deferred stage's map
-#pragma unroll
-    for (int j = 0; j < IPT; ++j)
-#pragma unroll
-        for (int r = 0; r < W; ++r) {
-            gid[j][r] = 0u;
-            didx[j][r] = 0u;
-        }
-
-    for (int s = 0; s < p.nstages; ++s) {
-        uint32_t any = 0;
-#pragma unroll
-        for (int j = 0; j < IPT; ++j) any |= live[j];
-        if (!__any(any != 0u)) return;            // no live row left in the wave
-        const StageDev& S = p.st[s];
-        const int32_t* col = p.cols[S.col];
-        int32_t x[IPT][W];
-#pragma unroll
-        for (int j = 0; j < IPT; ++j) {
-            if (live[j]) load_item<W>(col, item[j], x[j]);
-            else {
-#pragma unroll
-                for (int r = 0; r < W; ++r) x[j][r] = 0;
-            }
-        }
-        if (S.kind == ST_PRED) {
-#pragma unroll
-            for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                for (int r = 0; r < W; ++r)
-                    if (!range_pass(S.test, x[j][r])) live[j] &= ~(1u << r);
-        } else if (S.kind == ST_DENSE && S.lds_mode == LDS_BITS) {
-            // filter from the LDS bitmap; the code (if any) comes from the device map later
-#pragma unroll
-            for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                for (int r = 0; r < W; ++r) {
-                    const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
-                    const bool ok = ((live[j] >> r) & 1u) && idx < S.nslots && lds_bit(S, lds, idx);
-                    if (!ok) live[j] &= ~(1u << r);
-                    didx[j][r] = S.defer == 0 ? idx : didx[j][r];
-                }
-            if (S.n_gk && S.defer != 0) {
-                uint32_t c[IPT][W];
-#pragma unroll
-                for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                    for (int r = 0; r < W; ++r) {
-                        c[j][r] = 0u;
-                        if ((live[j] >> r) & 1u) c[j][r] = load_dense_code(S, (uint32_t)(x[j][r] - S.kmin));
-                    }
-#pragma unroll
-                for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                    for (int r = 0; r < W; ++r)
-                        if ((live[j] >> r) & 1u) gid[j][r] += code_contribution(S, c[j][r]);
-            }
-        } else if (S.kind == ST_DENSE) {
-            uint32_t c[IPT][W];
-            if (S.lds_mode == LDS_MAP) {
-#pragma unroll
-                for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                    for (int r = 0; r < W; ++r) {
-                        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
-                        c[j][r] = S.sentinel;
-                        if (((live[j] >> r) & 1u) && idx < S.nslots) c[j][r] = lds_code(S, lds, idx);
-                    }
-            } else {
-#pragma unroll
-                for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                    for (int r = 0; r < W; ++r) {
-                        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
-                        c[j][r] = S.sentinel;
-                        if (((live[j] >> r) & 1u) && idx < S.nslots) c[j][r] = load_dense_code(S, idx);
-                    }
-            }
-#pragma unroll
-            for (int j = 0; j < IPT; ++j)
-#pragma unroll
-                for (int r = 0; r < W; ++r) {
-                    if (c[j][r] == S.sentinel) live[j] &= ~(1u << r);
-                    else if (S.n_gk) gid[j][r] += code_contribution(S, c[j][r]);
-                }
-        } else {
-            // open addressing: first slots of two items in flight, then resolve
-            const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
-            constexpr int HJ = IPT < 2 ? IPT : 2;
-#pragma unroll
-            for (int j0 = 0; j0 < IPT; j0 += HJ) {
-                uint32_t h[HJ][W];
-                unsigned long long sl[HJ][W];
-#pragma unroll
-                for (int jj = 0; jj < HJ; ++jj)
-#pragma unroll
-                    for (int r = 0; r < W; ++r) {
-                        h[jj][r] = hash_slot(S, x[j0 + jj][r]);
-                        sl[jj][r] = 0ull;
-                        if ((live[j0 + jj] >> r) & 1u) sl[jj][r] = tab[h[jj][r]];
-                    }
-#pragma unroll
-                for (int jj = 0; jj < HJ; ++jj)
-#pragma unroll
-                    for (int r = 0; r < W; ++r) {
-                        if (!((live[j0 + jj] >> r) & 1u)) continue;
-                        const uint32_t c = hash_resolve(S, x[j0 + jj][r], h[jj][r], sl[jj][r]);
-                        if (c == S.sentinel) live[j0 + jj] &= ~(1u << r);
-                        else if (S.n_gk) gid[j0 + jj][r] += code_contribution(S, c);
-                    }
-            }
-        }
-    }
-
-    uint32_t any = 0;
-#pragma unroll
-    for (int j = 0; j < IPT; ++j) any |= live[j];
-    if (!__any(any != 0u)) return;
-
-    if (p.defer_stage >= 0) {
-        // group-key code of the LDS-bitmap stage, gathered only for the survivors
-        const StageDev& S = p.st[p.defer_stage];
-        uint32_t c[IPT][W];
-#pragma unroll
-        for (int j = 0; j < IPT; ++j)
-#pragma unroll
-            for (int r = 0; r < W; ++r) {
-                c[j][r] = 0u;
-                if ((live[j] >> r) & 1u) c[j][r] = load_dense_code(S, didx[j][r]);
-            }
-#pragma unroll
-        for (int j = 0; j < IPT; ++j)
-#pragma unroll
-            for (int r = 0; r < W; ++r)
-                if ((live[j] >> r) & 1u) gid[j][r] += code_contribution(S, c[j][r]);
-    }
-
-    int32_t a[IPT][W], b[IPT][W];
-    const int32_t* ca = p.cols[p.agg_a];
-    const int32_t* cb = p.cols[p.agg_b];
+template <int W, int IPT>
+__device__ __forceinline__ void load_column(const int32_t* col, const int64_t (&item)[IPT],
+                                            const bool (&al)[IPT][W], int32_t (&x)[IPT][W]) {
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
-        if (live[j]) load_item<W>(ca, item[j], a[j]);
-        if (live[j] && p.agg_kind != SDB_AGG_COL) load_item<W>(cb, item[j], b[j]);
+        bool any = false;
+#pragma unroll
+        for (int r = 0; r < W; ++r) any = any || al[j][r];
+        // an item with no live row reads item 0, a line every such item shares
+        load_item<W>(col, any ? item[j] : 0, x[j]);
     }
-#pragma unroll
-    for (int j = 0; j < IPT; ++j)
-#pragma unroll
-        for (int r = 0; r < W; ++r) {
-            if (!((live[j] >> r) & 1u)) continue;
-            const long long va = a[j][r];
-            long long v;
-            if (p.agg_kind == SDB_AGG_COL) v = va;
-            else if (p.agg_kind == SDB_AGG_MUL) v = (long long)((unsigned long long)va * (unsigned long long)(long long)b[j][r]);
-            else if (p.agg_kind == SDB_AGG_SUB) v = va - (long long)b[j][r];
-            else v = va + (long long)b[j][r];
-            accumulate<TERM>(p, ts, gid[j][r], v);
+}
+
+template <int W, int IPT>
+__device__ __forceinline__ void add_group(const StageDev& S, const uint32_t (&c)[IPT][W], uint32_t (&gid)[IPT][W]) {
+    // dead rows may add garbage: their group id is never used
+    if (S.gk_mode == GK_ONE) {
+        SDB_ROWS(j, r) gid[j][r] += c[j][r] * S.gk_stride[0];
+    } else if (S.gk_mode == GK_GENERAL) {
+        SDB_ROWS(j, r) gid[j][r] += code_contribution(S, c[j][r]);
+    }
+}
+
+// Dense map lookup (device memory or LDS): the code doubles as the filter.
+template <int W, int IPT, int WB, bool IN_LDS>
+__device__ __forceinline__ void stage_map(const StageDev& S, const unsigned char* lds, const int32_t (&x)[IPT][W],
+                                          bool (&al)[IPT][W], uint32_t (&gid)[IPT][W]) {
+    const void* base = IN_LDS ? static_cast<const void*>(lds + S.lds_off) : S.map;
+    uint32_t c[IPT][W];
+    SDB_ROWS(j, r) {
+        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+        const bool ok = al[j][r] && idx < S.nslots;
+        c[j][r] = ld_code<WB>(base, ok ? idx : 0u);
+        al[j][r] = ok;
+    }
+    SDB_ROWS(j, r) al[j][r] = al[j][r] && c[j][r] != S.sentinel;
+    add_group<W, IPT>(S, c, gid);
+}
+
+template <int W, int IPT>
+__device__ __forceinline__ void stage_bits(const StageDev& S, const unsigned char* lds, const int32_t (&x)[IPT][W],
+                                           bool (&al)[IPT][W], uint32_t (&gid)[IPT][W], uint32_t (&didx)[IPT][W]) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(lds + S.lds_off);
+    uint32_t idc[IPT][W];
+    SDB_ROWS(j, r) {
+        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+        const bool ok = al[j][r] && idx < S.nslots;
+        idc[j][r] = ok ? idx : 0u;
+        al[j][r] = ok && ((words[idc[j][r] >> 5] >> (idc[j][r] & 31u)) & 1u);
+    }
+    if (S.defer == 0) {
+        SDB_ROWS(j, r) didx[j][r] = idc[j][r];
+    } else if (S.gk_mode != GK_NONE) {
+        // gather the code now, from the device map, for the rows that passed
+        uint32_t c[IPT][W];
+        if (S.width == 1) {
+            SDB_ROWS(j, r) c[j][r] = ld_code<1>(S.map, al[j][r] ? idc[j][r] : 0u);
+        } else if (S.width == 2) {
+            SDB_ROWS(j, r) c[j][r] = ld_code<2>(S.map, al[j][r] ? idc[j][r] : 0u);
+        } else {
+            SDB_ROWS(j, r) c[j][r] = ld_code<4>(S.map, al[j][r] ? idc[j][r] : 0u);
         }
+        add_group<W, IPT>(S, c, gid);
+    }
+}
+
+template <int W, int IPT>
+__device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)[IPT][W], bool (&al)[IPT][W],
+                                           uint32_t (&gid)[IPT][W]) {
+    // open addressing: first slots of two items in flight, then resolve
+    const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
+    constexpr int HJ = IPT < 2 ? IPT : 2;
+#pragma unroll
+    for (int j0 = 0; j0 < IPT; j0 += HJ) {
+        uint32_t h[HJ][W];
+        unsigned long long sl[HJ][W];
+#pragma unroll
+        for (int jj = 0; jj < HJ; ++jj)
+#pragma unroll
+            for (int r = 0; r < W; ++r) {
+                h[jj][r] = hash_slot(S, x[j0 + jj][r]);
+                sl[jj][r] = tab[al[j0 + jj][r] ? h[jj][r] : 0u];
+            }
+#pragma unroll
+        for (int jj = 0; jj < HJ; ++jj)
+#pragma unroll
+            for (int r = 0; r < W; ++r) {
+                uint32_t c = S.sentinel;
+                if (al[j0 + jj][r]) c = hash_resolve(S, x[j0 + jj][r], h[jj][r], sl[jj][r]);
+                al[j0 + jj][r] = al[j0 + jj][r] && c != S.sentinel;
+                if (S.gk_mode == GK_ONE) gid[j0 + jj][r] += c * S.gk_stride[0];
+                else if (S.gk_mode == GK_GENERAL) gid[j0 + jj][r] += code_contribution(S, c);
+            }
+    }
+}
+
+template <int W, int IPT>
+__device__ __forceinline__ void gather_deferred(const StageDev& S, const bool (&al)[IPT][W],
+                                                const uint32_t (&didx)[IPT][W], uint32_t (&gid)[IPT][W]) {
+    uint32_t c[IPT][W];
+    if (S.width == 1) {
+        SDB_ROWS(j, r) c[j][r] = ld_code<1>(S.map, al[j][r] ? didx[j][r] : 0u);
+    } else if (S.width == 2) {
+        SDB_ROWS(j, r) c[j][r] = ld_code<2>(S.map, al[j][r] ? didx[j][r] : 0u);
+    } else {
+        SDB_ROWS(j, r) c[j][r] = ld_code<4>(S.map, al[j][r] ? didx[j][r] : 0u);
+    }
+    add_group<W, IPT>(S, c, gid);
+}
+
+template <int W, int IPT>
+__device__ __forceinline__ bool wave_has_live(const bool (&al)[IPT][W]) {
+    bool any = false;
+    SDB_ROWS(j, r) any = any || al[j][r];
+    return __any(any) != 0;
+}
+
+// Runs every stage and the terminal for IPT items of W rows each. All lanes
+// of the wave must call this together (the early exit is a wave-wide vote).
+template <int W, int IPT, int TERM>
+__device__ __forceinline__ void process_items(const FusedParams& p, const unsigned char* lds,
+                                              const int64_t (&item)[IPT], bool (&al)[IPT][W],
+                                              TermState<TERM>& ts) {
+    uint32_t gid[IPT][W];
+    uint32_t didx[IPT][W];   // deferred gather: slot in the deferred stage's map
+    SDB_ROWS(j, r) {
+        gid[j][r] = 0u;
+        didx[j][r] = 0u;
+    }
+
+    for (int s = 0; s < p.nstages; ++s) {
+        if (!wave_has_live<W, IPT>(al)) return;     // no live row left in the wave
+        const StageDev& S = p.st[s];
+        int32_t x[IPT][W];
+        load_column<W, IPT>(p.cols[S.col], item, al, x);
+        switch (S.op) {
+            case OP_PRED:
+                SDB_ROWS(j, r) al[j][r] = al[j][r] && range_pass(S.test, x[j][r]);
+                break;
+            case OP_LDS_BITS: stage_bits<W, IPT>(S, lds, x, al, gid, didx); break;
+            case OP_LDS_MAP1: stage_map<W, IPT, 1, true>(S, lds, x, al, gid); break;
+            case OP_LDS_MAP2: stage_map<W, IPT, 2, true>(S, lds, x, al, gid); break;
+            case OP_LDS_MAP4: stage_map<W, IPT, 4, true>(S, lds, x, al, gid); break;
+            case OP_MAP1: stage_map<W, IPT, 1, false>(S, lds, x, al, gid); break;
+            case OP_MAP2: stage_map<W, IPT, 2, false>(S, lds, x, al, gid); break;
+            case OP_MAP4: stage_map<W, IPT, 4, false>(S, lds, x, al, gid); break;
+            case OP_HASH: stage_hash<W, IPT>(S, x, al, gid); break;
+            default:   // OP_NEVER
+                SDB_ROWS(j, r) al[j][r] = false;
+                break;
+        }
+    }
+    if (!wave_has_live<W, IPT>(al)) return;
+    if (p.defer_stage >= 0) gather_deferred<W, IPT>(p.st[p.defer_stage], al, didx, gid);
+
+    int32_t a[IPT][W], b[IPT][W];
+    load_column<W, IPT>(p.cols[p.agg_a], item, al, a);
+    long long v[IPT][W];
+    switch (p.agg_kind) {
+        case SDB_AGG_COL:
+            SDB_ROWS(j, r) v[j][r] = a[j][r];
+            break;
+        case SDB_AGG_MUL:
+            load_column<W, IPT>(p.cols[p.agg_b], item, al, b);
+            SDB_ROWS(j, r) v[j][r] = (long long)a[j][r] * (long long)b[j][r];
+            break;
+        case SDB_AGG_SUB:
+            load_column<W, IPT>(p.cols[p.agg_b], item, al, b);
+            SDB_ROWS(j, r) v[j][r] = (long long)a[j][r] - (long long)b[j][r];
+            break;
+        default:
+            load_column<W, IPT>(p.cols[p.agg_b], item, al, b);
+            SDB_ROWS(j, r) v[j][r] = (long long)a[j][r] + (long long)b[j][r];
+            break;
+    }
+    if constexpr (TERM == TERM_SCALAR) {
+        SDB_ROWS(j, r) {
+            ts.sum += al[j][r] ? (unsigned long long)v[j][r] : 0ull;
+            ts.cnt += al[j][r] ? 1ull : 0ull;
+        }
+    } else {
+        SDB_ROWS(j, r) if (al[j][r]) accumulate<TERM>(p, ts, gid[j][r], v[j][r]);
+    }
 }
 
 // The kernel reads its parameters in place from the kernel-argument segment
@@ -659,20 +678,21 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
     const int64_t n_tiles = (n_items + tile - 1) / tile;
     for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
         int64_t item[IPT];
-        uint32_t live[IPT];
+        bool al[IPT][W];
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
             item[j] = t * tile + (int64_t)j * blockDim.x + threadIdx.x;
-            live[j] = item[j] < n_items ? (1u << W) - 1u : 0u;
+#pragma unroll
+            for (int r = 0; r < W; ++r) al[j][r] = item[j] < n_items;
         }
-        process_items<W, IPT, TERM>(p, lds, item, live, ts);
+        process_items<W, IPT, TERM>(p, lds, item, al, ts);
     }
     if constexpr (W > 1) {
         // the last n mod W rows, one per lane, by the last block
         if (blockIdx.x == gridDim.x - 1) {
             int64_t row[1] = {n_items * W + (int64_t)threadIdx.x};
-            uint32_t live1[1] = {row[0] < p.n ? 1u : 0u};
-            process_items<1, 1, TERM>(p, lds, row, live1, ts);
+            bool al1[1][1] = {{row[0] < p.n}};
+            process_items<1, 1, TERM>(p, lds, row, al1, ts);
         }
     }
 

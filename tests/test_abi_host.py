@@ -157,7 +157,7 @@ def test_plan_group_layout_and_terminals():
     p = _plan(_query([sup, date], [(0, 0), (1, 0)]))
     assert p.n_groups == 200 and list(p.radix[:2]) == [25, 8] and list(p.stride[:2]) == [8, 1]
     assert list(p.key_min[:2]) == [0, 1992]
-    assert sdb.TERMINAL_NAMES[p.terminal] == "lds" and p.ipt == 4 and p.vector == 1
+    assert sdb.TERMINAL_NAMES[p.terminal] == "lds" and p.ipt == 2 and p.vector == 1
     assert [p.stage_kind[i] for i in range(2)] == [1, 1]
     cust = _fake_dim(n_rows=3_000_000, radices=(250,), n_slots=3_000_000)
     sup2 = _fake_dim(radices=(250,))
@@ -166,7 +166,7 @@ def test_plan_group_layout_and_terminals():
     assert p3.n_groups == 375_000 and sdb.TERMINAL_NAMES[p3.terminal] == "global"
     assert list(p3.stride[:3]) == [1500, 6, 1]
     p1 = _plan(_query([date2], [], n_preds=2))
-    assert p1.n_groups == 1 and sdb.TERMINAL_NAMES[p1.terminal] == "scalar" and p1.ipt == 4
+    assert p1.n_groups == 1 and sdb.TERMINAL_NAMES[p1.terminal] == "scalar" and p1.ipt == 2
     assert [p1.stage_kind[i] for i in range(3)] == [0, 0, 1]
 
 
