@@ -84,7 +84,7 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c3_star3")
     ap.add_argument("--rows", type=int, default=None, help="fact rows (default: the workload's size)")
-    ap.add_argument("--cpu-rows", type=int, default=12_000_000, help="oracle sample rows")
+    ap.add_argument("--cpu-rows", type=int, default=40_000_000, help="oracle sample rows")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (scale for HBM byte counters)")
