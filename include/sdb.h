@@ -63,9 +63,12 @@ enum { SDB_AGG_COL = 0, SDB_AGG_MUL = 1, SDB_AGG_SUB = 2, SDB_AGG_ADD = 3 };
 
 /* Terminals (Sections 3.2, 3.3 and 4.3): one register accumulator per lane
  * reduced to one atomic per block; a block-private group table in LDS flushed
- * once per block; or one global atomic per surviving row. */
+ * once per block; one global atomic per surviving row; or partitioned
+ * aggregation for large group tables with many survivors (the fused kernel
+ * appends (group id, value) records, later passes sort them by group-id range
+ * and sum each range in LDS). */
 enum { SDB_TERMINAL_AUTO = 0, SDB_TERMINAL_SCALAR = 1, SDB_TERMINAL_LDS = 2,
-       SDB_TERMINAL_GLOBAL = 3 };
+       SDB_TERMINAL_GLOBAL = 3, SDB_TERMINAL_PART = 4 };
 
 #define SDB_MAX_DIM_COLS 8
 #define SDB_MAX_DIM_PREDS 4
@@ -219,6 +222,9 @@ typedef struct sdb_plan {
     int32_t grid;                         /* 0: chosen at launch */
     int32_t xcd_copies;
     int32_t lds_bytes;                    /* dynamic LDS per block */
+    int32_t part_shift;                   /* PART: partition of group g is g >> part_shift */
+    int32_t n_parts;
+    int64_t part_cap;                     /* PART: records per fused-kernel block */
     int32_t n_group_keys;
     int32_t key_min[SDB_MAX_GROUP_KEYS];
     uint32_t radix[SDB_MAX_GROUP_KEYS];

@@ -240,7 +240,7 @@ sdb_status check_query(const sdb_query* q) {
     if (q->agg.a < 0 || q->agg.a >= q->n_cols) return fail(SDB_INVALID_ARG, "aggregate operand a = %d", q->agg.a);
     if (q->agg.kind != SDB_AGG_COL && (q->agg.b < 0 || q->agg.b >= q->n_cols))
         return fail(SDB_INVALID_ARG, "aggregate operand b = %d", q->agg.b);
-    if (q->force_terminal < SDB_TERMINAL_AUTO || q->force_terminal > SDB_TERMINAL_GLOBAL)
+    if (q->force_terminal < SDB_TERMINAL_AUTO || q->force_terminal > SDB_TERMINAL_PART)
         return fail(SDB_INVALID_ARG, "bad force_terminal %d", q->force_terminal);
     if (q->force_ipt != 0 && q->force_ipt != 1 && q->force_ipt != 2 && q->force_ipt != 4)
         return fail(SDB_UNSUPPORTED, "force_ipt %d is not 0, 1, 2 or 4", q->force_ipt);
@@ -444,7 +444,9 @@ void place_lds(const sdb_query* q, sdb_plan* plan, uint64_t budget) {
 // Dynamic LDS layout of the fused kernel: the LDS group table, then each
 // staged table at a 16-byte aligned offset. Returns the total bytes.
 uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
-    uint64_t off = plan->terminal == TERM_LDS ? plan->n_groups * 16 : 0;
+    uint64_t off = 0;
+    if (plan->terminal == TERM_LDS) off = plan->n_groups * 16;
+    if (plan->terminal == TERM_PART) off = align_up((1 + (uint64_t)plan->n_parts) * 4, 16);
     if (p) p->term_lds_bytes = (uint32_t)off;
     for (int s = 0; s < plan->n_stages; ++s) {
         if (plan->stage_lds[s] == LDS_GLOBAL) continue;
@@ -491,6 +493,35 @@ bool columns_aligned(const sdb_query* q, const sdb_plan* plan) {
 }
 
 constexpr int kDefaultIpt = 2;
+
+// Run-scratch layout of the partitioned terminal.
+struct PartLayout {
+    uint64_t region_count, part_count, part_start, cursor, chunk_start, rec_gid, rec_val, sorted_gid,
+        sorted_val, total;
+};
+
+PartLayout part_layout(const sdb_plan* plan) {
+    PartLayout L;
+    const uint64_t grid = (uint64_t)plan->grid, P = (uint64_t)plan->n_parts;
+    const uint64_t recs = grid * (uint64_t)plan->part_cap;
+    uint64_t off = 0;
+    auto take = [&](uint64_t bytes) {
+        const uint64_t at = off;
+        off += align_up(bytes, 256);
+        return at;
+    };
+    L.region_count = take(grid * 4);
+    L.part_count = take(P * 4);
+    L.part_start = take((P + 1) * 4);
+    L.cursor = take(P * 4);
+    L.chunk_start = take((P + 1) * 4);
+    L.rec_gid = take(recs * 4);
+    L.rec_val = take(recs * 8);
+    L.sorted_gid = take(recs * 4);
+    L.sorted_val = take(recs * 8);
+    L.total = off;
+    return L;
+}
 
 sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) {
     const int64_t rows_per_item = plan->vector ? 4 : 1;
@@ -698,6 +729,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     if (term == TERM_LDS && plan->n_groups > (uint64_t)kLdsGroupLimit)
         return fail(SDB_CAPACITY, "LDS terminal holds at most %d groups, plan has %llu", kLdsGroupLimit,
                     (unsigned long long)plan->n_groups);
+    if (term == TERM_PART && q->n_fact == 0) term = TERM_GLOBAL;
     plan->terminal = term;
 
     // pass fraction of every stage on a strided sample of the fact rows
@@ -747,16 +779,54 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     plan->block = kBlock;
     plan->grid = q->grid_blocks;
 
-    // per-XCD private group tables for the global terminal when enough rows survive
+    // large group tables with many survivors: partitioned aggregation
     double f = 1.0;
     for (int s = 0; s < n; ++s) f *= plan->stage_pass[s];
     const double survivors = f * (double)q->n_fact;
+    if (term == TERM_GLOBAL || term == TERM_PART) {
+        int shift = 8;
+        while (shift < kPartMaxShift && (plan->n_groups >> shift) > 512) ++shift;
+        const uint64_t parts = (plan->n_groups + (1ull << shift) - 1) >> shift;
+        const bool fits = parts <= (uint64_t)kPartMaxParts;
+        // chosen automatically only where its passes beat direct atomics (many
+        // survivors per group; measured on c5, not yet on c3's 55 per group)
+        bool part = term == TERM_PART || (q->force_terminal == SDB_TERMINAL_AUTO && fits && q->n_fact > 0 &&
+                                          survivors >= 1.0e6 && survivors >= 512.0 * (double)plan->n_groups);
+        if (part && !fits)
+            return fail(SDB_CAPACITY, "partitioned terminal needs at most %d partitions of %d groups",
+                        kPartMaxParts, 1 << kPartMaxShift);
+        if (part) {
+            term = TERM_PART;
+            plan->terminal = TERM_PART;
+            plan->part_shift = shift;
+            plan->n_parts = (int32_t)parts;
+        }
+    }
+    plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
+
+    // per-XCD private group tables for the global terminal when enough rows survive
     const uint64_t copy_bytes = (uint64_t)kXcdCopies * plan->n_groups * 16;
     bool xcd = term == TERM_GLOBAL && survivors >= 2.0 * (double)plan->n_groups && copy_bytes <= (1ull << 30);
     if (q->force_xcd == 1) xcd = term == TERM_GLOBAL;
     if (q->force_xcd == -1) xcd = false;
     plan->xcd_copies = xcd ? kXcdCopies : 0;
     plan->run_scratch_bytes = xcd ? (int64_t)copy_bytes : 0;
+
+    if (term == TERM_PART) {
+        // records are written per block: the grid is fixed now
+        if (plan->grid <= 0) {
+            int grid = 0;
+            st = choose_grid(q, plan, &grid);
+            if (st != SDB_OK) return st;
+            plan->grid = grid;
+        }
+        const double cap_total = std::min((double)q->n_fact, 1.5 * survivors + 256.0 * plan->grid);
+        plan->part_cap = (int64_t)std::ceil(cap_total / plan->grid);
+        plan->part_cap = (int64_t)align_up((uint64_t)std::max<int64_t>(plan->part_cap, 64), 64);
+        if ((uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFF0ull)
+            plan->part_cap = (int64_t)(0xFFFFFFF0ull / (uint64_t)plan->grid) / 64 * 64;
+        plan->run_scratch_bytes = (int64_t)part_layout(plan).total;
+    }
     return ok();
 }
 
@@ -805,8 +875,15 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     if (n_groups_capacity < 0 || (uint64_t)n_groups_capacity < plan->n_groups)
         return fail(SDB_CAPACITY, "output holds %lld groups, plan needs %llu", (long long)n_groups_capacity,
                     (unsigned long long)plan->n_groups);
-    if (plan->terminal < TERM_SCALAR || plan->terminal > TERM_GLOBAL)
+    if (plan->terminal < TERM_SCALAR || plan->terminal > TERM_PART)
         return fail(SDB_INVALID_ARG, "bad plan terminal %d", plan->terminal);
+    if (plan->terminal == TERM_PART) {
+        if (plan->grid <= 0 || plan->part_cap <= 0 || plan->part_shift < 0 || plan->part_shift > kPartMaxShift ||
+            plan->n_parts <= 0 || plan->n_parts > kPartMaxParts ||
+            (uint64_t)plan->n_parts != ((plan->n_groups + (1ull << plan->part_shift) - 1) >> plan->part_shift) ||
+            (uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFFFull)
+            return fail(SDB_INVALID_ARG, "bad partitioned-terminal plan");
+    }
     if (plan->terminal == TERM_SCALAR && q->n_group_keys > 0)
         return fail(SDB_INVALID_ARG, "scalar terminal on a grouped query");
     if (plan->terminal == TERM_LDS && plan->n_groups > (uint64_t)kLdsGroupLimit)
@@ -819,7 +896,8 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         return fail(SDB_INVALID_ARG, "vector plan but a column is not 16-byte aligned");
     if (plan->xcd_copies != 0 && (plan->xcd_copies != kXcdCopies || plan->terminal != TERM_GLOBAL))
         return fail(SDB_INVALID_ARG, "bad plan xcd_copies %d", plan->xcd_copies);
-    const uint64_t need_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
+    uint64_t need_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
+    if (plan->terminal == TERM_PART) need_scratch = part_layout(plan).total;
     if (need_scratch) {
         if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
         if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
@@ -845,6 +923,36 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     p.counts = (unsigned long long*)counts;
     p.xcd_copies = plan->xcd_copies;
     p.xtab = plan->xcd_copies ? (unsigned long long*)scratch : nullptr;
+    PartParams pp;
+    std::memset(&pp, 0, sizeof pp);
+    if (plan->terminal == TERM_PART) {
+        const PartLayout L = part_layout(plan);
+        uint8_t* base = (uint8_t*)scratch;
+        p.region_count = (uint32_t*)(base + L.region_count);
+        p.rec_gid = (uint32_t*)(base + L.rec_gid);
+        p.rec_val = (long long*)(base + L.rec_val);
+        p.part_count = (uint32_t*)(base + L.part_count);
+        p.part_cap = (uint32_t)plan->part_cap;
+        p.part_shift = plan->part_shift;
+        p.n_parts = (uint32_t)plan->n_parts;
+        pp.n_groups = plan->n_groups;
+        pp.part_shift = plan->part_shift;
+        pp.n_parts = (uint32_t)plan->n_parts;
+        pp.n_regions = (uint32_t)plan->grid;
+        pp.part_cap = (uint32_t)plan->part_cap;
+        pp.region_count = p.region_count;
+        pp.rec_gid = p.rec_gid;
+        pp.rec_val = p.rec_val;
+        pp.part_count = p.part_count;
+        pp.part_start = (uint32_t*)(base + L.part_start);
+        pp.cursor = (uint32_t*)(base + L.cursor);
+        pp.chunk_start = (uint32_t*)(base + L.chunk_start);
+        pp.sorted_gid = (uint32_t*)(base + L.sorted_gid);
+        pp.sorted_val = (long long*)(base + L.sorted_val);
+        pp.sums = p.sums;
+        pp.counts = p.counts;
+        SDB_HIP(launch_fill_u32(p.part_count, (uint64_t)plan->n_parts, 0u, s), "partition count fill");
+    }
     if (q->n_fact > 0) {
         int grid = plan->grid;
         if (grid <= 0) {
@@ -853,6 +961,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         }
         SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, grid, plan->block, lds_bytes, s),
                 "fused kernel launch");
+        if (plan->terminal == TERM_PART) SDB_HIP(launch_part_passes(pp, s), "partition passes launch");
     }
     if (plan->xcd_copies)
         SDB_HIP(launch_xcd_merge((const unsigned long long*)scratch, plan->xcd_copies, plan->n_groups,

@@ -40,7 +40,12 @@ enum StageOp : int32_t {
 // How a table's code becomes part of the group id.
 enum GroupMode : int32_t { GK_NONE = 0, GK_ONE = 1, GK_GENERAL = 2 };
 enum LdsMode : int32_t { LDS_GLOBAL = SDB_LDS_GLOBAL, LDS_MAP = SDB_LDS_MAP, LDS_BITS = SDB_LDS_BITS };
-enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3 };
+enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3, TERM_PART = 4 };
+
+// Partitioned aggregation (TERM_PART): partition of group g is g >> part_shift.
+constexpr int kPartMaxParts = 4096;       // LDS histogram bins in the fused and scatter kernels
+constexpr int kPartMaxShift = 12;         // at most 4096 groups per partition (64 KB LDS table)
+constexpr int kPartChunk = 65536;         // records per aggregation work item
 
 // A literal comparison lowered to one unsigned range test over int32:
 // pass  <=>  ((uint32_t)(x - lo) <= span) != negate.
@@ -89,6 +94,15 @@ struct FusedParams {
     unsigned long long* sums;
     unsigned long long* counts;
     unsigned long long* xtab;  // interleaved {sum, count} x n_groups x xcd_copies
+    // TERM_PART: block b appends survivors to records [b * part_cap, (b+1) * part_cap)
+    uint32_t* region_count;    // records each block wrote
+    uint32_t* rec_gid;
+    long long* rec_val;
+    uint32_t* part_count;      // records per partition (global histogram)
+    uint32_t part_cap;
+    int32_t part_shift;
+    uint32_t n_parts;
+    uint32_t pad2_;
     StageDev st[kMaxStages];
 };
 
@@ -144,6 +158,26 @@ struct FinalizeParams {
     int64_t n_blocks;
 };
 
+// Scan, scatter and aggregation passes of TERM_PART (scratch layout in sdb_api.cpp).
+struct PartParams {
+    uint64_t n_groups;
+    int32_t part_shift;
+    uint32_t n_parts;
+    uint32_t n_regions;        // blocks of the fused kernel
+    uint32_t part_cap;
+    const uint32_t* region_count;
+    const uint32_t* rec_gid;
+    const long long* rec_val;
+    const uint32_t* part_count;
+    uint32_t* part_start;      // n_parts + 1 entries
+    uint32_t* cursor;          // n_parts
+    uint32_t* chunk_start;     // n_parts + 1 entries; [n_parts] = total work items
+    uint32_t* sorted_gid;
+    long long* sorted_val;
+    unsigned long long* sums;
+    unsigned long long* counts;
+};
+
 // ---- launchers (sdb_kernels.hip) -----------------------------------------
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s);
@@ -161,5 +195,6 @@ hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal,
 hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);
+hipError_t launch_part_passes(const PartParams& pp, hipStream_t s);
 
 }  // namespace sdb

@@ -424,6 +424,10 @@ struct TermState {
     unsigned long long* lsum = nullptr;   // LDS terminal
     unsigned long long* lcnt = nullptr;
     unsigned long long* xt = nullptr;     // global terminal: this XCD's interleaved copy, or null
+    uint32_t* lfill = nullptr;            // partitioned terminal: records this block appended
+    uint32_t* lhist = nullptr;            // partitioned terminal: records per partition
+    uint32_t* rgid = nullptr;             // this block's record region
+    long long* rval = nullptr;
 };
 
 template <int TERM>
@@ -541,7 +545,8 @@ __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)
 #pragma unroll
             for (int r = 0; r < W; ++r) {
                 h[jj][r] = hash_slot(S, x[j0 + jj][r]);
-                sl[jj][r] = tab[al[j0 + jj][r] ? h[jj][r] : 0u];
+                sl[jj][r] = 0ull;
+                if (al[j0 + jj][r]) sl[jj][r] = tab[h[jj][r]];
             }
 #pragma unroll
         for (int jj = 0; jj < HJ; ++jj)
@@ -640,6 +645,33 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
             ts.sum += al[j][r] ? (unsigned long long)v[j][r] : 0ull;
             ts.cnt += al[j][r] ? 1ull : 0ull;
         }
+    } else if constexpr (TERM == TERM_PART) {
+        // compact the wave's survivors into consecutive records of the block's region
+        unsigned long long m[IPT][W];
+        uint32_t total = 0;
+        SDB_ROWS(j, r) {
+            m[j][r] = __ballot(al[j][r]);
+            total += (uint32_t)__popcll(m[j][r]);
+        }
+        const uint32_t lane = threadIdx.x & 63u;
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(ts.lfill, total);
+        base = __shfl(base, 0, 64);
+        const unsigned long long below = (1ull << lane) - 1ull;
+        SDB_ROWS(j, r) {
+            const uint32_t pos = base + (uint32_t)__popcll(m[j][r] & below);
+            base += (uint32_t)__popcll(m[j][r]);
+            if (al[j][r]) {
+                if (pos < p.part_cap) {
+                    ts.rgid[pos] = gid[j][r];
+                    ts.rval[pos] = v[j][r];
+                    atomicAdd(&ts.lhist[gid[j][r] >> p.part_shift], 1u);
+                } else {   // region full: add straight into the group table
+                    atomicAdd(&p.sums[gid[j][r]], (unsigned long long)v[j][r]);
+                    atomicAdd(&p.counts[gid[j][r]], 1ull);
+                }
+            }
+        }
     } else {
         SDB_ROWS(j, r) if (al[j][r]) accumulate<TERM>(p, ts, gid[j][r], v[j][r]);
     }
@@ -662,6 +694,13 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
     if constexpr (TERM == TERM_GLOBAL) {
         if (p.xcd_copies > 0)
             ts.xt = p.xtab + 2ull * p.n_groups * (xcc_id() & (uint32_t)(p.xcd_copies - 1));
+    }
+    if constexpr (TERM == TERM_PART) {
+        ts.lfill = reinterpret_cast<uint32_t*>(lds);
+        ts.lhist = ts.lfill + 1;
+        for (uint32_t i = threadIdx.x; i < 1u + p.n_parts; i += blockDim.x) ts.lfill[i] = 0u;
+        ts.rgid = p.rec_gid + (uint64_t)blockIdx.x * p.part_cap;
+        ts.rval = p.rec_val + (uint64_t)blockIdx.x * p.part_cap;
     }
     // stage the LDS-resident dimension tables (16-byte copies; sources are padded)
     for (int s = 0; s < p.nstages; ++s) {
@@ -725,6 +764,11 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
                 atomicAdd(&p.counts[g], c);
             }
         }
+    } else if constexpr (TERM == TERM_PART) {
+        __syncthreads();
+        if (threadIdx.x == 0) p.region_count[blockIdx.x] = min(*ts.lfill, p.part_cap);
+        for (uint32_t q = threadIdx.x; q < p.n_parts; q += blockDim.x)
+            if (ts.lhist[q]) atomicAdd(&p.part_count[q], ts.lhist[q]);
     }
 }
 
@@ -764,6 +808,7 @@ static const void* pick_fused(int vector, int ipt, int terminal) {
         if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR>();    \
         if (terminal == TERM_LDS) return fused_fn<Wv, I, TERM_LDS>();          \
         if (terminal == TERM_GLOBAL) return fused_fn<Wv, I, TERM_GLOBAL>();    \
+        if (terminal == TERM_PART) return fused_fn<Wv, I, TERM_PART>();        \
     }
     if (vector) {
         SDB_PICK(4, 1)
@@ -793,6 +838,129 @@ hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal,
     if (!fn) return hipErrorInvalidValue;
     void* args[] = {const_cast<FusedParams*>(&p)};
     return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);
+}
+
+// ---------------------------------------------------------------------------
+// partitioned aggregation: scan, scatter by partition, LDS aggregation
+// ---------------------------------------------------------------------------
+
+// One block: exclusive scan of the partition counts into part_start (and the
+// scatter cursors), and of the per-partition work items into chunk_start.
+__global__ void __launch_bounds__(1024) part_scan_kernel(PartParams pp) {
+    __shared__ uint32_t buf_r[1024], buf_c[1024];
+    __shared__ uint32_t carry_r, carry_c;
+    if (threadIdx.x == 0) {
+        carry_r = 0u;
+        carry_c = 0u;
+    }
+    __syncthreads();
+    for (uint32_t base = 0; base < pp.n_parts; base += 1024u) {
+        const uint32_t i = base + threadIdx.x;
+        const uint32_t vr = i < pp.n_parts ? pp.part_count[i] : 0u;
+        const uint32_t vc = (vr + (uint32_t)kPartChunk - 1u) / (uint32_t)kPartChunk;
+        buf_r[threadIdx.x] = vr;
+        buf_c[threadIdx.x] = vc;
+        __syncthreads();
+        for (uint32_t off = 1; off < 1024u; off <<= 1) {
+            const uint32_t ar = threadIdx.x >= off ? buf_r[threadIdx.x - off] : 0u;
+            const uint32_t ac = threadIdx.x >= off ? buf_c[threadIdx.x - off] : 0u;
+            __syncthreads();
+            buf_r[threadIdx.x] += ar;
+            buf_c[threadIdx.x] += ac;
+            __syncthreads();
+        }
+        if (i < pp.n_parts) {
+            pp.part_start[i] = carry_r + buf_r[threadIdx.x] - vr;
+            pp.cursor[i] = carry_r + buf_r[threadIdx.x] - vr;
+            pp.chunk_start[i] = carry_c + buf_c[threadIdx.x] - vc;
+        }
+        __syncthreads();
+        if (threadIdx.x == 1023) {
+            carry_r += buf_r[1023];
+            carry_c += buf_c[1023];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        pp.part_start[pp.n_parts] = carry_r;
+        pp.chunk_start[pp.n_parts] = carry_c;
+    }
+}
+
+// One block per fused-kernel region: counting sort of the region's records
+// by partition into the partition-major record array.
+__global__ void __launch_bounds__(256) part_scatter_kernel(PartParams pp) {
+    extern __shared__ uint32_t lbin[];                 // n_parts counts, then n_parts bases
+    uint32_t* lcnt = lbin;
+    uint32_t* lbase = lbin + pp.n_parts;
+    for (uint32_t q = threadIdx.x; q < pp.n_parts; q += blockDim.x) lcnt[q] = 0u;
+    __syncthreads();
+    const uint32_t n = pp.region_count[blockIdx.x];
+    const uint32_t* g = pp.rec_gid + (uint64_t)blockIdx.x * pp.part_cap;
+    const long long* v = pp.rec_val + (uint64_t)blockIdx.x * pp.part_cap;
+    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) atomicAdd(&lcnt[g[i] >> pp.part_shift], 1u);
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < pp.n_parts; q += blockDim.x) {
+        const uint32_t c = lcnt[q];
+        lbase[q] = c ? atomicAdd(&pp.cursor[q], c) : 0u;
+        lcnt[q] = 0u;
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
+        const uint32_t gi = g[i];
+        const uint32_t q = gi >> pp.part_shift;
+        const uint32_t pos = lbase[q] + atomicAdd(&lcnt[q], 1u);
+        pp.sorted_gid[pos] = gi;
+        pp.sorted_val[pos] = v[i];
+    }
+}
+
+// Work item c covers up to kPartChunk records of one partition: sum them in
+// an LDS table of the partition's groups, then add the table to the outputs.
+__global__ void __launch_bounds__(256) part_agg_kernel(PartParams pp) {
+    extern __shared__ unsigned long long ltab[];       // groups of one partition: sums, then counts
+    const uint32_t gpp = 1u << pp.part_shift;
+    const uint32_t n_items = pp.chunk_start[pp.n_parts];
+    for (uint32_t c = blockIdx.x; c < n_items; c += gridDim.x) {
+        // partition holding work item c: last q with chunk_start[q] <= c
+        uint32_t lo = 0, hi = pp.n_parts;
+        while (hi - lo > 1u) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (pp.chunk_start[mid] <= c) lo = mid;
+            else hi = mid;
+        }
+        const uint32_t q = lo;
+        const uint32_t r0 = pp.part_start[q] + (c - pp.chunk_start[q]) * (uint32_t)kPartChunk;
+        const uint32_t r1 = min(r0 + (uint32_t)kPartChunk, pp.part_start[q + 1]);
+        for (uint32_t i = threadIdx.x; i < 2u * gpp; i += blockDim.x) ltab[i] = 0ull;
+        __syncthreads();
+        const uint32_t g0 = q << pp.part_shift;
+        for (uint32_t i = r0 + threadIdx.x; i < r1; i += blockDim.x) {
+            const uint32_t k = pp.sorted_gid[i] - g0;
+            atomicAdd(&ltab[k], (unsigned long long)pp.sorted_val[i]);
+            atomicAdd(&ltab[gpp + k], 1ull);
+        }
+        __syncthreads();
+        for (uint32_t k = threadIdx.x; k < gpp; k += blockDim.x) {
+            const unsigned long long cnt = ltab[gpp + k];
+            if (cnt) {
+                atomicAdd(&pp.sums[g0 + k], ltab[k]);
+                atomicAdd(&pp.counts[g0 + k], cnt);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_part_passes(const PartParams& pp, hipStream_t s) {
+    hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, pp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(part_scatter_kernel, dim3(pp.n_regions), dim3(256), (size_t)pp.n_parts * 8, s, pp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(part_agg_kernel, dim3(1024), dim3(256), (size_t)16u << pp.part_shift, s, pp);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

@@ -33,8 +33,8 @@ PLAN_SCRATCH_BYTES = 256
 OPS = {"eq": 0, "ne": 1, "lt": 2, "le": 3, "gt": 4, "ge": 5, "between": 6}
 TABLES = {"auto": 0, "dense": 1, "hash": 2}
 AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
-TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3}
-TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global"}
+TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3, "part": 4}
+TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global", 4: "part"}
 LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits"}
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
           4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
@@ -88,7 +88,8 @@ class SdbPlan(C.Structure):
                 ("stage_lds", i32 * MAX_STAGES), ("stage_defer", i32 * MAX_STAGES),
                 ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
                 ("vector", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
-                ("lds_bytes", i32), ("n_group_keys", i32),
+                ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
+                ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
                 ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64)]
 
@@ -423,6 +424,7 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
     return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
             "ipt": plan.ipt, "vector": plan.vector, "block": plan.block, "grid": plan.grid,
             "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
+            "n_parts": plan.n_parts, "part_cap": int(plan.part_cap),
             "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}

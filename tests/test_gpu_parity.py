@@ -210,3 +210,43 @@ def test_build_statistics_match_numpy():
     got = ws[256:256 + h.n_slots * 2].view(np.uint16)
     want = np.where(ok, part["brand"] - h.payload_min[0], 0xFFFF).astype(np.uint16)
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("name", ["c2_join_group", "c3_star3", "c4_star4_zipf", "c5_hash_stress", "c1_scalar_scan"])
+def test_partitioned_terminal(name):
+    w = workload(name)
+    want = oracle_rows(w)
+    got, q = run_gpu(w, force={"terminal": "part"})
+    assert q.plan_obj.terminal == 4
+    assert_same(got.as_rows(), want, f"{name} part")
+
+
+@pytest.mark.parametrize("cap", [64, 1024])
+def test_partitioned_terminal_region_overflow(cap):
+    """Records that do not fit a block's region go straight to the group table."""
+    from paper_2607_07632_amd import sdb
+    w = workload("c3_star3")
+    fact, dims = upload(w)
+    tables = sdb.build_dims(dims, w.dim_keys, w.query)
+    q = sdb.StarQuery(fact, tables, w.query, {"terminal": "part"})
+    plan = q.plan()
+    plan.part_cap = cap
+    plan.run_scratch_bytes = 0          # recomputed below from the smaller regions
+    sums, counts = q.alloc_outputs(plan)
+    import torch
+    scratch = torch.empty(1 << 26, dtype=torch.uint8, device="cuda")
+    q.run(sums, counts, plan=plan, scratch=scratch)
+    k, s, c, n, _ = q.finalize(sums, counts, plan=plan)
+    torch.cuda.synchronize()
+    m = int(n.item())
+    rows = [(tuple(int(x) for x in kk), int(ss), int(cc))
+            for kk, ss, cc in zip(k[:m].cpu().numpy(), s[:m].cpu().numpy(), c[:m].cpu().numpy())]
+    assert_same(rows, oracle_rows(w), f"overflow cap {cap}")
+
+
+@pytest.mark.parametrize("seed", [3, 11, 29, 41])
+def test_random_tiny_schemas_partitioned(seed):
+    w = random_tiny_workload(seed + 2000, max_fact=6000, max_dim_rows=500, n_fact=5003)
+    want = oracle_rows(w)
+    got, _ = run_gpu(w, force={"terminal": "part"})
+    assert_same(got.as_rows(), want, f"tiny {seed} part")
