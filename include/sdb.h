@@ -115,10 +115,11 @@ typedef struct sdb_dim_desc {
 /* A built lookup table: a plain handle into the caller's workspace.
  * A passing row's code is sum_p (payload_p - payload_min[p]) * payload_div[p]
  * with payload_div of the last payload 1; `domain` codes exist.
- *  DENSE: map[key - key_min] is the code (width bytes), or `sentinel` (all
- *         ones of the width) for a filtered row or a key no row holds; bit
- *         (key - key_min) of the bitmap `bits` (32-bit words) is set iff a
- *         passing row holds that key.
+ *  DENSE: map[key - key_min] is the code (width bytes) of a passing row,
+ *         `sentinel` (all ones of the width minus one) for a filtered row, or
+ *         all ones for a key no row holds, so a code >= sentinel means "no
+ *         passing row"; bit (key - key_min) of the bitmap `bits` (32-bit
+ *         words) is set iff a passing row holds that key.
  *  HASH:  n_slots = 2^hash_bits 8-byte slots {low 32 bits: key, high 32
  *         bits: code + 1, or 0xFFFFFFFF for a filtered row}; a slot with high
  *         half 0 is empty. Slot of key k starts at (k * 0x9E3779B1 mod 2^32)
@@ -254,8 +255,8 @@ SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n);
 
 /* Host only. Workspace bytes sdb_build_dim needs for `desc`: 256 bytes of
  * statistics, then the lookup table sized by an upper bound (a DENSE map of
- * max(2 * n_rows, 1024) 4-byte slots plus its occupancy and pass bitmaps,
- * and/or a HASH table of next_pow2(n_rows / load_factor) 8-byte slots). */
+ * max(2 * n_rows, 1024) 4-byte slots plus its pass bitmap, and/or a HASH
+ * table of next_pow2(n_rows / load_factor) 8-byte slots). */
 SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* bytes);
 
 /* Builds the lookup table for `desc` into `workspace` (device, 256-byte
@@ -263,9 +264,10 @@ SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* byt
  * `out` (host). Passes over the dimension rows: statistics (key range, pass
  * count, payload ranges), then the direct-mapped map (Section 3.3: one code
  * per key, the sentinel for filtered rows; 1, 2 or 4 bytes by payload domain)
- * or the open-addressing table (64-bit compare-and-swap inserts). Synchronizes
- * the stream twice (to read the statistics and the duplicate-key flag).
- * Errors: INVALID_ARG, UNSUPPORTED (payload domain >= 2^32 - 1), KEY_RANGE,
+ * and its pass bitmap, or the open-addressing table (64-bit compare-and-swap
+ * inserts). Synchronizes the stream twice (to read the statistics, then the
+ * duplicate-key check: a dense map must end with one occupied slot per row).
+ * Errors: INVALID_ARG, UNSUPPORTED (payload domain >= 2^32 - 2), KEY_RANGE,
  * WORKSPACE_TOO_SMALL, DUP_KEY, HIP_ERROR. */
 SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace,
                                  int64_t workspace_bytes, void* stream, sdb_dim* out);

@@ -122,9 +122,9 @@ uint64_t dense_slot_limit(int64_t n_rows) {
     return std::max<uint64_t>(2 * (uint64_t)n_rows, (uint64_t)kDenseSlack);
 }
 
-// map, occupancy bitmap, pass bitmap (each region 256-byte aligned)
+// map and pass bitmap (each region 256-byte aligned)
 uint64_t dense_bytes(uint64_t slots, int width) {
-    return align_up(slots * (uint64_t)width, 256) + 2 * align_up((slots + 31) / 32 * 4, 256);
+    return align_up(slots * (uint64_t)width, 256) + align_up((slots + 31) / 32 * 4, 256);
 }
 
 double effective_lf(const sdb_dim_desc* d) {
@@ -628,7 +628,7 @@ SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace, int6
         if (radix > 0xFFFFFFFFull) return fail(SDB_UNSUPPORTED, "payload %d spans more than 2^32 - 1 values", p);
         out->payload_radix[p] = (uint32_t)radix;
         domain *= radix;
-        if (domain >= 0xFFFFFFFFull) return fail(SDB_UNSUPPORTED, "payload domain reaches 2^32 - 1 codes");
+        if (domain >= 0xFFFFFFFEull) return fail(SDB_UNSUPPORTED, "payload domain reaches 2^32 - 2 codes");
     }
     out->domain = domain;
 
@@ -648,24 +648,22 @@ SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace, int6
     }
 
     if (kind == SDB_TABLE_DENSE) {
-        const int width = domain <= 0xFFull ? 1 : (domain <= 0xFFFFull ? 2 : 4);   // codes stay below the all-ones sentinel
-        const uint32_t sentinel = width == 1 ? 0xFFu : (width == 2 ? 0xFFFFu : 0xFFFFFFFFu);
+        // codes stay below the two reserved top values of the width
+        const int width = domain <= 0xFEull ? 1 : (domain <= 0xFFFEull ? 2 : 4);
+        const uint32_t missing = width == 1 ? 0xFFu : (width == 2 ? 0xFFFFu : 0xFFFFFFFFu);
         out->width = width;
-        out->sentinel = sentinel;
+        out->sentinel = missing - 1u;
         out->n_slots = range;
         const uint64_t map_bytes = align_up(range * width, 256);
-        const uint64_t bits_bytes = align_up((range + 31) / 32 * 4, 256);
-        uint32_t* occ = (uint32_t*)(table + map_bytes);
-        uint32_t* pass_bits = (uint32_t*)(table + map_bytes + bits_bytes);
+        uint32_t* pass_bits = (uint32_t*)(table + map_bytes);
         out->bits = pass_bits;
         bp.map = table;
-        bp.occ = occ;
         bp.pass_bits = pass_bits;
         bp.width = width;
         bp.nslots = range;
-        bp.sentinel = sentinel;
+        bp.sentinel = missing - 1u;
+        bp.missing = missing;
         SDB_HIP(launch_fill_u32((uint32_t*)table, map_bytes / 4, 0xFFFFFFFFu, s), "map fill");
-        SDB_HIP(launch_fill_u32(occ, 2 * bits_bytes / 4, 0u, s), "bitmap fill");
         SDB_HIP(launch_dense_scatter(bp, s), "dense scatter launch");
     } else {
         const uint64_t cap = hash_capacity(n, effective_lf(desc));
@@ -682,11 +680,14 @@ SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace, int6
         SDB_HIP(launch_fill_u32((uint32_t*)table, cap * 2, 0u, s), "hash table fill");
         SDB_HIP(launch_hash_insert(bp, s), "hash insert launch");
     }
-    uint32_t dup = 0;
-    SDB_HIP(hipMemcpyAsync(&dup, &dstats->dup, sizeof dup, hipMemcpyDeviceToHost, s), "flag copy");
+    DimStats fin;
+    SDB_HIP(hipMemcpyAsync(&fin, dstats, sizeof fin, hipMemcpyDeviceToHost, s), "flag copy");
     SDB_HIP(hipStreamSynchronize(s), "build sync");
-    if (dup & 1u) return fail(SDB_DUP_KEY, "dimension key column holds a duplicate key");
-    if (dup) return fail(SDB_HIP_ERROR, "dimension build inconsistency (flag %u)", dup);
+    if (fin.dup & 1u) return fail(SDB_DUP_KEY, "dimension key column holds a duplicate key");
+    if (kind == SDB_TABLE_DENSE && fin.occupied != (unsigned long long)n)
+        return fail(SDB_DUP_KEY, "dimension key column holds a duplicate key (%llu distinct keys in %lld rows)",
+                    (unsigned long long)fin.occupied, (long long)n);
+    if (fin.dup) return fail(SDB_HIP_ERROR, "dimension build inconsistency (flag %u)", fin.dup);
     return ok();
 }
 

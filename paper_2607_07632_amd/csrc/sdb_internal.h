@@ -114,7 +114,9 @@ struct DimStats {
     int32_t pmin[SDB_MAX_PAYLOADS];
     int32_t pmax[SDB_MAX_PAYLOADS];
     uint32_t dup;          // 1: duplicate key seen; 2: hash table full (cannot happen when sized)
-    uint32_t pad_[5];
+    uint32_t pad_;
+    unsigned long long occupied;   // dense: slots that some row holds
+    uint32_t pad2_[2];
 };
 static_assert(sizeof(DimStats) <= 256, "stats must fit the reserved 256 bytes");
 
@@ -131,12 +133,12 @@ struct BuildParams {
     uint32_t pdiv[SDB_MAX_PAYLOADS];
     DimStats* stats;
     void* map;                 // dense map or hash table
-    uint32_t* occ;             // dense occupancy bitmap
     uint32_t* pass_bits;       // dense pass bitmap
     int32_t width;
     int32_t kmin;
     uint64_t nslots;
-    uint32_t sentinel;
+    uint32_t sentinel;         // dense: code of a filtered row; codes >= sentinel mean "no passing row"
+    uint32_t missing;          // dense: code of a key no row holds (all ones)
     uint32_t hmask;
     int32_t hshift;
 };

@@ -80,7 +80,7 @@ __device__ __forceinline__ uint32_t hash_resolve(const StageDev& S, int32_t k, u
     for (uint32_t it = 0; it < S.nslots; ++it) {
         const uint32_t hi = (uint32_t)(slot >> 32);
         if (hi == 0u) return S.sentinel;                       // empty slot: key absent
-        if ((int32_t)(uint32_t)slot == k) return hi - 1u;      // filtered rows hold 0xFFFFFFFF -> sentinel
+        if ((int32_t)(uint32_t)slot == k) return hi - 1u;      // a filtered row holds 0xFFFFFFFF: the sentinel
         h = (h + 1u) & S.hmask;
         slot = tab[h];
     }
@@ -103,11 +103,11 @@ __device__ __forceinline__ bool stage_pass_one(const StageDev& S, int32_t x) {
     if (S.kind == ST_PRED) return range_pass(S.test, x);
     if (S.kind == ST_DENSE) {
         const uint32_t idx = (uint32_t)(x - S.kmin);
-        return idx < S.nslots && load_dense_code(S, idx) != S.sentinel;
+        return idx < S.nslots && load_dense_code(S, idx) < S.sentinel;
     }
     const uint32_t h = hash_slot(S, x);
     const unsigned long long* tab = static_cast<const unsigned long long*>(S.map);
-    return hash_resolve(S, x, h, tab[h]) != S.sentinel;
+    return hash_resolve(S, x, h, tab[h]) < S.sentinel;
 }
 
 // ---------------------------------------------------------------------------
@@ -177,6 +177,7 @@ __global__ void stats_init_kernel(DimStats* st) {
             st->pmax[p] = INT_MIN;
         }
         st->dup = 0u;
+        st->occupied = 0ull;
     }
 }
 
@@ -257,54 +258,53 @@ __device__ __forceinline__ uint32_t dim_row_code(const BuildParams& bp, int64_t 
     return c;
 }
 
-constexpr int kScatterRun = 32;   // consecutive dimension rows per thread in the dense scatter
-
-__device__ __forceinline__ void flush_bits(const BuildParams& bp, uint32_t word, uint32_t occ,
-                                           uint32_t pass) {
-    if (!occ) return;
-    const uint32_t old = atomicOr(&bp.occ[word], occ);
-    if (old & occ) atomicOr(&bp.stats->dup, 1u);
-    if (pass) atomicOr(&bp.pass_bits[word], pass);
+// Direct-mapped map over the keys [kmin, kmin + nslots): the fill leaves
+// every slot at `missing` (all ones: no row holds the key); a passing row then
+// stores its code and a filtered row the sentinel (`missing` - 1). Plain
+// stores, no atomics: each key owns its slot.
+__global__ void __launch_bounds__(256) dense_scatter_kernel(BuildParams bp) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
+        const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
+        if ((uint64_t)idx >= bp.nslots) {          // cannot happen: kmin/kmax cover all keys
+            atomicOr(&bp.stats->dup, 4u);
+            continue;
+        }
+        const uint32_t c = dim_row_passes(bp, i) ? dim_row_code(bp, i) : bp.sentinel;
+        if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx] = (uint8_t)c;
+        else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx] = (uint16_t)c;
+        else static_cast<uint32_t*>(bp.map)[idx] = c;
+    }
 }
 
-// Direct-mapped map: one entry per key in [kmin, kmin + nslots); a passing row
-// stores its code, a filtered row (and every key no row holds, from the fill)
-// the all-ones sentinel. One occupancy bit per slot detects duplicate keys and
-// one pass bit per slot forms the filter bitmap. A thread walks a run of
-// consecutive rows and merges their bits per 32-bit word before one atomic OR,
-// so dense keys stored in key order cost one atomic per 32 rows.
-__global__ void __launch_bounds__(256) dense_scatter_kernel(BuildParams bp) {
-    const int64_t n_runs = (bp.n + kScatterRun - 1) / kScatterRun;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t run = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; run < n_runs; run += stride) {
-        const int64_t r0 = run * kScatterRun;
-        const int64_t r1 = min(r0 + kScatterRun, bp.n);
-        uint32_t cur = 0xFFFFFFFFu, occ = 0u, pass = 0u;
-        for (int64_t i = r0; i < r1; ++i) {
-            const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
-            if ((uint64_t)idx >= bp.nslots) {      // cannot happen: kmin/kmax cover all keys
-                atomicOr(&bp.stats->dup, 4u);
-                continue;
-            }
-            const uint32_t word = idx >> 5, bit = 1u << (idx & 31u);
-            if (word != cur) {
-                flush_bits(bp, cur, occ, pass);
-                cur = word;
-                occ = 0u;
-                pass = 0u;
-            }
-            if (occ & bit) atomicOr(&bp.stats->dup, 1u);
-            occ |= bit;
-            uint32_t c = bp.sentinel;
-            if (dim_row_passes(bp, i)) {
-                c = dim_row_code(bp, i);
-                pass |= bit;
-            }
-            if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx] = (uint8_t)c;
-            else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx] = (uint16_t)c;
-            else static_cast<uint32_t*>(bp.map)[idx] = c;
+// One thread per 32 slots: the pass bitmap word (code below the sentinel)
+// and the number of occupied slots. Distinct keys occupy n slots; a duplicate
+// key leaves fewer, which the host detects from the total.
+__global__ void __launch_bounds__(256) dense_bits_kernel(BuildParams bp) {
+    const uint64_t n_words = (bp.nslots + 31) / 32;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    unsigned long long occupied = 0;
+    for (uint64_t w = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; w < n_words; w += stride) {
+        uint32_t bits = 0u;
+        for (uint32_t b = 0; b < 32u; ++b) {
+            const uint64_t slot = w * 32 + b;
+            if (slot >= bp.nslots) break;
+            uint32_t c;
+            if (bp.width == 1) c = static_cast<const uint8_t*>(bp.map)[slot];
+            else if (bp.width == 2) c = static_cast<const uint16_t*>(bp.map)[slot];
+            else c = static_cast<const uint32_t*>(bp.map)[slot];
+            if (c < bp.sentinel) bits |= 1u << b;
+            occupied += c != bp.missing;
         }
-        flush_bits(bp, cur, occ, pass);
+        bp.pass_bits[w] = bits;
+    }
+    occupied = wave_sum_u64(occupied);
+    __shared__ unsigned long long s_occ[4];
+    if ((threadIdx.x & 63) == 0) s_occ[threadIdx.x >> 6] = occupied;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned long long t = s_occ[0] + s_occ[1] + s_occ[2] + s_occ[3];
+        if (t) atomicAdd(&bp.stats->occupied, t);
     }
 }
 
@@ -337,7 +337,7 @@ __global__ void __launch_bounds__(256) hash_insert_kernel(BuildParams bp) {
 
 static int build_grid(int64_t n) {
     int64_t g = (n + 255) / 256;
-    if (g > 1024) g = 1024;
+    if (g > 2048) g = 2048;
     if (g < 1) g = 1;
     return (int)g;
 }
@@ -346,14 +346,19 @@ hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s) {
     hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, s, bp.stats);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || bp.n == 0) return e;
-    hipLaunchKernelGGL(dim_stats_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+    // few blocks: every block ends with one set of atomics on the same words
+    int g = build_grid(bp.n);
+    if (g > 256) g = 256;
+    hipLaunchKernelGGL(dim_stats_kernel, dim3(g), dim3(256), 0, s, bp);
     return hipGetLastError();
 }
 
 hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s) {
     if (bp.n == 0) return hipSuccess;
-    hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid((bp.n + kScatterRun - 1) / kScatterRun)),
-                       dim3(256), 0, s, bp);
+    hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(dense_bits_kernel, dim3(build_grid((int64_t)((bp.nslots + 31) / 32))), dim3(256), 0, s, bp);
     return hipGetLastError();
 }
 
@@ -499,7 +504,7 @@ __device__ __forceinline__ void stage_map(const StageDev& S, const unsigned char
         c[j][r] = ld_code<WB>(base, ok ? idx : 0u);
         al[j][r] = ok;
     }
-    SDB_ROWS(j, r) al[j][r] = al[j][r] && c[j][r] != S.sentinel;
+    SDB_ROWS(j, r) al[j][r] = al[j][r] && c[j][r] < S.sentinel;
     add_group<W, IPT>(S, c, gid);
 }
 
@@ -554,7 +559,7 @@ __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)
             for (int r = 0; r < W; ++r) {
                 uint32_t c = S.sentinel;
                 if (al[j0 + jj][r]) c = hash_resolve(S, x[j0 + jj][r], h[jj][r], sl[jj][r]);
-                al[j0 + jj][r] = al[j0 + jj][r] && c != S.sentinel;
+                al[j0 + jj][r] = al[j0 + jj][r] && c < S.sentinel;
                 if (S.gk_mode == GK_ONE) gid[j0 + jj][r] += c * S.gk_stride[0];
                 else if (S.gk_mode == GK_GENERAL) gid[j0 + jj][r] += code_contribution(S, c);
             }

@@ -62,8 +62,8 @@ def _desc(n_rows=1000, kind="auto", n_cols=2, lf=0.0):
 
 def test_required_bytes_bounds():
     dense = sdb.dim_required_bytes(_desc(1000, "dense"))
-    # stats + 2000 slots x 4 B + occupancy and pass bitmaps
-    assert dense == 256 + 8192 + 2 * 256
+    # stats + 2000 slots x 4 B + pass bitmap
+    assert dense == 256 + 8192 + 256
     h = sdb.dim_required_bytes(_desc(1000, "hash"))
     assert h == 256 + 2048 * 8
     a = sdb.dim_required_bytes(_desc(1000, "auto"))

@@ -204,12 +204,18 @@ def test_build_statistics_match_numpy():
     assert h.n_pass == int(ok.sum()) and h.kind == 1 and h.width == 2
     assert h.payload_min[0] == part["brand"][ok].min()
     assert h.payload_radix[0] == part["brand"][ok].max() - part["brand"][ok].min() + 1
-    # the map itself: the sentinel for filtered rows, brand - min otherwise
+    # the map itself: the sentinel (0xFFFE) for filtered rows, brand - min otherwise
+    assert h.sentinel == 0xFFFE
     torch.cuda.synchronize()
     ws = t.workspace.cpu().numpy()
     got = ws[256:256 + h.n_slots * 2].view(np.uint16)
-    want = np.where(ok, part["brand"] - h.payload_min[0], 0xFFFF).astype(np.uint16)
+    want = np.where(ok, part["brand"] - h.payload_min[0], 0xFFFE).astype(np.uint16)
     assert np.array_equal(got, want)
+    # and its pass bitmap
+    bits_off = h.bits - t.workspace.data_ptr()
+    words = ws[bits_off:bits_off + (h.n_slots + 31) // 32 * 4].view(np.uint32)
+    unpacked = np.unpackbits(words.view(np.uint8), bitorder="little")[:h.n_slots].astype(bool)
+    assert np.array_equal(unpacked, ok)
 
 
 @pytest.mark.parametrize("name", ["c2_join_group", "c3_star3", "c4_star4_zipf", "c5_hash_stress", "c1_scalar_scan"])
