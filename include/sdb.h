@@ -34,7 +34,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 2
+#define SDB_ABI_VERSION 3
 
 typedef enum sdb_status {
     SDB_OK = 0,

@@ -461,6 +461,10 @@ uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
     return (uint32_t)off;
 }
 
+int stage_column(const sdb_query* q, const sdb_plan* plan, int s) {
+    return plan->stage_kind[s] == 0 ? q->preds[plan->stage_index[s]].col : q->joins[plan->stage_index[s]].fact_key_col;
+}
+
 FusedParams fused_params(const sdb_query* q, const sdb_plan* plan, bool placed) {
     FusedParams p;
     std::memset(&p, 0, sizeof p);
@@ -482,28 +486,36 @@ FusedParams fused_params(const sdb_query* q, const sdb_plan* plan, bool placed) 
 
 // Every column the fused kernel reads: stage columns and aggregate operands.
 bool columns_aligned(const sdb_query* q, const sdb_plan* plan) {
-    for (int s = 0; s < plan->n_stages; ++s) {
-        const int col = plan->stage_kind[s] == 0 ? q->preds[plan->stage_index[s]].col
-                                                 : q->joins[plan->stage_index[s]].fact_key_col;
-        if (!aligned16(q->cols[col])) return false;
-    }
+    for (int s = 0; s < plan->n_stages; ++s)
+        if (!aligned16(q->cols[stage_column(q, plan, s)])) return false;
     if (!aligned16(q->cols[q->agg.a])) return false;
     if (q->agg.kind != SDB_AGG_COL && !aligned16(q->cols[q->agg.b])) return false;
     return true;
 }
 
 constexpr int kDefaultIpt = 2;
+// group tables from this size on (16 bytes a group, 8 XCD copies: 8 MiB) go
+// to the partitioned terminal when at least a million rows survive
+constexpr uint64_t kPartMinGroups = 65536;
+
+// Partitioned-terminal records carry 64-bit values only when the aggregate
+// combines two columns; a single int32 column's values fit 32 bits.
+bool records_wide(const sdb_query* q) { return q->agg.kind != SDB_AGG_COL; }
 
 // Run-scratch layout of the partitioned terminal.
 struct PartLayout {
-    uint64_t region_count, part_count, part_start, cursor, chunk_start, rec_gid, rec_val, sorted_gid,
-        sorted_val, total;
+    uint64_t region_count, part_count, part_start, chunk_start, part_hist, rec_gid, rec_val, sorted_gid,
+        sorted_val, item_sum, item_cnt, total;
 };
 
-PartLayout part_layout(const sdb_plan* plan) {
+PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
     PartLayout L;
     const uint64_t grid = (uint64_t)plan->grid, P = (uint64_t)plan->n_parts;
     const uint64_t recs = grid * (uint64_t)plan->part_cap;
+    const uint64_t vbytes = records_wide(q) ? 8 : 4;
+    // aggregation work items: at most one partial chunk per partition plus full chunks
+    const uint64_t items = P + recs / (uint64_t)kPartChunk;
+    const uint64_t gpp = 1ull << plan->part_shift;
     uint64_t off = 0;
     auto take = [&](uint64_t bytes) {
         const uint64_t at = off;
@@ -513,14 +525,27 @@ PartLayout part_layout(const sdb_plan* plan) {
     L.region_count = take(grid * 4);
     L.part_count = take(P * 4);
     L.part_start = take((P + 1) * 4);
-    L.cursor = take(P * 4);
     L.chunk_start = take((P + 1) * 4);
+    L.part_hist = take(P * grid * 4);
     L.rec_gid = take(recs * 4);
-    L.rec_val = take(recs * 8);
+    L.rec_val = take(recs * vbytes);
     L.sorted_gid = take(recs * 4);
-    L.sorted_val = take(recs * 8);
+    L.sorted_val = take(recs * vbytes);
+    L.item_sum = take(items * gpp * 8);
+    L.item_cnt = take(items * gpp * 4);
     L.total = off;
     return L;
+}
+
+// Dynamic LDS of a fused-kernel launch: the plan's layout, then (partitioned
+// terminal) one record ring per wave.
+uint32_t ring_lds_bytes(const sdb_query* q, const sdb_plan* plan) {
+    if (plan->terminal != TERM_PART) return 0u;
+    return (uint32_t)(plan->block / 64) * kRingEntries * (records_wide(q) ? 12u : 8u);
+}
+
+uint32_t launch_lds_bytes(const sdb_query* q, const sdb_plan* plan) {
+    return (uint32_t)plan->lds_bytes + ring_lds_bytes(q, plan);
 }
 
 sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) {
@@ -536,8 +561,12 @@ sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) 
     DeviceInfo di;
     sdb_status st = device_info(&di);
     if (st != SDB_OK) return st;
-    int per_cu = fused_blocks_per_cu(plan->vector, plan->ipt, plan->terminal, plan->block, (size_t)plan->lds_bytes);
+    int per_cu = fused_blocks_per_cu(plan->vector, plan->ipt, plan->terminal, plan->block,
+                                     (size_t)launch_lds_bytes(q, plan));
     if (per_cu <= 0) return fail(SDB_HIP_ERROR, "occupancy query failed for the fused kernel");
+    // partitioned terminal: measured fastest at 4 resident blocks per CU (its
+    // record rings make a fifth block per CU slower, not faster)
+    if (plan->terminal == TERM_PART && plan->block <= 256) per_cu = std::min(per_cu, 4);
     const int64_t full = (int64_t)di.cus * per_cu;
     *grid_out = (int)std::min<int64_t>(tiles, full);
     return SDB_OK;
@@ -785,14 +814,17 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     for (int s = 0; s < n; ++s) f *= plan->stage_pass[s];
     const double survivors = f * (double)q->n_fact;
     if (term == TERM_GLOBAL || term == TERM_PART) {
-        int shift = 8;
-        while (shift < kPartMaxShift && (plan->n_groups >> shift) > 512) ++shift;
+        // the largest partitions the LDS table holds: long runs in the scatter
+        int shift = 0;
+        while (shift < kPartMaxShift && (1ull << shift) < plan->n_groups) ++shift;
         const uint64_t parts = (plan->n_groups + (1ull << shift) - 1) >> shift;
         const bool fits = parts <= (uint64_t)kPartMaxParts;
-        // chosen automatically only where its passes beat direct atomics (many
-        // survivors per group; measured on c5, not yet on c3's 55 per group)
-        bool part = term == TERM_PART || (q->force_terminal == SDB_TERMINAL_AUTO && fits && q->n_fact > 0 &&
-                                          survivors >= 1.0e6 && survivors >= 512.0 * (double)plan->n_groups);
+        // chosen automatically for many survivors into a group table too large
+        // for the L2s to hold its per-XCD copies, or many survivors per group
+        const bool big_table = plan->n_groups >= kPartMinGroups;
+        bool part = term == TERM_PART ||
+                    (q->force_terminal == SDB_TERMINAL_AUTO && fits && q->n_fact > 0 && survivors >= 1.0e6 &&
+                     (big_table || survivors >= 512.0 * (double)plan->n_groups));
         if (part && !fits)
             return fail(SDB_CAPACITY, "partitioned terminal needs at most %d partitions of %d groups",
                         kPartMaxParts, 1 << kPartMaxShift);
@@ -826,7 +858,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         plan->part_cap = (int64_t)align_up((uint64_t)std::max<int64_t>(plan->part_cap, 64), 64);
         if ((uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFF0ull)
             plan->part_cap = (int64_t)(0xFFFFFFF0ull / (uint64_t)plan->grid) / 64 * 64;
-        plan->run_scratch_bytes = (int64_t)part_layout(plan).total;
+        plan->run_scratch_bytes = (int64_t)part_layout(q, plan).total;
     }
     return ok();
 }
@@ -898,7 +930,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     if (plan->xcd_copies != 0 && (plan->xcd_copies != kXcdCopies || plan->terminal != TERM_GLOBAL))
         return fail(SDB_INVALID_ARG, "bad plan xcd_copies %d", plan->xcd_copies);
     uint64_t need_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
-    if (plan->terminal == TERM_PART) need_scratch = part_layout(plan).total;
+    if (plan->terminal == TERM_PART) need_scratch = part_layout(q, plan).total;
     if (need_scratch) {
         if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
         if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
@@ -908,10 +940,11 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     }
 
     FusedParams p = fused_params(q, plan, true);
-    const uint32_t lds_bytes = lds_layout(q, plan, nullptr);
-    if ((int64_t)lds_bytes != (int64_t)plan->lds_bytes)
+    if ((int64_t)lds_layout(q, plan, nullptr) != (int64_t)plan->lds_bytes)
         return fail(SDB_INVALID_ARG, "plan LDS size does not match the tables");
+    const uint32_t lds_bytes = launch_lds_bytes(q, plan);
     if (lds_bytes > 160u * 1024u) return fail(SDB_UNSUPPORTED, "plan needs %u bytes of LDS", lds_bytes);
+    p.ring_off = (uint32_t)plan->lds_bytes;
 
     hipStream_t s = (hipStream_t)stream;
     if (plan->xcd_copies) {
@@ -927,12 +960,13 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     PartParams pp;
     std::memset(&pp, 0, sizeof pp);
     if (plan->terminal == TERM_PART) {
-        const PartLayout L = part_layout(plan);
+        const PartLayout L = part_layout(q, plan);
         uint8_t* base = (uint8_t*)scratch;
         p.region_count = (uint32_t*)(base + L.region_count);
         p.rec_gid = (uint32_t*)(base + L.rec_gid);
-        p.rec_val = (long long*)(base + L.rec_val);
-        p.part_count = (uint32_t*)(base + L.part_count);
+        p.rec_val = base + L.rec_val;
+        p.rec_wide = records_wide(q) ? 1 : 0;
+        p.part_hist = (uint32_t*)(base + L.part_hist);
         p.part_cap = (uint32_t)plan->part_cap;
         p.part_shift = plan->part_shift;
         p.n_parts = (uint32_t)plan->n_parts;
@@ -944,15 +978,17 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         pp.region_count = p.region_count;
         pp.rec_gid = p.rec_gid;
         pp.rec_val = p.rec_val;
-        pp.part_count = p.part_count;
+        pp.rec_wide = p.rec_wide;
+        pp.part_hist = p.part_hist;
+        pp.part_count = (uint32_t*)(base + L.part_count);
         pp.part_start = (uint32_t*)(base + L.part_start);
-        pp.cursor = (uint32_t*)(base + L.cursor);
         pp.chunk_start = (uint32_t*)(base + L.chunk_start);
         pp.sorted_gid = (uint32_t*)(base + L.sorted_gid);
-        pp.sorted_val = (long long*)(base + L.sorted_val);
+        pp.sorted_val = base + L.sorted_val;
+        pp.item_sum = (unsigned long long*)(base + L.item_sum);
+        pp.item_cnt = (uint32_t*)(base + L.item_cnt);
         pp.sums = p.sums;
         pp.counts = p.counts;
-        SDB_HIP(launch_fill_u32(p.part_count, (uint64_t)plan->n_parts, 0u, s), "partition count fill");
     }
     if (q->n_fact > 0) {
         int grid = plan->grid;

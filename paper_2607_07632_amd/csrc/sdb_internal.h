@@ -46,6 +46,8 @@ enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3, TERM_P
 constexpr int kPartMaxParts = 4096;       // LDS histogram bins in the fused and scatter kernels
 constexpr int kPartMaxShift = 12;         // at most 4096 groups per partition (64 KB LDS table)
 constexpr int kPartChunk = 65536;         // records per aggregation work item
+constexpr int kScatterChunk = 4096;       // records one scatter block sorts in LDS at a time
+constexpr uint32_t kRingEntries = 128;     // fused kernel: per-wave record ring (group id + value)
 
 // A literal comparison lowered to one unsigned range test over int32:
 // pass  <=>  ((uint32_t)(x - lo) <= span) != negate.
@@ -97,12 +99,14 @@ struct FusedParams {
     // TERM_PART: block b appends survivors to records [b * part_cap, (b+1) * part_cap)
     uint32_t* region_count;    // records each block wrote
     uint32_t* rec_gid;
-    long long* rec_val;
-    uint32_t* part_count;      // records per partition (global histogram)
+    void* rec_val;             // int64 values if rec_wide, else int32
+    uint32_t* part_hist;       // records per (partition, block): [q * gridDim.x + block]
     uint32_t part_cap;
     int32_t part_shift;
     uint32_t n_parts;
-    uint32_t pad2_;
+    uint32_t ring_off;         // byte offset of the per-wave record rings in dynamic LDS
+    int32_t rec_wide;          // 1: record values need 64 bits (aggregate of two columns)
+    int32_t pad3_;
     StageDev st[kMaxStages];
 };
 
@@ -169,13 +173,17 @@ struct PartParams {
     uint32_t part_cap;
     const uint32_t* region_count;
     const uint32_t* rec_gid;
-    const long long* rec_val;
-    const uint32_t* part_count;
+    const void* rec_val;
+    int32_t rec_wide;
+    uint32_t pad_;
+    uint32_t* part_hist;       // [q * n_regions + b]: counts, then exclusive offsets within partition q
+    uint32_t* part_count;      // records per partition
     uint32_t* part_start;      // n_parts + 1 entries
-    uint32_t* cursor;          // n_parts
     uint32_t* chunk_start;     // n_parts + 1 entries; [n_parts] = total work items
     uint32_t* sorted_gid;
-    long long* sorted_val;
+    void* sorted_val;
+    unsigned long long* item_sum;   // per work item partial tables: [item * groups per partition + k]
+    uint32_t* item_cnt;
     unsigned long long* sums;
     unsigned long long* counts;
 };

@@ -429,11 +429,49 @@ struct TermState {
     unsigned long long* lsum = nullptr;   // LDS terminal
     unsigned long long* lcnt = nullptr;
     unsigned long long* xt = nullptr;     // global terminal: this XCD's interleaved copy, or null
-    uint32_t* lfill = nullptr;            // partitioned terminal: records this block appended
-    uint32_t* lhist = nullptr;            // partitioned terminal: records per partition
+    // partitioned terminal: survivors collect in a per-wave LDS ring and leave
+    // in 64-record flushes to this block's region (full coalesced stores)
+    uint32_t* lfill = nullptr;            // records this block claimed in its region
+    uint32_t* lhist = nullptr;            // records per partition in the region
+    uint32_t* ring_gid = nullptr;         // this wave's ring (kRing entries)
+    void* ring_val = nullptr;             // int64 values (FusedParams::rec_wide) or int32
+    uint32_t head = 0;                    // ring index of the oldest pending record (wave-uniform)
+    uint32_t pend = 0;                    // pending records (wave-uniform, < kRing)
     uint32_t* rgid = nullptr;             // this block's record region
-    long long* rval = nullptr;
+    void* rval = nullptr;
 };
+
+constexpr uint32_t kRing = 128;   // per-wave ring entries: < 64 pending + one 64-lane step
+static_assert(kRing == kRingEntries, "ring layout");
+
+// Writes `cnt` (<= 64) pending ring records to the block's region, one per
+// lane; records past the region's capacity go straight into the group table.
+__device__ __forceinline__ void part_flush(const FusedParams& p, TermState<TERM_PART>& ts, uint32_t cnt) {
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t lane = threadIdx.x & 63u;
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(ts.lfill, cnt);
+    base = __shfl(base, 0, 64);
+    if (lane < cnt) {
+        const uint32_t slot = (ts.head + lane) & (kRing - 1u);
+        const uint32_t g = ts.ring_gid[slot];
+        const long long v = p.rec_wide ? static_cast<const long long*>(ts.ring_val)[slot]
+                                       : (long long)static_cast<const int32_t*>(ts.ring_val)[slot];
+        const uint32_t pos = base + lane;
+        if (pos < p.part_cap) {
+            ts.rgid[pos] = g;
+            if (p.rec_wide) static_cast<long long*>(ts.rval)[pos] = v;
+            else static_cast<int32_t*>(ts.rval)[pos] = (int32_t)v;
+            atomicAdd(&ts.lhist[g >> p.part_shift], 1u);
+        } else {
+            atomicAdd(&p.sums[g], (unsigned long long)v);
+            atomicAdd(&p.counts[g], 1ull);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    ts.head = (ts.head + cnt) & (kRing - 1u);
+    ts.pend -= cnt;
+}
 
 template <int TERM>
 __device__ __forceinline__ void accumulate(const FusedParams& p, TermState<TERM>& ts, uint32_t g,
@@ -651,31 +689,19 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
             ts.cnt += al[j][r] ? 1ull : 0ull;
         }
     } else if constexpr (TERM == TERM_PART) {
-        // compact the wave's survivors into consecutive records of the block's region
-        unsigned long long m[IPT][W];
-        uint32_t total = 0;
-        SDB_ROWS(j, r) {
-            m[j][r] = __ballot(al[j][r]);
-            total += (uint32_t)__popcll(m[j][r]);
-        }
+        // append the wave's survivors to its ring; flush every full 64
         const uint32_t lane = threadIdx.x & 63u;
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(ts.lfill, total);
-        base = __shfl(base, 0, 64);
         const unsigned long long below = (1ull << lane) - 1ull;
         SDB_ROWS(j, r) {
-            const uint32_t pos = base + (uint32_t)__popcll(m[j][r] & below);
-            base += (uint32_t)__popcll(m[j][r]);
+            const unsigned long long m = __ballot(al[j][r]);
             if (al[j][r]) {
-                if (pos < p.part_cap) {
-                    ts.rgid[pos] = gid[j][r];
-                    ts.rval[pos] = v[j][r];
-                    atomicAdd(&ts.lhist[gid[j][r] >> p.part_shift], 1u);
-                } else {   // region full: add straight into the group table
-                    atomicAdd(&p.sums[gid[j][r]], (unsigned long long)v[j][r]);
-                    atomicAdd(&p.counts[gid[j][r]], 1ull);
-                }
+                const uint32_t slot = (ts.head + ts.pend + (uint32_t)__popcll(m & below)) & (kRing - 1u);
+                ts.ring_gid[slot] = gid[j][r];
+                if (p.rec_wide) static_cast<long long*>(ts.ring_val)[slot] = v[j][r];
+                else static_cast<int32_t*>(ts.ring_val)[slot] = (int32_t)v[j][r];
             }
+            ts.pend += (uint32_t)__popcll(m);
+            if (ts.pend >= 64u) part_flush(p, ts, 64u);
         }
     } else {
         SDB_ROWS(j, r) if (al[j][r]) accumulate<TERM>(p, ts, gid[j][r], v[j][r]);
@@ -704,8 +730,14 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
         ts.lfill = reinterpret_cast<uint32_t*>(lds);
         ts.lhist = ts.lfill + 1;
         for (uint32_t i = threadIdx.x; i < 1u + p.n_parts; i += blockDim.x) ts.lfill[i] = 0u;
+        // rings: every wave's values, then every wave's group ids
+        const uint32_t wave = threadIdx.x >> 6;
+        const uint32_t vbytes = p.rec_wide ? 8u : 4u;
+        ts.ring_val = lds + p.ring_off + (size_t)wave * kRing * vbytes;
+        ts.ring_gid = reinterpret_cast<uint32_t*>(lds + p.ring_off + (blockDim.x >> 6) * kRing * vbytes) +
+                      (size_t)wave * kRing;
         ts.rgid = p.rec_gid + (uint64_t)blockIdx.x * p.part_cap;
-        ts.rval = p.rec_val + (uint64_t)blockIdx.x * p.part_cap;
+        ts.rval = static_cast<unsigned char*>(p.rec_val) + (uint64_t)blockIdx.x * p.part_cap * vbytes;
     }
     // stage the LDS-resident dimension tables (16-byte copies; sources are padded)
     for (int s = 0; s < p.nstages; ++s) {
@@ -770,10 +802,12 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
             }
         }
     } else if constexpr (TERM == TERM_PART) {
+        if (ts.pend) part_flush(p, ts, ts.pend);
         __syncthreads();
         if (threadIdx.x == 0) p.region_count[blockIdx.x] = min(*ts.lfill, p.part_cap);
+        // this block's column of the partition x block histogram
         for (uint32_t q = threadIdx.x; q < p.n_parts; q += blockDim.x)
-            if (ts.lhist[q]) atomicAdd(&p.part_count[q], ts.lhist[q]);
+            p.part_hist[(uint64_t)q * gridDim.x + blockIdx.x] = ts.lhist[q];
     }
 }
 
@@ -807,6 +841,7 @@ static const void* fused_fn() {
     return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM>);
 }
 
+// Instances: 4-row or 1-row items, 1/2/4 items per lane, every terminal.
 static const void* pick_fused(int vector, int ipt, int terminal) {
 #define SDB_PICK(Wv, I)                                                        \
     if (ipt == I) {                                                            \
@@ -849,8 +884,8 @@ hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal,
 // partitioned aggregation: scan, scatter by partition, LDS aggregation
 // ---------------------------------------------------------------------------
 
-// One block: exclusive scan of the partition counts into part_start (and the
-// scatter cursors), and of the per-partition work items into chunk_start.
+// One block: exclusive scan of the partition counts into part_start, and of
+// the per-partition work items into chunk_start.
 __global__ void __launch_bounds__(1024) part_scan_kernel(PartParams pp) {
     __shared__ uint32_t buf_r[1024], buf_c[1024];
     __shared__ uint32_t carry_r, carry_c;
@@ -876,7 +911,6 @@ __global__ void __launch_bounds__(1024) part_scan_kernel(PartParams pp) {
         }
         if (i < pp.n_parts) {
             pp.part_start[i] = carry_r + buf_r[threadIdx.x] - vr;
-            pp.cursor[i] = carry_r + buf_r[threadIdx.x] - vr;
             pp.chunk_start[i] = carry_c + buf_c[threadIdx.x] - vc;
         }
         __syncthreads();
@@ -892,39 +926,143 @@ __global__ void __launch_bounds__(1024) part_scan_kernel(PartParams pp) {
     }
 }
 
-// One block per fused-kernel region: counting sort of the region's records
-// by partition into the partition-major record array.
+// Exclusive scan of n values by a 256-thread block: out[i] = carry + sum of
+// in[0..i). in and out may be the same array (each thread reads its own run
+// before writing it). Every thread must call it; returns the sum of in[0..n).
+__device__ uint32_t block_scan_256(const uint32_t* in, uint32_t* out, uint32_t n, uint32_t carry,
+                                   uint32_t* wtmp) {
+    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+    const uint32_t per = (n + 255u) / 256u;
+    const uint32_t b0 = threadIdx.x * per;
+    uint32_t loc = 0;
+    for (uint32_t k = 0; k < per; ++k)
+        if (b0 + k < n) loc += in[b0 + k];
+    uint32_t x = loc;
+    for (uint32_t off = 1; off < 64u; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63u) wtmp[wave] = x;
+    __syncthreads();
+    uint32_t before = 0, total = 0;
+    for (uint32_t w = 0; w < 4u; ++w) {
+        const uint32_t t = wtmp[w];
+        if (w < wave) before += t;
+        total += t;
+    }
+    uint32_t run = carry + before + x - loc;
+    for (uint32_t k = 0; k < per; ++k)
+        if (b0 + k < n) {
+            const uint32_t v = in[b0 + k];
+            out[b0 + k] = run;
+            run += v;
+        }
+    __syncthreads();
+    return total;
+}
+
+// One block per partition q: the fused kernel's per-block counts of q become
+// exclusive offsets within q (in place); their sum is q's record count.
+__global__ void __launch_bounds__(256) part_offsets_kernel(PartParams pp) {
+    __shared__ uint32_t wtmp[4];
+    uint32_t* h = pp.part_hist + (uint64_t)blockIdx.x * pp.n_regions;
+    uint32_t carry = 0;
+    for (uint32_t b0 = 0; b0 < pp.n_regions; b0 += 4096u) {
+        const uint32_t n = min(4096u, pp.n_regions - b0);
+        carry += block_scan_256(h + b0, h + b0, n, carry, wtmp);
+    }
+    if (threadIdx.x == 0) pp.part_count[blockIdx.x] = carry;
+}
+
+// One block per fused-kernel region: the region's records, kScatterChunk at a
+// time, are counting-sorted by partition in LDS and written out so that each
+// partition's records of the chunk form one contiguous run.
+template <typename VT>
 __global__ void __launch_bounds__(256) part_scatter_kernel(PartParams pp) {
-    extern __shared__ uint32_t lbin[];                 // n_parts counts, then n_parts bases
-    uint32_t* lcnt = lbin;
-    uint32_t* lbase = lbin + pp.n_parts;
-    for (uint32_t q = threadIdx.x; q < pp.n_parts; q += blockDim.x) lcnt[q] = 0u;
-    __syncthreads();
-    const uint32_t n = pp.region_count[blockIdx.x];
-    const uint32_t* g = pp.rec_gid + (uint64_t)blockIdx.x * pp.part_cap;
-    const long long* v = pp.rec_val + (uint64_t)blockIdx.x * pp.part_cap;
-    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) atomicAdd(&lcnt[g[i] >> pp.part_shift], 1u);
-    __syncthreads();
-    for (uint32_t q = threadIdx.x; q < pp.n_parts; q += blockDim.x) {
-        const uint32_t c = lcnt[q];
-        lbase[q] = c ? atomicAdd(&pp.cursor[q], c) : 0u;
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    __shared__ uint32_t wtmp[4];
+    constexpr int PER = kScatterChunk / 256;
+    const uint32_t P = pp.n_parts;
+    const int shift = pp.part_shift;
+    VT* sval = reinterpret_cast<VT*>(smem);
+    uint32_t* sgid = reinterpret_cast<uint32_t*>(sval + kScatterChunk);
+    uint32_t* lcnt = sgid + kScatterChunk;
+    uint32_t* lstart = lcnt + P;
+    uint32_t* lcur = lstart + P;
+    const uint32_t b = blockIdx.x;
+    for (uint32_t q = threadIdx.x; q < P; q += blockDim.x) {
+        lcur[q] = pp.part_start[q] + pp.part_hist[(uint64_t)q * pp.n_regions + b];
         lcnt[q] = 0u;
     }
     __syncthreads();
-    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
-        const uint32_t gi = g[i];
-        const uint32_t q = gi >> pp.part_shift;
-        const uint32_t pos = lbase[q] + atomicAdd(&lcnt[q], 1u);
-        pp.sorted_gid[pos] = gi;
-        pp.sorted_val[pos] = v[i];
+    const uint32_t n = pp.region_count[b];
+    const uint32_t* rg = pp.rec_gid + (uint64_t)b * pp.part_cap;
+    const VT* rv = static_cast<const VT*>(pp.rec_val) + (uint64_t)b * pp.part_cap;
+    VT* out_val = static_cast<VT*>(pp.sorted_val);
+    for (uint32_t c0 = 0; c0 < n; c0 += (uint32_t)kScatterChunk) {
+        const uint32_t cn = min((uint32_t)kScatterChunk, n - c0);
+        uint32_t g[PER], rk[PER];
+        VT v[PER];
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const uint32_t i = (uint32_t)k * 256u + threadIdx.x;
+            g[k] = 0u;
+            v[k] = 0;
+            rk[k] = 0u;
+            if (i < cn) {
+                g[k] = rg[c0 + i];
+                v[k] = rv[c0 + i];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < PER; ++k)
+            if ((uint32_t)k * 256u + threadIdx.x < cn) rk[k] = atomicAdd(&lcnt[g[k] >> shift], 1u);
+        __syncthreads();
+        block_scan_256(lcnt, lstart, P, 0u, wtmp);
+#pragma unroll
+        for (int k = 0; k < PER; ++k)
+            if ((uint32_t)k * 256u + threadIdx.x < cn) {
+                const uint32_t pos = lstart[g[k] >> shift] + rk[k];
+                sgid[pos] = g[k];
+                sval[pos] = v[k];
+            }
+        __syncthreads();
+        for (uint32_t i = threadIdx.x; i < cn; i += blockDim.x) {
+            const uint32_t gi = sgid[i];
+            const uint32_t q = gi >> shift;
+            const uint32_t dest = lcur[q] + (i - lstart[q]);
+            pp.sorted_gid[dest] = gi;
+            out_val[dest] = sval[i];
+        }
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < P; q += blockDim.x) {
+            lcur[q] += lcnt[q];
+            lcnt[q] = 0u;
+        }
+        __syncthreads();
     }
 }
 
-// Work item c covers up to kPartChunk records of one partition: sum them in
-// an LDS table of the partition's groups, then add the table to the outputs.
+size_t part_scatter_lds_bytes(uint32_t n_parts, bool wide) {
+    return (size_t)kScatterChunk * (wide ? 12u : 8u) + (size_t)n_parts * 12u;
+}
+
+// Work item c covers up to kPartChunk records of one partition q: sum them in
+// an LDS table of q's groups. A partition with one work item adds its table
+// straight into the outputs; otherwise each item stores its table as a partial
+// that part_merge_kernel adds up. Either way each output group has exactly one
+// writer in this pass, so plain read-add-write suffices (the outputs already
+// hold what the fused kernel added for records past a region's capacity).
+constexpr int kAggUnroll = 8;
+
+template <typename VT>
 __global__ void __launch_bounds__(256) part_agg_kernel(PartParams pp) {
-    extern __shared__ unsigned long long ltab[];       // groups of one partition: sums, then counts
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const uint32_t gpp = 1u << pp.part_shift;
+    unsigned long long* lsum = reinterpret_cast<unsigned long long*>(smem);
+    uint32_t* lcnt = reinterpret_cast<uint32_t*>(lsum + gpp);
+    const uint32_t* sg = pp.sorted_gid;
+    const VT* sv = static_cast<const VT*>(pp.sorted_val);
     const uint32_t n_items = pp.chunk_start[pp.n_parts];
     for (uint32_t c = blockIdx.x; c < n_items; c += gridDim.x) {
         // partition holding work item c: last q with chunk_start[q] <= c
@@ -937,34 +1075,95 @@ __global__ void __launch_bounds__(256) part_agg_kernel(PartParams pp) {
         const uint32_t q = lo;
         const uint32_t r0 = pp.part_start[q] + (c - pp.chunk_start[q]) * (uint32_t)kPartChunk;
         const uint32_t r1 = min(r0 + (uint32_t)kPartChunk, pp.part_start[q + 1]);
-        for (uint32_t i = threadIdx.x; i < 2u * gpp; i += blockDim.x) ltab[i] = 0ull;
-        __syncthreads();
-        const uint32_t g0 = q << pp.part_shift;
-        for (uint32_t i = r0 + threadIdx.x; i < r1; i += blockDim.x) {
-            const uint32_t k = pp.sorted_gid[i] - g0;
-            atomicAdd(&ltab[k], (unsigned long long)pp.sorted_val[i]);
-            atomicAdd(&ltab[gpp + k], 1ull);
+        for (uint32_t k = threadIdx.x; k < gpp; k += blockDim.x) {
+            lsum[k] = 0ull;
+            lcnt[k] = 0u;
         }
         __syncthreads();
-        for (uint32_t k = threadIdx.x; k < gpp; k += blockDim.x) {
-            const unsigned long long cnt = ltab[gpp + k];
-            if (cnt) {
-                atomicAdd(&pp.sums[g0 + k], ltab[k]);
-                atomicAdd(&pp.counts[g0 + k], cnt);
+        const uint32_t g0 = q << pp.part_shift;
+        // kAggUnroll records per thread in flight per step
+        for (uint32_t i0 = r0; i0 < r1; i0 += kAggUnroll * blockDim.x) {
+            uint32_t k[kAggUnroll];
+            VT v[kAggUnroll];
+#pragma unroll
+            for (int u = 0; u < kAggUnroll; ++u) {
+                const uint32_t i = i0 + (uint32_t)u * blockDim.x + threadIdx.x;
+                k[u] = 0xFFFFFFFFu;
+                v[u] = 0;
+                if (i < r1) {
+                    k[u] = sg[i] - g0;
+                    v[u] = sv[i];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kAggUnroll; ++u) {
+                if (k[u] != 0xFFFFFFFFu) {
+                    atomicAdd(&lsum[k[u]], (unsigned long long)(long long)v[u]);
+                    atomicAdd(&lcnt[k[u]], 1u);
+                }
+            }
+        }
+        __syncthreads();
+        const bool single = pp.chunk_start[q + 1] - pp.chunk_start[q] == 1u;
+        const uint32_t kend = (uint32_t)min((uint64_t)gpp, pp.n_groups - g0);
+        if (single) {
+            for (uint32_t k = threadIdx.x; k < kend; k += blockDim.x) {
+                pp.sums[g0 + k] += lsum[k];
+                pp.counts[g0 + k] += lcnt[k];
+            }
+        } else {
+            for (uint32_t k = threadIdx.x; k < kend; k += blockDim.x) {
+                pp.item_sum[(uint64_t)c * gpp + k] = lsum[k];
+                pp.item_cnt[(uint64_t)c * gpp + k] = lcnt[k];
             }
         }
         __syncthreads();
     }
 }
 
+// Groups of partitions with several work items: add the items' partials.
+__global__ void __launch_bounds__(256) part_merge_kernel(PartParams pp) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    const uint32_t gpp = 1u << pp.part_shift;
+    for (uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; g < pp.n_groups; g += stride) {
+        const uint32_t q = (uint32_t)(g >> pp.part_shift);
+        const uint32_t k = (uint32_t)g & (gpp - 1u);
+        const uint32_t c0 = pp.chunk_start[q], c1 = pp.chunk_start[q + 1];
+        if (c1 - c0 < 2u) continue;
+        unsigned long long s = 0;
+        unsigned long long n = 0;
+        for (uint32_t c = c0; c < c1; ++c) {
+            s += pp.item_sum[(uint64_t)c * gpp + k];
+            n += pp.item_cnt[(uint64_t)c * gpp + k];
+        }
+        pp.sums[g] += s;
+        pp.counts[g] += n;
+    }
+}
+
 hipError_t launch_part_passes(const PartParams& pp, hipStream_t s) {
-    hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, pp);
+    hipLaunchKernelGGL(part_offsets_kernel, dim3(pp.n_parts), dim3(256), 0, s, pp);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(part_scatter_kernel, dim3(pp.n_regions), dim3(256), (size_t)pp.n_parts * 8, s, pp);
+    hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, pp);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(part_agg_kernel, dim3(1024), dim3(256), (size_t)16u << pp.part_shift, s, pp);
+    const bool wide = pp.rec_wide != 0;
+    const size_t agg_lds = (size_t)12u << pp.part_shift;
+    if (wide) {
+        hipLaunchKernelGGL(part_scatter_kernel<long long>, dim3(pp.n_regions), dim3(256),
+                           part_scatter_lds_bytes(pp.n_parts, true), s, pp);
+    } else {
+        hipLaunchKernelGGL(part_scatter_kernel<int32_t>, dim3(pp.n_regions), dim3(256),
+                           part_scatter_lds_bytes(pp.n_parts, false), s, pp);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (wide) hipLaunchKernelGGL(part_agg_kernel<long long>, dim3(1024), dim3(256), agg_lds, s, pp);
+    else hipLaunchKernelGGL(part_agg_kernel<int32_t>, dim3(1024), dim3(256), agg_lds, s, pp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(part_merge_kernel, dim3(fill_grid(pp.n_groups)), dim3(256), 0, s, pp);
     return hipGetLastError();
 }
 
