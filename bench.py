@@ -135,16 +135,7 @@ def main(argv=None) -> int:
     stream = torch.cuda.current_stream()
 
     def build_tables():
-        out = []
-        for jd, ws in zip(query["joins"], workspaces):
-            t = dims[jd["dim"]]
-            cols = {}
-            for c in [p["col"] for p in jd.get("preds", [])] + list(jd.get("payloads", [])):
-                cols.setdefault(c, t[c])
-            out.append(sdb.build_dim(t[wdims.dim_keys[jd["dim"]]], cols, jd.get("preds", []),
-                                     list(jd.get("payloads", [])), jd.get("kind", "auto"),
-                                     jd.get("load_factor", 0.0), workspace=ws))
-        return out
+        return sdb.build_dims(dims, wdims.dim_keys, query, workspaces=workspaces)
 
     def step(ev_pair=None):
         tabs = build_tables()

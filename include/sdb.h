@@ -272,6 +272,17 @@ SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* byt
 SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace,
                                  int64_t workspace_bytes, void* stream, sdb_dim* out);
 
+/* sdb_build_dim for n_dims tables (0 <= n_dims <= SDB_MAX_JOINS) at once:
+ * descs[d] is built into workspaces[d] (workspace_bytes[d] bytes) and
+ * described in outs[d] (all arrays host). Every table's statistics pass runs
+ * before the one synchronization that reads them, and every table's map
+ * before the one that checks them, so a star query's tables cost two stream
+ * synchronizations in all. Arguments of every table are checked before
+ * anything launches. On error the message names the dimension index; the
+ * outputs are then undefined. Errors: as sdb_build_dim. */
+SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, void* const* workspaces,
+                                  const int64_t* workspace_bytes, void* stream, sdb_dim* outs);
+
 /* ---- planning ----------------------------------------------------------- */
 
 /* Orders the stages of `q` (host) into `plan` (host). Unless q->force_order

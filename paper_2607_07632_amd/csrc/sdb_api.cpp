@@ -616,108 +616,139 @@ SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* byt
     return ok();
 }
 
+SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, void* const* workspaces,
+                                  const int64_t* workspace_bytes, void* stream, sdb_dim* outs) {
+    if (n_dims < 0 || n_dims > SDB_MAX_JOINS) return fail(SDB_INVALID_ARG, "n_dims %d is not in 0..%d", n_dims, SDB_MAX_JOINS);
+    if (n_dims > 0 && (!descs || !workspaces || !workspace_bytes || !outs)) return fail(SDB_INVALID_ARG, "null argument");
+    hipStream_t s = (hipStream_t)stream;
+    BuildParams bp[SDB_MAX_JOINS];
+    DimStats hs[SDB_MAX_JOINS];
+    // every table's arguments first, so nothing launches for an invalid batch
+    for (int d = 0; d < n_dims; ++d) {
+        const sdb_dim_desc* desc = &descs[d];
+        sdb_status st = check_dim_desc(desc);
+        if (st != SDB_OK) return fail(st, "dimension %d: %s", d, g_error.c_str());
+        void* workspace = workspaces[d];
+        if (!workspace) return fail(SDB_INVALID_ARG, "dimension %d: null workspace", d);
+        if (((uintptr_t)workspace & 255u) != 0)
+            return fail(SDB_INVALID_ARG, "dimension %d: workspace is not 256-byte aligned", d);
+        const uint64_t need = required_bytes(desc);
+        if (workspace_bytes[d] < 0 || (uint64_t)workspace_bytes[d] < need)
+            return fail(SDB_WORKSPACE_TOO_SMALL, "dimension %d: workspace holds %lld bytes, %llu needed", d,
+                        (long long)workspace_bytes[d], (unsigned long long)need);
+        std::memset(&outs[d], 0, sizeof outs[d]);
+    }
+
+    // pass 1 for every table: statistics, read back with one synchronization
+    for (int d = 0; d < n_dims; ++d) {
+        bp[d] = build_params(&descs[d], (DimStats*)workspaces[d]);
+        SDB_HIP(launch_dim_stats(bp[d], s), "dimension statistics launch");
+    }
+    for (int d = 0; d < n_dims; ++d)
+        SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "statistics copy");
+    if (n_dims > 0) SDB_HIP(hipStreamSynchronize(s), "statistics sync");
+
+    // pass 2 for every table: layout from the statistics, then the map or hash table
+    int kinds[SDB_MAX_JOINS];
+    for (int d = 0; d < n_dims; ++d) {
+        const sdb_dim_desc* desc = &descs[d];
+        sdb_dim* out = &outs[d];
+        uint8_t* table = (uint8_t*)workspaces[d] + kStatsBytes;
+        const int64_t n = desc->n_rows;
+        out->n_rows = n;
+        out->n_pass = (int64_t)hs[d].npass;
+        out->key_min = n > 0 ? hs[d].kmin : 0;
+        out->key_max = n > 0 ? hs[d].kmax : -1;
+        out->n_payloads = desc->n_payloads;
+        // payload codes: mixed radix over the payload ranges of passing rows, last payload fastest
+        uint64_t domain = 1;
+        for (int p = desc->n_payloads - 1; p >= 0; --p) {
+            const bool any = hs[d].npass > 0;
+            const int32_t lo = any ? hs[d].pmin[p] : 0;
+            const uint64_t radix = any ? (uint64_t)((int64_t)hs[d].pmax[p] - (int64_t)lo + 1) : 1;
+            out->payload_min[p] = lo;
+            out->payload_div[p] = domain;
+            if (radix > 0xFFFFFFFFull)
+                return fail(SDB_UNSUPPORTED, "dimension %d: payload %d spans more than 2^32 - 1 values", d, p);
+            out->payload_radix[p] = (uint32_t)radix;
+            domain *= radix;
+            if (domain >= 0xFFFFFFFEull)
+                return fail(SDB_UNSUPPORTED, "dimension %d: payload domain reaches 2^32 - 2 codes", d);
+        }
+        out->domain = domain;
+
+        const uint64_t range = n > 0 ? (uint64_t)((int64_t)out->key_max - (int64_t)out->key_min + 1) : 0;
+        int kind = desc->kind;
+        if (kind == SDB_TABLE_AUTO) kind = range <= dense_slot_limit(n) ? SDB_TABLE_DENSE : SDB_TABLE_HASH;
+        if (kind == SDB_TABLE_DENSE && range > dense_slot_limit(n))
+            return fail(SDB_KEY_RANGE, "dimension %d: key range %llu exceeds the dense limit %llu", d,
+                        (unsigned long long)range, (unsigned long long)dense_slot_limit(n));
+        kinds[d] = kind;
+        out->kind = kind;
+        out->stats = workspaces[d];
+        out->map = table;
+        bp[d].kmin = out->key_min;
+        for (int p = 0; p < desc->n_payloads; ++p) {
+            bp[d].pmin[p] = out->payload_min[p];
+            bp[d].pdiv[p] = (uint32_t)out->payload_div[p];
+        }
+
+        if (kind == SDB_TABLE_DENSE) {
+            // codes stay below the two reserved top values of the width
+            const int width = domain <= 0xFEull ? 1 : (domain <= 0xFFFEull ? 2 : 4);
+            const uint32_t missing = width == 1 ? 0xFFu : (width == 2 ? 0xFFFFu : 0xFFFFFFFFu);
+            out->width = width;
+            out->sentinel = missing - 1u;
+            out->n_slots = range;
+            const uint64_t map_bytes = align_up(range * width, 256);
+            uint32_t* pass_bits = (uint32_t*)(table + map_bytes);
+            out->bits = pass_bits;
+            bp[d].map = table;
+            bp[d].pass_bits = pass_bits;
+            bp[d].width = width;
+            bp[d].nslots = range;
+            bp[d].sentinel = missing - 1u;
+            bp[d].missing = missing;
+            SDB_HIP(launch_fill_u32((uint32_t*)table, map_bytes / 4, 0xFFFFFFFFu, s), "map fill");
+            SDB_HIP(launch_dense_scatter(bp[d], s), "dense scatter launch");
+        } else {
+            const uint64_t cap = hash_capacity(n, effective_lf(desc));
+            int bits = 0;
+            while ((1ull << bits) < cap) ++bits;
+            out->width = 8;
+            out->sentinel = 0xFFFFFFFEu;   // code + 1 == 0xFFFFFFFF marks a filtered row
+            out->n_slots = cap;
+            out->hash_bits = bits;
+            bp[d].map = table;
+            bp[d].nslots = cap;
+            bp[d].hmask = (uint32_t)(cap - 1);
+            bp[d].hshift = 32 - bits;
+            SDB_HIP(launch_fill_u32((uint32_t*)table, cap * 2, 0u, s), "hash table fill");
+            SDB_HIP(launch_hash_insert(bp[d], s), "hash insert launch");
+        }
+    }
+
+    // duplicate-key checks of every table, with one synchronization
+    for (int d = 0; d < n_dims; ++d)
+        SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "flag copy");
+    if (n_dims > 0) SDB_HIP(hipStreamSynchronize(s), "build sync");
+    for (int d = 0; d < n_dims; ++d) {
+        const DimStats& fin = hs[d];
+        if (fin.dup & 1u) return fail(SDB_DUP_KEY, "dimension %d: key column holds a duplicate key", d);
+        if (kinds[d] == SDB_TABLE_DENSE && fin.occupied != (unsigned long long)descs[d].n_rows)
+            return fail(SDB_DUP_KEY, "dimension %d: key column holds a duplicate key (%llu distinct keys in %lld rows)",
+                        d, (unsigned long long)fin.occupied, (long long)descs[d].n_rows);
+        if (fin.dup) return fail(SDB_HIP_ERROR, "dimension %d: build inconsistency (flag %u)", d, fin.dup);
+    }
+    return ok();
+}
+
 SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace, int64_t workspace_bytes,
                                  void* stream, sdb_dim* out) {
-    sdb_status st = check_dim_desc(desc);
-    if (st != SDB_OK) return st;
-    if (!out) return fail(SDB_INVALID_ARG, "null output handle");
-    if (!workspace) return fail(SDB_INVALID_ARG, "null workspace");
-    if (((uintptr_t)workspace & 255u) != 0) return fail(SDB_INVALID_ARG, "workspace is not 256-byte aligned");
-    const uint64_t need = required_bytes(desc);
-    if (workspace_bytes < 0 || (uint64_t)workspace_bytes < need)
-        return fail(SDB_WORKSPACE_TOO_SMALL, "workspace holds %lld bytes, %llu needed",
-                    (long long)workspace_bytes, (unsigned long long)need);
-    hipStream_t s = (hipStream_t)stream;
-    std::memset(out, 0, sizeof *out);
-
-    DimStats* dstats = (DimStats*)workspace;
-    uint8_t* table = (uint8_t*)workspace + kStatsBytes;
-    BuildParams bp = build_params(desc, dstats);
-
-    // pass 1: statistics
-    SDB_HIP(launch_dim_stats(bp, s), "dimension statistics launch");
-    DimStats hs;
-    SDB_HIP(hipMemcpyAsync(&hs, dstats, sizeof hs, hipMemcpyDeviceToHost, s), "statistics copy");
-    SDB_HIP(hipStreamSynchronize(s), "statistics sync");
-
-    const int64_t n = desc->n_rows;
-    out->n_rows = n;
-    out->n_pass = (int64_t)hs.npass;
-    out->key_min = n > 0 ? hs.kmin : 0;
-    out->key_max = n > 0 ? hs.kmax : -1;
-    out->n_payloads = desc->n_payloads;
-    // payload codes: mixed radix over the payload ranges of passing rows, last payload fastest
-    uint64_t domain = 1;
-    for (int p = desc->n_payloads - 1; p >= 0; --p) {
-        const bool any = hs.npass > 0;
-        const int32_t lo = any ? hs.pmin[p] : 0;
-        const uint64_t radix = any ? (uint64_t)((int64_t)hs.pmax[p] - (int64_t)lo + 1) : 1;
-        out->payload_min[p] = lo;
-        out->payload_div[p] = domain;
-        if (radix > 0xFFFFFFFFull) return fail(SDB_UNSUPPORTED, "payload %d spans more than 2^32 - 1 values", p);
-        out->payload_radix[p] = (uint32_t)radix;
-        domain *= radix;
-        if (domain >= 0xFFFFFFFEull) return fail(SDB_UNSUPPORTED, "payload domain reaches 2^32 - 2 codes");
-    }
-    out->domain = domain;
-
-    const uint64_t range = n > 0 ? (uint64_t)((int64_t)out->key_max - (int64_t)out->key_min + 1) : 0;
-    int kind = desc->kind;
-    if (kind == SDB_TABLE_AUTO) kind = range <= dense_slot_limit(n) ? SDB_TABLE_DENSE : SDB_TABLE_HASH;
-    if (kind == SDB_TABLE_DENSE && range > dense_slot_limit(n))
-        return fail(SDB_KEY_RANGE, "key range %llu exceeds the dense limit %llu",
-                    (unsigned long long)range, (unsigned long long)dense_slot_limit(n));
-    out->kind = kind;
-    out->stats = workspace;
-    out->map = table;
-    bp.kmin = out->key_min;
-    for (int p = 0; p < desc->n_payloads; ++p) {
-        bp.pmin[p] = out->payload_min[p];
-        bp.pdiv[p] = (uint32_t)out->payload_div[p];
-    }
-
-    if (kind == SDB_TABLE_DENSE) {
-        // codes stay below the two reserved top values of the width
-        const int width = domain <= 0xFEull ? 1 : (domain <= 0xFFFEull ? 2 : 4);
-        const uint32_t missing = width == 1 ? 0xFFu : (width == 2 ? 0xFFFFu : 0xFFFFFFFFu);
-        out->width = width;
-        out->sentinel = missing - 1u;
-        out->n_slots = range;
-        const uint64_t map_bytes = align_up(range * width, 256);
-        uint32_t* pass_bits = (uint32_t*)(table + map_bytes);
-        out->bits = pass_bits;
-        bp.map = table;
-        bp.pass_bits = pass_bits;
-        bp.width = width;
-        bp.nslots = range;
-        bp.sentinel = missing - 1u;
-        bp.missing = missing;
-        SDB_HIP(launch_fill_u32((uint32_t*)table, map_bytes / 4, 0xFFFFFFFFu, s), "map fill");
-        SDB_HIP(launch_dense_scatter(bp, s), "dense scatter launch");
-    } else {
-        const uint64_t cap = hash_capacity(n, effective_lf(desc));
-        int bits = 0;
-        while ((1ull << bits) < cap) ++bits;
-        out->width = 8;
-        out->sentinel = 0xFFFFFFFEu;   // code + 1 == 0xFFFFFFFF marks a filtered row
-        out->n_slots = cap;
-        out->hash_bits = bits;
-        bp.map = table;
-        bp.nslots = cap;
-        bp.hmask = (uint32_t)(cap - 1);
-        bp.hshift = 32 - bits;
-        SDB_HIP(launch_fill_u32((uint32_t*)table, cap * 2, 0u, s), "hash table fill");
-        SDB_HIP(launch_hash_insert(bp, s), "hash insert launch");
-    }
-    DimStats fin;
-    SDB_HIP(hipMemcpyAsync(&fin, dstats, sizeof fin, hipMemcpyDeviceToHost, s), "flag copy");
-    SDB_HIP(hipStreamSynchronize(s), "build sync");
-    if (fin.dup & 1u) return fail(SDB_DUP_KEY, "dimension key column holds a duplicate key");
-    if (kind == SDB_TABLE_DENSE && fin.occupied != (unsigned long long)n)
-        return fail(SDB_DUP_KEY, "dimension key column holds a duplicate key (%llu distinct keys in %lld rows)",
-                    (unsigned long long)fin.occupied, (long long)n);
-    if (fin.dup) return fail(SDB_HIP_ERROR, "dimension build inconsistency (flag %u)", fin.dup);
-    return ok();
+    if (!desc || !out) return fail(SDB_INVALID_ARG, "null argument");
+    void* ws[1] = {workspace};
+    const int64_t wb[1] = {workspace_bytes};
+    return sdb_build_dims(1, desc, ws, wb, stream, out);
 }
 
 SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_t scratch_bytes,

@@ -23,6 +23,7 @@
 namespace sdb {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // small helpers
@@ -182,6 +183,8 @@ __global__ void stats_init_kernel(DimStats* st) {
 }
 
 // Key range over all rows; pass count and payload ranges over passing rows.
+constexpr int kStatsRows = 16;
+
 // Each block reduces in registers and LDS and then adds its result with one
 // set of atomics, so the atomics stay few however large the dimension.
 __global__ void __launch_bounds__(256) dim_stats_kernel(BuildParams bp) {
@@ -196,19 +199,46 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildParams bp) {
         pmin[p] = INT_MAX;
         pmax[p] = INT_MIN;
     }
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
-        const int32_t k = bp.key[i];
-        kmin = min(kmin, k);
-        kmax = max(kmax, k);
-        if (dim_row_passes(bp, i)) {
-            ++npass;
-            for (int p = 0; p < bp.n_payloads; ++p) {
-                const int32_t v = bp.cols[bp.payload_col[p]][i];
-                pmin[p] = min(pmin[p], v);
-                pmax[p] = max(pmax[p], v);
-            }
+    // kStatsRows rows per thread per step, each column's loads issued together
+    constexpr int U = kStatsRows;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x * U;
+    for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x * U + threadIdx.x; i0 < bp.n; i0 += stride) {
+        bool ok[U], pass[U];
+        int32_t x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + (int64_t)u * blockDim.x;
+            ok[u] = i < bp.n;
+            x[u] = ok[u] ? bp.key[i] : 0;
         }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (ok[u]) {
+                kmin = min(kmin, x[u]);
+                kmax = max(kmax, x[u]);
+            }
+            pass[u] = ok[u];
+        }
+        for (int q = 0; q < bp.n_preds; ++q) {
+            const int32_t* col = bp.cols[bp.pred_col[q]];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = ok[u] ? col[i0 + (int64_t)u * blockDim.x] : 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) pass[u] = pass[u] && range_pass(bp.pred[q], x[u]);
+        }
+        for (int p = 0; p < bp.n_payloads; ++p) {
+            const int32_t* col = bp.cols[bp.payload_col[p]];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = pass[u] ? col[i0 + (int64_t)u * blockDim.x] : 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (pass[u]) {
+                    pmin[p] = min(pmin[p], x[u]);
+                    pmax[p] = max(pmax[p], x[u]);
+                }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) npass += pass[u] ? 1ull : 0ull;
     }
     kmin = wave_min_i32(kmin);
     kmax = wave_max_i32(kmax);
@@ -285,16 +315,56 @@ __global__ void __launch_bounds__(256) dense_bits_kernel(BuildParams bp) {
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     unsigned long long occupied = 0;
     for (uint64_t w = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; w < n_words; w += stride) {
+        // the word's 32 map entries as 16-byte loads (the map is padded to 256
+        // bytes and filled, so the last word's loads stay inside it)
         uint32_t bits = 0u;
-        for (uint32_t b = 0; b < 32u; ++b) {
-            const uint64_t slot = w * 32 + b;
-            if (slot >= bp.nslots) break;
-            uint32_t c;
-            if (bp.width == 1) c = static_cast<const uint8_t*>(bp.map)[slot];
-            else if (bp.width == 2) c = static_cast<const uint16_t*>(bp.map)[slot];
-            else c = static_cast<const uint32_t*>(bp.map)[slot];
-            if (c < bp.sentinel) bits |= 1u << b;
-            occupied += c != bp.missing;
+        const uint32_t valid = (uint32_t)min<uint64_t>(32, bp.nslots - w * 32);
+        if (bp.width == 1) {
+            const v4u* src = reinterpret_cast<const v4u*>(static_cast<const uint8_t*>(bp.map) + w * 32);
+            const v4u a = src[0], b = src[1];
+            const uint32_t d[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (uint32_t e = 0; e < 32u; ++e) {
+                const uint32_t c = (d[e >> 2] >> ((e & 3u) * 8u)) & 0xFFu;
+                if (e < valid) {
+                    bits |= (c < bp.sentinel ? 1u : 0u) << e;
+                    occupied += c != bp.missing;
+                }
+            }
+        } else if (bp.width == 2) {
+            const v4u* src = reinterpret_cast<const v4u*>(static_cast<const uint16_t*>(bp.map) + w * 32);
+            uint32_t d[16];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const v4u a = src[k];
+                d[4 * k] = a.x;
+                d[4 * k + 1] = a.y;
+                d[4 * k + 2] = a.z;
+                d[4 * k + 3] = a.w;
+            }
+#pragma unroll
+            for (uint32_t e = 0; e < 32u; ++e) {
+                const uint32_t c = (d[e >> 1] >> ((e & 1u) * 16u)) & 0xFFFFu;
+                if (e < valid) {
+                    bits |= (c < bp.sentinel ? 1u : 0u) << e;
+                    occupied += c != bp.missing;
+                }
+            }
+        } else {
+            const v4u* src = reinterpret_cast<const v4u*>(static_cast<const uint32_t*>(bp.map) + w * 32);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const v4u a = src[k];
+                const uint32_t d[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+                for (uint32_t e4 = 0; e4 < 4u; ++e4) {
+                    const uint32_t e = (uint32_t)k * 4u + e4;
+                    if (e < valid) {
+                        bits |= (d[e4] < bp.sentinel ? 1u : 0u) << e;
+                        occupied += d[e4] != bp.missing;
+                    }
+                }
+            }
         }
         bp.pass_bits[w] = bits;
     }

@@ -104,6 +104,7 @@ SIGNATURES = {
     "sdb_struct_sizes": (i32, [C.POINTER(i64), i32]),
     "sdb_dim_required_bytes": (i32, [C.POINTER(SdbDimDesc), C.POINTER(i64)]),
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
+    "sdb_build_dims": (i32, [i32, C.POINTER(SdbDimDesc), C.POINTER(vp), C.POINTER(i64), vp, C.POINTER(SdbDim)]),
     "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
     "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
     "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
@@ -189,14 +190,11 @@ def dim_required_bytes(desc: SdbDimDesc) -> int:
     return out.value
 
 
-def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
-              load_factor: float = 0.0, stream=None, workspace=None) -> DimTable:
-    """Builds the lookup table of one dimension.
-
-    ``key`` and the values of ``cols`` are int32 device tensors of equal
-    length; ``preds`` are predicate dicts naming columns of ``cols``;
-    ``payloads`` name the columns to gather.
-    """
+def dim_desc(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
+             load_factor: float = 0.0) -> SdbDimDesc:
+    """The C descriptor of one dimension: ``key`` and the values of ``cols``
+    are int32 device tensors of equal length; ``preds`` are predicate dicts
+    naming columns of ``cols``; ``payloads`` name the columns to gather."""
     import torch
     names = list(cols)
     if len(names) > MAX_DIM_COLS:
@@ -221,28 +219,54 @@ def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
         d.payload_cols[i] = idx[p]
     d.kind = TABLES[kind]
     d.load_factor = float(load_factor or 0.0)
+    return d
+
+
+def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
+              load_factor: float = 0.0, stream=None, workspace=None) -> DimTable:
+    """Builds the lookup table of one dimension (arguments as dim_desc)."""
+    import torch
+    d = dim_desc(key, cols, preds, payloads, kind, load_factor)
     need = dim_required_bytes(d)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=key.device)
     h = SdbDim()
     _check(lib().sdb_build_dim(C.byref(d), _ptr(workspace), workspace.numel(),
                                _stream_handle(stream), C.byref(h)))
-    return DimTable(h, d, workspace, [key] + [cols[n] for n in names])
+    return DimTable(h, d, workspace, [key] + list(cols.values()))
 
 
-def build_dims(dims: dict, dim_keys: dict, query: dict, stream=None) -> list:
-    """One DimTable per join of ``query`` (dims: name -> {column: int32 device tensor})."""
-    out = []
-    for jd in query.get("joins", []):
-        t = dims[jd["dim"]]
-        key_name = dim_keys[jd["dim"]]
-        needed = [p["col"] for p in jd.get("preds", [])] + list(jd.get("payloads", []))
-        cols = {}
-        for n in needed:
-            cols.setdefault(n, t[n])
-        out.append(build_dim(t[key_name], cols, jd.get("preds", []), list(jd.get("payloads", [])),
-                             jd.get("kind", "auto"), jd.get("load_factor", 0.0), stream=stream))
-    return out
+def _join_inputs(dims: dict, dim_keys: dict, jd: dict):
+    t = dims[jd["dim"]]
+    cols = {}
+    for n in [p["col"] for p in jd.get("preds", [])] + list(jd.get("payloads", [])):
+        cols.setdefault(n, t[n])
+    return (t[dim_keys[jd["dim"]]], cols, jd.get("preds", []), list(jd.get("payloads", [])),
+            jd.get("kind", "auto"), jd.get("load_factor", 0.0))
+
+
+def build_dims(dims: dict, dim_keys: dict, query: dict, stream=None, workspaces=None) -> list:
+    """One DimTable per join of ``query`` (dims: name -> {column: int32 device
+    tensor}), built by one batched call (two stream synchronizations in all).
+    ``workspaces`` (one uint8 device tensor per join, large enough) are reused
+    when given."""
+    import torch
+    joins = query.get("joins", [])
+    if not joins:
+        return []
+    inputs = [_join_inputs(dims, dim_keys, jd) for jd in joins]
+    descs = (SdbDimDesc * len(joins))()
+    for i, args in enumerate(inputs):
+        descs[i] = dim_desc(*args)
+    if workspaces is None:
+        workspaces = [torch.empty(dim_required_bytes(descs[i]), dtype=torch.uint8, device=inputs[i][0].device)
+                      for i in range(len(joins))]
+    ws_ptrs = (C.c_void_p * len(joins))(*[_ptr(w) for w in workspaces])
+    ws_bytes = (C.c_int64 * len(joins))(*[w.numel() for w in workspaces])
+    outs = (SdbDim * len(joins))()
+    _check(lib().sdb_build_dims(len(joins), descs, ws_ptrs, ws_bytes, _stream_handle(stream), outs))
+    return [DimTable(outs[i], descs[i], workspaces[i], [inputs[i][0]] + list(inputs[i][1].values()))
+            for i in range(len(joins))]
 
 
 # ---------------------------------------------------------------------------

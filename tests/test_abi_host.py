@@ -250,3 +250,28 @@ def test_finalize_scratch_and_validation():
     st = L.sdb_finalize_groups(C.byref(p), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 62_500, 0x6000,
                                0x7000, 8, None)
     assert st == 4
+
+
+def test_batched_build_validates_every_table_before_any_launch():
+    L = sdb.lib()
+    descs = (sdb.SdbDimDesc * 2)(_desc(1000, "dense"), _desc(1000, "hash"))
+    need = [sdb.dim_required_bytes(descs[0]), sdb.dim_required_bytes(descs[1])]
+    ws = (C.c_void_p * 2)(0x100000, 0x40000000)          # never dereferenced: validation fails first
+    outs = (sdb.SdbDim * 2)()
+
+    def status(n, wsb, w=ws, d=descs):
+        return sdb.STATUS[L.sdb_build_dims(n, d, w, (C.c_int64 * 2)(*wsb), None, outs)]
+
+    assert status(-1, need) == "SDB_INVALID_ARG"
+    assert status(7, need) == "SDB_INVALID_ARG"
+    assert status(0, need) == "SDB_OK"                   # nothing to build
+    # the second table's workspace is one byte short: nothing may launch
+    assert status(2, [need[0], need[1] - 1]) == "SDB_WORKSPACE_TOO_SMALL"
+    assert "dimension 1" in L.sdb_last_error().decode()
+    bad = (C.c_void_p * 2)(0x100000, 0x40000010)          # not 256-byte aligned
+    assert status(2, need, w=bad) == "SDB_INVALID_ARG"
+    assert "dimension 1" in L.sdb_last_error().decode()
+    d2 = (sdb.SdbDimDesc * 2)(_desc(1000, "dense"), _desc(1000, "dense"))
+    d2[0].n_rows = -1
+    assert status(2, need, d=d2) == "SDB_INVALID_ARG"
+    assert "dimension 0" in L.sdb_last_error().decode()

@@ -258,3 +258,44 @@ def test_random_tiny_schemas_partitioned(seed):
     want = oracle_rows(w)
     got, _ = run_gpu(w, force={"terminal": "part"})
     assert_same(got.as_rows(), want, f"tiny {seed} part")
+
+
+def test_batched_build_matches_single_builds():
+    """sdb_build_dims gives every table exactly what sdb_build_dim gives it."""
+    from paper_2607_07632_amd import sdb
+    import torch
+    w = workload("c4_star4_zipf")
+    _, dims = upload(w)
+    batch = sdb.build_dims(dims, w.dim_keys, w.query)
+    torch.cuda.synchronize()
+    for jd, b in zip(w.query["joins"], batch):
+        args = sdb._join_inputs(dims, w.dim_keys, jd)
+        one = sdb.build_dim(*args)
+        torch.cuda.synchronize()
+        for f, _ in sdb.SdbDim._fields_:
+            if f in ("stats", "map", "bits"):
+                continue
+            a, c = getattr(b.handle, f), getattr(one.handle, f)
+            if hasattr(a, "__len__"):
+                a, c = list(a), list(c)
+            assert a == c, (jd["dim"], f, a, c)
+        n = min(b.workspace.numel(), one.workspace.numel())
+        used = 256 + (b.handle.n_slots * b.handle.width + 255) // 256 * 256 + (b.handle.n_slots + 31) // 32 * 4
+        n = min(n, used)
+        assert torch.equal(b.workspace[256:n], one.workspace[256:n]), jd["dim"]
+
+
+def test_batched_build_reports_failing_dimension():
+    from paper_2607_07632_amd import sdb
+    import torch
+    w = workload("c3_star3")
+    _, dims = upload(w)
+    bad = {d: dict(t) for d, t in dims.items()}
+    key = w.dim_keys["supplier"]
+    k = bad["supplier"][key].clone()
+    k[5] = k[6]
+    bad["supplier"][key] = k
+    with pytest.raises(sdb.SdbError) as e:
+        sdb.build_dims(bad, w.dim_keys, w.query)
+    idx = [j["dim"] for j in w.query["joins"]].index("supplier")
+    assert "DUP_KEY" in str(e.value) and f"dimension {idx}" in str(e.value)
