@@ -316,6 +316,13 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
                                       int64_t n_groups_capacity, void* scratch,
                                       int64_t scratch_bytes, void* stream);
 
+/* Measurement hook, host only. With both events non-NULL (hipEvent_t
+ * handles the caller created and owns), every later sdb_run_star_query on
+ * this thread records `start` on its stream just before the fused kernel and
+ * `stop` just after it (before any terminal pass), so the elapsed time
+ * between them is that kernel's duration. NULL, NULL turns it off. */
+SDB_API sdb_status sdb_set_fused_events(void* start, void* stop);
+
 /* ---- finalize ----------------------------------------------------------- */
 
 /* Host only. Scratch bytes sdb_finalize_groups needs for `plan`. */

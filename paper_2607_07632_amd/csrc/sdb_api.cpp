@@ -20,6 +20,8 @@ using namespace sdb;
 namespace {
 
 thread_local std::string g_error;
+thread_local hipEvent_t g_fused_start = nullptr;   // sdb_set_fused_events
+thread_local hipEvent_t g_fused_stop = nullptr;
 
 sdb_status fail(sdb_status s, const char* fmt, ...) {
     char buf[512];
@@ -1027,14 +1029,24 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
             st = choose_grid(q, plan, &grid);
             if (st != SDB_OK) return st;
         }
+        const bool timed = g_fused_start && g_fused_stop;
+        if (timed) SDB_HIP(hipEventRecord(g_fused_start, s), "event record");
         SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, grid, plan->block, lds_bytes, s),
                 "fused kernel launch");
+        if (timed) SDB_HIP(hipEventRecord(g_fused_stop, s), "event record");
         if (plan->terminal == TERM_PART) SDB_HIP(launch_part_passes(pp, s), "partition passes launch");
     }
     if (plan->xcd_copies)
         SDB_HIP(launch_xcd_merge((const unsigned long long*)scratch, plan->xcd_copies, plan->n_groups,
                                  (unsigned long long*)sums, (unsigned long long*)counts, s),
                 "copy merge launch");
+    return ok();
+}
+
+SDB_API sdb_status sdb_set_fused_events(void* start, void* stop) {
+    if ((start == nullptr) != (stop == nullptr)) return fail(SDB_INVALID_ARG, "set both events or neither");
+    g_fused_start = (hipEvent_t)start;
+    g_fused_stop = (hipEvent_t)stop;
     return ok();
 }
 

@@ -105,6 +105,7 @@ SIGNATURES = {
     "sdb_dim_required_bytes": (i32, [C.POINTER(SdbDimDesc), C.POINTER(i64)]),
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
     "sdb_build_dims": (i32, [i32, C.POINTER(SdbDimDesc), C.POINTER(vp), C.POINTER(i64), vp, C.POINTER(SdbDim)]),
+    "sdb_set_fused_events": (i32, [vp, vp]),
     "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
     "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
     "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
@@ -452,3 +453,16 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
             "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}
+
+
+def set_fused_events(start=None, stop=None) -> None:
+    """Times the fused kernel of later runs on this thread between two
+    torch.cuda.Event objects (recorded on the run's stream), or stops doing so
+    when called without events."""
+    if start is None or stop is None:
+        _check(lib().sdb_set_fused_events(None, None))
+        return
+    for e in (start, stop):
+        if not e.cuda_event:                       # torch creates the HIP event on first record
+            e.record()
+    _check(lib().sdb_set_fused_events(C.c_void_p(start.cuda_event), C.c_void_p(stop.cuda_event)))

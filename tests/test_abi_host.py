@@ -275,3 +275,10 @@ def test_batched_build_validates_every_table_before_any_launch():
     d2[0].n_rows = -1
     assert status(2, need, d=d2) == "SDB_INVALID_ARG"
     assert "dimension 0" in L.sdb_last_error().decode()
+
+
+def test_fused_events_hook_validation():
+    L = sdb.lib()
+    assert sdb.STATUS[L.sdb_set_fused_events(C.c_void_p(0x1000), None)] == "SDB_INVALID_ARG"
+    assert sdb.STATUS[L.sdb_set_fused_events(None, C.c_void_p(0x1000))] == "SDB_INVALID_ARG"
+    assert sdb.STATUS[L.sdb_set_fused_events(None, None)] == "SDB_OK"

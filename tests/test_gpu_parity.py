@@ -299,3 +299,29 @@ def test_batched_build_reports_failing_dimension():
         sdb.build_dims(bad, w.dim_keys, w.query)
     idx = [j["dim"] for j in w.query["joins"]].index("supplier")
     assert "DUP_KEY" in str(e.value) and f"dimension {idx}" in str(e.value)
+
+
+def test_fused_events_bracket_the_kernel():
+    """The library's events time the fused kernel alone: within the run window."""
+    from paper_2607_07632_amd import sdb
+    import torch
+    w = workload("c3_star3")
+    fact, dims = upload(w)
+    q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query, {"terminal": "part"})
+    plan = q.plan()
+    sums, counts = q.alloc_outputs(plan)
+    scratch = q.run_scratch(plan)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    sdb.set_fused_events(ev[0], ev[1])
+    ev[2].record()
+    q.run(sums, counts, plan=plan, scratch=scratch)
+    ev[3].record()
+    sdb.set_fused_events()
+    torch.cuda.synchronize()
+    fused, whole = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+    assert 0.0 < fused < whole
+    k, s, c, n, _ = q.finalize(sums, counts, plan=plan)
+    m = int(n.item())
+    rows = [(tuple(int(x) for x in kk), int(ss), int(cc))
+            for kk, ss, cc in zip(k[:m].cpu().numpy(), s[:m].cpu().numpy(), c[:m].cpu().numpy())]
+    assert_same(rows, oracle_rows(w), "timed run")
