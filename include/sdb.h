@@ -79,6 +79,8 @@ enum { SDB_TERMINAL_AUTO = 0, SDB_TERMINAL_SCALAR = 1, SDB_TERMINAL_LDS = 2,
 #define SDB_MAX_GROUP_KEYS 4
 #define SDB_MAX_STAGES (SDB_MAX_FACT_PREDS + SDB_MAX_JOINS)
 #define SDB_PLAN_SCRATCH_BYTES 256
+/* fact columns the fused kernel can load eagerly (sdb_plan.eager) */
+#define SDB_MAX_EAGER 4
 
 /* One predicate. `col` indexes the owning descriptor's `cols[]`. `hi` is
  * used by SDB_OP_BETWEEN only. */
@@ -171,7 +173,11 @@ typedef struct sdb_agg {
  *  force_order     1: keep query order (predicates, then joins), no sampling
  *  grid_blocks     blocks of the fused kernel
  *  force_lds       -1: every probe uses the device table (no LDS staging)
- *  force_xcd       -1: no per-XCD group-table copies; 1: use them */
+ *  force_xcd       -1: no per-XCD group-table copies; 1: use them
+ *  force_eager     -1: every column is loaded when its stage is reached, for
+ *                  the items that still hold a live row; k in 1..SDB_MAX_EAGER:
+ *                  the first k columns in order of use are loaded together
+ *                  when the items start (needs 4-row items and ipt 1 or 2) */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -190,6 +196,7 @@ typedef struct sdb_query {
     int32_t grid_blocks;
     int32_t force_lds;
     int32_t force_xcd;
+    int32_t force_eager;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -219,6 +226,7 @@ typedef struct sdb_plan {
     int32_t terminal;
     int32_t ipt;
     int32_t vector;                       /* 1: 4-row items with 128-bit loads */
+    int32_t eager;                        /* columns loaded together when items start (first in order of use) */
     int32_t block;
     int32_t grid;                         /* 0: chosen at launch */
     int32_t xcd_copies;

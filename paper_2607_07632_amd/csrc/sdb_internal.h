@@ -11,6 +11,7 @@
 namespace sdb {
 
 constexpr int kMaxStages = SDB_MAX_STAGES;
+constexpr int kMaxEager = SDB_MAX_EAGER;
 constexpr int kBlock = 256;              // default threads per block of the fused kernel
 constexpr int kMaxBlock = 512;           // launch bound of the fused kernel
 constexpr int kLdsGroupLimit = 2048;     // LDS terminal: sums + counts of G <= 2048 groups (32 KB)
@@ -80,6 +81,7 @@ struct StageDev {
     uint32_t gk_div[SDB_MAX_PAYLOADS];     // key code = (code / div) % radix (div 1: skip)
     uint32_t gk_radix[SDB_MAX_PAYLOADS];   // 0: no modulo needed
     uint32_t gk_stride[SDB_MAX_PAYLOADS];  // group-id stride of that key
+    int32_t eg_slot;       // eager slot holding this stage's column, or -1
 };
 
 struct FusedParams {
@@ -106,7 +108,11 @@ struct FusedParams {
     uint32_t n_parts;
     uint32_t ring_off;         // byte offset of the per-wave record rings in dynamic LDS
     int32_t rec_wide;          // 1: record values need 64 bits (aggregate of two columns)
-    int32_t pad3_;
+    // eager columns (4-row items): slot k holds cols[eg_col[k]] for the current items
+    int32_t eg_n;
+    int32_t eg_col[kMaxEager];
+    int32_t agg_a_slot;        // eager slot of agg_a / agg_b, or -1
+    int32_t agg_b_slot;
     StageDev st[kMaxStages];
 };
 
@@ -199,8 +205,8 @@ hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
                          unsigned long long* pass_counts, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if
 // the instance does not exist.
-int fused_blocks_per_cu(int vector, int ipt, int terminal, int block, size_t lds_bytes);
-hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid, int block,
+int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, size_t lds_bytes);
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
                         size_t lds_bytes, hipStream_t s);
 hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);

@@ -590,6 +590,37 @@ __device__ __forceinline__ void load_column(const int32_t* col, const int64_t (&
     }
 }
 
+// A column for the current items: from its eager slot (loaded with the
+// other eager columns when the items started; the slot number is
+// wave-uniform) or loaded now, skipping items without a live row.
+template <int W, int IPT, bool EG>
+__device__ __forceinline__ void fetch_column(const FusedParams& p, int col, int slot, const int64_t (&item)[IPT],
+                                             const bool (&al)[IPT][W], const int32_t (&eg)[kMaxEager][IPT][W],
+                                             int32_t (&x)[IPT][W]) {
+    if constexpr (EG) {
+        if (slot >= 0) {
+#pragma unroll
+            for (int k = 0; k < kMaxEager; ++k)
+                if (slot == k) {
+                    SDB_ROWS(j, r) x[j][r] = eg[k][j][r];
+                }
+            return;
+        }
+    }
+    load_column<W, IPT>(p.cols[col], item, al, x);
+}
+
+// Issues the loads of every eager column for the current items at once, so
+// their latencies overlap instead of adding up stage after stage.
+template <int W, int IPT>
+__device__ __forceinline__ void load_eager(const FusedParams& p, const int64_t (&item)[IPT], const bool (&al)[IPT][W],
+                                           int32_t (&eg)[kMaxEager][IPT][W]) {
+#pragma unroll
+    for (int k = 0; k < kMaxEager; ++k) {
+        if (k < p.eg_n) load_column<W, IPT>(p.cols[p.eg_col[k]], item, al, eg[k]);
+    }
+}
+
 template <int W, int IPT>
 __device__ __forceinline__ void add_group(const StageDev& S, const uint32_t (&c)[IPT][W], uint32_t (&gid)[IPT][W]) {
     // dead rows may add garbage: their group id is never used
@@ -697,7 +728,7 @@ __device__ __forceinline__ bool wave_has_live(const bool (&al)[IPT][W]) {
 
 // Runs every stage and the terminal for IPT items of W rows each. All lanes
 // of the wave must call this together (the early exit is a wave-wide vote).
-template <int W, int IPT, int TERM>
+template <int W, int IPT, int TERM, bool EG>
 __device__ __forceinline__ void process_items(const FusedParams& p, const unsigned char* lds,
                                               const int64_t (&item)[IPT], bool (&al)[IPT][W],
                                               TermState<TERM>& ts) {
@@ -707,12 +738,14 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
         gid[j][r] = 0u;
         didx[j][r] = 0u;
     }
+    int32_t eg[kMaxEager][IPT][W];
+    if constexpr (EG) load_eager<W, IPT>(p, item, al, eg);
 
     for (int s = 0; s < p.nstages; ++s) {
         if (!wave_has_live<W, IPT>(al)) return;     // no live row left in the wave
         const StageDev& S = p.st[s];
         int32_t x[IPT][W];
-        load_column<W, IPT>(p.cols[S.col], item, al, x);
+        fetch_column<W, IPT, EG>(p, S.col, S.eg_slot, item, al, eg, x);
         switch (S.op) {
             case OP_PRED:
                 SDB_ROWS(j, r) al[j][r] = al[j][r] && range_pass(S.test, x[j][r]);
@@ -734,22 +767,22 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
     if (p.defer_stage >= 0) gather_deferred<W, IPT>(p.st[p.defer_stage], al, didx, gid);
 
     int32_t a[IPT][W], b[IPT][W];
-    load_column<W, IPT>(p.cols[p.agg_a], item, al, a);
+    fetch_column<W, IPT, EG>(p, p.agg_a, p.agg_a_slot, item, al, eg, a);
     long long v[IPT][W];
     switch (p.agg_kind) {
         case SDB_AGG_COL:
             SDB_ROWS(j, r) v[j][r] = a[j][r];
             break;
         case SDB_AGG_MUL:
-            load_column<W, IPT>(p.cols[p.agg_b], item, al, b);
+            fetch_column<W, IPT, EG>(p, p.agg_b, p.agg_b_slot, item, al, eg, b);
             SDB_ROWS(j, r) v[j][r] = (long long)a[j][r] * (long long)b[j][r];
             break;
         case SDB_AGG_SUB:
-            load_column<W, IPT>(p.cols[p.agg_b], item, al, b);
+            fetch_column<W, IPT, EG>(p, p.agg_b, p.agg_b_slot, item, al, eg, b);
             SDB_ROWS(j, r) v[j][r] = (long long)a[j][r] - (long long)b[j][r];
             break;
         default:
-            load_column<W, IPT>(p.cols[p.agg_b], item, al, b);
+            fetch_column<W, IPT, EG>(p, p.agg_b, p.agg_b_slot, item, al, eg, b);
             SDB_ROWS(j, r) v[j][r] = (long long)a[j][r] + (long long)b[j][r];
             break;
     }
@@ -781,7 +814,7 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
 // The kernel reads its parameters in place from the kernel-argument segment
 // (constant memory, scalar loads); indexing the by-value copy with a runtime
 // stage number could otherwise make the compiler copy it to scratch.
-template <int W, int IPT, int TERM>
+template <int W, int IPT, int TERM, bool EG>
 __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kernel_args) {
     (void)kernel_args;
     const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -831,14 +864,14 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
 #pragma unroll
             for (int r = 0; r < W; ++r) al[j][r] = item[j] < n_items;
         }
-        process_items<W, IPT, TERM>(p, lds, item, al, ts);
+        process_items<W, IPT, TERM, EG>(p, lds, item, al, ts);
     }
     if constexpr (W > 1) {
         // the last n mod W rows, one per lane, by the last block
         if (blockIdx.x == gridDim.x - 1) {
             int64_t row[1] = {n_items * W + (int64_t)threadIdx.x};
             bool al1[1][1] = {{row[0] < p.n}};
-            process_items<1, 1, TERM>(p, lds, row, al1, ts);
+            process_items<1, 1, TERM, false>(p, lds, row, al1, ts);
         }
     }
 
@@ -906,35 +939,40 @@ hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t
     return hipGetLastError();
 }
 
-template <int W, int IPT, int TERM>
+template <int W, int IPT, int TERM, bool EG>
 static const void* fused_fn() {
-    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM>);
+    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM, EG>);
 }
 
-// Instances: 4-row or 1-row items, 1/2/4 items per lane, every terminal.
-static const void* pick_fused(int vector, int ipt, int terminal) {
-#define SDB_PICK(Wv, I)                                                        \
-    if (ipt == I) {                                                            \
-        if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR>();    \
-        if (terminal == TERM_LDS) return fused_fn<Wv, I, TERM_LDS>();          \
-        if (terminal == TERM_GLOBAL) return fused_fn<Wv, I, TERM_GLOBAL>();    \
-        if (terminal == TERM_PART) return fused_fn<Wv, I, TERM_PART>();        \
+// Instances: 4-row or 1-row items, 1/2/4 items per lane, every terminal;
+// eager column loads for 4-row items with 1 or 2 items per lane.
+static const void* pick_fused(int vector, int ipt, int terminal, int eager) {
+#define SDB_PICK(Wv, I, EGv)                                                        \
+    if (ipt == I) {                                                                 \
+        if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR, EGv>();    \
+        if (terminal == TERM_LDS) return fused_fn<Wv, I, TERM_LDS, EGv>();          \
+        if (terminal == TERM_GLOBAL) return fused_fn<Wv, I, TERM_GLOBAL, EGv>();    \
+        if (terminal == TERM_PART) return fused_fn<Wv, I, TERM_PART, EGv>();        \
     }
-    if (vector) {
-        SDB_PICK(4, 1)
-        SDB_PICK(4, 2)
-        SDB_PICK(4, 4)
+    if (eager > 0) {
+        if (!vector) return nullptr;
+        SDB_PICK(4, 1, true)
+        SDB_PICK(4, 2, true)
+    } else if (vector) {
+        SDB_PICK(4, 1, false)
+        SDB_PICK(4, 2, false)
+        SDB_PICK(4, 4, false)
     } else {
-        SDB_PICK(1, 1)
-        SDB_PICK(1, 2)
-        SDB_PICK(1, 4)
+        SDB_PICK(1, 1, false)
+        SDB_PICK(1, 2, false)
+        SDB_PICK(1, 4, false)
     }
 #undef SDB_PICK
     return nullptr;
 }
 
-int fused_blocks_per_cu(int vector, int ipt, int terminal, int block, size_t lds_bytes) {
-    const void* fn = pick_fused(vector, ipt, terminal);
+int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, size_t lds_bytes) {
+    const void* fn = pick_fused(vector, ipt, terminal, eager);
     if (!fn) return -1;
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, block, lds_bytes) != hipSuccess)
@@ -942,9 +980,9 @@ int fused_blocks_per_cu(int vector, int ipt, int terminal, int block, size_t lds
     return blocks;
 }
 
-hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int grid, int block,
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
                         size_t lds_bytes, hipStream_t s) {
-    const void* fn = pick_fused(vector, ipt, terminal);
+    const void* fn = pick_fused(vector, ipt, terminal, eager);
     if (!fn) return hipErrorInvalidValue;
     void* args[] = {const_cast<FusedParams*>(&p)};
     return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);

@@ -79,7 +79,7 @@ class SdbQuery(C.Structure):
                 ("n_group_keys", i32), ("group_keys", SdbGroupKey * MAX_GROUP_KEYS),
                 ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
-                ("force_lds", i32), ("force_xcd", i32)]
+                ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32)]
 
 
 class SdbPlan(C.Structure):
@@ -87,7 +87,7 @@ class SdbPlan(C.Structure):
                 ("stage_index", i32 * MAX_STAGES), ("stage_pass", C.c_double * MAX_STAGES),
                 ("stage_lds", i32 * MAX_STAGES), ("stage_defer", i32 * MAX_STAGES),
                 ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
-                ("vector", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
+                ("vector", i32), ("eager", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
                 ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
                 ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
@@ -349,6 +349,7 @@ class StarQuery:
         q.grid_blocks = int(force.get("grid", 0))
         q.force_lds = int(force.get("lds", 0))
         q.force_xcd = int(force.get("xcd", 0))
+        q.force_eager = int(force.get("eager", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -447,7 +448,7 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
                 st["deferred_gather"] = True
         stages.append(st)
     return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
-            "ipt": plan.ipt, "vector": plan.vector, "block": plan.block, "grid": plan.grid,
+            "ipt": plan.ipt, "vector": plan.vector, "eager": plan.eager, "block": plan.block, "grid": plan.grid,
             "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
             "n_parts": plan.n_parts, "part_cap": int(plan.part_cap),
             "est_cost": round(plan.est_cost, 4),

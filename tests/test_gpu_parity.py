@@ -48,6 +48,8 @@ def test_config_parity(name):
     {"ipt": 4, "vector": -1, "terminal": "global"}, {"grid": 7}, {"grid": 1, "ipt": 2},
     {"terminal": "part"}, {"terminal": "part", "ipt": 1}, {"terminal": "part", "ipt": 4, "vector": -1},
     {"terminal": "part", "grid": 5},
+    {"eager": 4}, {"eager": 4, "ipt": 1}, {"eager": 2, "terminal": "part"}, {"eager": 1, "terminal": "global", "grid": 3},
+    {"eager": -1},
 ])
 def test_forced_plans_agree(name, force):
     w = workload(name)
@@ -102,7 +104,8 @@ def test_random_tiny_schemas_forced(seed):
     w = random_tiny_workload(seed + 1000, max_fact=5000, max_dim_rows=500, n_fact=4099)
     want = oracle_rows(w)
     for force in [{"vector": -1}, {"ipt": 1, "grid": 2}, {"ipt": 4}, {"order": True},
-                  {"terminal": "global"}, {"terminal": "part", "ipt": 1}, {"terminal": "part", "vector": -1, "grid": 3}]:
+                  {"terminal": "global"}, {"terminal": "part", "ipt": 1}, {"terminal": "part", "vector": -1, "grid": 3},
+                  {"eager": 4}, {"eager": 3, "ipt": 1, "terminal": "part"}, {"eager": -1}]:
         got, _ = run_gpu(w, force=force)
         assert_same(got.as_rows(), want, f"tiny {seed} {force}")
 
