@@ -58,6 +58,54 @@ def traffic_from_profile(workload: str):
     return float(m_bytes.group(1))
 
 
+def _in_range(x, p) -> "np.ndarray":
+    """Predicate dict {op, lo, hi} on an int64 array (measurement helper)."""
+    op, lo, hi = p["op"], p["lo"], p.get("hi")
+    if op == "between":
+        return (x >= lo) & (x <= hi)
+    return {"eq": x == lo, "ne": x != lo, "lt": x < lo, "le": x <= lo, "gt": x > lo, "ge": x >= lo}[op]
+
+
+def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_info: dict) -> float:
+    """B_alg: 4 bytes per fact column times the fraction of 128-byte lines (32
+    rows) holding a row that is still live where the plan first reads that
+    column, on the sample rows."""
+    import numpy as np
+    m = next(iter(sample.values())).size
+    m32 = m // 32 * 32
+    live = np.ones(m, dtype=bool)
+    seen, total = set(), 0.0
+
+    def read(col):
+        nonlocal total
+        if col not in seen:
+            seen.add(col)
+            total += 4.0 * float(live[:m32].reshape(-1, 32).any(axis=1).mean())
+
+    for st in plan_info["stages"]:
+        if st["kind"] == "pred":
+            p = query["fact_preds"][st["index"]]
+            read(p["col"])
+            live &= _in_range(sample[p["col"]].astype(np.int64), p)
+        else:
+            j = query["joins"][st["index"]]
+            read(j["fact_key"])
+            t = dims[j["dim"]]
+            keys = t[dim_keys[j["dim"]]].astype(np.int64)
+            ok = np.ones(keys.size, dtype=bool)
+            for p in j.get("preds", []):
+                ok &= _in_range(t[p["col"]].astype(np.int64), p)
+            order = np.argsort(keys, kind="stable")
+            fk = sample[j["fact_key"]].astype(np.int64)
+            pos = np.clip(np.searchsorted(keys[order], fk), 0, keys.size - 1)
+            live &= (keys[order][pos] == fk) & ok[order][pos]
+    agg = query["agg"]
+    read(agg["a"])
+    if agg["kind"] != "col":
+        read(agg["b"])
+    return total
+
+
 def upload_fact(cfg_name: str, n: int, device) -> dict:
     """Generate each fact column into one pinned host buffer and copy it to HBM."""
     import torch
@@ -138,8 +186,12 @@ def main(argv=None) -> int:
     def build_tables():
         return sdb.build_dims(dims, wdims.dim_keys, query, workspaces=workspaces)
 
+    build_ms = []
+
     def step(ev=None):
-        tabs = build_tables()
+        t0 = time.perf_counter()
+        tabs = build_tables()              # returns after the build's own synchronizations
+        build_ms.append(1000.0 * (time.perf_counter() - t0))
         q = sdb.StarQuery(fact, tabs, query, force)
         plan = q.plan()
         if ev is not None:
@@ -157,6 +209,7 @@ def main(argv=None) -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    build_ms.clear()
 
     events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(args.steps)]
     for ev in events:                      # create the HIP events before the timed region
@@ -172,7 +225,8 @@ def main(argv=None) -> int:
     t_total = time.perf_counter() - t_start
     kernel_ms = [ev[0].elapsed_time(ev[1]) for ev in events]
     kernel_ms_mean = float(np.mean(kernel_ms))
-    run_ms_mean = float(np.mean([ev[2].elapsed_time(ev[3]) for ev in events]))
+    run_ms = [ev[2].elapsed_time(ev[3]) for ev in events]
+    run_ms_mean = float(np.mean(run_ms))
 
     ms_per_step = 1000.0 * t_total / max(args.steps, 1)
     rows_per_s = n / (t_total / max(args.steps, 1))
@@ -210,7 +264,10 @@ def main(argv=None) -> int:
         },
         "effective_GBps_step": rows_per_s * b_dense_per_row / 1e9,
         "fused_kernel_ms": kernel_ms_mean,
+        "fused_kernel_ms_median_min": [float(np.median(kernel_ms)), float(np.min(kernel_ms))],
         "run_ms": run_ms_mean,
+        "run_ms_median_min": [float(np.median(run_ms)), float(np.min(run_ms))],
+        "build_ms": float(np.mean(build_ms)) if build_ms else None,
         "fused_kernel_rows_per_s": n / (kernel_ms_mean * 1e-3),
         "roofline": {
             "bound": "hbm",
@@ -254,6 +311,9 @@ def main(argv=None) -> int:
                       f"numpy oracle, one thread, {t_oracle:.1f} s",
         }
         result["parity_on_cpu_sample"] = parity
+        b_alg = b_alg_per_row(sample, wdims.dims, wdims.dim_keys, query, plan_info)
+        result["b_alg_bytes_per_row"] = b_alg
+        result["b_alg_GBps_fused"] = n * b_alg / (kernel_ms_mean * 1e-3) / 1e9
         log(f"[bench] oracle {m} rows in {t_oracle:.1f} s; GPU result on the sample "
             f"{'equals' if parity else 'DIFFERS FROM'} the oracle")
 
