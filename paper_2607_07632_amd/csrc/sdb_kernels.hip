@@ -503,8 +503,10 @@ struct TermState {
     // in 64-record flushes to this block's region (full coalesced stores)
     uint32_t* lfill = nullptr;            // records this block claimed in its region
     uint32_t* lhist = nullptr;            // records per partition in the region
-    uint32_t* ring_gid = nullptr;         // this wave's ring (kRing entries)
-    void* ring_val = nullptr;             // int64 values (FusedParams::rec_wide) or int32
+    // this wave's ring (kRing entries): with 64-bit values a group-id array
+    // and a value array; with 32-bit values one 8-byte {group id, value} each
+    uint32_t* ring_gid = nullptr;
+    void* ring_val = nullptr;
     uint32_t head = 0;                    // ring index of the oldest pending record (wave-uniform)
     uint32_t pend = 0;                    // pending records (wave-uniform, < kRing)
     uint32_t* rgid = nullptr;             // this block's record region
@@ -524,9 +526,16 @@ __device__ __forceinline__ void part_flush(const FusedParams& p, TermState<TERM_
     base = __shfl(base, 0, 64);
     if (lane < cnt) {
         const uint32_t slot = (ts.head + lane) & (kRing - 1u);
-        const uint32_t g = ts.ring_gid[slot];
-        const long long v = p.rec_wide ? static_cast<const long long*>(ts.ring_val)[slot]
-                                       : (long long)static_cast<const int32_t*>(ts.ring_val)[slot];
+        uint32_t g;
+        long long v;
+        if (p.rec_wide) {
+            g = ts.ring_gid[slot];
+            v = static_cast<const long long*>(ts.ring_val)[slot];
+        } else {
+            const unsigned long long e = static_cast<const unsigned long long*>(ts.ring_val)[slot];
+            g = (uint32_t)e;
+            v = (long long)(int32_t)(uint32_t)(e >> 32);
+        }
         const uint32_t pos = base + lane;
         if (pos < p.part_cap) {
             ts.rgid[pos] = g;
@@ -705,10 +714,11 @@ __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)
     }
 }
 
+// The deferred stage's codes for the rows still live (dead rows read slot 0,
+// a line every such row shares).
 template <int W, int IPT>
-__device__ __forceinline__ void gather_deferred(const StageDev& S, const bool (&al)[IPT][W],
-                                                const uint32_t (&didx)[IPT][W], uint32_t (&gid)[IPT][W]) {
-    uint32_t c[IPT][W];
+__device__ __forceinline__ void load_deferred(const StageDev& S, const bool (&al)[IPT][W],
+                                              const uint32_t (&didx)[IPT][W], uint32_t (&c)[IPT][W]) {
     if (S.width == 1) {
         SDB_ROWS(j, r) c[j][r] = ld_code<1>(S.map, al[j][r] ? didx[j][r] : 0u);
     } else if (S.width == 2) {
@@ -716,7 +726,6 @@ __device__ __forceinline__ void gather_deferred(const StageDev& S, const bool (&
     } else {
         SDB_ROWS(j, r) c[j][r] = ld_code<4>(S.map, al[j][r] ? didx[j][r] : 0u);
     }
-    add_group<W, IPT>(S, c, gid);
 }
 
 template <int W, int IPT>
@@ -764,10 +773,13 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
         }
     }
     if (!wave_has_live<W, IPT>(al)) return;
-    if (p.defer_stage >= 0) gather_deferred<W, IPT>(p.st[p.defer_stage], al, didx, gid);
+    // deferred codes and the aggregate column are loaded together, used after
+    uint32_t dc[IPT][W];
+    if (p.defer_stage >= 0) load_deferred<W, IPT>(p.st[p.defer_stage], al, didx, dc);
 
     int32_t a[IPT][W], b[IPT][W];
     fetch_column<W, IPT, EG>(p, p.agg_a, p.agg_a_slot, item, al, eg, a);
+    if (p.defer_stage >= 0) add_group<W, IPT>(p.st[p.defer_stage], dc, gid);
     long long v[IPT][W];
     switch (p.agg_kind) {
         case SDB_AGG_COL:
@@ -799,9 +811,13 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
             const unsigned long long m = __ballot(al[j][r]);
             if (al[j][r]) {
                 const uint32_t slot = (ts.head + ts.pend + (uint32_t)__popcll(m & below)) & (kRing - 1u);
-                ts.ring_gid[slot] = gid[j][r];
-                if (p.rec_wide) static_cast<long long*>(ts.ring_val)[slot] = v[j][r];
-                else static_cast<int32_t*>(ts.ring_val)[slot] = (int32_t)v[j][r];
+                if (p.rec_wide) {
+                    ts.ring_gid[slot] = gid[j][r];
+                    static_cast<long long*>(ts.ring_val)[slot] = v[j][r];
+                } else {
+                    static_cast<unsigned long long*>(ts.ring_val)[slot] =
+                        ((unsigned long long)(uint32_t)(int32_t)v[j][r] << 32) | gid[j][r];
+                }
             }
             ts.pend += (uint32_t)__popcll(m);
             if (ts.pend >= 64u) part_flush(p, ts, 64u);
@@ -833,11 +849,12 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
         ts.lfill = reinterpret_cast<uint32_t*>(lds);
         ts.lhist = ts.lfill + 1;
         for (uint32_t i = threadIdx.x; i < 1u + p.n_parts; i += blockDim.x) ts.lfill[i] = 0u;
-        // rings: every wave's values, then every wave's group ids
+        // rings: every wave's 8-byte entries (values, or {group id, value}),
+        // then (64-bit values) every wave's group ids
         const uint32_t wave = threadIdx.x >> 6;
         const uint32_t vbytes = p.rec_wide ? 8u : 4u;
-        ts.ring_val = lds + p.ring_off + (size_t)wave * kRing * vbytes;
-        ts.ring_gid = reinterpret_cast<uint32_t*>(lds + p.ring_off + (blockDim.x >> 6) * kRing * vbytes) +
+        ts.ring_val = lds + p.ring_off + (size_t)wave * kRing * 8u;
+        ts.ring_gid = reinterpret_cast<uint32_t*>(lds + p.ring_off + (blockDim.x >> 6) * kRing * 8u) +
                       (size_t)wave * kRing;
         ts.rgid = p.rec_gid + (uint64_t)blockIdx.x * p.part_cap;
         ts.rval = static_cast<unsigned char*>(p.rec_val) + (uint64_t)blockIdx.x * p.part_cap * vbytes;
