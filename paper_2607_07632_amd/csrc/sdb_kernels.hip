@@ -1179,9 +1179,10 @@ size_t part_scatter_lds_bytes(uint32_t n_parts, bool wide) {
 // writer in this pass, so plain read-add-write suffices (the outputs already
 // hold what the fused kernel added for records past a region's capacity).
 constexpr int kAggUnroll = 8;
+constexpr int kAggBlock = 1024;   // one work item is summed by 16 waves sharing its LDS table
 
 template <typename VT>
-__global__ void __launch_bounds__(256) part_agg_kernel(PartParams pp) {
+__global__ void __launch_bounds__(kAggBlock) part_agg_kernel(PartParams pp) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const uint32_t gpp = 1u << pp.part_shift;
     unsigned long long* lsum = reinterpret_cast<unsigned long long*>(smem);
@@ -1284,8 +1285,8 @@ hipError_t launch_part_passes(const PartParams& pp, hipStream_t s) {
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (wide) hipLaunchKernelGGL(part_agg_kernel<long long>, dim3(1024), dim3(256), agg_lds, s, pp);
-    else hipLaunchKernelGGL(part_agg_kernel<int32_t>, dim3(1024), dim3(256), agg_lds, s, pp);
+    if (wide) hipLaunchKernelGGL(part_agg_kernel<long long>, dim3(512), dim3(kAggBlock), agg_lds, s, pp);
+    else hipLaunchKernelGGL(part_agg_kernel<int32_t>, dim3(512), dim3(kAggBlock), agg_lds, s, pp);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(part_merge_kernel, dim3(fill_grid(pp.n_groups)), dim3(256), 0, s, pp);
