@@ -174,6 +174,8 @@ typedef struct sdb_agg {
  *  grid_blocks     blocks of the fused kernel
  *  force_lds       -1: every probe uses the device table (no LDS staging)
  *  force_xcd       -1: no per-XCD group-table copies; 1: use them
+ *  force_block     threads per block of the fused kernel: 64, 128, 256, 512
+ *                  or 1024 (1024 needs 4-row items, ipt 1 or 2, no eager loads)
  *  force_eager     -1: every column is loaded when its stage is reached, for
  *                  the items that still hold a live row; k in 1..SDB_MAX_EAGER:
  *                  the first k columns in order of use are loaded together
@@ -197,6 +199,7 @@ typedef struct sdb_query {
     int32_t force_lds;
     int32_t force_xcd;
     int32_t force_eager;
+    int32_t force_block;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):

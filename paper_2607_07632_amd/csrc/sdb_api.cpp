@@ -248,6 +248,12 @@ sdb_status check_query(const sdb_query* q) {
         return fail(SDB_UNSUPPORTED, "force_ipt %d is not 0, 1, 2 or 4", q->force_ipt);
     if (q->force_vector < -1 || q->force_vector > 1) return fail(SDB_INVALID_ARG, "bad force_vector %d", q->force_vector);
     if (q->grid_blocks < 0) return fail(SDB_INVALID_ARG, "negative grid_blocks");
+    if (q->force_block != 0 && q->force_block != 64 && q->force_block != 128 && q->force_block != 256 &&
+        q->force_block != kMaxBlock && q->force_block != kBigBlock)
+        return fail(SDB_INVALID_ARG, "force_block %d is not 0, 64, 128, 256, %d or %d", q->force_block, kMaxBlock,
+                    kBigBlock);
+    if (q->force_block == kBigBlock && (q->force_vector == -1 || q->force_ipt == 4 || q->force_eager > 0))
+        return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items, ipt 1 or 2 and no eager loads", kBigBlock);
     if (q->force_eager < -1 || q->force_eager > kMaxEager)
         return fail(SDB_INVALID_ARG, "force_eager %d is not in -1..%d", q->force_eager, kMaxEager);
     return SDB_OK;
@@ -881,31 +887,11 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     }
     plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
 
-    plan->ipt = q->force_ipt ? q->force_ipt : kDefaultIpt;
     const bool aligned = columns_aligned(q, plan);
     if (q->force_vector == 1 && !aligned && q->n_fact > 0)
         return fail(SDB_INVALID_ARG, "vector loads forced but a column is not 16-byte aligned");
     plan->vector = q->force_vector == -1 ? 0 : (aligned ? 1 : 0);
-    plan->block = kBlock;
     plan->grid = q->grid_blocks;
-
-    // eager columns: those whose lines the kernel reads anyway (enough rows
-    // still live where the column is first used)
-    plan->eager = 0;
-    if (q->force_eager > 0 && (!plan->vector || plan->ipt > 2))
-        return fail(SDB_INVALID_ARG, "eager loads need 4-row items and ipt 1 or 2");
-    if (plan->vector && plan->ipt <= 2 && q->n_fact > 0 && q->force_eager >= 0) {
-        int cols[SDB_MAX_FACT_COLS];
-        double live[SDB_MAX_FACT_COLS];
-        const int n_used = columns_in_use_order(q, plan, cols, live);
-        int k = 0;
-        if (q->force_eager > 0) {
-            k = std::min(q->force_eager, n_used);
-        } else if (kAutoEager) {
-            while (k < n_used && k < kMaxEager && live[k] >= kEagerMinLive) ++k;
-        }
-        plan->eager = k;
-    }
 
     // large group tables with many survivors: partitioned aggregation
     double f = 1.0;
@@ -933,6 +919,45 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             plan->n_parts = (int32_t)parts;
         }
     }
+
+    // Items per lane and block size, measured on the five workloads: plans
+    // with two or more lookups in device memory (dense maps outside LDS, hash
+    // tables) run fastest with one 4-row item per lane in blocks of 1024
+    // (more waves in flight per CU); the others with two items per lane in
+    // blocks of 512. 1-row items keep blocks of 256.
+    int device_lookups = 0;
+    for (int s = 0; s < n; ++s) {
+        if (plan->stage_kind[s] != 1) continue;
+        const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
+        if (d->kind == SDB_TABLE_HASH) device_lookups += 2;
+        else if (plan->stage_lds[s] == LDS_GLOBAL) device_lookups += 1;
+    }
+    const bool many_waves = plan->vector && device_lookups >= 2 && q->force_eager <= 0;
+    plan->ipt = q->force_ipt ? q->force_ipt : (many_waves ? 1 : kDefaultIpt);
+    if (q->force_block) plan->block = q->force_block;
+    else if (!plan->vector) plan->block = kBlock;
+    else plan->block = many_waves && plan->ipt <= 2 ? kBigBlock : kMaxBlock;
+    if (plan->block == kBigBlock && (!plan->vector || plan->ipt > 2))
+        return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items and ipt 1 or 2", kBigBlock);
+
+    // eager columns: those whose lines the kernel reads anyway (enough rows
+    // still live where the column is first used)
+    plan->eager = 0;
+    if (q->force_eager > 0 && (!plan->vector || plan->ipt > 2 || plan->block == kBigBlock))
+        return fail(SDB_INVALID_ARG, "eager loads need 4-row items, ipt 1 or 2 and blocks of at most %d", kMaxBlock);
+    if (plan->vector && plan->ipt <= 2 && plan->block <= kMaxBlock && q->n_fact > 0 && q->force_eager >= 0) {
+        int cols[SDB_MAX_FACT_COLS];
+        double live[SDB_MAX_FACT_COLS];
+        const int n_used = columns_in_use_order(q, plan, cols, live);
+        int k = 0;
+        if (q->force_eager > 0) {
+            k = std::min(q->force_eager, n_used);
+        } else if (kAutoEager) {
+            while (k < n_used && k < kMaxEager && live[k] >= kEagerMinLive) ++k;
+        }
+        plan->eager = k;
+    }
+
     plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
 
     // per-XCD private group tables for the global terminal when enough rows survive
@@ -1021,8 +1046,12 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         return fail(SDB_CAPACITY, "LDS terminal holds at most %d groups", kLdsGroupLimit);
     if (plan->ipt != 1 && plan->ipt != 2 && plan->ipt != 4)
         return fail(SDB_INVALID_ARG, "bad plan ipt %d", plan->ipt);
-    if (plan->block != 64 && plan->block != 128 && plan->block != 256 && plan->block != kMaxBlock)
+    if (plan->block != 64 && plan->block != 128 && plan->block != 256 && plan->block != kMaxBlock &&
+        plan->block != kBigBlock)
         return fail(SDB_INVALID_ARG, "bad plan block %d", plan->block);
+    if (plan->block == kBigBlock && (!plan->vector || plan->ipt > 2 || plan->eager > 0))
+        return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items, ipt 1 or 2 and no eager loads",
+                    kBigBlock);
     if (plan->vector && q->n_fact > 0 && !columns_aligned(q, plan))
         return fail(SDB_INVALID_ARG, "vector plan but a column is not 16-byte aligned");
     if (plan->eager < 0 || plan->eager > kMaxEager || (plan->eager > 0 && (!plan->vector || plan->ipt > 2)))

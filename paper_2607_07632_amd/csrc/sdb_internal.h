@@ -14,6 +14,7 @@ constexpr int kMaxStages = SDB_MAX_STAGES;
 constexpr int kMaxEager = SDB_MAX_EAGER;
 constexpr int kBlock = 256;              // default threads per block of the fused kernel
 constexpr int kMaxBlock = 512;           // launch bound of the fused kernel
+constexpr int kBigBlock = 1024;          // launch bound of its big-block instances (4-row items, IPT 1 or 2)
 constexpr int kLdsGroupLimit = 2048;     // LDS terminal: sums + counts of G <= 2048 groups (32 KB)
 constexpr int kLdsStageBudget = 32768;   // LDS bytes per block for staged dimension tables
 constexpr int kXcdCopies = 8;            // XCDs of an MI355X: private group-table copies

@@ -830,8 +830,8 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
 // The kernel reads its parameters in place from the kernel-argument segment
 // (constant memory, scalar loads); indexing the by-value copy with a runtime
 // stage number could otherwise make the compiler copy it to scratch.
-template <int W, int IPT, int TERM, bool EG>
-__global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kernel_args) {
+template <int W, int IPT, int TERM, bool EG, int LB>
+__global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args) {
     (void)kernel_args;
     const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
@@ -893,7 +893,7 @@ __global__ void __launch_bounds__(kMaxBlock) star_fused_kernel(FusedParams kerne
     }
 
     if constexpr (TERM == TERM_SCALAR) {
-        __shared__ unsigned long long red[2][kMaxBlock / 64];
+        __shared__ unsigned long long red[2][LB / 64];
         const unsigned long long s = wave_sum_u64(ts.sum);
         const unsigned long long c = wave_sum_u64(ts.cnt);
         if ((threadIdx.x & 63) == 0) {
@@ -956,40 +956,48 @@ hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t
     return hipGetLastError();
 }
 
-template <int W, int IPT, int TERM, bool EG>
+template <int W, int IPT, int TERM, bool EG, int LB = kMaxBlock>
 static const void* fused_fn() {
-    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM, EG>);
+    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM, EG, LB>);
 }
 
 // Instances: 4-row or 1-row items, 1/2/4 items per lane, every terminal;
-// eager column loads for 4-row items with 1 or 2 items per lane.
-static const void* pick_fused(int vector, int ipt, int terminal, int eager) {
-#define SDB_PICK(Wv, I, EGv)                                                        \
-    if (ipt == I) {                                                                 \
-        if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR, EGv>();    \
-        if (terminal == TERM_LDS) return fused_fn<Wv, I, TERM_LDS, EGv>();          \
-        if (terminal == TERM_GLOBAL) return fused_fn<Wv, I, TERM_GLOBAL, EGv>();    \
-        if (terminal == TERM_PART) return fused_fn<Wv, I, TERM_PART, EGv>();        \
+// eager column loads for 4-row items with 1 or 2 items per lane; blocks of
+// kBigBlock threads for 4-row items with 1 or 2 items per lane.
+static const void* pick_fused(int vector, int ipt, int terminal, int eager, int block) {
+#define SDB_PICK(Wv, I, EGv, LBv)                                                        \
+    if (ipt == I) {                                                                      \
+        if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR, EGv, LBv>();    \
+        if (terminal == TERM_LDS) return fused_fn<Wv, I, TERM_LDS, EGv, LBv>();          \
+        if (terminal == TERM_GLOBAL) return fused_fn<Wv, I, TERM_GLOBAL, EGv, LBv>();    \
+        if (terminal == TERM_PART) return fused_fn<Wv, I, TERM_PART, EGv, LBv>();        \
     }
+    if (block == kBigBlock) {
+        if (!vector || eager > 0) return nullptr;
+        SDB_PICK(4, 1, false, kBigBlock)
+        SDB_PICK(4, 2, false, kBigBlock)
+        return nullptr;
+    }
+    if (block > kMaxBlock) return nullptr;
     if (eager > 0) {
         if (!vector) return nullptr;
-        SDB_PICK(4, 1, true)
-        SDB_PICK(4, 2, true)
+        SDB_PICK(4, 1, true, kMaxBlock)
+        SDB_PICK(4, 2, true, kMaxBlock)
     } else if (vector) {
-        SDB_PICK(4, 1, false)
-        SDB_PICK(4, 2, false)
-        SDB_PICK(4, 4, false)
+        SDB_PICK(4, 1, false, kMaxBlock)
+        SDB_PICK(4, 2, false, kMaxBlock)
+        SDB_PICK(4, 4, false, kMaxBlock)
     } else {
-        SDB_PICK(1, 1, false)
-        SDB_PICK(1, 2, false)
-        SDB_PICK(1, 4, false)
+        SDB_PICK(1, 1, false, kMaxBlock)
+        SDB_PICK(1, 2, false, kMaxBlock)
+        SDB_PICK(1, 4, false, kMaxBlock)
     }
 #undef SDB_PICK
     return nullptr;
 }
 
 int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, size_t lds_bytes) {
-    const void* fn = pick_fused(vector, ipt, terminal, eager);
+    const void* fn = pick_fused(vector, ipt, terminal, eager, block);
     if (!fn) return -1;
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, block, lds_bytes) != hipSuccess)
@@ -999,7 +1007,7 @@ int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block,
 
 hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
                         size_t lds_bytes, hipStream_t s) {
-    const void* fn = pick_fused(vector, ipt, terminal, eager);
+    const void* fn = pick_fused(vector, ipt, terminal, eager, block);
     if (!fn) return hipErrorInvalidValue;
     void* args[] = {const_cast<FusedParams*>(&p)};
     return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);

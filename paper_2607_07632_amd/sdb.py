@@ -79,7 +79,8 @@ class SdbQuery(C.Structure):
                 ("n_group_keys", i32), ("group_keys", SdbGroupKey * MAX_GROUP_KEYS),
                 ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
-                ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32)]
+                ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
+                ("force_block", i32)]
 
 
 class SdbPlan(C.Structure):
@@ -350,6 +351,7 @@ class StarQuery:
         q.force_lds = int(force.get("lds", 0))
         q.force_xcd = int(force.get("xcd", 0))
         q.force_eager = int(force.get("eager", 0))
+        q.force_block = int(force.get("block", 0))
         self.q = q
         self.query = query
         self.tables = tables

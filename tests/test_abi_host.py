@@ -282,3 +282,31 @@ def test_fused_events_hook_validation():
     assert sdb.STATUS[L.sdb_set_fused_events(C.c_void_p(0x1000), None)] == "SDB_INVALID_ARG"
     assert sdb.STATUS[L.sdb_set_fused_events(None, C.c_void_p(0x1000))] == "SDB_INVALID_ARG"
     assert sdb.STATUS[L.sdb_set_fused_events(None, None)] == "SDB_OK"
+
+
+def test_plan_block_and_items_per_lane():
+    """Block size and items per lane: the planner's choice and the forcing rules."""
+    d = _fake_dim()                                   # dense, too large for LDS: a device-memory lookup
+    q = _query([d], [(0, 0)])
+    p = _plan(q)
+    assert (p.ipt, p.block) == (2, 512)
+    q2 = _query([d, _fake_dim()], [(0, 0)])          # two device-memory lookups
+    p2 = _plan(q2)
+    assert (p2.ipt, p2.block) == (1, 1024)
+    q3 = _query([d], [(0, 0)], align=False)          # 1-row items keep blocks of 256
+    assert _plan(q3).block == 256
+    for block, ipt, status in [(300, 0, "SDB_INVALID_ARG"), (1024, 4, "SDB_INVALID_ARG"), (128, 0, None)]:
+        qq = _query([d], [(0, 0)])
+        qq.force_block = block
+        qq.force_ipt = ipt
+        if status is None:
+            assert _plan(qq).block == block
+            continue
+        with pytest.raises(sdb.SdbError) as e:
+            _plan(qq)
+        assert e.value.name == status
+    qq = _query([d], [(0, 0)], align=False)
+    qq.force_block = 1024
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(qq)
+    assert e.value.name == "SDB_INVALID_ARG"
