@@ -172,7 +172,9 @@ typedef struct sdb_agg {
  *                  aligned); -1: 1-row items
  *  force_order     1: keep query order (predicates, then joins), no sampling
  *  grid_blocks     blocks of the fused kernel
- *  force_lds       -1: every probe uses the device table (no LDS staging)
+ *  force_lds       -1: every probe uses the device table (no LDS staging);
+ *                  2: LDS maps and bitmaps, but no rank tables; 3: rank tables
+ *                  for every deferred bitmap stage whose tables fit
  *  force_xcd       -1: no per-XCD group-table copies; 1: use them
  *  force_block     threads per block of the fused kernel: 64, 128, 256, 512
  *                  or 1024 (1024 needs 4-row items, ipt 1 or 2, no eager loads)
@@ -207,8 +209,13 @@ typedef struct sdb_query {
  *  MAP     the whole dense map copied into each block's LDS;
  *  BITS    the dense table's pass bitmap copied into LDS; the group-key code,
  *          if any, is gathered from the device map for the rows that survive
- *          every stage (stage_defer >= 0) or right after the bit test. */
-enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2 };
+ *          every stage (stage_defer >= 0) or right after the bit test;
+ *  RANK    the pass bitmap, the number of passing slots before every 64-slot
+ *          group, and the codes of the passing slots alone in slot order, all
+ *          copied into LDS (sdb_run_star_query derives the last two in its
+ *          run scratch): a passing key's code is the code at its rank, so the
+ *          group key needs no device-memory gather. Needs blocks of 1024. */
+enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3 };
 
 /* The one-pass plan. Stages run in the listed order; each is a fact
  * predicate (kind 0, index into preds[]) or a join probe (kind 1, index into

@@ -248,6 +248,8 @@ sdb_status check_query(const sdb_query* q) {
         return fail(SDB_UNSUPPORTED, "force_ipt %d is not 0, 1, 2 or 4", q->force_ipt);
     if (q->force_vector < -1 || q->force_vector > 1) return fail(SDB_INVALID_ARG, "bad force_vector %d", q->force_vector);
     if (q->grid_blocks < 0) return fail(SDB_INVALID_ARG, "negative grid_blocks");
+    if (q->force_lds < -1 || q->force_lds > 3 || q->force_lds == 1)
+        return fail(SDB_INVALID_ARG, "force_lds %d is not -1, 0, 2 or 3", q->force_lds);
     if (q->force_block != 0 && q->force_block != 64 && q->force_block != 128 && q->force_block != 256 &&
         q->force_block != kMaxBlock && q->force_block != kBigBlock)
         return fail(SDB_INVALID_ARG, "force_block %d is not 0, 64, 128, 256, %d or %d", q->force_block, kMaxBlock,
@@ -334,6 +336,7 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
     if (S.kind == ST_HASH) S.op = OP_HASH;
     else if (S.nslots == 0) S.op = OP_NEVER;
     else if (S.lds_mode == LDS_BITS) S.op = OP_LDS_BITS;
+    else if (S.lds_mode == LDS_RANK) S.op = OP_LDS_RANK1 + wsel;
     else if (S.lds_mode == LDS_MAP) S.op = OP_LDS_MAP1 + wsel;
     else S.op = OP_MAP1 + wsel;
     return S;
@@ -348,6 +351,18 @@ uint64_t stage_table_bytes(const sdb_query* q, int kind, int index) {
 // Bytes a dense table occupies in LDS as its whole map or as its pass bitmap.
 uint64_t lds_map_bytes(const sdb_dim* d) { return align_up(d->n_slots * (uint64_t)d->width, 16); }
 uint64_t lds_bits_bytes(const sdb_dim* d) { return align_up((d->n_slots + 31) / 32 * 4, 16); }
+// Rank tables of LDS_RANK behind the bitmap: one uint32 count per 64 slots,
+// then the passing slots' codes (at least 16 bytes each part).
+uint64_t lds_rank_bytes(const sdb_dim* d) { return std::max<uint64_t>(16, align_up((d->n_slots + 63) / 64 * 4, 16)); }
+uint64_t lds_codes_bytes(const sdb_dim* d) {
+    return std::max<uint64_t>(16, align_up((uint64_t)d->n_pass * (uint64_t)d->width, 16));
+}
+bool rank_fits(const sdb_dim* d) {
+    return d->kind == SDB_TABLE_DENSE && d->bits && d->n_slots > 0 && (d->n_slots + 63) / 64 <= kRankGroups &&
+           lds_bits_bytes(d) + lds_rank_bytes(d) + lds_codes_bytes(d) <= kLdsRankBudget;
+}
+// Device-memory copies of a stage's rank tables in the run scratch (256-byte aligned parts).
+uint64_t rank_scratch_part(uint64_t bytes) { return align_up(bytes, 256); }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -467,6 +482,15 @@ uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
             p->st[s].lds_bytes = (uint32_t)bytes;
         }
         off += bytes;
+        if (plan->stage_lds[s] == LDS_RANK) {
+            if (p) {
+                p->st[s].lds_rank_off = (uint32_t)off;
+                p->st[s].lds_rank_bytes = (uint32_t)lds_rank_bytes(d);
+                p->st[s].lds_codes_off = (uint32_t)(off + lds_rank_bytes(d));
+                p->st[s].lds_codes_bytes = (uint32_t)lds_codes_bytes(d);
+            }
+            off += lds_rank_bytes(d) + lds_codes_bytes(d);
+        }
     }
     return (uint32_t)off;
 }
@@ -585,6 +609,17 @@ PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
     return L;
 }
 
+// Run scratch of the LDS_RANK stages' tables; the terminal's scratch follows it.
+uint64_t rank_scratch_bytes(const sdb_query* q, const sdb_plan* plan) {
+    uint64_t b = 0;
+    for (int s = 0; s < plan->n_stages; ++s) {
+        if (plan->stage_lds[s] != LDS_RANK) continue;
+        const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
+        b += rank_scratch_part(lds_rank_bytes(d)) + rank_scratch_part(lds_codes_bytes(d));
+    }
+    return b;
+}
+
 // Dynamic LDS of a fused-kernel launch: the plan's layout, then (partitioned
 // terminal) one record ring per wave.
 uint32_t ring_lds_bytes(const sdb_query* q, const sdb_plan* plan) {
@@ -595,6 +630,9 @@ uint32_t ring_lds_bytes(const sdb_query* q, const sdb_plan* plan) {
 uint32_t launch_lds_bytes(const sdb_query* q, const sdb_plan* plan) {
     return (uint32_t)plan->lds_bytes + ring_lds_bytes(q, plan);
 }
+
+// LDS a block may use so that the blocks the grid counts on all fit (see choose_grid).
+constexpr uint32_t kLdsUsable = 152u * 1024u;
 
 sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) {
     const int64_t rows_per_item = plan->vector ? 4 : 1;
@@ -618,7 +656,7 @@ sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) 
     // late) while five of 27,568 do. Count LDS in 2 KB granules out of 152 KB.
     const uint32_t lds = launch_lds_bytes(q, plan);
     if (lds > 0) {
-        const uint32_t granule = 2048, usable = 152u * 1024u;
+        const uint32_t granule = 2048, usable = kLdsUsable;
         const int by_lds = (int)(usable / (uint32_t)align_up(lds, granule));
         per_cu = std::max(1, std::min(per_cu, by_lds));
     }
@@ -958,7 +996,28 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         plan->eager = k;
     }
 
+    // LDS rank tables instead of the deferred gather of a bitmap stage's code.
+    // Their LDS footprint leaves one block of 1024 per CU, which pays only when
+    // no other lookup goes to device memory (measured: c2 0.185 -> 0.173 ms;
+    // c3, with its device-memory customer map, unchanged; c4 much slower).
+    const bool want_rank = q->force_lds == 3 || (q->force_lds == 0 && device_lookups == 0);
+    if (want_rank && plan->vector && plan->ipt <= 2 && plan->eager == 0 &&
+        (q->force_block == 0 || q->force_block == kBigBlock)) {
+        for (int s = 0; s < n; ++s) {
+            if (plan->stage_defer[s] != 0 || !rank_fits(q->joins[plan->stage_index[s]].dim)) continue;
+            plan->stage_lds[s] = LDS_RANK;
+            plan->stage_defer[s] = -1;
+            const int block_before = plan->block;
+            plan->block = kBigBlock;
+            if (lds_layout(q, plan, nullptr) + ring_lds_bytes(q, plan) > kLdsUsable) {   // keep the bitmap
+                plan->stage_lds[s] = LDS_BITS;
+                plan->stage_defer[s] = 0;
+                plan->block = block_before;
+            }
+        }
+    }
     plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
+    const uint64_t rank_bytes = rank_scratch_bytes(q, plan);
 
     // per-XCD private group tables for the global terminal when enough rows survive
     const uint64_t copy_bytes = (uint64_t)kXcdCopies * plan->n_groups * 16;
@@ -966,7 +1025,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     if (q->force_xcd == 1) xcd = term == TERM_GLOBAL;
     if (q->force_xcd == -1) xcd = false;
     plan->xcd_copies = xcd ? kXcdCopies : 0;
-    plan->run_scratch_bytes = xcd ? (int64_t)copy_bytes : 0;
+    plan->run_scratch_bytes = (int64_t)rank_bytes + (xcd ? (int64_t)copy_bytes : 0);
 
     if (term == TERM_PART) {
         // records are written per block: the grid is fixed now
@@ -981,7 +1040,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         plan->part_cap = (int64_t)align_up((uint64_t)std::max<int64_t>(plan->part_cap, 64), 64);
         if ((uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFF0ull)
             plan->part_cap = (int64_t)(0xFFFFFFF0ull / (uint64_t)plan->grid) / 64 * 64;
-        plan->run_scratch_bytes = (int64_t)part_layout(q, plan).total;
+        plan->run_scratch_bytes = (int64_t)rank_bytes + (int64_t)part_layout(q, plan).total;
     }
     return ok();
 }
@@ -1008,9 +1067,12 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
             if (lm != LDS_GLOBAL) {
                 if (k != 1 || q->joins[i].dim->kind != SDB_TABLE_DENSE)
                     return fail(SDB_INVALID_ARG, "plan stage %d: LDS placement needs a dense table", s);
-                if (lm != LDS_MAP && lm != LDS_BITS) return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
-                if (lm == LDS_BITS && !q->joins[i].dim->bits)
+                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
+                if ((lm == LDS_BITS || lm == LDS_RANK) && !q->joins[i].dim->bits)
                     return fail(SDB_INVALID_ARG, "plan stage %d: table has no bitmap", s);
+                if (lm == LDS_RANK && !rank_fits(q->joins[i].dim))
+                    return fail(SDB_INVALID_ARG, "plan stage %d: rank tables do not fit LDS", s);
             }
             if (plan->stage_defer[s] != -1) {
                 if (plan->stage_defer[s] != 0 || lm != LDS_BITS)
@@ -1058,8 +1120,11 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         return fail(SDB_INVALID_ARG, "bad plan eager %d (needs 4-row items and ipt 1 or 2)", plan->eager);
     if (plan->xcd_copies != 0 && (plan->xcd_copies != kXcdCopies || plan->terminal != TERM_GLOBAL))
         return fail(SDB_INVALID_ARG, "bad plan xcd_copies %d", plan->xcd_copies);
-    uint64_t need_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
-    if (plan->terminal == TERM_PART) need_scratch = part_layout(q, plan).total;
+    // run scratch: the rank tables, then the terminal's part
+    const uint64_t rank_bytes = rank_scratch_bytes(q, plan);
+    uint64_t term_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
+    if (plan->terminal == TERM_PART) term_scratch = part_layout(q, plan).total;
+    const uint64_t need_scratch = rank_bytes + term_scratch;
     if (need_scratch) {
         if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
         if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
@@ -1076,8 +1141,29 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     p.ring_off = (uint32_t)plan->lds_bytes;
 
     hipStream_t s = (hipStream_t)stream;
+    uint8_t* term_base = (uint8_t*)scratch + rank_bytes;
+    {
+        // the rank tables of LDS_RANK stages, derived from their bitmaps and maps
+        uint64_t off = 0;
+        for (int st_i = 0; st_i < plan->n_stages; ++st_i) {
+            if (plan->stage_lds[st_i] != LDS_RANK) continue;
+            const sdb_dim* d = q->joins[plan->stage_index[st_i]].dim;
+            RankParams rp;
+            rp.bits = (const uint32_t*)d->bits;
+            rp.map = d->map;
+            rp.width = d->width;
+            rp.nslots = (uint32_t)d->n_slots;
+            rp.prefix = (uint32_t*)((uint8_t*)scratch + off);
+            off += rank_scratch_part(lds_rank_bytes(d));
+            rp.codes = (uint8_t*)scratch + off;
+            off += rank_scratch_part(lds_codes_bytes(d));
+            p.st[st_i].rank = rp.prefix;
+            p.st[st_i].codes = rp.codes;
+            if (q->n_fact > 0) SDB_HIP(launch_rank_build(rp, s), "rank table launch");
+        }
+    }
     if (plan->xcd_copies) {
-        SDB_HIP(launch_fill_u64((unsigned long long*)scratch, need_scratch / 8, s), "copy fill");
+        SDB_HIP(launch_fill_u64((unsigned long long*)term_base, term_scratch / 8, s), "copy fill");
     } else {
         SDB_HIP(launch_zero_pair((unsigned long long*)sums, (unsigned long long*)counts, plan->n_groups, s),
                 "output fill");
@@ -1085,12 +1171,12 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     p.sums = (unsigned long long*)sums;
     p.counts = (unsigned long long*)counts;
     p.xcd_copies = plan->xcd_copies;
-    p.xtab = plan->xcd_copies ? (unsigned long long*)scratch : nullptr;
+    p.xtab = plan->xcd_copies ? (unsigned long long*)term_base : nullptr;
     PartParams pp;
     std::memset(&pp, 0, sizeof pp);
     if (plan->terminal == TERM_PART) {
         const PartLayout L = part_layout(q, plan);
-        uint8_t* base = (uint8_t*)scratch;
+        uint8_t* base = term_base;
         p.region_count = (uint32_t*)(base + L.region_count);
         p.rec_gid = (uint32_t*)(base + L.rec_gid);
         p.rec_val = base + L.rec_val;
@@ -1134,7 +1220,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         if (plan->terminal == TERM_PART) SDB_HIP(launch_part_passes(pp, s), "partition passes launch");
     }
     if (plan->xcd_copies)
-        SDB_HIP(launch_xcd_merge((const unsigned long long*)scratch, plan->xcd_copies, plan->n_groups,
+        SDB_HIP(launch_xcd_merge((const unsigned long long*)term_base, plan->xcd_copies, plan->n_groups,
                                  (unsigned long long*)sums, (unsigned long long*)counts, s),
                 "copy merge launch");
     return ok();

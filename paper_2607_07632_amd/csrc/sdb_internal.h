@@ -37,11 +37,19 @@ enum StageOp : int32_t {
     OP_MAP1 = 6,      // map in device memory, 1/2/4-byte codes
     OP_MAP2 = 7,
     OP_MAP4 = 8,
-    OP_HASH = 9       // open-addressing table in device memory
+    OP_HASH = 9,      // open-addressing table in device memory
+    OP_LDS_RANK1 = 10,  // pass bitmap, ranks and passing codes in LDS, 1/2/4-byte codes
+    OP_LDS_RANK2 = 11,
+    OP_LDS_RANK4 = 12
 };
 // How a table's code becomes part of the group id.
 enum GroupMode : int32_t { GK_NONE = 0, GK_ONE = 1, GK_GENERAL = 2 };
-enum LdsMode : int32_t { LDS_GLOBAL = SDB_LDS_GLOBAL, LDS_MAP = SDB_LDS_MAP, LDS_BITS = SDB_LDS_BITS };
+enum LdsMode : int32_t {
+    LDS_GLOBAL = SDB_LDS_GLOBAL,
+    LDS_MAP = SDB_LDS_MAP,
+    LDS_BITS = SDB_LDS_BITS,
+    LDS_RANK = SDB_LDS_RANK
+};
 enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3, TERM_PART = 4 };
 
 // Partitioned aggregation (TERM_PART): partition of group g is g >> part_shift.
@@ -50,6 +58,8 @@ constexpr int kPartMaxShift = 12;         // at most 4096 groups per partition (
 constexpr int kPartChunk = 65536;         // records per aggregation work item
 constexpr int kScatterChunk = 4096;       // records one scatter block sorts in LDS at a time
 constexpr uint32_t kRingEntries = 128;     // fused kernel: per-wave record ring (group id + value)
+constexpr uint32_t kLdsRankBudget = 98304;  // LDS for a stage's rank tables (bitmap, counts, codes)
+constexpr uint32_t kRankGroups = 4096;      // at most this many 64-slot groups (one scan block)
 
 // A literal comparison lowered to one unsigned range test over int32:
 // pass  <=>  ((uint32_t)(x - lo) <= span) != negate.
@@ -83,6 +93,24 @@ struct StageDev {
     uint32_t gk_radix[SDB_MAX_PAYLOADS];   // 0: no modulo needed
     uint32_t gk_stride[SDB_MAX_PAYLOADS];  // group-id stride of that key
     int32_t eg_slot;       // eager slot holding this stage's column, or -1
+    // LDS_RANK: running counts (uint32 per 64 slots) and the passing slots'
+    // codes, staged from device memory (run scratch) behind the bitmap
+    const void* rank;
+    const void* codes;
+    uint32_t lds_rank_off;
+    uint32_t lds_rank_bytes;
+    uint32_t lds_codes_off;
+    uint32_t lds_codes_bytes;
+};
+
+// Derives a dense table's rank tables (LDS_RANK) in device memory.
+struct RankParams {
+    const uint32_t* bits;      // pass bitmap, nslots bits
+    const void* map;           // packed codes, width bytes per slot
+    int32_t width;
+    uint32_t nslots;
+    uint32_t* prefix;          // (nslots + 63) / 64 entries: passing slots before each 64-slot group
+    void* codes;               // codes of the passing slots in slot order
 };
 
 struct FusedParams {
@@ -209,6 +237,7 @@ hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
 int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, size_t lds_bytes);
 hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
                         size_t lds_bytes, hipStream_t s);
+hipError_t launch_rank_build(const RankParams& rp, hipStream_t s);
 hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);

@@ -439,6 +439,77 @@ hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
+// rank tables of a dense table (LDS_RANK placement)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint32_t rank_word(const RankParams& rp, uint32_t w) {
+    return w < (rp.nslots + 31u) / 32u ? rp.bits[w] : 0u;
+}
+
+// One block of 1024 threads: prefix[g] = passing slots in 64-slot groups
+// before g (exclusive scan of the groups' popcounts).
+__global__ void __launch_bounds__(1024) rank_prefix_kernel(RankParams rp) {
+    __shared__ uint32_t wsum[16];
+    const uint32_t n64 = (rp.nslots + 63u) / 64u;
+    constexpr uint32_t kPer = kRankGroups / 1024;
+    const uint32_t g0 = threadIdx.x * kPer;
+    uint32_t c[kPer];
+    uint32_t loc = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k) {
+        const uint32_t g = g0 + k;
+        c[k] = g < n64 ? (uint32_t)(__popc(rank_word(rp, 2 * g)) + __popc(rank_word(rp, 2 * g + 1))) : 0u;
+        loc += c[k];
+    }
+    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+    uint32_t x = loc;
+    for (uint32_t off = 1; off < 64u; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63u) wsum[wave] = x;
+    __syncthreads();
+    uint32_t run = x - loc;
+    for (uint32_t w = 0; w < wave; ++w) run += wsum[w];
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k) {
+        const uint32_t g = g0 + k;
+        if (g < n64) rp.prefix[g] = run;
+        run += c[k];
+    }
+}
+
+// One thread per bitmap word: the word's passing slots store their codes at
+// their ranks.
+__global__ void __launch_bounds__(256) rank_codes_kernel(RankParams rp) {
+    const uint32_t n_words = (rp.nslots + 31u) / 32u;
+    const uint32_t w = blockIdx.x * blockDim.x + threadIdx.x;
+    if (w >= n_words) return;
+    uint32_t bits = rp.bits[w];
+    uint32_t r = rp.prefix[w >> 1] + ((w & 1u) ? (uint32_t)__popc(rp.bits[w - 1]) : 0u);
+    while (bits) {
+        const uint32_t b = (uint32_t)__ffs(bits) - 1u;
+        bits &= bits - 1u;
+        const uint32_t slot = w * 32u + b;
+        if (rp.width == 1) static_cast<uint8_t*>(rp.codes)[r] = static_cast<const uint8_t*>(rp.map)[slot];
+        else if (rp.width == 2) static_cast<uint16_t*>(rp.codes)[r] = static_cast<const uint16_t*>(rp.map)[slot];
+        else static_cast<uint32_t*>(rp.codes)[r] = static_cast<const uint32_t*>(rp.map)[slot];
+        ++r;
+    }
+}
+
+hipError_t launch_rank_build(const RankParams& rp, hipStream_t s) {
+    if (rp.nslots == 0) return hipSuccess;
+    if ((rp.nslots + 63u) / 64u > kRankGroups) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(rank_prefix_kernel, dim3(1), dim3(1024), 0, s, rp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const uint32_t n_words = (rp.nslots + 31u) / 32u;
+    hipLaunchKernelGGL(rank_codes_kernel, dim3((n_words + 255u) / 256u), dim3(256), 0, s, rp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // plan sampling: pass count of every stage on its own over a strided sample
 // ---------------------------------------------------------------------------
 
@@ -683,6 +754,29 @@ __device__ __forceinline__ void stage_bits(const StageDev& S, const unsigned cha
     }
 }
 
+// Pass bitmap, ranks and passing codes in LDS: a passing key's code is the
+// rank-th code (rank = passing slots before it).
+template <int W, int IPT, int WB>
+__device__ __forceinline__ void stage_rank(const StageDev& S, const unsigned char* lds, const int32_t (&x)[IPT][W],
+                                           bool (&al)[IPT][W], uint32_t (&gid)[IPT][W]) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(lds + S.lds_off);
+    const uint32_t* pre = reinterpret_cast<const uint32_t*>(lds + S.lds_rank_off);
+    const void* codes = static_cast<const void*>(lds + S.lds_codes_off);
+    uint32_t c[IPT][W];
+    SDB_ROWS(j, r) {
+        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+        const bool ok = al[j][r] && idx < S.nslots;
+        const uint32_t i = ok ? idx : 0u;
+        const uint32_t w = words[i >> 5];
+        const bool pass = ok && ((w >> (i & 31u)) & 1u);
+        const uint32_t lower = (i & 32u) ? (uint32_t)__popc(words[(i >> 5) - 1u]) : 0u;
+        const uint32_t rank = pre[i >> 6] + lower + (uint32_t)__popc(w & ((1u << (i & 31u)) - 1u));
+        c[j][r] = ld_code<WB>(codes, pass ? rank : 0u);
+        al[j][r] = pass;
+    }
+    add_group<W, IPT>(S, c, gid);
+}
+
 template <int W, int IPT>
 __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)[IPT][W], bool (&al)[IPT][W],
                                            uint32_t (&gid)[IPT][W]) {
@@ -767,6 +861,9 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
             case OP_MAP2: stage_map<W, IPT, 2, false>(S, lds, x, al, gid); break;
             case OP_MAP4: stage_map<W, IPT, 4, false>(S, lds, x, al, gid); break;
             case OP_HASH: stage_hash<W, IPT>(S, x, al, gid); break;
+            case OP_LDS_RANK1: stage_rank<W, IPT, 1>(S, lds, x, al, gid); break;
+            case OP_LDS_RANK2: stage_rank<W, IPT, 2>(S, lds, x, al, gid); break;
+            case OP_LDS_RANK4: stage_rank<W, IPT, 4>(S, lds, x, al, gid); break;
             default:   // OP_NEVER
                 SDB_ROWS(j, r) al[j][r] = false;
                 break;
@@ -866,6 +963,14 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
         const v4i* src = reinterpret_cast<const v4i*>(S.lds_mode == LDS_MAP ? S.map : S.bits);
         v4i* dst = reinterpret_cast<v4i*>(lds + S.lds_off);
         for (uint32_t i = threadIdx.x; i < S.lds_bytes / 16u; i += blockDim.x) dst[i] = src[i];
+        if (S.lds_mode == LDS_RANK) {
+            const v4i* rsrc = reinterpret_cast<const v4i*>(S.rank);
+            v4i* rdst = reinterpret_cast<v4i*>(lds + S.lds_rank_off);
+            for (uint32_t i = threadIdx.x; i < S.lds_rank_bytes / 16u; i += blockDim.x) rdst[i] = rsrc[i];
+            const v4i* csrc = reinterpret_cast<const v4i*>(S.codes);
+            v4i* cdst = reinterpret_cast<v4i*>(lds + S.lds_codes_off);
+            for (uint32_t i = threadIdx.x; i < S.lds_codes_bytes / 16u; i += blockDim.x) cdst[i] = csrc[i];
+        }
     }
     __syncthreads();
 

@@ -35,7 +35,7 @@ TABLES = {"auto": 0, "dense": 1, "hash": 2}
 AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
 TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3, "part": 4}
 TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global", 4: "part"}
-LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits"}
+LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank"}
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
           4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
 

@@ -50,7 +50,9 @@ def test_config_parity(name):
     {"terminal": "part", "grid": 5},
     {"eager": 4}, {"eager": 4, "ipt": 1}, {"eager": 2, "terminal": "part"}, {"eager": 1, "terminal": "global", "grid": 3},
     {"eager": -1}, {"block": 1024}, {"block": 1024, "ipt": 1, "terminal": "part"}, {"block": 512, "ipt": 1},
-    {"block": 64, "ipt": 2, "terminal": "global"},
+    {"block": 64, "ipt": 2, "terminal": "global"}, {"lds": 2}, {"lds": 2, "terminal": "part"},
+    {"lds": 3}, {"lds": 3, "terminal": "global"}, {"lds": 3, "ipt": 1, "terminal": "part"},
+    {"ipt": 1, "block": 1024, "terminal": "global"},
 ])
 def test_forced_plans_agree(name, force):
     w = workload(name)
@@ -107,7 +109,9 @@ def test_random_tiny_schemas_forced(seed):
     for force in [{"vector": -1}, {"ipt": 1, "grid": 2}, {"ipt": 4}, {"order": True},
                   {"terminal": "global"}, {"terminal": "part", "ipt": 1}, {"terminal": "part", "vector": -1, "grid": 3},
                   {"eager": 4}, {"eager": 3, "ipt": 1, "terminal": "part"}, {"eager": -1},
-                  {"block": 1024, "ipt": 1}, {"block": 1024, "terminal": "part", "grid": 2}]:
+                  {"block": 1024, "ipt": 1}, {"block": 1024, "terminal": "part", "grid": 2}, {"lds": 2},
+                  {"lds": 3}, {"lds": 3, "terminal": "part", "grid": 3},
+                  {"lds": -1, "terminal": "part"}]:
         got, _ = run_gpu(w, force=force)
         assert_same(got.as_rows(), want, f"tiny {seed} {force}")
 
