@@ -786,21 +786,32 @@ __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)
 #pragma unroll
     for (int j0 = 0; j0 < IPT; j0 += HJ) {
         uint32_t h[HJ][W];
-        unsigned long long sl[HJ][W];
+        unsigned long long sl[HJ][W], sn[HJ][W];
 #pragma unroll
         for (int jj = 0; jj < HJ; ++jj)
 #pragma unroll
             for (int r = 0; r < W; ++r) {
                 h[jj][r] = hash_slot(S, x[j0 + jj][r]);
                 sl[jj][r] = 0ull;
-                if (al[j0 + jj][r]) sl[jj][r] = tab[h[jj][r]];
+                sn[jj][r] = 0ull;
+                if (al[j0 + jj][r]) {
+                    // the home slot and the next one (mostly the same cache line)
+                    sl[jj][r] = tab[h[jj][r]];
+                    sn[jj][r] = tab[(h[jj][r] + 1u) & S.hmask];
+                }
             }
 #pragma unroll
         for (int jj = 0; jj < HJ; ++jj)
 #pragma unroll
             for (int r = 0; r < W; ++r) {
                 uint32_t c = S.sentinel;
-                if (al[j0 + jj][r]) c = hash_resolve(S, x[j0 + jj][r], h[jj][r], sl[jj][r]);
+                if (al[j0 + jj][r]) {
+                    const unsigned long long a = sl[jj][r];
+                    const uint32_t ahi = (uint32_t)(a >> 32);
+                    if (ahi == 0u) c = S.sentinel;
+                    else if ((int32_t)(uint32_t)a == x[j0 + jj][r]) c = ahi - 1u;
+                    else c = hash_resolve(S, x[j0 + jj][r], (h[jj][r] + 1u) & S.hmask, sn[jj][r]);
+                }
                 al[j0 + jj][r] = al[j0 + jj][r] && c < S.sentinel;
                 if (S.gk_mode == GK_ONE) gid[j0 + jj][r] += c * S.gk_stride[0];
                 else if (S.gk_mode == GK_GENERAL) gid[j0 + jj][r] += code_contribution(S, c);
