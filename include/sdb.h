@@ -281,10 +281,11 @@ SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* byt
  * aligned, workspace_bytes >= sdb_dim_required_bytes) on `stream`, and fills
  * `out` (host). Passes over the dimension rows: statistics (key range, pass
  * count, payload ranges), then the direct-mapped map (Section 3.3: one code
- * per key, the sentinel for filtered rows; 1, 2 or 4 bytes by payload domain)
- * and its pass bitmap, or the open-addressing table (64-bit compare-and-swap
- * inserts). Synchronizes the stream twice (to read the statistics, then the
- * duplicate-key check: a dense map must end with one occupied slot per row).
+ * per key, the sentinel for a filtered row, all ones for an absent key; 1, 2
+ * or 4 bytes by payload domain) and its pass bitmap, or the open-addressing
+ * table (64-bit compare-and-swap inserts). Synchronizes the stream twice (to
+ * read the statistics, then the duplicate-key check: a dense map must end
+ * with one occupied slot per row).
  * Errors: INVALID_ARG, UNSUPPORTED (payload domain >= 2^32 - 2), KEY_RANGE,
  * WORKSPACE_TOO_SMALL, DUP_KEY, HIP_ERROR. */
 SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace,
