@@ -714,7 +714,10 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
     if (n_dims < 0 || n_dims > SDB_MAX_JOINS) return fail(SDB_INVALID_ARG, "n_dims %d is not in 0..%d", n_dims, SDB_MAX_JOINS);
     if (n_dims > 0 && (!descs || !workspaces || !workspace_bytes || !outs)) return fail(SDB_INVALID_ARG, "null argument");
     hipStream_t s = (hipStream_t)stream;
-    BuildParams bp[SDB_MAX_JOINS];
+    BuildBatch bb;
+    std::memset(&bb, 0, sizeof bb);
+    bb.n = n_dims;
+    BuildParams* bp = bb.bp;
     DimStats hs[SDB_MAX_JOINS];
     // every table's arguments first, so nothing launches for an invalid batch
     for (int d = 0; d < n_dims; ++d) {
@@ -733,10 +736,8 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
     }
 
     // pass 1 for every table: statistics, read back with one synchronization
-    for (int d = 0; d < n_dims; ++d) {
-        bp[d] = build_params(&descs[d], (DimStats*)workspaces[d]);
-        SDB_HIP(launch_dim_stats(bp[d], s), "dimension statistics launch");
-    }
+    for (int d = 0; d < n_dims; ++d) bp[d] = build_params(&descs[d], (DimStats*)workspaces[d]);
+    SDB_HIP(launch_build_stats(bb, s), "dimension statistics launch");
     for (int d = 0; d < n_dims; ++d)
         SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "statistics copy");
     if (n_dims > 0) SDB_HIP(hipStreamSynchronize(s), "statistics sync");
@@ -802,8 +803,9 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
             bp[d].nslots = range;
             bp[d].sentinel = missing - 1u;
             bp[d].missing = missing;
-            SDB_HIP(launch_fill_u32((uint32_t*)table, map_bytes / 4, 0xFFFFFFFFu, s), "map fill");
-            SDB_HIP(launch_dense_scatter(bp[d], s), "dense scatter launch");
+            bp[d].dense = 1;
+            bp[d].fill_value = 0xFFFFFFFFu;
+            bp[d].fill_words = map_bytes / 4;
         } else {
             const uint64_t cap = hash_capacity(n, effective_lf(desc));
             int bits = 0;
@@ -816,10 +818,13 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
             bp[d].nslots = cap;
             bp[d].hmask = (uint32_t)(cap - 1);
             bp[d].hshift = 32 - bits;
-            SDB_HIP(launch_fill_u32((uint32_t*)table, cap * 2, 0u, s), "hash table fill");
-            SDB_HIP(launch_hash_insert(bp[d], s), "hash insert launch");
+            bp[d].dense = 0;
+            bp[d].fill_value = 0u;
+            bp[d].fill_words = cap * 2;
         }
     }
+
+    SDB_HIP(launch_build_tables(bb, s), "table build launch");
 
     // duplicate-key checks of every table, with one synchronization
     for (int d = 0; d < n_dims; ++d)

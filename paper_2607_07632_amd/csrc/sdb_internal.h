@@ -180,6 +180,16 @@ struct BuildParams {
     uint32_t missing;          // dense: code of a key no row holds (all ones)
     uint32_t hmask;
     int32_t hshift;
+    int32_t dense;             // 1: dense map (scatter + bitmap), 0: hash table (inserts)
+    uint32_t fill_value;       // the table's initial word value (all ones dense, 0 hash)
+    uint64_t fill_words;       // 32-bit words of the table to fill before the scatter / inserts
+};
+
+// Every table of one sdb_build_dims call; kernels take table blockIdx.y.
+struct BuildBatch {
+    int32_t n;
+    int32_t pad_;
+    BuildParams bp[SDB_MAX_JOINS];
 };
 
 struct FinalizeParams {
@@ -227,9 +237,10 @@ struct PartParams {
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s);
 hipError_t launch_zero_pair(unsigned long long* a, unsigned long long* b, uint64_t n, hipStream_t s);
-hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s);
-hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s);
-hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s);
+// statistics pass of every table (their stats blocks are reset first)
+hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s);
+// table fill, then dense scatter + pass bitmap or hash inserts, of every table
+hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s);
 hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
                          unsigned long long* pass_counts, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if

@@ -16,6 +16,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 
 #include "sdb_internal.h"
@@ -168,8 +169,19 @@ __device__ __forceinline__ bool dim_row_passes(const BuildParams& bp, int64_t i)
     return pass;
 }
 
-__global__ void stats_init_kernel(DimStats* st) {
-    if (threadIdx.x == 0 && blockIdx.x == 0) {
+// The build kernels read their table's parameters in place from the batch in
+// the kernel-argument segment (table = blockIdx.y).
+#define SDB_BATCH_TABLE                                                                     \
+    (void)kernel_args;                                                                      \
+    const BuildBatch& bb = *(const BuildBatch*)__builtin_amdgcn_kernarg_segment_ptr();      \
+    const BuildParams& bp = bb.bp[blockIdx.y];                                              \
+    (void)bb
+
+__global__ void stats_init_kernel(BuildBatch kernel_args) {
+    (void)kernel_args;
+    const BuildBatch& bb = *(const BuildBatch*)__builtin_amdgcn_kernarg_segment_ptr();
+    if (blockIdx.x == 0 && threadIdx.x < (uint32_t)bb.n) {
+        DimStats* st = bb.bp[threadIdx.x].stats;
         st->kmin = INT_MAX;
         st->kmax = INT_MIN;
         st->npass = 0ull;
@@ -187,7 +199,8 @@ constexpr int kStatsRows = 16;
 
 // Each block reduces in registers and LDS and then adds its result with one
 // set of atomics, so the atomics stay few however large the dimension.
-__global__ void __launch_bounds__(256) dim_stats_kernel(BuildParams bp) {
+__global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
     constexpr int kWaves = 256 / 64;
     __shared__ int32_t s_kmin[kWaves], s_kmax[kWaves];
     __shared__ unsigned long long s_np[kWaves];
@@ -292,7 +305,17 @@ __device__ __forceinline__ uint32_t dim_row_code(const BuildParams& bp, int64_t 
 // every slot at `missing` (all ones: no row holds the key); a passing row then
 // stores its code and a filtered row the sentinel (`missing` - 1). Plain
 // stores, no atomics: each key owns its slot.
-__global__ void __launch_bounds__(256) dense_scatter_kernel(BuildParams bp) {
+__global__ void __launch_bounds__(256) fill_table_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    uint32_t* w = static_cast<uint32_t*>(bp.map);
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.fill_words; i += stride)
+        w[i] = bp.fill_value;
+}
+
+__global__ void __launch_bounds__(256) dense_scatter_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    if (!bp.dense) return;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
         const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
@@ -310,7 +333,9 @@ __global__ void __launch_bounds__(256) dense_scatter_kernel(BuildParams bp) {
 // One thread per 32 slots: the pass bitmap word (code below the sentinel)
 // and the number of occupied slots. Distinct keys occupy n slots; a duplicate
 // key leaves fewer, which the host detects from the total.
-__global__ void __launch_bounds__(256) dense_bits_kernel(BuildParams bp) {
+__global__ void __launch_bounds__(256) dense_bits_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    if (!bp.dense) return;
     const uint64_t n_words = (bp.nslots + 31) / 32;
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     unsigned long long occupied = 0;
@@ -379,7 +404,9 @@ __global__ void __launch_bounds__(256) dense_bits_kernel(BuildParams bp) {
 }
 
 // Open addressing, linear probing, 8-byte slots {key, code + 1 | 0xFFFFFFFF}.
-__global__ void __launch_bounds__(256) hash_insert_kernel(BuildParams bp) {
+__global__ void __launch_bounds__(256) hash_insert_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    if (bp.dense) return;
     unsigned long long* tab = static_cast<unsigned long long*>(bp.map);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
@@ -412,30 +439,56 @@ static int build_grid(int64_t n) {
     return (int)g;
 }
 
-hipError_t launch_dim_stats(const BuildParams& bp, hipStream_t s) {
-    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, s, bp.stats);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || bp.n == 0) return e;
-    // few blocks: every block ends with one set of atomics on the same words
-    int g = build_grid(bp.n);
-    if (g > 256) g = 256;
-    hipLaunchKernelGGL(dim_stats_kernel, dim3(g), dim3(256), 0, s, bp);
-    return hipGetLastError();
-}
-
-hipError_t launch_dense_scatter(const BuildParams& bp, hipStream_t s) {
-    if (bp.n == 0) return hipSuccess;
-    hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
+hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s) {
+    if (bb.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, s, bb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(dense_bits_kernel, dim3(build_grid((int64_t)((bp.nslots + 31) / 32))), dim3(256), 0, s, bp);
+    int64_t n_max = 0;
+    for (int d = 0; d < bb.n; ++d) n_max = std::max<int64_t>(n_max, bb.bp[d].n);
+    if (n_max == 0) return hipSuccess;
+    // few blocks per table: every block ends with one set of atomics on the same words
+    int g = build_grid((n_max + kStatsRows - 1) / kStatsRows);
+    if (g > 256) g = 256;
+    hipLaunchKernelGGL(dim_stats_kernel, dim3(g, bb.n), dim3(256), 0, s, bb);
     return hipGetLastError();
 }
 
-hipError_t launch_hash_insert(const BuildParams& bp, hipStream_t s) {
-    if (bp.n == 0) return hipSuccess;
-    hipLaunchKernelGGL(hash_insert_kernel, dim3(build_grid(bp.n)), dim3(256), 0, s, bp);
-    return hipGetLastError();
+hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s) {
+    if (bb.n <= 0) return hipSuccess;
+    uint64_t words = 0, n_words32 = 0;
+    int64_t n_dense = 0, n_hash = 0;
+    for (int d = 0; d < bb.n; ++d) {
+        const BuildParams& bp = bb.bp[d];
+        words = std::max<uint64_t>(words, bp.fill_words);
+        if (bp.dense) {
+            n_dense = std::max<int64_t>(n_dense, bp.n);
+            n_words32 = std::max<uint64_t>(n_words32, (bp.nslots + 31) / 32);
+        } else {
+            n_hash = std::max<int64_t>(n_hash, bp.n);
+        }
+    }
+    if (words > 0) {
+        hipLaunchKernelGGL(fill_table_kernel, dim3(fill_grid(words), bb.n), dim3(256), 0, s, bb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (n_dense > 0) {
+        hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid(n_dense), bb.n), dim3(256), 0, s, bb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (n_words32 > 0) {
+        hipLaunchKernelGGL(dense_bits_kernel, dim3(build_grid((int64_t)n_words32), bb.n), dim3(256), 0, s, bb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (n_hash > 0) {
+        hipLaunchKernelGGL(hash_insert_kernel, dim3(build_grid(n_hash), bb.n), dim3(256), 0, s, bb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 // ---------------------------------------------------------------------------
