@@ -106,6 +106,66 @@ def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_in
     return total
 
 
+# The plan features of the fused pass added one at a time, each rung a set of
+# planner overrides (the last rung is the planner's own choice).
+ABLATION_RUNGS = [
+    ("fused; query order; device-memory tables; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
+                                                              "terminal": "global", "xcd": -1, "block": 256}),
+    ("+ 4-row items (128-bit loads)", {"order": True, "lds": -1, "ipt": 1, "terminal": "global", "xcd": -1,
+                                       "block": 256}),
+    ("+ two items per lane", {"order": True, "lds": -1, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256}),
+    ("+ LDS-staged maps and bitmaps", {"order": True, "lds": 2, "ipt": 2, "terminal": "global", "xcd": -1,
+                                      "block": 256}),
+    ("+ sampled stage order", {"lds": 2, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256}),
+    ("+ per-XCD group tables", {"lds": 2, "ipt": 2, "terminal": "global", "block": 256}),
+    ("planner's choice (terminal, block size, rank tables)", {}),
+]
+
+
+def ablation_ladder(sdb, fact, dims, wdims, query, stream, base_force) -> list:
+    """Run-window time (fill, fused kernel, terminal passes) of every rung;
+    every rung's group table must equal the planner's own."""
+    import numpy as np
+    import torch
+    out, ref = [], None
+    for name, f in list(ABLATION_RUNGS)[::-1]:
+        force = dict(base_force)
+        force.update(f)
+        if query.get("group_by") == [] and force.get("terminal") == "global":
+            force.pop("terminal")
+        tabs = sdb.build_dims(dims, wdims.dim_keys, query)
+        try:
+            q = sdb.StarQuery(fact, tabs, query, force)
+            plan = q.plan()
+        except sdb.SdbError as e:
+            out.append({"rung": name, "force": f, "run_ms": float("nan"), "error": str(e), "plan": None})
+            continue
+        sums, counts = q.alloc_outputs(plan)
+        scratch = q.run_scratch(plan)
+        for _ in range(2):
+            q.run(sums, counts, plan=plan, scratch=scratch)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            q.run(sums, counts, plan=plan, scratch=scratch)
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        tab = (sums.cpu().numpy(), counts.cpu().numpy())
+        if ref is None:
+            ref = tab
+        same = bool(np.array_equal(tab[0], ref[0]) and np.array_equal(tab[1], ref[1]))
+        info = sdb.plan_summary(plan, query)
+        out.append({"rung": name, "force": f, "run_ms": float(np.mean(ts)), "same_result": same,
+                    "plan": {k: info[k] for k in ("terminal", "ipt", "vector", "block", "xcd_copies")} |
+                            {"stages": [(s["name"], s.get("table", "pred")) for s in info["stages"]]}})
+        if not same:
+            raise AssertionError(f"ablation rung {name!r} changed the result")
+    return out[::-1]
+
+
 def upload_fact(cfg_name: str, n: int, device) -> dict:
     """Generate each fact column into one pinned host buffer and copy it to HBM."""
     import torch
@@ -138,6 +198,8 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (scale for HBM byte counters)")
     ap.add_argument("--force", default="", help="planner overrides, e.g. ipt=4,vector=1,terminal=global")
+    ap.add_argument("--ablation", default=None, metavar="PATH",
+                    help="also time the fused-plan ablation ladder and write it as JSON to PATH")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -280,6 +342,13 @@ def main(argv=None) -> int:
         },
         "cpu_baseline": None,
     }
+
+    if args.ablation:
+        ladder = ablation_ladder(sdb, fact, dims, wdims, query, stream, force)
+        with open(args.ablation, "w") as f:
+            json.dump({"workload": args.config, "fact_rows": n, "rungs": ladder}, f, indent=1)
+        for r in ladder:
+            log(f"[ablation] {r['rung']:58s} {r['run_ms']:8.3f} ms  {r['plan']}")
 
     if args.copy_calibration:
         src = torch.empty(1 << 28, dtype=torch.int32, device=dev)
