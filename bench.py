@@ -109,6 +109,7 @@ def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_in
 # The plan features of the fused pass added one at a time, each rung a set of
 # planner overrides (the last rung is the planner's own choice).
 ABLATION_RUNGS = [
+    ("kernel at a time: flags and group ids through HBM; query order", {"order": True, "unfused": True}),
     ("fused; query order; device-memory tables; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
                                                               "terminal": "global", "xcd": -1, "block": 256}),
     ("+ 4-row items (128-bit loads)", {"order": True, "lds": -1, "ipt": 1, "terminal": "global", "xcd": -1,
@@ -131,6 +132,7 @@ def ablation_ladder(sdb, fact, dims, wdims, query, stream, base_force) -> list:
     for name, f in list(ABLATION_RUNGS)[::-1]:
         force = dict(base_force)
         force.update(f)
+        unfused = bool(force.pop("unfused", False))
         if query.get("group_by") == [] and force.get("terminal") == "global":
             force.pop("terminal")
         tabs = sdb.build_dims(dims, wdims.dim_keys, query)
@@ -141,15 +143,20 @@ def ablation_ladder(sdb, fact, dims, wdims, query, stream, base_force) -> list:
             out.append({"rung": name, "force": f, "run_ms": float("nan"), "error": str(e), "plan": None})
             continue
         sums, counts = q.alloc_outputs(plan)
-        scratch = q.run_scratch(plan)
+        if unfused:
+            scratch = q.unfused_scratch(sums.device)
+            run = q.run_unfused
+        else:
+            scratch = q.run_scratch(plan)
+            run = q.run
         for _ in range(2):
-            q.run(sums, counts, plan=plan, scratch=scratch)
+            run(sums, counts, plan=plan, scratch=scratch)
         torch.cuda.synchronize()
         ts = []
         for _ in range(5):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            q.run(sums, counts, plan=plan, scratch=scratch)
+            run(sums, counts, plan=plan, scratch=scratch)
             b.record(stream)
             b.synchronize()
             ts.append(a.elapsed_time(b))
@@ -158,9 +165,13 @@ def ablation_ladder(sdb, fact, dims, wdims, query, stream, base_force) -> list:
             ref = tab
         same = bool(np.array_equal(tab[0], ref[0]) and np.array_equal(tab[1], ref[1]))
         info = sdb.plan_summary(plan, query)
+        shape = {k: info[k] for k in ("terminal", "ipt", "vector", "block", "xcd_copies")}
+        stages = [(s["name"], s.get("table", "pred")) for s in info["stages"]]
+        if unfused:
+            shape = {"terminal": "unfused kernels"}
+            stages = [(nm, "pred" if t == "pred" else "device") for nm, t in stages]
         out.append({"rung": name, "force": f, "run_ms": float(np.mean(ts)), "same_result": same,
-                    "plan": {k: info[k] for k in ("terminal", "ipt", "vector", "block", "xcd_copies")} |
-                            {"stages": [(s["name"], s.get("table", "pred")) for s in info["stages"]]}})
+                    "plan": shape | {"stages": stages}})
         if not same:
             raise AssertionError(f"ablation rung {name!r} changed the result")
     return out[::-1]

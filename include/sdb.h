@@ -342,6 +342,28 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
  * between them is that kernel's duration. NULL, NULL turns it off. */
 SDB_API sdb_status sdb_set_fused_events(void* start, void* stop);
 
+/* ---- kernel-at-a-time execution (the unfused baseline) ------------------ */
+
+/* Host only. Scratch bytes sdb_run_star_query_unfused needs for n_fact rows:
+ * a live flag (1 byte) and a group id (4 bytes) per fact row, 256-byte
+ * aligned parts. */
+SDB_API sdb_status sdb_unfused_scratch_bytes(int64_t n_fact, int64_t* bytes);
+
+/* Runs `q` with the stage order of `plan` one operator at a time, the way a
+ * kernel-at-a-time engine does (Sections 3.1 and 4.1: one kernel per operator, flags
+ * and intermediates round-trip through global memory): one kernel sets every
+ * row's flag, one kernel per stage reads its fact column, the flags and group
+ * ids and writes them back, and one kernel adds the live rows into the
+ * outputs with device-scope atomics. Tables are read in device memory; the
+ * plan's LDS placements, terminal, items per lane and block size are ignored.
+ * Results equal sdb_run_star_query's. For measurement (the first rung of the
+ * fusion ablation). Arguments as sdb_run_star_query, with scratch >=
+ * sdb_unfused_scratch_bytes(q->n_fact). Errors: as sdb_run_star_query. */
+SDB_API sdb_status sdb_run_star_query_unfused(const sdb_query* q, const sdb_plan* plan,
+                                              int64_t* sums, int64_t* counts,
+                                              int64_t n_groups_capacity, void* scratch,
+                                              int64_t scratch_bytes, void* stream);
+
 /* ---- finalize ----------------------------------------------------------- */
 
 /* Host only. Scratch bytes sdb_finalize_groups needs for `plan`. */

@@ -665,6 +665,58 @@ sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) 
     return SDB_OK;
 }
 
+// Checks shared by both run entry points: the query, the plan's stage list
+// and deferred gathers, the group layout and the output capacity.
+sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, int64_t* counts,
+                     int64_t n_groups_capacity) {
+    sdb_status st = check_query(q);
+    if (st != SDB_OK) return st;
+    if (!plan) return fail(SDB_INVALID_ARG, "null plan");
+    if (!sums || !counts) return fail(SDB_INVALID_ARG, "null output");
+    if (plan->n_stages != q->n_preds + q->n_joins) return fail(SDB_INVALID_ARG, "plan does not match the query");
+    int n_defer = 0;
+    {
+        bool seen[SDB_MAX_STAGES] = {false};
+        for (int s = 0; s < plan->n_stages; ++s) {
+            const int k = plan->stage_kind[s], i = plan->stage_index[s];
+            if ((k != 0 && k != 1) || i < 0 || (k == 0 && i >= q->n_preds) || (k == 1 && i >= q->n_joins))
+                return fail(SDB_INVALID_ARG, "plan stage %d is invalid", s);
+            const int slot = k == 0 ? i : q->n_preds + i;
+            if (seen[slot]) return fail(SDB_INVALID_ARG, "plan stage %d repeats a stage", s);
+            seen[slot] = true;
+            const int lm = plan->stage_lds[s];
+            if (lm != LDS_GLOBAL) {
+                if (k != 1 || q->joins[i].dim->kind != SDB_TABLE_DENSE)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: LDS placement needs a dense table", s);
+                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
+                if ((lm == LDS_BITS || lm == LDS_RANK) && !q->joins[i].dim->bits)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: table has no bitmap", s);
+                if (lm == LDS_RANK && !rank_fits(q->joins[i].dim))
+                    return fail(SDB_INVALID_ARG, "plan stage %d: rank tables do not fit LDS", s);
+            }
+            if (plan->stage_defer[s] != -1) {
+                if (plan->stage_defer[s] != 0 || lm != LDS_BITS)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: bad deferred gather", s);
+                ++n_defer;
+            }
+        }
+    }
+    if (n_defer > 1) return fail(SDB_INVALID_ARG, "plan defers more than one gather");
+    sdb_plan layout;
+    std::memset(&layout, 0, sizeof layout);
+    st = group_layout(q, &layout);
+    if (st != SDB_OK) return st;
+    if (layout.n_groups != plan->n_groups) return fail(SDB_INVALID_ARG, "plan group count does not match the query");
+    for (int k = 0; k < q->n_group_keys; ++k)
+        if (layout.stride[k] != plan->stride[k] || layout.radix[k] != plan->radix[k])
+            return fail(SDB_INVALID_ARG, "plan group layout does not match the query");
+    if (n_groups_capacity < 0 || (uint64_t)n_groups_capacity < plan->n_groups)
+        return fail(SDB_CAPACITY, "output holds %lld groups, plan needs %llu", (long long)n_groups_capacity,
+                    (unsigned long long)plan->n_groups);
+    return SDB_OK;
+}
+
 }  // namespace
 
 // ============================================================================
@@ -1053,51 +1105,8 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
 SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
                                       int64_t* counts, int64_t n_groups_capacity, void* scratch,
                                       int64_t scratch_bytes, void* stream) {
-    sdb_status st = check_query(q);
+    sdb_status st = check_run(q, plan, sums, counts, n_groups_capacity);
     if (st != SDB_OK) return st;
-    if (!plan) return fail(SDB_INVALID_ARG, "null plan");
-    if (!sums || !counts) return fail(SDB_INVALID_ARG, "null output");
-    if (plan->n_stages != q->n_preds + q->n_joins) return fail(SDB_INVALID_ARG, "plan does not match the query");
-    int n_defer = 0;
-    {
-        bool seen[SDB_MAX_STAGES] = {false};
-        for (int s = 0; s < plan->n_stages; ++s) {
-            const int k = plan->stage_kind[s], i = plan->stage_index[s];
-            if ((k != 0 && k != 1) || i < 0 || (k == 0 && i >= q->n_preds) || (k == 1 && i >= q->n_joins))
-                return fail(SDB_INVALID_ARG, "plan stage %d is invalid", s);
-            const int slot = k == 0 ? i : q->n_preds + i;
-            if (seen[slot]) return fail(SDB_INVALID_ARG, "plan stage %d repeats a stage", s);
-            seen[slot] = true;
-            const int lm = plan->stage_lds[s];
-            if (lm != LDS_GLOBAL) {
-                if (k != 1 || q->joins[i].dim->kind != SDB_TABLE_DENSE)
-                    return fail(SDB_INVALID_ARG, "plan stage %d: LDS placement needs a dense table", s);
-                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK)
-                    return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
-                if ((lm == LDS_BITS || lm == LDS_RANK) && !q->joins[i].dim->bits)
-                    return fail(SDB_INVALID_ARG, "plan stage %d: table has no bitmap", s);
-                if (lm == LDS_RANK && !rank_fits(q->joins[i].dim))
-                    return fail(SDB_INVALID_ARG, "plan stage %d: rank tables do not fit LDS", s);
-            }
-            if (plan->stage_defer[s] != -1) {
-                if (plan->stage_defer[s] != 0 || lm != LDS_BITS)
-                    return fail(SDB_INVALID_ARG, "plan stage %d: bad deferred gather", s);
-                ++n_defer;
-            }
-        }
-    }
-    if (n_defer > 1) return fail(SDB_INVALID_ARG, "plan defers more than one gather");
-    sdb_plan layout;
-    std::memset(&layout, 0, sizeof layout);
-    st = group_layout(q, &layout);
-    if (st != SDB_OK) return st;
-    if (layout.n_groups != plan->n_groups) return fail(SDB_INVALID_ARG, "plan group count does not match the query");
-    for (int k = 0; k < q->n_group_keys; ++k)
-        if (layout.stride[k] != plan->stride[k] || layout.radix[k] != plan->radix[k])
-            return fail(SDB_INVALID_ARG, "plan group layout does not match the query");
-    if (n_groups_capacity < 0 || (uint64_t)n_groups_capacity < plan->n_groups)
-        return fail(SDB_CAPACITY, "output holds %lld groups, plan needs %llu", (long long)n_groups_capacity,
-                    (unsigned long long)plan->n_groups);
     if (plan->terminal < TERM_SCALAR || plan->terminal > TERM_PART)
         return fail(SDB_INVALID_ARG, "bad plan terminal %d", plan->terminal);
     if (plan->terminal == TERM_PART) {
@@ -1228,6 +1237,48 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         SDB_HIP(launch_xcd_merge((const unsigned long long*)term_base, plan->xcd_copies, plan->n_groups,
                                  (unsigned long long*)sums, (unsigned long long*)counts, s),
                 "copy merge launch");
+    return ok();
+}
+
+SDB_API sdb_status sdb_unfused_scratch_bytes(int64_t n_fact, int64_t* bytes) {
+    if (!bytes) return fail(SDB_INVALID_ARG, "null argument");
+    if (n_fact < 0) return fail(SDB_INVALID_ARG, "negative n_fact");
+    *bytes = (int64_t)(align_up((uint64_t)n_fact, 256) + align_up((uint64_t)n_fact * 4, 256));
+    return ok();
+}
+
+SDB_API sdb_status sdb_run_star_query_unfused(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
+                                              int64_t* counts, int64_t n_groups_capacity, void* scratch,
+                                              int64_t scratch_bytes, void* stream) {
+    sdb_status st = check_run(q, plan, sums, counts, n_groups_capacity);
+    if (st != SDB_OK) return st;
+    int64_t need = 0;
+    sdb_unfused_scratch_bytes(q->n_fact, &need);
+    if (need > 0) {
+        if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
+        if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
+        if (scratch_bytes < need)
+            return fail(SDB_WORKSPACE_TOO_SMALL, "run scratch holds %lld bytes, %lld needed", (long long)scratch_bytes,
+                        (long long)need);
+    }
+    // stages in the plan's order, every table read in device memory
+    FusedParams p;
+    std::memset(&p, 0, sizeof p);
+    for (int c = 0; c < q->n_cols; ++c) p.cols[c] = q->cols[c];
+    p.n = q->n_fact;
+    p.nstages = plan->n_stages;
+    for (int s = 0; s < plan->n_stages; ++s)
+        p.st[s] = make_stage(q, plan, plan->stage_kind[s], plan->stage_index[s], -1);
+    p.agg_kind = q->agg.kind;
+    p.agg_a = q->agg.a;
+    p.agg_b = q->agg.kind == SDB_AGG_COL ? q->agg.a : q->agg.b;
+    p.sums = (unsigned long long*)sums;
+    p.counts = (unsigned long long*)counts;
+    hipStream_t s = (hipStream_t)stream;
+    SDB_HIP(launch_zero_pair(p.sums, p.counts, plan->n_groups, s), "output fill");
+    uint8_t* flags = (uint8_t*)scratch;
+    uint32_t* gid = (uint32_t*)((uint8_t*)scratch + align_up((uint64_t)q->n_fact, 256));
+    SDB_HIP(launch_unfused(p, flags, gid, s), "unfused launch");
     return ok();
 }
 

@@ -249,6 +249,8 @@ int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block,
 hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
                         size_t lds_bytes, hipStream_t s);
 hipError_t launch_rank_build(const RankParams& rp, hipStream_t s);
+// kernel-at-a-time run of the stages and aggregate of p (device tables only)
+hipError_t launch_unfused(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s);
 hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);

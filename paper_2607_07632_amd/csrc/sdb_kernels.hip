@@ -17,6 +17,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstring>
 #include <climits>
 
 #include "sdb_internal.h"
@@ -1180,6 +1181,117 @@ hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal,
     if (!fn) return hipErrorInvalidValue;
     void* args[] = {const_cast<FusedParams*>(&p)};
     return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);
+}
+
+// ---------------------------------------------------------------------------
+// kernel-at-a-time execution: one kernel per operator, flags and group ids in
+// global memory between them (the unfused baseline)
+// ---------------------------------------------------------------------------
+
+struct UnfusedParams {
+    const int32_t* col;        // the stage's fact column (stage kernels), agg operand a (aggregate kernel)
+    const int32_t* col_b;      // agg operand b
+    int64_t n;
+    uint8_t* flags;            // live flag per row
+    uint32_t* gid;             // group id per row
+    unsigned long long* sums;
+    unsigned long long* counts;
+    int32_t agg_kind;
+    int32_t pad_;
+    StageDev st;
+};
+
+__global__ void __launch_bounds__(256) unfused_init_kernel(UnfusedParams up) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < up.n; i += stride) {
+        up.flags[i] = 1u;
+        up.gid[i] = 0u;
+    }
+}
+
+// One stage over every row still flagged: predicate, dense map or hash probe.
+__global__ void __launch_bounds__(256) unfused_stage_kernel(UnfusedParams kernel_args) {
+    (void)kernel_args;
+    const UnfusedParams& up = *(const UnfusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
+    const StageDev& S = up.st;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < up.n; i += stride) {
+        if (!up.flags[i]) continue;
+        const int32_t x = up.col[i];
+        uint32_t c = 0u;
+        bool pass;
+        if (S.kind == ST_PRED) {
+            pass = range_pass(S.test, x);
+        } else if (S.kind == ST_DENSE) {
+            const uint32_t idx = (uint32_t)(x - S.kmin);
+            pass = idx < S.nslots;
+            if (pass) {
+                c = load_dense_code(S, idx);
+                pass = c < S.sentinel;
+            }
+        } else {
+            const uint32_t h = hash_slot(S, x);
+            c = hash_resolve(S, x, h, static_cast<const unsigned long long*>(S.map)[h]);
+            pass = c < S.sentinel;
+        }
+        if (!pass) {
+            up.flags[i] = 0u;
+        } else if (S.gk_mode == GK_ONE) {
+            up.gid[i] += c * S.gk_stride[0];
+        } else if (S.gk_mode == GK_GENERAL) {
+            up.gid[i] += code_contribution(S, c);
+        }
+    }
+}
+
+// The aggregate of every flagged row, added into the outputs with atomics.
+__global__ void __launch_bounds__(256) unfused_agg_kernel(UnfusedParams up) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < up.n; i += stride) {
+        if (!up.flags[i]) continue;
+        const long long a = up.col[i];
+        long long v = a;
+        if (up.agg_kind == SDB_AGG_MUL) v = a * (long long)up.col_b[i];
+        else if (up.agg_kind == SDB_AGG_SUB) v = a - (long long)up.col_b[i];
+        else if (up.agg_kind == SDB_AGG_ADD) v = a + (long long)up.col_b[i];
+        const uint32_t g = up.gid[i];
+        atomicAdd(&up.sums[g], (unsigned long long)v);
+        atomicAdd(&up.counts[g], 1ull);
+    }
+}
+
+static int unfused_grid(int64_t n) {
+    int64_t g = (n + 255) / 256;
+    if (g > 8192) g = 8192;
+    if (g < 1) g = 1;
+    return (int)g;
+}
+
+hipError_t launch_unfused(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s) {
+    if (p.n == 0) return hipSuccess;
+    UnfusedParams up;
+    memset(&up, 0, sizeof up);
+    up.n = p.n;
+    up.flags = flags;
+    up.gid = gid;
+    up.sums = p.sums;
+    up.counts = p.counts;
+    up.agg_kind = p.agg_kind;
+    const int grid = unfused_grid(p.n);
+    hipLaunchKernelGGL(unfused_init_kernel, dim3(grid), dim3(256), 0, s, up);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    for (int st = 0; st < p.nstages; ++st) {
+        up.st = p.st[st];
+        up.col = p.cols[up.st.col];
+        hipLaunchKernelGGL(unfused_stage_kernel, dim3(grid), dim3(256), 0, s, up);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    up.col = p.cols[p.agg_a];
+    up.col_b = p.cols[p.agg_b];
+    hipLaunchKernelGGL(unfused_agg_kernel, dim3(grid), dim3(256), 0, s, up);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

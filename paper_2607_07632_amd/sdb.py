@@ -107,6 +107,8 @@ SIGNATURES = {
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
     "sdb_build_dims": (i32, [i32, C.POINTER(SdbDimDesc), C.POINTER(vp), C.POINTER(i64), vp, C.POINTER(SdbDim)]),
     "sdb_set_fused_events": (i32, [vp, vp]),
+    "sdb_unfused_scratch_bytes": (i32, [i64, C.POINTER(i64)]),
+    "sdb_run_star_query_unfused": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
     "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
     "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
     "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
@@ -393,6 +395,23 @@ class StarQuery:
             self._run_scratch = torch.empty(need, dtype=torch.uint8, device=dev)
         return self._run_scratch
 
+    def unfused_scratch(self, device):
+        """Per-row flags and group ids for :meth:`run_unfused`."""
+        import torch
+        need = i64(0)
+        _check(lib().sdb_unfused_scratch_bytes(int(self.q.n_fact), C.byref(need)))
+        return torch.empty(max(int(need.value), 256), dtype=torch.uint8, device=device)
+
+    def run_unfused(self, sums, counts, plan: SdbPlan | None = None, stream=None, scratch=None) -> None:
+        """The same query one operator per kernel (flags and group ids through
+        global memory): the unfused baseline."""
+        plan = plan or self.plan_obj
+        if scratch is None:
+            scratch = self.unfused_scratch(sums.device)
+        _check(lib().sdb_run_star_query_unfused(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
+                                                sums.numel(), _ptr(scratch), scratch.numel(),
+                                                _stream_handle(stream)))
+
     def run(self, sums, counts, plan: SdbPlan | None = None, stream=None, scratch=None) -> None:
         plan = plan or self.plan_obj
         if scratch is None:
@@ -421,13 +440,14 @@ class StarQuery:
                                          _stream_handle(stream)))
         return outputs
 
-    def execute(self, stream=None, replan: bool = True) -> QueryResult:
-        """plan -> fused pass -> compaction, then copy the groups to the host."""
+    def execute(self, stream=None, replan: bool = True, unfused: bool = False) -> QueryResult:
+        """plan -> fused pass (or, with ``unfused``, one kernel per operator)
+        -> compaction, then copy the groups to the host."""
         import torch
         if replan or self.plan_obj is None:
             self.plan(stream)
         sums, counts = self.alloc_outputs()
-        self.run(sums, counts, stream=stream)
+        (self.run_unfused if unfused else self.run)(sums, counts, stream=stream)
         k, s, c, n, _ = self.finalize(sums, counts, stream=stream)
         (stream or torch.cuda.current_stream()).synchronize()
         m = int(n.item())
