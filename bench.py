@@ -22,6 +22,8 @@ rows of the same workload; the GPU result on those rows is compared with it.
 from __future__ import annotations
 
 import argparse
+import copy
+import functools
 import hashlib
 import json
 import os
@@ -109,9 +111,14 @@ def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_in
 # The plan features of the fused pass added one at a time, each rung a set of
 # planner overrides (the last rung is the planner's own choice).
 ABLATION_RUNGS = [
-    ("kernel at a time: flags and group ids through HBM; query order", {"order": True, "unfused": True}),
-    ("fused; query order; device-memory tables; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
-                                                              "terminal": "global", "xcd": -1, "block": 256}),
+    ("kernel at a time: flags and group ids through HBM; hash tables; query order",
+     {"order": True, "baseline": "per_operator", "tables": "hash"}),
+    ("one kernel; operators hand off through HBM", {"order": True, "baseline": "global_handoff", "tables": "hash"}),
+    ("+ register table; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
+                                                     "terminal": "global", "xcd": -1, "block": 256,
+                                                     "tables": "hash"}),
+    ("+ packed direct-mapped maps", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
+                                     "terminal": "global", "xcd": -1, "block": 256}),
     ("+ 4-row items (128-bit loads)", {"order": True, "lds": -1, "ipt": 1, "terminal": "global", "xcd": -1,
                                        "block": 256}),
     ("+ two items per lane", {"order": True, "lds": -1, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256}),
@@ -132,20 +139,25 @@ def ablation_ladder(sdb, fact, dims, wdims, query, stream, base_force) -> list:
     for name, f in list(ABLATION_RUNGS)[::-1]:
         force = dict(base_force)
         force.update(f)
-        unfused = bool(force.pop("unfused", False))
-        if query.get("group_by") == [] and force.get("terminal") == "global":
+        baseline = force.pop("baseline", None)
+        rq = query
+        if force.pop("tables", None) == "hash":
+            rq = copy.deepcopy(query)
+            for jd in rq["joins"]:
+                jd["kind"] = "hash"
+        if rq.get("group_by") == [] and force.get("terminal") == "global":
             force.pop("terminal")
-        tabs = sdb.build_dims(dims, wdims.dim_keys, query)
+        tabs = sdb.build_dims(dims, wdims.dim_keys, rq)
         try:
-            q = sdb.StarQuery(fact, tabs, query, force)
+            q = sdb.StarQuery(fact, tabs, rq, force)
             plan = q.plan()
         except sdb.SdbError as e:
             out.append({"rung": name, "force": f, "run_ms": float("nan"), "error": str(e), "plan": None})
             continue
         sums, counts = q.alloc_outputs(plan)
-        if unfused:
-            scratch = q.unfused_scratch(sums.device)
-            run = q.run_unfused
+        if baseline:
+            scratch = q.baseline_scratch(sums.device)
+            run = functools.partial(q.run_baseline, baseline)
         else:
             scratch = q.run_scratch(plan)
             run = q.run
@@ -164,11 +176,11 @@ def ablation_ladder(sdb, fact, dims, wdims, query, stream, base_force) -> list:
         if ref is None:
             ref = tab
         same = bool(np.array_equal(tab[0], ref[0]) and np.array_equal(tab[1], ref[1]))
-        info = sdb.plan_summary(plan, query)
+        info = sdb.plan_summary(plan, rq)
         shape = {k: info[k] for k in ("terminal", "ipt", "vector", "block", "xcd_copies")}
         stages = [(s["name"], s.get("table", "pred")) for s in info["stages"]]
-        if unfused:
-            shape = {"terminal": "unfused kernels"}
+        if baseline:
+            shape = {"terminal": baseline}
             stages = [(nm, "pred" if t == "pred" else "device") for nm, t in stages]
         out.append({"rung": name, "force": f, "run_ms": float(np.mean(ts)), "same_result": same,
                     "plan": shape | {"stages": stages}})

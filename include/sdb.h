@@ -342,27 +342,41 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
  * between them is that kernel's duration. NULL, NULL turns it off. */
 SDB_API sdb_status sdb_set_fused_events(void* start, void* stop);
 
-/* ---- kernel-at-a-time execution (the unfused baseline) ------------------ */
+/* ---- baselines for the fusion ablation ---------------------------------- */
 
-/* Host only. Scratch bytes sdb_run_star_query_unfused needs for n_fact rows:
- * a live flag (1 byte) and a group id (4 bytes) per fact row, 256-byte
- * aligned parts. */
-SDB_API sdb_status sdb_unfused_scratch_bytes(int64_t n_fact, int64_t* bytes);
+/* How sdb_run_star_query_baseline executes a query (Sections 4.1 and 4.2):
+ *  SDB_BASELINE_PER_OPERATOR  kernel at a time: one kernel sets every row's
+ *                             live flag, one kernel per stage reads its fact
+ *                             column, the flags and the group ids and writes
+ *                             them back, one kernel adds the live rows into
+ *                             the outputs with device-scope atomics;
+ *  SDB_BASELINE_GLOBAL_HANDOFF one fused kernel, one row per thread, whose
+ *                             operators still hand the live flag and the
+ *                             group id to each other through the per-row
+ *                             arrays in global memory (the fused engine
+ *                             before its register table). */
+typedef enum {
+    SDB_BASELINE_PER_OPERATOR = 0,
+    SDB_BASELINE_GLOBAL_HANDOFF = 1
+} sdb_baseline_mode;
 
-/* Runs `q` with the stage order of `plan` one operator at a time, the way a
- * kernel-at-a-time engine does (Sections 3.1 and 4.1: one kernel per operator, flags
- * and intermediates round-trip through global memory): one kernel sets every
- * row's flag, one kernel per stage reads its fact column, the flags and group
- * ids and writes them back, and one kernel adds the live rows into the
- * outputs with device-scope atomics. Tables are read in device memory; the
- * plan's LDS placements, terminal, items per lane and block size are ignored.
- * Results equal sdb_run_star_query's. For measurement (the first rung of the
- * fusion ablation). Arguments as sdb_run_star_query, with scratch >=
- * sdb_unfused_scratch_bytes(q->n_fact). Errors: as sdb_run_star_query. */
-SDB_API sdb_status sdb_run_star_query_unfused(const sdb_query* q, const sdb_plan* plan,
-                                              int64_t* sums, int64_t* counts,
-                                              int64_t n_groups_capacity, void* scratch,
-                                              int64_t scratch_bytes, void* stream);
+/* Host only. Scratch bytes sdb_run_star_query_baseline needs for n_fact
+ * rows: a live flag (1 byte) and a group id (4 bytes) per fact row, in two
+ * 256-byte aligned parts. Errors: INVALID_ARG (null `bytes`, n_fact < 0). */
+SDB_API sdb_status sdb_baseline_scratch_bytes(int64_t n_fact, int64_t* bytes);
+
+/* Runs `q` in the stage order of `plan` the way `mode` says, asynchronously
+ * on `stream`. Every table is read in device memory; the plan's LDS
+ * placements, terminal, items per lane and block size are ignored. Results
+ * equal sdb_run_star_query's. For measurement only: these are the slow rungs
+ * of the fusion ablation. Arguments as sdb_run_star_query, with scratch
+ * (device, 256-byte aligned, caller-owned) >= sdb_baseline_scratch_bytes(
+ * q->n_fact). Errors: as sdb_run_star_query, and INVALID_ARG for an unknown
+ * mode. */
+SDB_API sdb_status sdb_run_star_query_baseline(const sdb_query* q, const sdb_plan* plan,
+                                               int32_t mode, int64_t* sums, int64_t* counts,
+                                               int64_t n_groups_capacity, void* scratch,
+                                               int64_t scratch_bytes, void* stream);
 
 /* ---- finalize ----------------------------------------------------------- */
 

@@ -1240,20 +1240,22 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     return ok();
 }
 
-SDB_API sdb_status sdb_unfused_scratch_bytes(int64_t n_fact, int64_t* bytes) {
+SDB_API sdb_status sdb_baseline_scratch_bytes(int64_t n_fact, int64_t* bytes) {
     if (!bytes) return fail(SDB_INVALID_ARG, "null argument");
     if (n_fact < 0) return fail(SDB_INVALID_ARG, "negative n_fact");
     *bytes = (int64_t)(align_up((uint64_t)n_fact, 256) + align_up((uint64_t)n_fact * 4, 256));
     return ok();
 }
 
-SDB_API sdb_status sdb_run_star_query_unfused(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
-                                              int64_t* counts, int64_t n_groups_capacity, void* scratch,
-                                              int64_t scratch_bytes, void* stream) {
+SDB_API sdb_status sdb_run_star_query_baseline(const sdb_query* q, const sdb_plan* plan, int32_t mode,
+                                               int64_t* sums, int64_t* counts, int64_t n_groups_capacity,
+                                               void* scratch, int64_t scratch_bytes, void* stream) {
     sdb_status st = check_run(q, plan, sums, counts, n_groups_capacity);
     if (st != SDB_OK) return st;
+    if (mode != SDB_BASELINE_PER_OPERATOR && mode != SDB_BASELINE_GLOBAL_HANDOFF)
+        return fail(SDB_INVALID_ARG, "unknown baseline mode %d", (int)mode);
     int64_t need = 0;
-    sdb_unfused_scratch_bytes(q->n_fact, &need);
+    sdb_baseline_scratch_bytes(q->n_fact, &need);
     if (need > 0) {
         if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
         if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
@@ -1278,7 +1280,8 @@ SDB_API sdb_status sdb_run_star_query_unfused(const sdb_query* q, const sdb_plan
     SDB_HIP(launch_zero_pair(p.sums, p.counts, plan->n_groups, s), "output fill");
     uint8_t* flags = (uint8_t*)scratch;
     uint32_t* gid = (uint32_t*)((uint8_t*)scratch + align_up((uint64_t)q->n_fact, 256));
-    SDB_HIP(launch_unfused(p, flags, gid, s), "unfused launch");
+    if (mode == SDB_BASELINE_PER_OPERATOR) SDB_HIP(launch_unfused(p, flags, gid, s), "per-operator launch");
+    else SDB_HIP(launch_handoff(p, flags, gid, s), "global hand-off launch");
     return ok();
 }
 

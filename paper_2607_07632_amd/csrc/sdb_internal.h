@@ -158,6 +158,7 @@ struct DimStats {
     uint32_t pad2_[2];
 };
 static_assert(sizeof(DimStats) <= 256, "stats must fit the reserved 256 bytes");
+static_assert(sizeof(FusedParams) <= 4096, "kernel arguments must fit the 4 KB kernarg segment");
 
 struct BuildParams {
     const int32_t* key;
@@ -251,6 +252,7 @@ hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal,
 hipError_t launch_rank_build(const RankParams& rp, hipStream_t s);
 // kernel-at-a-time run of the stages and aggregate of p (device tables only)
 hipError_t launch_unfused(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s);
+hipError_t launch_handoff(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s);
 hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);

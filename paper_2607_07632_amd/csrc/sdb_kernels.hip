@@ -1209,6 +1209,37 @@ __global__ void __launch_bounds__(256) unfused_init_kernel(UnfusedParams up) {
     }
 }
 
+// One row of one stage with its table in device memory: whether the row
+// passes, and the dimension code it gathers (pass implies c < sentinel).
+__device__ __forceinline__ bool device_stage_row(const StageDev& S, int32_t x, uint32_t& c) {
+    c = 0u;
+    if (S.kind == ST_PRED) return range_pass(S.test, x);
+    if (S.kind == ST_DENSE) {
+        const uint32_t idx = (uint32_t)(x - S.kmin);
+        if (idx >= S.nslots) return false;
+        c = load_dense_code(S, idx);
+        return c < S.sentinel;
+    }
+    const uint32_t h = hash_slot(S, x);
+    c = hash_resolve(S, x, h, static_cast<const unsigned long long*>(S.map)[h]);
+    return c < S.sentinel;
+}
+
+// The part of the mixed-radix group id that a passing row's code adds.
+__device__ __forceinline__ uint32_t stage_gid_part(const StageDev& S, uint32_t c) {
+    if (S.gk_mode == GK_ONE) return c * S.gk_stride[0];
+    if (S.gk_mode == GK_GENERAL) return code_contribution(S, c);
+    return 0u;
+}
+
+__device__ __forceinline__ long long row_value(int32_t kind, int32_t a, int32_t b) {
+    const long long x = a;
+    if (kind == SDB_AGG_MUL) return x * (long long)b;
+    if (kind == SDB_AGG_SUB) return x - (long long)b;
+    if (kind == SDB_AGG_ADD) return x + (long long)b;
+    return x;
+}
+
 // One stage over every row still flagged: predicate, dense map or hash probe.
 __global__ void __launch_bounds__(256) unfused_stage_kernel(UnfusedParams kernel_args) {
     (void)kernel_args;
@@ -1217,30 +1248,9 @@ __global__ void __launch_bounds__(256) unfused_stage_kernel(UnfusedParams kernel
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < up.n; i += stride) {
         if (!up.flags[i]) continue;
-        const int32_t x = up.col[i];
-        uint32_t c = 0u;
-        bool pass;
-        if (S.kind == ST_PRED) {
-            pass = range_pass(S.test, x);
-        } else if (S.kind == ST_DENSE) {
-            const uint32_t idx = (uint32_t)(x - S.kmin);
-            pass = idx < S.nslots;
-            if (pass) {
-                c = load_dense_code(S, idx);
-                pass = c < S.sentinel;
-            }
-        } else {
-            const uint32_t h = hash_slot(S, x);
-            c = hash_resolve(S, x, h, static_cast<const unsigned long long*>(S.map)[h]);
-            pass = c < S.sentinel;
-        }
-        if (!pass) {
-            up.flags[i] = 0u;
-        } else if (S.gk_mode == GK_ONE) {
-            up.gid[i] += c * S.gk_stride[0];
-        } else if (S.gk_mode == GK_GENERAL) {
-            up.gid[i] += code_contribution(S, c);
-        }
+        uint32_t c;
+        if (!device_stage_row(S, up.col[i], c)) up.flags[i] = 0u;
+        else if (S.gk_mode != GK_NONE) up.gid[i] += stage_gid_part(S, c);
     }
 }
 
@@ -1249,11 +1259,7 @@ __global__ void __launch_bounds__(256) unfused_agg_kernel(UnfusedParams up) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < up.n; i += stride) {
         if (!up.flags[i]) continue;
-        const long long a = up.col[i];
-        long long v = a;
-        if (up.agg_kind == SDB_AGG_MUL) v = a * (long long)up.col_b[i];
-        else if (up.agg_kind == SDB_AGG_SUB) v = a - (long long)up.col_b[i];
-        else if (up.agg_kind == SDB_AGG_ADD) v = a + (long long)up.col_b[i];
+        const long long v = row_value(up.agg_kind, up.col[i], up.col_b[i]);
         const uint32_t g = up.gid[i];
         atomicAdd(&up.sums[g], (unsigned long long)v);
         atomicAdd(&up.counts[g], 1ull);
@@ -1291,6 +1297,52 @@ hipError_t launch_unfused(const FusedParams& p, uint8_t* flags, uint32_t* gid, h
     up.col = p.cols[p.agg_a];
     up.col_b = p.cols[p.agg_b];
     hipLaunchKernelGGL(unfused_agg_kernel, dim3(grid), dim3(256), 0, s, up);
+    return hipGetLastError();
+}
+
+struct HandoffParams {
+    uint8_t* flags;
+    uint32_t* gid;
+    FusedParams p;
+};
+static_assert(sizeof(HandoffParams) <= 4096, "kernel arguments must fit the 4 KB kernarg segment");
+
+// The whole query in one kernel, one row per thread, but with every hand-off
+// between operators a store to and a later load from the per-row flag and
+// group-id arrays in global memory (volatile, so none is kept in registers).
+__global__ void __launch_bounds__(256) handoff_kernel(HandoffParams kernel_args) {
+    (void)kernel_args;
+    const HandoffParams& hp = *(const HandoffParams*)__builtin_amdgcn_kernarg_segment_ptr();
+    const FusedParams& p = hp.p;
+    volatile uint8_t* flags = hp.flags;
+    volatile uint32_t* gid = hp.gid;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < p.n; i += stride) {
+        flags[i] = 1u;
+        gid[i] = 0u;
+        for (int st = 0; st < p.nstages; ++st) {
+            if (!flags[i]) break;
+            const StageDev& S = p.st[st];
+            uint32_t c;
+            if (!device_stage_row(S, p.cols[S.col][i], c)) flags[i] = 0u;
+            else if (S.gk_mode != GK_NONE) gid[i] = gid[i] + stage_gid_part(S, c);
+        }
+        if (!flags[i]) continue;
+        const long long v = row_value(p.agg_kind, p.cols[p.agg_a][i], p.cols[p.agg_b][i]);
+        const uint32_t g = gid[i];
+        atomicAdd(&p.sums[g], (unsigned long long)v);
+        atomicAdd(&p.counts[g], 1ull);
+    }
+}
+
+hipError_t launch_handoff(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s) {
+    if (p.n == 0) return hipSuccess;
+    HandoffParams hp;
+    memset(&hp, 0, sizeof hp);
+    hp.flags = flags;
+    hp.gid = gid;
+    hp.p = p;
+    hipLaunchKernelGGL(handoff_kernel, dim3(unfused_grid(p.n)), dim3(256), 0, s, hp);
     return hipGetLastError();
 }
 

@@ -34,6 +34,7 @@ OPS = {"eq": 0, "ne": 1, "lt": 2, "le": 3, "gt": 4, "ge": 5, "between": 6}
 TABLES = {"auto": 0, "dense": 1, "hash": 2}
 AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
 TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3, "part": 4}
+BASELINES = {"per_operator": 0, "global_handoff": 1}
 TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global", 4: "part"}
 LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank"}
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
@@ -107,8 +108,9 @@ SIGNATURES = {
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
     "sdb_build_dims": (i32, [i32, C.POINTER(SdbDimDesc), C.POINTER(vp), C.POINTER(i64), vp, C.POINTER(SdbDim)]),
     "sdb_set_fused_events": (i32, [vp, vp]),
-    "sdb_unfused_scratch_bytes": (i32, [i64, C.POINTER(i64)]),
-    "sdb_run_star_query_unfused": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
+    "sdb_baseline_scratch_bytes": (i32, [i64, C.POINTER(i64)]),
+    "sdb_run_star_query_baseline": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), i32, vp, vp, i64, vp, i64,
+                                          vp]),
     "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
     "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
     "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
@@ -395,22 +397,24 @@ class StarQuery:
             self._run_scratch = torch.empty(need, dtype=torch.uint8, device=dev)
         return self._run_scratch
 
-    def unfused_scratch(self, device):
-        """Per-row flags and group ids for :meth:`run_unfused`."""
+    def baseline_scratch(self, device):
+        """Per-row flags and group ids for :meth:`run_baseline`."""
         import torch
         need = i64(0)
-        _check(lib().sdb_unfused_scratch_bytes(int(self.q.n_fact), C.byref(need)))
+        _check(lib().sdb_baseline_scratch_bytes(int(self.q.n_fact), C.byref(need)))
         return torch.empty(max(int(need.value), 256), dtype=torch.uint8, device=device)
 
-    def run_unfused(self, sums, counts, plan: SdbPlan | None = None, stream=None, scratch=None) -> None:
-        """The same query one operator per kernel (flags and group ids through
-        global memory): the unfused baseline."""
+    def run_baseline(self, mode: str, sums, counts, plan: SdbPlan | None = None, stream=None,
+                     scratch=None) -> None:
+        """The same query as a slow baseline of the fusion ablation: ``mode``
+        'per_operator' (one kernel per operator) or 'global_handoff' (one
+        kernel whose operators pass flags and group ids through global memory)."""
         plan = plan or self.plan_obj
         if scratch is None:
-            scratch = self.unfused_scratch(sums.device)
-        _check(lib().sdb_run_star_query_unfused(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
-                                                sums.numel(), _ptr(scratch), scratch.numel(),
-                                                _stream_handle(stream)))
+            scratch = self.baseline_scratch(sums.device)
+        _check(lib().sdb_run_star_query_baseline(C.byref(self.q), C.byref(plan), BASELINES[mode], _ptr(sums),
+                                                 _ptr(counts), sums.numel(), _ptr(scratch), scratch.numel(),
+                                                 _stream_handle(stream)))
 
     def run(self, sums, counts, plan: SdbPlan | None = None, stream=None, scratch=None) -> None:
         plan = plan or self.plan_obj
@@ -440,14 +444,17 @@ class StarQuery:
                                          _stream_handle(stream)))
         return outputs
 
-    def execute(self, stream=None, replan: bool = True, unfused: bool = False) -> QueryResult:
-        """plan -> fused pass (or, with ``unfused``, one kernel per operator)
-        -> compaction, then copy the groups to the host."""
+    def execute(self, stream=None, replan: bool = True, baseline: str | None = None) -> QueryResult:
+        """plan -> fused pass (or a ``baseline`` execution, see
+        :meth:`run_baseline`) -> compaction, then copy the groups to the host."""
         import torch
         if replan or self.plan_obj is None:
             self.plan(stream)
         sums, counts = self.alloc_outputs()
-        (self.run_unfused if unfused else self.run)(sums, counts, stream=stream)
+        if baseline is None:
+            self.run(sums, counts, stream=stream)
+        else:
+            self.run_baseline(baseline, sums, counts, stream=stream)
         k, s, c, n, _ = self.finalize(sums, counts, stream=stream)
         (stream or torch.cuda.current_stream()).synchronize()
         m = int(n.item())

@@ -236,20 +236,22 @@ def test_run_rejects_mismatched_plan_before_any_launch():
     assert L.sdb_run_star_query(C.byref(q), C.byref(p5), 0x1000, 0x2000, 100, None, 0, None) == 1
 
 
-def test_unfused_scratch_and_validation():
+def test_baseline_scratch_and_validation():
     L = sdb.lib()
     nb = C.c_int64(0)
-    assert L.sdb_unfused_scratch_bytes(1000, C.byref(nb)) == 0
+    assert L.sdb_baseline_scratch_bytes(1000, C.byref(nb)) == 0
     assert nb.value == 1024 + 4096                        # flags, then 256-aligned group ids
-    assert L.sdb_unfused_scratch_bytes(0, C.byref(nb)) == 0 and nb.value == 0
-    assert L.sdb_unfused_scratch_bytes(-1, C.byref(nb)) == 1
+    assert L.sdb_baseline_scratch_bytes(0, C.byref(nb)) == 0 and nb.value == 0
+    assert L.sdb_baseline_scratch_bytes(-1, C.byref(nb)) == 1
     d = _fake_dim()
     q = _query([d], [(0, 0)])
     p = _plan(q)
-    assert L.sdb_run_star_query_unfused(C.byref(q), C.byref(p), 0x1000, 0x2000, 10, None, 0, None) == 3
-    assert L.sdb_run_star_query_unfused(C.byref(q), C.byref(p), 0x1000, 0x2000, 100, None, 0, None) == 1
-    assert L.sdb_run_star_query_unfused(C.byref(q), C.byref(p), 0x1000, 0x2000, 100, 0x180, 1 << 20, None) == 1
-    assert L.sdb_run_star_query_unfused(C.byref(q), C.byref(p), 0x1000, 0x2000, 100, 0x100, 16, None) == 4
+    run = L.sdb_run_star_query_baseline
+    assert run(C.byref(q), C.byref(p), 0, 0x1000, 0x2000, 10, None, 0, None) == 3           # CAPACITY
+    assert run(C.byref(q), C.byref(p), 2, 0x1000, 0x2000, 100, 0x100, 1 << 20, None) == 1   # mode
+    assert run(C.byref(q), C.byref(p), 1, 0x1000, 0x2000, 100, None, 0, None) == 1
+    assert run(C.byref(q), C.byref(p), 0, 0x1000, 0x2000, 100, 0x180, 1 << 20, None) == 1   # alignment
+    assert run(C.byref(q), C.byref(p), 1, 0x1000, 0x2000, 100, 0x100, 16, None) == 4        # too small
 
 
 def test_finalize_scratch_and_validation():

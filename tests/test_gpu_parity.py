@@ -61,23 +61,25 @@ def test_forced_plans_agree(name, force):
     assert_same(got.as_rows(), want, f"{name} {force}")
 
 
+@pytest.mark.parametrize("mode", ["per_operator", "global_handoff"])
 @pytest.mark.parametrize("name", list(SIZES))
-def test_unfused_baseline_agrees(name):
+def test_baselines_agree(name, mode):
     from paper_2607_07632_amd import sdb
     w = workload(name)
     fact, dims = upload(w)
     q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query)
-    assert_same(q.execute(unfused=True).as_rows(), oracle_rows(w), f"{name} unfused")
+    assert_same(q.execute(baseline=mode).as_rows(), oracle_rows(w), f"{name} {mode}")
 
 
+@pytest.mark.parametrize("mode", ["per_operator", "global_handoff"])
 @pytest.mark.parametrize("n", [0, 1, 5, 257, 4097])
-def test_unfused_baseline_small_and_tiny_schemas(n):
+def test_baselines_small_and_tiny_schemas(n, mode):
     from paper_2607_07632_amd import sdb
     for seed in (5, 17):
         w = random_tiny_workload(seed, n_fact=n)
         fact, dims = upload(w)
         q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query)
-        assert_same(q.execute(unfused=True).as_rows(), oracle_rows(w), f"unfused seed {seed} n {n}")
+        assert_same(q.execute(baseline=mode).as_rows(), oracle_rows(w), f"{mode} seed {seed} n {n}")
 
 
 def test_c1_forced_plans_agree():
