@@ -110,22 +110,25 @@ def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_in
 
 # The plan features of the fused pass added one at a time, each rung a set of
 # planner overrides (the last rung is the planner's own choice).
+_NR = {"range": -1}     # the rungs before the key-range rewrite keep every probe a lookup
 ABLATION_RUNGS = [
     ("kernel at a time: flags and group ids through HBM; hash tables; query order",
      {"order": True, "baseline": "per_operator", "tables": "hash"}),
     ("one kernel; operators hand off through HBM", {"order": True, "baseline": "global_handoff", "tables": "hash"}),
-    ("+ register table; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
-                                                     "terminal": "global", "xcd": -1, "block": 256,
-                                                     "tables": "hash"}),
+    ("+ register table; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1, "terminal": "global",
+                                       "xcd": -1, "block": 256, "tables": "hash"} | _NR),
     ("+ packed direct-mapped maps", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
-                                     "terminal": "global", "xcd": -1, "block": 256}),
+                                     "terminal": "global", "xcd": -1, "block": 256} | _NR),
     ("+ 4-row items (128-bit loads)", {"order": True, "lds": -1, "ipt": 1, "terminal": "global", "xcd": -1,
-                                       "block": 256}),
-    ("+ two items per lane", {"order": True, "lds": -1, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256}),
+                                       "block": 256} | _NR),
+    ("+ two items per lane", {"order": True, "lds": -1, "ipt": 2, "terminal": "global", "xcd": -1,
+                              "block": 256} | _NR),
     ("+ LDS-staged maps and bitmaps", {"order": True, "lds": 2, "ipt": 2, "terminal": "global", "xcd": -1,
-                                      "block": 256}),
-    ("+ sampled stage order", {"lds": 2, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256}),
-    ("+ per-XCD group tables", {"lds": 2, "ipt": 2, "terminal": "global", "block": 256}),
+                                      "block": 256} | _NR),
+    ("+ sampled stage order", {"lds": 2, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256} | _NR),
+    ("+ per-XCD group tables", {"lds": 2, "ipt": 2, "terminal": "global", "block": 256} | _NR),
+    ("+ probes of one contiguous passing key range run as BETWEEN", {"lds": 2, "ipt": 2, "terminal": "global",
+                                                                     "block": 256}),
     ("planner's choice (terminal, block size, rank tables)", {}),
 ]
 

@@ -34,7 +34,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 3
+#define SDB_ABI_VERSION 4
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -133,6 +133,8 @@ typedef struct sdb_dim {
     int64_t n_pass;               /* rows that pass the dimension predicates */
     int32_t key_min;              /* over all rows (0 when n_rows == 0) */
     int32_t key_max;
+    int32_t pass_key_min;         /* over passing rows (0 and -1 when none pass) */
+    int32_t pass_key_max;
     uint64_t n_slots;
     int32_t hash_bits;
     uint32_t sentinel;
@@ -181,7 +183,9 @@ typedef struct sdb_agg {
  *  force_eager     -1: every column is loaded when its stage is reached, for
  *                  the items that still hold a live row; k in 1..SDB_MAX_EAGER:
  *                  the first k columns in order of use are loaded together
- *                  when the items start (needs 4-row items and ipt 1 or 2) */
+ *                  when the items start (needs 4-row items and ipt 1 or 2)
+ *  force_range     -1: never evaluate a probe as a key range (see
+ *                  sdb_plan.stage_range) */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -202,6 +206,7 @@ typedef struct sdb_query {
     int32_t force_xcd;
     int32_t force_eager;
     int32_t force_block;
+    int32_t force_range;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -231,6 +236,10 @@ typedef struct sdb_plan {
     double stage_pass[SDB_MAX_STAGES];    /* pass fraction on the sample, or the estimate used */
     int32_t stage_lds[SDB_MAX_STAGES];    /* SDB_LDS_* */
     int32_t stage_defer[SDB_MAX_STAGES];  /* deferred-gather slot (0 or 1), or -1 */
+    int32_t stage_range[SDB_MAX_STAGES];  /* 1: a probe run as `fact key BETWEEN pass_key_min AND
+                                             pass_key_max` (its dimension's passing keys are exactly
+                                             that range and it feeds no group key; Section 3.2's
+                                             date-range scan, generalized); 0 otherwise */
     int64_t sampled_rows;                 /* 0 when no sample was taken */
     double est_cost;                      /* cost model value of the chosen order */
     int32_t terminal;

@@ -254,6 +254,8 @@ sdb_status check_query(const sdb_query* q) {
         q->force_block != kMaxBlock && q->force_block != kBigBlock)
         return fail(SDB_INVALID_ARG, "force_block %d is not 0, 64, 128, 256, %d or %d", q->force_block, kMaxBlock,
                     kBigBlock);
+    if (q->force_range != 0 && q->force_range != -1)
+        return fail(SDB_INVALID_ARG, "force_range %d is not 0 or -1", q->force_range);
     if (q->force_block == kBigBlock && (q->force_vector == -1 || q->force_ipt == 4 || q->force_eager > 0))
         return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items, ipt 1 or 2 and no eager loads", kBigBlock);
     if (q->force_eager < -1 || q->force_eager > kMaxEager)
@@ -282,6 +284,37 @@ sdb_status group_layout(const sdb_query* q, sdb_plan* plan) {
 }
 
 // The stage of a fact predicate or join probe in FusedParams form, with the
+// A probe that feeds no group key and whose dimension's passing keys are
+// exactly one contiguous range passes a fact row iff the row's key lies in
+// that range: the build rejects duplicate keys, so n_pass distinct keys in
+// [pass_key_min, pass_key_max] fill it when the range holds n_pass values.
+bool range_eligible(const sdb_query* q, int join) {
+    for (int k = 0; k < q->n_group_keys; ++k)
+        if (q->group_keys[k].join == join) return false;
+    const sdb_dim* d = q->joins[join].dim;
+    if (d->n_pass == 0) return true;
+    if (d->pass_key_max < d->pass_key_min) return false;
+    return (int64_t)d->pass_key_max - (int64_t)d->pass_key_min + 1 == d->n_pass;
+}
+
+// The probe of join `join` as a predicate on its fact key column.
+StageDev range_stage(const sdb_query* q, int join) {
+    const sdb_dim* d = q->joins[join].dim;
+    StageDev S;
+    std::memset(&S, 0, sizeof S);
+    S.defer = -1;
+    S.kind = ST_PRED;
+    S.op = OP_PRED;
+    S.col = q->joins[join].fact_key_col;
+    sdb_pred pr;
+    std::memset(&pr, 0, sizeof pr);
+    pr.op = SDB_OP_BETWEEN;
+    pr.lo = d->n_pass > 0 ? d->pass_key_min : 1;   // no passing key: an empty range
+    pr.hi = d->n_pass > 0 ? d->pass_key_max : 0;
+    S.test = lower_pred(pr);
+    return S;
+}
+
 // LDS placement and deferred-gather slot the plan chose for position `pos`
 // (pos < 0: no placement, used by the sampling kernel).
 StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int index, int pos) {
@@ -379,6 +412,11 @@ double probe_cost(const sdb_query* q, int kind, int index, int lds_mode) {
     return bytes > (2ull << 20) ? 6.0 : 3.0;
 }
 
+double stage_cost(const sdb_query* q, const sdb_plan* plan, int s) {
+    if (plan->stage_range[s]) return probe_cost(q, 0, 0, LDS_GLOBAL);   // a predicate
+    return probe_cost(q, plan->stage_kind[s], plan->stage_index[s], plan->stage_lds[s]);
+}
+
 // Fraction of 128-byte lines (32 int32 rows) holding at least one live row.
 double line_fraction(double f) { return 1.0 - std::pow(1.0 - std::min(std::max(f, 0.0), 1.0), 32.0); }
 
@@ -389,7 +427,7 @@ double order_cost(const sdb_query* q, const sdb_plan* plan, const int* order, in
     double f = 1.0, cost = 0.0;
     for (int i = 0; i < n; ++i) {
         const int s = order[i];
-        cost += line_fraction(f) + f * probe_cost(q, plan->stage_kind[s], plan->stage_index[s], plan->stage_lds[s]);
+        cost += line_fraction(f) + f * stage_cost(q, plan, s);
         f *= plan->stage_pass[s];
     }
     const int agg_cols = q->agg.kind == SDB_AGG_COL ? 1 : 2;
@@ -423,8 +461,8 @@ void choose_order(const sdb_query* q, sdb_plan* plan) {
         }
     } else {
         std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-            const double cx = 1.0 + probe_cost(q, plan->stage_kind[x], plan->stage_index[x], plan->stage_lds[x]);
-            const double cy = 1.0 + probe_cost(q, plan->stage_kind[y], plan->stage_index[y], plan->stage_lds[y]);
+            const double cx = 1.0 + stage_cost(q, plan, x);
+            const double cy = 1.0 + stage_cost(q, plan, y);
             return (1.0 - plan->stage_pass[x]) / cx > (1.0 - plan->stage_pass[y]) / cy;
         });
         best = order;
@@ -436,6 +474,7 @@ void choose_order(const sdb_query* q, sdb_plan* plan) {
         plan->stage_index[i] = tmp.stage_index[best[i]];
         plan->stage_pass[i] = tmp.stage_pass[best[i]];
         plan->stage_lds[i] = tmp.stage_lds[best[i]];
+        plan->stage_range[i] = tmp.stage_range[best[i]];
     }
     plan->est_cost = best_cost;
 }
@@ -446,7 +485,8 @@ void place_lds(const sdb_query* q, sdb_plan* plan, uint64_t budget) {
     std::vector<int> cand;
     for (int s = 0; s < plan->n_stages; ++s) {
         plan->stage_lds[s] = LDS_GLOBAL;
-        if (plan->stage_kind[s] == 1 && q->joins[plan->stage_index[s]].dim->kind == SDB_TABLE_DENSE &&
+        if (plan->stage_kind[s] == 1 && !plan->stage_range[s] &&
+            q->joins[plan->stage_index[s]].dim->kind == SDB_TABLE_DENSE &&
             q->joins[plan->stage_index[s]].dim->n_slots > 0)
             cand.push_back(s);
     }
@@ -528,6 +568,10 @@ FusedParams fused_params(const sdb_query* q, const sdb_plan* plan, bool placed) 
     p.nstages = plan->n_stages;
     p.defer_stage = -1;
     for (int s = 0; s < plan->n_stages; ++s) {
+        if (plan->stage_range[s]) {
+            p.st[s] = range_stage(q, plan->stage_index[s]);
+            continue;
+        }
         p.st[s] = make_stage(q, plan, plan->stage_kind[s], plan->stage_index[s], placed ? s : -1);
         if (placed && p.st[s].defer == 0) p.defer_stage = s;
     }
@@ -700,6 +744,11 @@ sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, in
                     return fail(SDB_INVALID_ARG, "plan stage %d: bad deferred gather", s);
                 ++n_defer;
             }
+            if (plan->stage_range[s] != 0) {
+                if (plan->stage_range[s] != 1 || k != 1 || lm != LDS_GLOBAL || plan->stage_defer[s] != -1 ||
+                    !range_eligible(q, i))
+                    return fail(SDB_INVALID_ARG, "plan stage %d: the probe is not a key range", s);
+            }
         }
     }
     if (n_defer > 1) return fail(SDB_INVALID_ARG, "plan defers more than one gather");
@@ -805,6 +854,8 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
         out->n_pass = (int64_t)hs[d].npass;
         out->key_min = n > 0 ? hs[d].kmin : 0;
         out->key_max = n > 0 ? hs[d].kmax : -1;
+        out->pass_key_min = hs[d].npass > 0 ? hs[d].pkmin : 0;
+        out->pass_key_max = hs[d].npass > 0 ? hs[d].pkmax : -1;
         out->n_payloads = desc->n_payloads;
         // payload codes: mixed radix over the payload ranges of passing rows, last payload fastest
         uint64_t domain = 1;
@@ -925,6 +976,9 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     }
     plan->n_stages = n;
     for (int s = 0; s < SDB_MAX_STAGES; ++s) plan->stage_defer[s] = -1;
+    for (int s = 0; s < n; ++s)
+        plan->stage_range[s] = q->force_range != -1 && plan->stage_kind[s] == 1 &&
+                               range_eligible(q, plan->stage_index[s]);
 
     st = group_layout(q, plan);
     if (st != SDB_OK) return st;
@@ -1022,7 +1076,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     // blocks of 512. 1-row items keep blocks of 256.
     int device_lookups = 0;
     for (int s = 0; s < n; ++s) {
-        if (plan->stage_kind[s] != 1) continue;
+        if (plan->stage_kind[s] != 1 || plan->stage_range[s]) continue;
         const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
         if (d->kind == SDB_TABLE_HASH) device_lookups += 2;
         else if (plan->stage_lds[s] == LDS_GLOBAL) device_lookups += 1;

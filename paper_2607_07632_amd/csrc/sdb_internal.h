@@ -155,7 +155,8 @@ struct DimStats {
     uint32_t dup;          // 1: duplicate key seen; 2: hash table full (cannot happen when sized)
     uint32_t pad_;
     unsigned long long occupied;   // dense: slots that some row holds
-    uint32_t pad2_[2];
+    int32_t pkmin;                 // key range over passing rows
+    int32_t pkmax;
 };
 static_assert(sizeof(DimStats) <= 256, "stats must fit the reserved 256 bytes");
 static_assert(sizeof(FusedParams) <= 4096, "kernel arguments must fit the 4 KB kernarg segment");

@@ -192,6 +192,8 @@ __global__ void stats_init_kernel(BuildBatch kernel_args) {
         }
         st->dup = 0u;
         st->occupied = 0ull;
+        st->pkmin = INT_MAX;
+        st->pkmax = INT_MIN;
     }
 }
 
@@ -203,10 +205,10 @@ constexpr int kStatsRows = 16;
 __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) {
     SDB_BATCH_TABLE;
     constexpr int kWaves = 256 / 64;
-    __shared__ int32_t s_kmin[kWaves], s_kmax[kWaves];
+    __shared__ int32_t s_kmin[kWaves], s_kmax[kWaves], s_pkmin[kWaves], s_pkmax[kWaves];
     __shared__ unsigned long long s_np[kWaves];
     __shared__ int32_t s_pmin[SDB_MAX_PAYLOADS][kWaves], s_pmax[SDB_MAX_PAYLOADS][kWaves];
-    int32_t kmin = INT_MAX, kmax = INT_MIN;
+    int32_t kmin = INT_MAX, kmax = INT_MIN, pkmin = INT_MAX, pkmax = INT_MIN;
     unsigned long long npass = 0;
     int32_t pmin[SDB_MAX_PAYLOADS], pmax[SDB_MAX_PAYLOADS];
     for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
@@ -218,18 +220,18 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
     const int64_t stride = (int64_t)gridDim.x * blockDim.x * U;
     for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x * U + threadIdx.x; i0 < bp.n; i0 += stride) {
         bool ok[U], pass[U];
-        int32_t x[U];
+        int32_t x[U], key[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t i = i0 + (int64_t)u * blockDim.x;
             ok[u] = i < bp.n;
-            x[u] = ok[u] ? bp.key[i] : 0;
+            key[u] = ok[u] ? bp.key[i] : 0;
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (ok[u]) {
-                kmin = min(kmin, x[u]);
-                kmax = max(kmax, x[u]);
+                kmin = min(kmin, key[u]);
+                kmax = max(kmax, key[u]);
             }
             pass[u] = ok[u];
         }
@@ -252,10 +254,18 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
                 }
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) npass += pass[u] ? 1ull : 0ull;
+        for (int u = 0; u < U; ++u) {
+            npass += pass[u] ? 1ull : 0ull;
+            if (pass[u]) {
+                pkmin = min(pkmin, key[u]);
+                pkmax = max(pkmax, key[u]);
+            }
+        }
     }
     kmin = wave_min_i32(kmin);
     kmax = wave_max_i32(kmax);
+    pkmin = wave_min_i32(pkmin);
+    pkmax = wave_max_i32(pkmax);
     npass = wave_sum_u64(npass);
     for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
         pmin[p] = wave_min_i32(pmin[p]);
@@ -265,6 +275,8 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
     if ((threadIdx.x & 63) == 0) {
         s_kmin[wave] = kmin;
         s_kmax[wave] = kmax;
+        s_pkmin[wave] = pkmin;
+        s_pkmax[wave] = pkmax;
         s_np[wave] = npass;
         for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
             s_pmin[p][wave] = pmin[p];
@@ -276,6 +288,8 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
         for (int w = 1; w < kWaves; ++w) {
             kmin = min(kmin, s_kmin[w]);
             kmax = max(kmax, s_kmax[w]);
+            pkmin = min(pkmin, s_pkmin[w]);
+            pkmax = max(pkmax, s_pkmax[w]);
             npass += s_np[w];
             for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
                 pmin[p] = min(pmin[p], s_pmin[p][w]);
@@ -287,6 +301,8 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
         if (kmax != INT_MIN) atomicMax(&st->kmax, kmax);
         if (npass) {
             atomicAdd(&st->npass, npass);
+            atomicMin(&st->pkmin, pkmin);
+            atomicMax(&st->pkmax, pkmax);
             for (int p = 0; p < bp.n_payloads; ++p) {
                 atomicMin(&st->pmin[p], pmin[p]);
                 atomicMax(&st->pmax[p], pmax[p]);

@@ -55,7 +55,8 @@ class SdbDimDesc(C.Structure):
 
 class SdbDim(C.Structure):
     _fields_ = [("kind", i32), ("width", i32), ("n_rows", i64), ("n_pass", i64),
-                ("key_min", i32), ("key_max", i32), ("n_slots", u64), ("hash_bits", i32),
+                ("key_min", i32), ("key_max", i32), ("pass_key_min", i32), ("pass_key_max", i32),
+                ("n_slots", u64), ("hash_bits", i32),
                 ("sentinel", u32), ("domain", u64), ("n_payloads", i32),
                 ("payload_min", i32 * MAX_PAYLOADS), ("payload_radix", u32 * MAX_PAYLOADS),
                 ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp), ("bits", vp)]
@@ -81,13 +82,14 @@ class SdbQuery(C.Structure):
                 ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
-                ("force_block", i32)]
+                ("force_block", i32), ("force_range", i32)]
 
 
 class SdbPlan(C.Structure):
     _fields_ = [("n_stages", i32), ("stage_kind", i32 * MAX_STAGES),
                 ("stage_index", i32 * MAX_STAGES), ("stage_pass", C.c_double * MAX_STAGES),
                 ("stage_lds", i32 * MAX_STAGES), ("stage_defer", i32 * MAX_STAGES),
+                ("stage_range", i32 * MAX_STAGES),
                 ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
                 ("vector", i32), ("eager", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
                 ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
@@ -295,8 +297,10 @@ class StarQuery:
 
     ``fact`` maps column name to an int32 device tensor; ``tables`` is the
     list of DimTable per join (``build_dims``); ``query`` the plain-data
-    description. ``force`` may hold terminal ('scalar'|'lds'|'global'), ipt,
-    vector (1 / -1), order (True = keep query order) and grid.
+    description. ``force`` may hold terminal ('scalar'|'lds'|'global'|'part'),
+    ipt, vector (1 / -1), order (True = keep query order), grid, lds, xcd,
+    eager, block and range (-1: no key-range probes), the sdb_query force_*
+    fields of the same names.
     """
 
     def __init__(self, fact: dict, tables: list, query: dict, force: dict | None = None):
@@ -356,6 +360,7 @@ class StarQuery:
         q.force_xcd = int(force.get("xcd", 0))
         q.force_eager = int(force.get("eager", 0))
         q.force_block = int(force.get("block", 0))
+        q.force_range = int(force.get("range", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -471,7 +476,9 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
             name = (query["fact_preds"][i]["col"] if kind == 0 else query["joins"][i]["dim"])
         st = {"kind": "pred" if kind == 0 else "probe", "index": i, "name": name,
               "pass": round(plan.stage_pass[s], 6)}
-        if kind == 1:
+        if kind == 1 and plan.stage_range[s]:
+            st["table"] = "key_range"
+        elif kind == 1:
             st["table"] = LDS_NAMES.get(plan.stage_lds[s], plan.stage_lds[s])
             if plan.stage_defer[s] >= 0:
                 st["deferred_gather"] = True

@@ -38,7 +38,7 @@ def test_struct_layout_matches_binding():
     sizes = (C.c_int64 * 8)()
     assert L.sdb_struct_sizes(sizes, 8) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
-    assert L.sdb_abi_version() == 3
+    assert L.sdb_abi_version() == 4
 
 
 def test_status_strings():
@@ -99,7 +99,7 @@ def test_dim_descriptor_validation(mutate, status):
 
 
 def _fake_dim(kind=1, width=1, n_rows=200_000, n_pass=40_000, radices=(25,), mins=(0,),
-              key_min=0, n_slots=200_000, bits=0):
+              key_min=0, n_slots=200_000, bits=0, pass_range=(0, 0)):
     h = sdb.SdbDim()
     h.kind = kind
     h.width = width
@@ -107,6 +107,7 @@ def _fake_dim(kind=1, width=1, n_rows=200_000, n_pass=40_000, radices=(25,), min
     h.n_pass = n_pass
     h.key_min = key_min
     h.key_max = key_min + n_slots - 1
+    h.pass_key_min, h.pass_key_max = pass_range
     h.n_slots = n_slots if kind == 1 else (1 << bits)
     h.hash_bits = bits
     h.sentinel = 0xFF
@@ -234,6 +235,46 @@ def test_run_rejects_mismatched_plan_before_any_launch():
     p5 = sdb.SdbPlan.from_buffer_copy(p)
     p5.xcd_copies = 8                                     # copies need the global terminal
     assert L.sdb_run_star_query(C.byref(q), C.byref(p5), 0x1000, 0x2000, 100, None, 0, None) == 1
+
+
+def test_probe_as_key_range():
+    d_gk = _fake_dim(pass_range=(100, 40_099))              # contiguous, but it feeds a group key
+    d_f = _fake_dim(pass_range=(5, 40_004))                 # contiguous, filter only: a key range
+    d_gap = _fake_dim(pass_range=(5, 40_005))               # 40,001 values for 40,000 keys: a gap
+    d_none = _fake_dim(n_pass=0, pass_range=(0, -1))        # nothing passes: the empty range
+    q = _query([d_gk, d_f, d_gap, d_none], [(0, 0)])
+    p = _plan(q)
+    got = {p.stage_index[s]: p.stage_range[s] for s in range(p.n_stages) if p.stage_kind[s] == 1}
+    assert got == {0: 0, 1: 1, 2: 0, 3: 1}
+    for s in range(p.n_stages):
+        if p.stage_range[s]:
+            assert p.stage_lds[s] == 0 and p.stage_defer[s] == -1
+    assert sdb.plan_summary(p)["stages"][1]["table"] == "key_range"
+    # the cost-model order (no sample without fact rows) moves the flags with their stages
+    q.n_fact = 0
+    q.force_order = 0
+    p2 = _plan(q)
+    order = [p2.stage_index[s] for s in range(p2.n_stages)]
+    assert order != [0, 1, 2, 3]
+    assert {p2.stage_index[s]: p2.stage_range[s] for s in range(p2.n_stages)} == {0: 0, 1: 1, 2: 0, 3: 1}
+    q.n_fact = 1000
+    q.force_order = 1
+    q.force_range = -1
+    p_off = _plan(q)
+    assert all(p_off.stage_range[s] == 0 for s in range(p_off.n_stages))
+    q.force_range = 2
+    with pytest.raises(sdb.SdbError) as e:
+        _plan(q)
+    assert e.value.name == "SDB_INVALID_ARG"
+    q.force_range = 0
+    # a plan that marks a probe with a gap in its passing keys is refused before any launch
+    bad = sdb.SdbPlan.from_buffer_copy(p)
+    s_gap = next(s for s in range(p.n_stages) if p.stage_kind[s] == 1 and p.stage_index[s] == 2)
+    bad.stage_lds[s_gap] = 0
+    bad.stage_range[s_gap] = 1
+    L = sdb.lib()
+    assert L.sdb_run_star_query(C.byref(q), C.byref(bad), 0x1000, 0x2000, 100, None, 0, None) == 1
+    assert "key range" in L.sdb_last_error().decode()
 
 
 def test_baseline_scratch_and_validation():

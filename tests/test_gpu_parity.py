@@ -234,6 +234,7 @@ def test_build_statistics_match_numpy():
     ok = part["category"] == 1
     h = t.handle
     assert h.n_pass == int(ok.sum()) and h.kind == 1 and h.width == 2
+    assert h.pass_key_min == part["part_key"][ok].min() and h.pass_key_max == part["part_key"][ok].max()
     assert h.payload_min[0] == part["brand"][ok].min()
     assert h.payload_radix[0] == part["brand"][ok].max() - part["brand"][ok].min() + 1
     # the map itself: the sentinel (0xFFFE) for filtered rows, brand - min otherwise
@@ -355,3 +356,70 @@ def test_fused_events_bracket_the_kernel():
     rows = [(tuple(int(x) for x in kk), int(ss), int(cc))
             for kk, ss, cc in zip(k[:m].cpu().numpy(), s[:m].cpu().numpy(), c[:m].cpu().numpy())]
     assert_same(rows, oracle_rows(w), "timed run")
+
+
+def _range_workload(seed, n=50_003, empty_join=False):
+    """Dimensions whose passing keys are one contiguous range (a day-to-year
+    style attribute, a predicate on the key itself, on a dense and on a hash
+    table, with fact keys partly outside the key set) next to a grouped one."""
+    rng = np.random.default_rng([2607, 7632, 77, seed])
+    dims, keys, joins, fact = {}, {}, [], {}
+    m = 700
+    off = int(rng.integers(-500, 500))
+    r_key = (rng.permutation(m) + off).astype(np.int32)
+    dims["r"] = {"k": r_key, "y": ((r_key - off) // 50).astype(np.int32)}
+    joins.append({"fact_key": "fr", "dim": "r", "preds": [{"col": "y", "op": "eq", "lo": 3, "hi": None}],
+                  "payloads": []})
+    g_key = rng.permutation(300).astype(np.int32)
+    dims["g"] = {"k": g_key, "a": rng.integers(0, 20, size=300, dtype=np.int32)}
+    joins.append({"fact_key": "fg", "dim": "g", "preds": [], "payloads": ["a"]})
+    h_key = (rng.permutation(900) * 3 + 11).astype(np.int32)      # keys 3 apart: hash table
+    h_sorted = np.sort(h_key)
+    dims["h"] = {"k": h_key}
+    joins.append({"fact_key": "fh", "dim": "h", "kind": "hash",
+                  "preds": [{"col": "k", "op": "between", "lo": int(h_sorted[100]), "hi": int(h_sorted[100])}],
+                  "payloads": []})
+    if empty_join:
+        dims["e"] = {"k": np.arange(50, dtype=np.int32), "y": np.zeros(50, dtype=np.int32)}
+        joins.append({"fact_key": "fe", "dim": "e", "preds": [{"col": "y", "op": "eq", "lo": 1, "hi": None}],
+                      "payloads": []})
+        fact["fe"] = rng.integers(0, 50, size=n, dtype=np.int32)
+    fact["fr"] = rng.integers(off - 30, off + m + 30, size=n, dtype=np.int32)
+    fact["fg"] = rng.integers(0, 300, size=n, dtype=np.int32)
+    fact["fh"] = np.where(rng.random(n) < 0.5, h_sorted[100], h_key[rng.integers(0, 900, size=n)]).astype(np.int32)
+    fact["v"] = rng.integers(-1000, 1000, size=n, dtype=np.int32)
+    for name in dims:
+        keys[name] = "k"
+    query = {"fact_preds": [], "joins": joins, "group_by": [["g", "a"]], "agg": {"kind": "col", "a": "v", "b": None}}
+    return datagen.Workload(f"range{seed}", n, fact, dims, keys, query)
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_key_range_probes(seed):
+    from paper_2607_07632_amd import sdb
+    w = _range_workload(seed)
+    want = oracle_rows(w)
+    assert want, "the workload should keep some groups"
+    got, q = run_gpu(w)
+    tables = {st["name"]: st["table"] for st in sdb.plan_summary(q.plan_obj, w.query)["stages"]}
+    assert tables["r"] == "key_range" and tables["h"] == "key_range" and tables["g"] != "key_range"
+    assert_same(got.as_rows(), want, f"range {seed}")
+    for force in [{"range": -1}, {"terminal": "global"}, {"vector": -1}, {"order": True}]:
+        got, q = run_gpu(w, force=force)
+        assert_same(got.as_rows(), want, f"range {seed} {force}")
+        if force.get("range") == -1:
+            assert all(st.get("table") != "key_range" for st in sdb.plan_summary(q.plan_obj)["stages"])
+    w0 = _range_workload(seed, empty_join=True)
+    got, q = run_gpu(w0)
+    assert got.as_rows() == oracle_rows(w0) == []
+    tables = {st["name"]: st.get("table") for st in sdb.plan_summary(q.plan_obj, w0.query)["stages"]}
+    assert tables["e"] == "key_range"
+
+
+def test_c1_date_join_is_a_key_range():
+    from paper_2607_07632_amd import sdb
+    w = workload("c1_scalar_scan")
+    got, q = run_gpu(w)
+    tables = {st["name"]: st.get("table") for st in sdb.plan_summary(q.plan_obj, w.query)["stages"]}
+    assert tables["date"] == "key_range"
+    assert_same(got.as_rows(), oracle_rows(w), "c1 key range")
