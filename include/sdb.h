@@ -184,8 +184,9 @@ typedef struct sdb_agg {
  *                  the items that still hold a live row; k in 1..SDB_MAX_EAGER:
  *                  the first k columns in order of use are loaded together
  *                  when the items start (needs 4-row items and ipt 1 or 2)
- *  force_range     -1: never evaluate a probe as a key range (see
- *                  sdb_plan.stage_range) */
+ *  force_range     which probes run as a key range (sdb_plan.stage_range):
+ *                  0: those that would otherwise look up a table in device
+ *                  memory; 1: every one that can; -1: none */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -350,6 +351,17 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
  * `stop` just after it (before any terminal pass), so the elapsed time
  * between them is that kernel's duration. NULL, NULL turns it off. */
 SDB_API sdb_status sdb_set_fused_events(void* start, void* stop);
+
+/* Measurement only: the plain streaming read the fused pass is compared
+ * with (the practical bandwidth ceiling of reading fact columns). Adds every
+ * int32 of the n_cols columns of n rows (host array of device pointers, each
+ * 16-byte aligned) into *sum (device int64[1], zeroed first), mod 2^64,
+ * asynchronously on `stream`, with the fused kernel's load shape: 128-bit
+ * non-temporal loads, two 4-row items per lane, four columns at a time, in
+ * blocks of 512 threads, blocks_per_cu (1 to 4; 0: 2) per compute unit.
+ * Errors: INVALID_ARG, HIP_ERROR. */
+SDB_API sdb_status sdb_read_columns(const int32_t* const* cols, int32_t n_cols, int64_t n,
+                                    int32_t blocks_per_cu, int64_t* sum, void* stream);
 
 /* ---- baselines for the fusion ablation ---------------------------------- */
 

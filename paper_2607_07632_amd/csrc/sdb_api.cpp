@@ -254,8 +254,8 @@ sdb_status check_query(const sdb_query* q) {
         q->force_block != kMaxBlock && q->force_block != kBigBlock)
         return fail(SDB_INVALID_ARG, "force_block %d is not 0, 64, 128, 256, %d or %d", q->force_block, kMaxBlock,
                     kBigBlock);
-    if (q->force_range != 0 && q->force_range != -1)
-        return fail(SDB_INVALID_ARG, "force_range %d is not 0 or -1", q->force_range);
+    if (q->force_range < -1 || q->force_range > 1)
+        return fail(SDB_INVALID_ARG, "force_range %d is not -1, 0 or 1", q->force_range);
     if (q->force_block == kBigBlock && (q->force_vector == -1 || q->force_ipt == 4 || q->force_eager > 0))
         return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items, ipt 1 or 2 and no eager loads", kBigBlock);
     if (q->force_eager < -1 || q->force_eager > kMaxEager)
@@ -976,9 +976,9 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     }
     plan->n_stages = n;
     for (int s = 0; s < SDB_MAX_STAGES; ++s) plan->stage_defer[s] = -1;
-    for (int s = 0; s < n; ++s)
-        plan->stage_range[s] = q->force_range != -1 && plan->stage_kind[s] == 1 &&
-                               range_eligible(q, plan->stage_index[s]);
+    if (q->force_range == 1)
+        for (int s = 0; s < n; ++s)
+            plan->stage_range[s] = plan->stage_kind[s] == 1 && range_eligible(q, plan->stage_index[s]);
 
     st = group_layout(q, plan);
     if (st != SDB_OK) return st;
@@ -1018,6 +1018,12 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
 
     // LDS placement of small dense tables, then the cheapest stage order
     if (q->force_lds != -1) place_lds(q, plan, (uint64_t)kLdsStageBudget);
+    // Probes left to device-memory lookups become key-range predicates where
+    // they can (an LDS lookup costs about as much as the compare: measured).
+    if (q->force_range == 0)
+        for (int s = 0; s < n; ++s)
+            plan->stage_range[s] = plan->stage_kind[s] == 1 && plan->stage_lds[s] == LDS_GLOBAL &&
+                                   range_eligible(q, plan->stage_index[s]);
     if (!q->force_order && n > 1) choose_order(q, plan);
     else {
         int order[SDB_MAX_STAGES];
@@ -1343,6 +1349,34 @@ SDB_API sdb_status sdb_set_fused_events(void* start, void* stop) {
     if ((start == nullptr) != (stop == nullptr)) return fail(SDB_INVALID_ARG, "set both events or neither");
     g_fused_start = (hipEvent_t)start;
     g_fused_stop = (hipEvent_t)stop;
+    return ok();
+}
+
+SDB_API sdb_status sdb_read_columns(const int32_t* const* cols, int32_t n_cols, int64_t n, int32_t blocks_per_cu,
+                                    int64_t* sum, void* stream) {
+    if (!cols || !sum) return fail(SDB_INVALID_ARG, "null argument");
+    if (blocks_per_cu < 0 || blocks_per_cu > 4)
+        return fail(SDB_INVALID_ARG, "blocks_per_cu %d is not in [0, 4]", (int)blocks_per_cu);
+    if (n_cols < 0 || n_cols > SDB_MAX_FACT_COLS)
+        return fail(SDB_INVALID_ARG, "n_cols %d is not in [0, %d]", (int)n_cols, SDB_MAX_FACT_COLS);
+    if (n < 0) return fail(SDB_INVALID_ARG, "negative n");
+    ReadParams p;
+    std::memset(&p, 0, sizeof p);
+    for (int c = 0; c < n_cols; ++c) {
+        if (!cols[c] && n > 0) return fail(SDB_INVALID_ARG, "column %d is null", c);
+        if (!aligned16(cols[c])) return fail(SDB_INVALID_ARG, "column %d is not 16-byte aligned", c);
+        p.cols[c] = cols[c];
+    }
+    p.n_cols = n_cols;
+    p.n = n;
+    p.out = (unsigned long long*)sum;
+    int dev = 0, cus = 0;
+    SDB_HIP(hipGetDevice(&dev), "device query");
+    SDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "device query");
+    const int64_t tiles = (n / 4 + 1023) / 1024;
+    const int per_cu = blocks_per_cu > 0 ? blocks_per_cu : 2;
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(tiles, (int64_t)cus * per_cu));
+    SDB_HIP(launch_read_columns(p, grid, (hipStream_t)stream), "read launch");
     return ok();
 }
 

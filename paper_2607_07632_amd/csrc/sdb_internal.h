@@ -254,6 +254,15 @@ hipError_t launch_rank_build(const RankParams& rp, hipStream_t s);
 // kernel-at-a-time run of the stages and aggregate of p (device tables only)
 hipError_t launch_unfused(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s);
 hipError_t launch_handoff(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s);
+
+struct ReadParams {
+    const int32_t* cols[SDB_MAX_FACT_COLS];
+    int32_t n_cols;
+    int32_t pad_;
+    int64_t n;
+    unsigned long long* out;
+};
+hipError_t launch_read_columns(const ReadParams& p, int grid, hipStream_t s);
 hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t n_groups,
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);

@@ -1363,6 +1363,54 @@ hipError_t launch_handoff(const FusedParams& p, uint8_t* flags, uint32_t* gid, h
 }
 
 // ---------------------------------------------------------------------------
+// streaming read of fact columns: the bandwidth the fused pass is compared with
+// ---------------------------------------------------------------------------
+
+// Adds every int32 of n_cols columns of n rows into *out (mod 2^64), reading
+// the columns four at a time with 128-bit non-temporal loads, two 4-row
+// items per lane: the fused kernel's load shape without any of its work.
+__global__ void __launch_bounds__(512) read_columns_kernel(ReadParams kernel_args) {
+    (void)kernel_args;
+    const ReadParams& p = *(const ReadParams*)__builtin_amdgcn_kernarg_segment_ptr();
+    const int64_t n_items = p.n / 4;
+    const int64_t tile = (int64_t)blockDim.x * 2;
+    unsigned long long acc = 0;
+    for (int64_t base = (int64_t)blockIdx.x * tile; base < n_items; base += (int64_t)gridDim.x * tile) {
+        for (int c0 = 0; c0 < p.n_cols; c0 += 4) {
+            v4i x[4][2];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const int64_t it = base + (int64_t)j * blockDim.x + threadIdx.x;
+                    x[k][j] = v4i{0, 0, 0, 0};
+                    if (c0 + k < p.n_cols && it < n_items)
+                        x[k][j] = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p.cols[c0 + k]) + it);
+                }
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc += (unsigned long long)((long long)x[k][j].x + x[k][j].y + x[k][j].z + x[k][j].w);
+        }
+    }
+    if (blockIdx.x == 0) {   // the last n mod 4 rows
+        const int64_t r = n_items * 4 + (int64_t)threadIdx.x;
+        if (r < p.n)
+            for (int c = 0; c < p.n_cols; ++c) acc += (unsigned long long)(long long)p.cols[c][r];
+    }
+    acc = wave_sum_u64(acc);
+    if ((threadIdx.x & 63u) == 0u) atomicAdd(p.out, acc);
+}
+
+hipError_t launch_read_columns(const ReadParams& p, int grid, hipStream_t s) {
+    hipError_t e = launch_fill_u64(p.out, 1, s);
+    if (e != hipSuccess || p.n == 0 || p.n_cols == 0) return e;
+    hipLaunchKernelGGL(read_columns_kernel, dim3(grid), dim3(512), 0, s, p);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // partitioned aggregation: scan, scatter by partition, LDS aggregation
 // ---------------------------------------------------------------------------
 

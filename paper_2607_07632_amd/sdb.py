@@ -110,6 +110,7 @@ SIGNATURES = {
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
     "sdb_build_dims": (i32, [i32, C.POINTER(SdbDimDesc), C.POINTER(vp), C.POINTER(i64), vp, C.POINTER(SdbDim)]),
     "sdb_set_fused_events": (i32, [vp, vp]),
+    "sdb_read_columns": (i32, [C.POINTER(vp), i32, i64, i32, vp, vp]),
     "sdb_baseline_scratch_bytes": (i32, [i64, C.POINTER(i64)]),
     "sdb_run_star_query_baseline": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), i32, vp, vp, i64, vp, i64,
                                           vp]),
@@ -490,6 +491,15 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
             "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}
+
+
+def read_columns(cols: list, out, stream=None, blocks_per_cu: int = 0) -> None:
+    """Streaming read of int32 device columns (equal length, 16-byte aligned):
+    adds all their values into ``out`` (int64 device tensor of one element),
+    asynchronously; the bandwidth reference for the fused pass."""
+    n = int(cols[0].numel()) if cols else 0
+    ptrs = (vp * max(len(cols), 1))(*[_ptr(c) for c in cols])
+    _check(lib().sdb_read_columns(ptrs, len(cols), n, int(blocks_per_cu), _ptr(out), _stream_handle(stream)))
 
 
 def set_fused_events(start=None, stop=None) -> None:

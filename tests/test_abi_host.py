@@ -243,6 +243,7 @@ def test_probe_as_key_range():
     d_gap = _fake_dim(pass_range=(5, 40_005))               # 40,001 values for 40,000 keys: a gap
     d_none = _fake_dim(n_pass=0, pass_range=(0, -1))        # nothing passes: the empty range
     q = _query([d_gk, d_f, d_gap, d_none], [(0, 0)])
+    q.force_range = 1
     p = _plan(q)
     got = {p.stage_index[s]: p.stage_range[s] for s in range(p.n_stages) if p.stage_kind[s] == 1}
     assert got == {0: 0, 1: 1, 2: 0, 3: 1}
@@ -250,6 +251,13 @@ def test_probe_as_key_range():
         if p.stage_range[s]:
             assert p.stage_lds[s] == 0 and p.stage_defer[s] == -1
     assert sdb.plan_summary(p)["stages"][1]["table"] == "key_range"
+    # automatic: only probes that would look up device memory; a small table staged in LDS stays a lookup
+    d_small = _fake_dim(n_rows=1000, n_pass=200, n_slots=1000, pass_range=(300, 499))
+    d_big = _fake_dim(n_rows=4_000_000, n_pass=800_000, n_slots=4_000_000, pass_range=(7, 800_006))
+    qa = _query([d_small, d_big, d_gk], [(2, 0)])
+    pa = _plan(qa)
+    table = {st["index"]: st["table"] for st in sdb.plan_summary(pa)["stages"]}
+    assert table[0] == "lds_map" and table[1] == "key_range" and table[2] != "key_range"
     # the cost-model order (no sample without fact rows) moves the flags with their stages
     q.n_fact = 0
     q.force_order = 0
@@ -266,7 +274,7 @@ def test_probe_as_key_range():
     with pytest.raises(sdb.SdbError) as e:
         _plan(q)
     assert e.value.name == "SDB_INVALID_ARG"
-    q.force_range = 0
+    q.force_range = 1
     # a plan that marks a probe with a gap in its passing keys is refused before any launch
     bad = sdb.SdbPlan.from_buffer_copy(p)
     s_gap = next(s for s in range(p.n_stages) if p.stage_kind[s] == 1 and p.stage_index[s] == 2)
@@ -275,6 +283,19 @@ def test_probe_as_key_range():
     L = sdb.lib()
     assert L.sdb_run_star_query(C.byref(q), C.byref(bad), 0x1000, 0x2000, 100, None, 0, None) == 1
     assert "key range" in L.sdb_last_error().decode()
+
+
+def test_read_columns_validation():
+    L = sdb.lib()
+    cols = (C.c_void_p * 2)(0x10000, 0x20000)
+    assert L.sdb_read_columns(None, 1, 10, 0, 0x3000, None) == 1
+    assert L.sdb_read_columns(cols, 2, 10, 0, None, None) == 1
+    assert L.sdb_read_columns(cols, 17, 10, 0, 0x3000, None) == 1
+    assert L.sdb_read_columns(cols, 2, -1, 0, 0x3000, None) == 1
+    assert L.sdb_read_columns(cols, 2, 10, 5, 0x3000, None) == 1
+    bad = (C.c_void_p * 2)(0x10000, 0x20004)
+    assert L.sdb_read_columns(bad, 2, 10, 0, 0x3000, None) == 1
+    assert "aligned" in L.sdb_last_error().decode()
 
 
 def test_baseline_scratch_and_validation():

@@ -400,26 +400,51 @@ def test_key_range_probes(seed):
     w = _range_workload(seed)
     want = oracle_rows(w)
     assert want, "the workload should keep some groups"
-    got, q = run_gpu(w)
-    tables = {st["name"]: st["table"] for st in sdb.plan_summary(q.plan_obj, w.query)["stages"]}
-    assert tables["r"] == "key_range" and tables["h"] == "key_range" and tables["g"] != "key_range"
+
+    def tables_of(q, query):
+        return {st["name"]: st["table"] for st in sdb.plan_summary(q.plan_obj, query)["stages"]}
+
+    got, q = run_gpu(w)                      # automatic: only the device-memory probe
+    t = tables_of(q, w.query)
+    assert t["h"] == "key_range" and t["r"] == "lds_map" and t["g"] != "key_range"
     assert_same(got.as_rows(), want, f"range {seed}")
-    for force in [{"range": -1}, {"terminal": "global"}, {"vector": -1}, {"order": True}]:
+    for force in [{"range": 1}, {"range": -1}, {"range": 1, "terminal": "global"}, {"range": 1, "vector": -1},
+                  {"range": 1, "order": True}, {"range": 1, "lds": -1}]:
         got, q = run_gpu(w, force=force)
         assert_same(got.as_rows(), want, f"range {seed} {force}")
-        if force.get("range") == -1:
-            assert all(st.get("table") != "key_range" for st in sdb.plan_summary(q.plan_obj)["stages"])
+        t = tables_of(q, w.query)
+        if force["range"] == 1:
+            assert t["r"] == "key_range" and t["h"] == "key_range"
+        else:
+            assert "key_range" not in t.values()
     w0 = _range_workload(seed, empty_join=True)
-    got, q = run_gpu(w0)
+    got, q = run_gpu(w0, force={"range": 1})
     assert got.as_rows() == oracle_rows(w0) == []
-    tables = {st["name"]: st.get("table") for st in sdb.plan_summary(q.plan_obj, w0.query)["stages"]}
-    assert tables["e"] == "key_range"
+    assert tables_of(q, w0.query)["e"] == "key_range"
 
 
-def test_c1_date_join_is_a_key_range():
+def test_c1_date_join_as_key_range():
     from paper_2607_07632_amd import sdb
     w = workload("c1_scalar_scan")
-    got, q = run_gpu(w)
-    tables = {st["name"]: st.get("table") for st in sdb.plan_summary(q.plan_obj, w.query)["stages"]}
-    assert tables["date"] == "key_range"
-    assert_same(got.as_rows(), oracle_rows(w), "c1 key range")
+    for force, table in [({}, "lds_map"), ({"range": 1}, "key_range")]:
+        got, q = run_gpu(w, force=force)
+        tables = {st["name"]: st.get("table") for st in sdb.plan_summary(q.plan_obj, w.query)["stages"]}
+        assert tables["date"] == table
+        assert_same(got.as_rows(), oracle_rows(w), f"c1 {force}")
+
+
+@pytest.mark.parametrize("n_cols", [1, 3, 4, 5, 9])
+def test_read_columns_sums_every_value(n_cols):
+    import torch
+    from paper_2607_07632_amd import sdb
+    rng = np.random.default_rng([2607, 7632, 88, n_cols])
+    out = torch.zeros(1, dtype=torch.int64, device="cuda")
+    for n in [0, 1, 5, 4097, 1_000_003]:
+        host = [rng.integers(-2**31, 2**31, size=n, dtype=np.int64).astype(np.int32) for _ in range(n_cols)]
+        dev = [torch.from_numpy(h).cuda() for h in host]
+        want = sum(int(h.astype(np.int64).sum()) for h in host)
+        want = (want + 2**63) % 2**64 - 2**63
+        for per_cu in (0, 1, 4):
+            sdb.read_columns(dev, out, blocks_per_cu=per_cu)
+            torch.cuda.synchronize()
+            assert int(out.item()) == want, (n_cols, n, per_cu)
