@@ -131,7 +131,7 @@ def _run(fact_dev, dims_dev, w, lo=None, hi=None):
     return res, q
 
 
-@pytest.mark.parametrize("name", ["c3_star3", "c4_star4_zipf", "c5_hash_stress"])
+@pytest.mark.parametrize("name", ["c2_join_group", "c3_star3", "c4_star4_zipf", "c5_hash_stress"])
 def test_full_size(name):
     import torch
     t0 = time.time()
@@ -159,7 +159,7 @@ def test_full_size(name):
     _log(f"{name}: oracle window of {hi - lo} rows agrees")
 
     # 3. unaligned row ranges add up to the full result
-    cuts = [0, 199_999_999, 400_000_002, w.n_fact]
+    cuts = [0, w.n_fact // 3 - 1, 2 * (w.n_fact // 3) + 2, w.n_fact]
     acc = {}
     for a, b in zip(cuts[:-1], cuts[1:]):
         r, _ = _run(fact_dev, dims_dev, w, a, b)
@@ -170,4 +170,79 @@ def test_full_size(name):
     assert merged == full.as_rows()
     _log(f"{name}: row ranges add up")
     del fact_dev
+    torch.cuda.empty_cache()
+
+
+def test_more_than_2g_rows():
+    """c3's query over 2^31 + 4,099 fact rows drawn on the device: 64-bit row
+    indexing end to end. Every group's count and sum against torch (gathers,
+    masks and bincount, in chunks; every partial sum stays below 2^53, so the
+    float64 weights are exact), and two row ranges, the second starting at an
+    unaligned row (1-row items), add up to the whole."""
+    import torch
+    from paper_2607_07632_amd import sdb
+    w = datagen.make_workload("c3_star3", n_fact=0)
+    q = w.query
+    n = 2**31 + 4099
+    g = torch.Generator(device="cuda")
+    g.manual_seed(26077632)
+    spans = {"cust_key": (0, 3_000_000), "supp_key": (0, 200_000), "date_key": (0, 2556), "revenue": (1, 1_000_001)}
+    fact = {c: torch.randint(lo, hi, (n,), generator=g, device="cuda", dtype=torch.int32)
+            for c, (lo, hi) in spans.items()}
+    dims = {d: {c: torch.from_numpy(a).cuda() for c, a in t.items()} for d, t in w.dims.items()}
+    _log(f"2g rows: {n} rows drawn on the device")
+
+    # per join: pass flag and payload value by key (keys are 0 .. rows-1 here)
+    per_join = []
+    for jd in q["joins"]:
+        t = w.dims[jd["dim"]]
+        keys = t[w.dim_keys[jd["dim"]]]
+        assert np.array_equal(keys, np.arange(keys.size))
+        ok = _pass_mask(t, jd["preds"])
+        per_join.append((jd, torch.from_numpy(ok).cuda()))
+    radix, kmin, vals = [], [], []
+    for dim, col in q["group_by"]:
+        jd, ok = next(x for x in per_join if x[0]["dim"] == dim)
+        v = w.dims[dim][col][ok.cpu().numpy()]
+        kmin.append(int(v.min()))
+        radix.append(int(v.max()) - int(v.min()) + 1)
+        vals.append((dim, jd["fact_key"], torch.from_numpy(w.dims[dim][col].astype(np.int64)).cuda()))
+    stride = [int(np.prod(radix[k + 1:])) for k in range(len(radix))]
+    G = int(np.prod(radix))
+    counts = torch.zeros(G, dtype=torch.int64, device="cuda")
+    sums = torch.zeros(G, dtype=torch.float64, device="cuda")
+    chunk = 1 << 28
+    for lo in range(0, n, chunk):
+        hi = min(n, lo + chunk)
+        live = torch.ones(hi - lo, dtype=torch.bool, device="cuda")
+        for jd, ok in per_join:
+            live &= ok[fact[jd["fact_key"]][lo:hi].long()]
+        gid = torch.zeros(hi - lo, dtype=torch.int64, device="cuda")
+        for k, (dim, fk, v) in enumerate(vals):
+            gid += (v[fact[fk][lo:hi].long()] - kmin[k]) * stride[k]
+        gl = gid[live]
+        counts += torch.bincount(gl, minlength=G)
+        sums += torch.bincount(gl, weights=fact["revenue"][lo:hi][live].double(), minlength=G)
+    assert float(sums.max()) < 2.0**53
+    present = torch.nonzero(counts).flatten().cpu().numpy()
+    c_h, s_h = counts.cpu().numpy(), sums.cpu().numpy().astype(np.int64)
+    want = [(tuple(int((p // stride[k]) % radix[k] + kmin[k]) for k in range(len(radix))), int(s_h[p]), int(c_h[p]))
+            for p in present]
+    _log(f"2g rows: torch reference has {len(want)} groups")
+
+    tables = sdb.build_dims(dims, w.dim_keys, q)
+    full = sdb.StarQuery(fact, tables, q).execute()
+    assert_same(full.as_rows(), want, "2^31 + 4099 rows")
+    _log("2g rows: full result agrees")
+
+    cut = 2**30 + 3
+    acc = {}
+    for a, b in [(0, cut), (cut, n)]:
+        part = sdb.StarQuery({k: v[a:b] for k, v in fact.items()}, tables, q).execute()
+        for k, s, c in part.as_rows():
+            s0, c0 = acc.get(k, (0, 0))
+            acc[k] = (s0 + s, c0 + c)
+    assert sorted((k, s, c) for k, (s, c) in acc.items()) == full.as_rows()
+    _log("2g rows: row ranges add up")
+    del fact
     torch.cuda.empty_cache()
