@@ -414,6 +414,29 @@ def main(argv=None) -> int:
     log(f"[bench] streaming read of {len(used_cols)} columns: {best[1]:.4f} ms, {read_gbps:.0f} GB/s "
         f"({best[0]} blocks per CU)")
 
+    # the run and the compaction replayed from one HIP graph (no host launch gaps)
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    scratch_g = q0.run_scratch(plan)
+    with torch.cuda.graph(graph, stream=side):
+        q0.run(sums, counts, plan=plan, scratch=scratch_g)
+        q0.finalize(sums, counts, plan=plan, outputs=fin_out)
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    if int(fin_out[3].item()) != n_groups_out:
+        raise AssertionError("graph replay changed the number of groups")
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(10):
+        graph.replay()
+    b.record(stream)
+    b.synchronize()
+    result["run_finalize_ms_graph"] = a.elapsed_time(b) / 10
+    log(f"[bench] run + finalize replayed from a HIP graph: {result['run_finalize_ms_graph']:.4f} ms")
+    del graph
+
     # end to end once: builds, plan, fused pass, compaction and the copy of the groups to the host
     torch.cuda.synchronize()
     t0 = time.perf_counter()

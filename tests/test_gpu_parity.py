@@ -448,3 +448,50 @@ def test_read_columns_sums_every_value(n_cols):
             sdb.read_columns(dev, out, blocks_per_cu=per_cu)
             torch.cuda.synchronize()
             assert int(out.item()) == want, (n_cols, n, per_cu)
+
+
+@pytest.mark.parametrize("name", list(SIZES))
+def test_graph_replay_of_run_and_finalize(name):
+    """The run and the compaction enqueue only kernels (no memset, copy or
+    synchronization), so they can be captured in a HIP graph: every replay,
+    with eager work scribbling over the outputs in between, must give the
+    eager result, which must equal the oracle's."""
+    import torch
+    from paper_2607_07632_amd import sdb
+    w = workload(name)
+    fact, dims = upload(w)
+    q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query)
+    plan = q.plan()
+    sums, counts = q.alloc_outputs(plan)
+    scratch = q.run_scratch(plan)
+    outs = q.finalize(sums, counts, plan=plan)
+    q.run(sums, counts, plan=plan, scratch=scratch)
+    q.finalize(sums, counts, plan=plan, outputs=outs)
+    torch.cuda.synchronize()
+    m = int(outs[3].item())
+    want = [t[:m].clone() for t in outs[:3]]
+    got_rows = sdb.QueryResult(want[0][:, :q.n_keys].long().cpu().numpy().reshape(m, q.n_keys),
+                               want[1].cpu().numpy(), want[2].cpu().numpy()).as_rows()
+    assert_same(got_rows, oracle_rows(w), f"{name} eager")
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        q.run(sums, counts, plan=plan, scratch=scratch)
+        q.finalize(sums, counts, plan=plan, outputs=outs)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        sums.fill_(-1)
+        counts.fill_(7)
+        outs[1].zero_()
+        outs[3].fill_(-5)
+        outs[4].fill_(0xCD)
+        if scratch is not None:
+            scratch.fill_(0xAB)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert int(outs[3].item()) == m, (name, rep)
+        for a, b in zip(outs[:3], want):
+            assert torch.equal(a[:m], b), (name, rep)
