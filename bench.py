@@ -386,6 +386,11 @@ def main(argv=None) -> int:
         },
         "cpu_baseline": None,
     }
+    if traffic:
+        # measured HBM bytes per launch (profiles/) over the kernel's time: the
+        # rate the memory actually delivered, gathers and probe lines included
+        result["hbm_traffic_GBps_fused"] = traffic / (kernel_ms_mean * 1e-3) / 1e9
+        result["hbm_traffic_frac_fused"] = result["hbm_traffic_GBps_fused"] / HBM_PEAK_GBPS
 
     # context: a plain streaming read of the same columns (the practical ceiling)
     used_cols = [fact[c] for c in query_columns(query)]
