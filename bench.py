@@ -454,6 +454,12 @@ def main(argv=None) -> int:
     host = (k[:m_out].cpu(), s_[:m_out].cpu(), c_[:m_out].cpu())
     result["e2e_ms"] = 1000.0 * (time.perf_counter() - t0)
     result["e2e_includes"] = f"build + plan + run + finalize + copy of {m_out} groups to the host"
+    # a digest of the whole result (keys, sums, counts as little-endian bytes), for
+    # comparing runs across machines the way the paper compares its outputs
+    digest = hashlib.md5()
+    for t in host:
+        digest.update(np.ascontiguousarray(t.numpy()).tobytes())
+    result["result_md5"] = digest.hexdigest()
     del host
 
     if cfg.n_fact <= 100_000_000:
