@@ -15,7 +15,9 @@
  *    workspace, the planner and finalize scratch, and all outputs. They must
  *    stay valid until the work queued on the stream has finished. The library
  *    allocates no device memory and keeps no global mutable state besides a
- *    per-thread error string and a per-device properties cache.
+ *    per-thread error string, the per-thread measurement events of
+ *    sdb_set_fused_events and a per-device properties cache; calls on
+ *    different streams may run concurrently.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *  - Every call returns an sdb_status; nothing throws across the ABI.
  *    sdb_last_error() returns a message for the last failing call on the
@@ -220,7 +222,8 @@ typedef struct sdb_query {
  *          group, and the codes of the passing slots alone in slot order, all
  *          copied into LDS (sdb_run_star_query derives the last two in its
  *          run scratch): a passing key's code is the code at its rank, so the
- *          group key needs no device-memory gather. Needs blocks of 1024. */
+ *          group key needs no device-memory gather. Its LDS footprint leaves room
+ *          for one block per CU, so the planner pairs it with blocks of 1024. */
 enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3 };
 
 /* The one-pass plan. Stages run in the listed order; each is a fact
@@ -314,17 +317,23 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
 
 /* ---- planning ----------------------------------------------------------- */
 
-/* Orders the stages of `q` (host) into `plan` (host). Unless q->force_order
- * is set, a sampling kernel evaluates every stage on its own over every
- * ceil(n_fact / 65536)-th fact row and the stages are sorted by ascending
- * pass fraction (ties: predicates before probes, smaller tables first, then
- * query order); this needs `scratch` (device, >= SDB_PLAN_SCRATCH_BYTES) and
- * synchronizes `stream` once. With force_order set, scratch and stream are
- * unused and no GPU call is made. Also fixes group radices and strides from
- * the built tables' payload ranges, the terminal (scalar without GROUP BY;
- * LDS when the group table fits a block's LDS; else global), items per lane
- * and the block size. Errors: INVALID_ARG, UNSUPPORTED, CAPACITY,
- * WORKSPACE_TOO_SMALL, HIP_ERROR. */
+/* Plans `q` (host) into `plan` (host). Unless q->force_order is set, a
+ * sampling kernel evaluates every stage on its own over every
+ * ceil(n_fact / 65536)-th fact row; this needs `scratch` (device,
+ * >= SDB_PLAN_SCRATCH_BYTES) and synchronizes `stream` once. With
+ * force_order set, scratch and stream are unused, no GPU call is made and
+ * the stages keep query order (predicates, then joins). The plan fixes:
+ * which small dense tables are staged in LDS (whole maps, pass bitmaps or
+ * rank tables) and which probes run as key ranges; the stage order with the
+ * least modelled cost (fact columns streamed at 128-byte line granularity
+ * plus each stage's lookups for the rows that reach it; every order is tried
+ * up to 7 stages, a greedy rank beyond); group radices and strides from the
+ * built tables' payload ranges; the terminal (scalar without GROUP BY, LDS
+ * when the group table fits a block's LDS, partitioned for many survivors
+ * into a large table, else global, with per-XCD copies when enough rows
+ * survive); items per lane, block size, eager columns, and for the
+ * partitioned terminal the grid and region sizes. Errors: INVALID_ARG,
+ * UNSUPPORTED, CAPACITY, WORKSPACE_TOO_SMALL, HIP_ERROR. */
 SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_t scratch_bytes,
                                        void* stream, sdb_plan* plan);
 
@@ -332,8 +341,12 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
 
 /* Runs `q` with `plan` (from sdb_plan_star_query for this query and these
  * tables) as one fused probe-filter-aggregate kernel (Sections 3.2 and 4.2),
- * all queued on `stream` (asynchronous). The outputs are zeroed first (or,
- * with per-XCD copies, the copies are zeroed and then added into them).
+ * all queued on `stream` (asynchronous): rank tables are derived first when
+ * the plan stages any, and the partitioned terminal's sort and sum passes or
+ * the per-XCD copies' merge follow the fused kernel. Only kernels are
+ * enqueued (no memset, copy or synchronization), so the call can be captured
+ * in a HIP graph. The outputs are zeroed first (or, with per-XCD copies, the
+ * copies are zeroed and then added into them).
  * sums/counts: device int64[plan->n_groups], indexed by group id;
  * n_groups_capacity >= plan->n_groups. Without GROUP BY, sums[0] and
  * counts[0] hold the total and the live row count. scratch: device,
