@@ -82,6 +82,16 @@ def test_baselines_small_and_tiny_schemas(n, mode):
         assert_same(q.execute(baseline=mode).as_rows(), oracle_rows(w), f"{mode} seed {seed} n {n}")
 
 
+@pytest.mark.parametrize("force", [
+    {"ipt": 2, "block": 512}, {"ipt": 2, "block": 1024}, {"ipt": 4}, {"vector": -1}, {"terminal": "global"},
+    {"terminal": "global", "xcd": -1}, {"eager": 2, "ipt": 1, "block": 512}, {"grid": 3}, {"order": True},
+])
+def test_c5_forced_plans_agree(force):
+    w = workload("c5_hash_stress")
+    got, _ = run_gpu(w, force=force)
+    assert_same(got.as_rows(), oracle_rows(w), f"c5 {force}")
+
+
 def test_c1_forced_plans_agree():
     w = workload("c1_scalar_scan")
     want = oracle_rows(w)
