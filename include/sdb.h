@@ -36,7 +36,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 4
+#define SDB_ABI_VERSION 5
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -188,7 +188,11 @@ typedef struct sdb_agg {
  *                  when the items start (needs 4-row items and ipt 1 or 2)
  *  force_range     which probes run as a key range (sdb_plan.stage_range):
  *                  0: those that would otherwise look up a table in device
- *                  memory; 1: every one that can; -1: none */
+ *                  memory; 1: every one that can; -1: none
+ *  force_coarse    coarse LDS pre-filters for dense tables left in device
+ *                  memory (SDB_LDS_COARSE): 0: chosen by the planner; -1:
+ *                  none; k in 1..SDB_MAX_COARSE_SHIFT: every such table whose
+ *                  coarse bitmap of 2^k slots per bit fits in LDS */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -210,6 +214,7 @@ typedef struct sdb_query {
     int32_t force_eager;
     int32_t force_block;
     int32_t force_range;
+    int32_t force_coarse;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -223,8 +228,16 @@ typedef struct sdb_query {
  *          copied into LDS (sdb_run_star_query derives the last two in its
  *          run scratch): a passing key's code is the code at its rank, so the
  *          group key needs no device-memory gather. Its LDS footprint leaves room
- *          for one block per CU, so the planner pairs it with blocks of 1024. */
-enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3 };
+ *          for one block per CU, so the planner pairs it with blocks of 1024;
+ *  COARSE  the map stays in device memory, but a coarse pass bitmap sits in
+ *          LDS: bit j is set iff any of the 2^stage_coarse[s] slots
+ *          j * 2^stage_coarse[s] ... holds a passing key (sdb_run_star_query
+ *          derives it from the pass bitmap in its run scratch). A row whose
+ *          bit is clear dies without touching device memory; the others
+ *          gather their code from the map as with GLOBAL. */
+enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, SDB_LDS_COARSE = 4 };
+/* log2 of the slots one coarse bit covers: 1 ... SDB_MAX_COARSE_SHIFT */
+#define SDB_MAX_COARSE_SHIFT 5
 
 /* The one-pass plan. Stages run in the listed order; each is a fact
  * predicate (kind 0, index into preds[]) or a join probe (kind 1, index into
@@ -244,6 +257,7 @@ typedef struct sdb_plan {
                                              pass_key_max` (its dimension's passing keys are exactly
                                              that range and it feeds no group key; Section 3.2's
                                              date-range scan, generalized); 0 otherwise */
+    int32_t stage_coarse[SDB_MAX_STAGES]; /* SDB_LDS_COARSE: log2 of the slots per coarse bit; else 0 */
     int64_t sampled_rows;                 /* 0 when no sample was taken */
     double est_cost;                      /* cost model value of the chosen order */
     int32_t terminal;

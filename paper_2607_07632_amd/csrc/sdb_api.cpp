@@ -256,6 +256,8 @@ sdb_status check_query(const sdb_query* q) {
                     kBigBlock);
     if (q->force_range < -1 || q->force_range > 1)
         return fail(SDB_INVALID_ARG, "force_range %d is not -1, 0 or 1", q->force_range);
+    if (q->force_coarse < -1 || q->force_coarse > SDB_MAX_COARSE_SHIFT)
+        return fail(SDB_INVALID_ARG, "force_coarse %d is not in [-1, %d]", q->force_coarse, SDB_MAX_COARSE_SHIFT);
     if (q->force_block == kBigBlock && (q->force_vector == -1 || q->force_ipt == 4 || q->force_eager > 0))
         return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items, ipt 1 or 2 and no eager loads", kBigBlock);
     if (q->force_eager < -1 || q->force_eager > kMaxEager)
@@ -361,6 +363,7 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
         if (pos >= 0) {
             S.lds_mode = plan->stage_lds[pos];
             S.defer = plan->stage_defer[pos];
+            S.coarse_shift = plan->stage_coarse[pos];
         }
     }
     S.gk_mode = S.n_gk == 0 ? GK_NONE
@@ -370,6 +373,7 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
     else if (S.nslots == 0) S.op = OP_NEVER;
     else if (S.lds_mode == LDS_BITS) S.op = OP_LDS_BITS;
     else if (S.lds_mode == LDS_RANK) S.op = OP_LDS_RANK1 + wsel;
+    else if (S.lds_mode == LDS_COARSE) S.op = OP_COARSE1 + wsel;
     else if (S.lds_mode == LDS_MAP) S.op = OP_LDS_MAP1 + wsel;
     else S.op = OP_MAP1 + wsel;
     return S;
@@ -394,6 +398,12 @@ bool rank_fits(const sdb_dim* d) {
     return d->kind == SDB_TABLE_DENSE && d->bits && d->n_slots > 0 && (d->n_slots + 63) / 64 <= kRankGroups &&
            lds_bits_bytes(d) + lds_rank_bytes(d) + lds_codes_bytes(d) <= kLdsRankBudget;
 }
+// Coarse pass bitmap of LDS_COARSE: one bit per 2^shift slots, whole 16-byte groups.
+uint64_t coarse_bits_bytes(const sdb_dim* d, int shift) {
+    const uint64_t bits = (d->n_slots + (1ull << shift) - 1) >> shift;
+    return std::max<uint64_t>(16, align_up((bits + 31) / 32 * 4, 16));
+}
+bool coarse_fits_table(const sdb_dim* d) { return d->kind == SDB_TABLE_DENSE && d->bits && d->n_slots > 0; }
 // Device-memory copies of a stage's rank tables in the run scratch (256-byte aligned parts).
 uint64_t rank_scratch_part(uint64_t bytes) { return align_up(bytes, 256); }
 
@@ -516,7 +526,9 @@ uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
     for (int s = 0; s < plan->n_stages; ++s) {
         if (plan->stage_lds[s] == LDS_GLOBAL) continue;
         const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
-        const uint64_t bytes = plan->stage_lds[s] == LDS_MAP ? lds_map_bytes(d) : lds_bits_bytes(d);
+        const uint64_t bytes = plan->stage_lds[s] == LDS_MAP      ? lds_map_bytes(d)
+                               : plan->stage_lds[s] == LDS_COARSE ? coarse_bits_bytes(d, plan->stage_coarse[s])
+                                                                  : lds_bits_bytes(d);
         if (p) {
             p->st[s].lds_off = (uint32_t)off;
             p->st[s].lds_bytes = (uint32_t)bytes;
@@ -653,13 +665,16 @@ PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
     return L;
 }
 
-// Run scratch of the LDS_RANK stages' tables; the terminal's scratch follows it.
+// Run scratch of the LDS_RANK stages' tables and the LDS_COARSE stages'
+// coarse bitmaps, in stage order; the terminal's scratch follows it.
 uint64_t rank_scratch_bytes(const sdb_query* q, const sdb_plan* plan) {
     uint64_t b = 0;
     for (int s = 0; s < plan->n_stages; ++s) {
-        if (plan->stage_lds[s] != LDS_RANK) continue;
-        const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
-        b += rank_scratch_part(lds_rank_bytes(d)) + rank_scratch_part(lds_codes_bytes(d));
+        const sdb_dim* d = plan->stage_kind[s] == 1 ? q->joins[plan->stage_index[s]].dim : nullptr;
+        if (plan->stage_lds[s] == LDS_RANK)
+            b += rank_scratch_part(lds_rank_bytes(d)) + rank_scratch_part(lds_codes_bytes(d));
+        else if (plan->stage_lds[s] == LDS_COARSE)
+            b += rank_scratch_part(coarse_bits_bytes(d, plan->stage_coarse[s]));
     }
     return b;
 }
@@ -732,9 +747,9 @@ sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, in
             if (lm != LDS_GLOBAL) {
                 if (k != 1 || q->joins[i].dim->kind != SDB_TABLE_DENSE)
                     return fail(SDB_INVALID_ARG, "plan stage %d: LDS placement needs a dense table", s);
-                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK)
+                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK && lm != LDS_COARSE)
                     return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
-                if ((lm == LDS_BITS || lm == LDS_RANK) && !q->joins[i].dim->bits)
+                if ((lm == LDS_BITS || lm == LDS_RANK || lm == LDS_COARSE) && !q->joins[i].dim->bits)
                     return fail(SDB_INVALID_ARG, "plan stage %d: table has no bitmap", s);
                 if (lm == LDS_RANK && !rank_fits(q->joins[i].dim))
                     return fail(SDB_INVALID_ARG, "plan stage %d: rank tables do not fit LDS", s);
@@ -749,6 +764,11 @@ sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, in
                     !range_eligible(q, i))
                     return fail(SDB_INVALID_ARG, "plan stage %d: the probe is not a key range", s);
             }
+            if ((lm == LDS_COARSE) != (plan->stage_coarse[s] != 0))
+                return fail(SDB_INVALID_ARG, "plan stage %d: coarse shift without the coarse placement", s);
+            if (lm == LDS_COARSE && (plan->stage_coarse[s] < 1 || plan->stage_coarse[s] > SDB_MAX_COARSE_SHIFT ||
+                                     plan->stage_defer[s] != -1 || plan->stage_range[s] != 0))
+                return fail(SDB_INVALID_ARG, "plan stage %d: bad coarse placement", s);
         }
     }
     if (n_defer > 1) return fail(SDB_INVALID_ARG, "plan defers more than one gather");
@@ -1133,6 +1153,19 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             }
         }
     }
+    // coarse LDS pre-filters for dense tables left in device memory
+    if (q->force_coarse > 0) {
+        for (int s = 0; s < n; ++s) {
+            if (plan->stage_kind[s] != 1 || plan->stage_lds[s] != LDS_GLOBAL || plan->stage_range[s]) continue;
+            if (!coarse_fits_table(q->joins[plan->stage_index[s]].dim)) continue;
+            plan->stage_lds[s] = LDS_COARSE;
+            plan->stage_coarse[s] = q->force_coarse;
+            if (lds_layout(q, plan, nullptr) + ring_lds_bytes(q, plan) > kLdsUsable) {
+                plan->stage_lds[s] = LDS_GLOBAL;
+                plan->stage_coarse[s] = 0;
+            }
+        }
+    }
     plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
     const uint64_t rank_bytes = rank_scratch_bytes(q, plan);
 
@@ -1217,9 +1250,23 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     hipStream_t s = (hipStream_t)stream;
     uint8_t* term_base = (uint8_t*)scratch + rank_bytes;
     {
-        // the rank tables of LDS_RANK stages, derived from their bitmaps and maps
+        // the rank tables of LDS_RANK stages and the coarse bitmaps of
+        // LDS_COARSE stages, derived from their pass bitmaps and maps
         uint64_t off = 0;
         for (int st_i = 0; st_i < plan->n_stages; ++st_i) {
+            if (plan->stage_lds[st_i] == LDS_COARSE) {
+                const sdb_dim* d = q->joins[plan->stage_index[st_i]].dim;
+                CoarseParams cp;
+                cp.bits = (const uint32_t*)d->bits;
+                cp.nslots = (uint32_t)d->n_slots;
+                cp.shift = (uint32_t)plan->stage_coarse[st_i];
+                cp.out = (uint32_t*)((uint8_t*)scratch + off);
+                cp.n_words = (uint32_t)(coarse_bits_bytes(d, plan->stage_coarse[st_i]) / 4);
+                off += rank_scratch_part(coarse_bits_bytes(d, plan->stage_coarse[st_i]));
+                p.st[st_i].bits = cp.out;
+                if (q->n_fact > 0) SDB_HIP(launch_coarse_build(cp, s), "coarse bitmap launch");
+                continue;
+            }
             if (plan->stage_lds[st_i] != LDS_RANK) continue;
             const sdb_dim* d = q->joins[plan->stage_index[st_i]].dim;
             RankParams rp;

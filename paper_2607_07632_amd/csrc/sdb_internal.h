@@ -40,7 +40,10 @@ enum StageOp : int32_t {
     OP_HASH = 9,      // open-addressing table in device memory
     OP_LDS_RANK1 = 10,  // pass bitmap, ranks and passing codes in LDS, 1/2/4-byte codes
     OP_LDS_RANK2 = 11,
-    OP_LDS_RANK4 = 12
+    OP_LDS_RANK4 = 12,
+    OP_COARSE1 = 13,    // coarse pass bitmap in LDS, then the device map, 1/2/4-byte codes
+    OP_COARSE2 = 14,
+    OP_COARSE4 = 15
 };
 // How a table's code becomes part of the group id.
 enum GroupMode : int32_t { GK_NONE = 0, GK_ONE = 1, GK_GENERAL = 2 };
@@ -48,7 +51,8 @@ enum LdsMode : int32_t {
     LDS_GLOBAL = SDB_LDS_GLOBAL,
     LDS_MAP = SDB_LDS_MAP,
     LDS_BITS = SDB_LDS_BITS,
-    LDS_RANK = SDB_LDS_RANK
+    LDS_RANK = SDB_LDS_RANK,
+    LDS_COARSE = SDB_LDS_COARSE
 };
 enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3, TERM_PART = 4 };
 
@@ -101,7 +105,22 @@ struct StageDev {
     uint32_t lds_rank_bytes;
     uint32_t lds_codes_off;
     uint32_t lds_codes_bytes;
+    // LDS_COARSE: bit j of the staged bitmap (at lds_off, staged from `bits`,
+    // which then points at the coarse bitmap in the run scratch) covers
+    // slots [j << coarse_shift, (j + 1) << coarse_shift)
+    int32_t coarse_shift;
+    int32_t pad_;
 };
+
+// Derives a coarse pass bitmap (LDS_COARSE) from a dense table's pass bitmap.
+struct CoarseParams {
+    const uint32_t* bits;      // pass bitmap, nslots bits
+    uint32_t nslots;
+    uint32_t shift;            // 1 .. SDB_MAX_COARSE_SHIFT
+    uint32_t* out;             // n_words words
+    uint32_t n_words;          // ceil(ceil(nslots / 2^shift) / 32), padded to whole 16-byte groups
+};
+hipError_t launch_coarse_build(const CoarseParams& cp, hipStream_t s);
 
 // Derives a dense table's rank tables (LDS_RANK) in device memory.
 struct RankParams {

@@ -509,6 +509,36 @@ hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
+// coarse pass bitmap of a dense table (LDS_COARSE placement)
+// ---------------------------------------------------------------------------
+
+// Thread w writes coarse word w: bit b is set iff one of the 2^shift slots
+// starting at slot (32 w + b) << shift passes. 2^shift divides 32, so every
+// group of slots lies inside one word of the pass bitmap.
+__global__ void __launch_bounds__(256) coarse_bits_kernel(CoarseParams cp) {
+    const uint32_t w = blockIdx.x * blockDim.x + threadIdx.x;
+    if (w >= cp.n_words) return;
+    const uint32_t per = 1u << cp.shift;
+    const uint32_t mask = per >= 32u ? 0xFFFFFFFFu : ((1u << per) - 1u);
+    const uint32_t n_fine = (cp.nslots + 31u) / 32u;
+    uint32_t out = 0u;
+    for (uint32_t b = 0; b < 32u; ++b) {
+        const uint64_t first = ((uint64_t)w * 32u + b) << cp.shift;
+        if (first >= cp.nslots) break;
+        const uint32_t fw = (uint32_t)(first >> 5);
+        const uint32_t word = fw < n_fine ? cp.bits[fw] : 0u;
+        if ((word >> (uint32_t)(first & 31u)) & mask) out |= 1u << b;
+    }
+    cp.out[w] = out;
+}
+
+hipError_t launch_coarse_build(const CoarseParams& cp, hipStream_t s) {
+    if (cp.n_words == 0) return hipSuccess;
+    hipLaunchKernelGGL(coarse_bits_kernel, dim3((cp.n_words + 255u) / 256u), dim3(256), 0, s, cp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // rank tables of a dense table (LDS_RANK placement)
 // ---------------------------------------------------------------------------
 
@@ -847,6 +877,25 @@ __device__ __forceinline__ void stage_rank(const StageDev& S, const unsigned cha
     add_group<W, IPT>(S, c, gid);
 }
 
+// Device map behind a coarse pass bitmap in LDS: a row whose coarse bit is
+// clear dies without a device-memory gather.
+template <int W, int IPT, int WB>
+__device__ __forceinline__ void stage_coarse(const StageDev& S, const unsigned char* lds, const int32_t (&x)[IPT][W],
+                                             bool (&al)[IPT][W], uint32_t (&gid)[IPT][W]) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(lds + S.lds_off);
+    uint32_t c[IPT][W];
+    SDB_ROWS(j, r) {
+        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+        bool ok = al[j][r] && idx < S.nslots;
+        const uint32_t cb = (ok ? idx : 0u) >> S.coarse_shift;
+        ok = ok && ((words[cb >> 5] >> (cb & 31u)) & 1u);
+        c[j][r] = ld_code<WB>(S.map, ok ? idx : 0u);
+        al[j][r] = ok;
+    }
+    SDB_ROWS(j, r) al[j][r] = al[j][r] && c[j][r] < S.sentinel;
+    add_group<W, IPT>(S, c, gid);
+}
+
 template <int W, int IPT>
 __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)[IPT][W], bool (&al)[IPT][W],
                                            uint32_t (&gid)[IPT][W]) {
@@ -945,6 +994,9 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
             case OP_LDS_RANK1: stage_rank<W, IPT, 1>(S, lds, x, al, gid); break;
             case OP_LDS_RANK2: stage_rank<W, IPT, 2>(S, lds, x, al, gid); break;
             case OP_LDS_RANK4: stage_rank<W, IPT, 4>(S, lds, x, al, gid); break;
+            case OP_COARSE1: stage_coarse<W, IPT, 1>(S, lds, x, al, gid); break;
+            case OP_COARSE2: stage_coarse<W, IPT, 2>(S, lds, x, al, gid); break;
+            case OP_COARSE4: stage_coarse<W, IPT, 4>(S, lds, x, al, gid); break;
             default:   // OP_NEVER
                 SDB_ROWS(j, r) al[j][r] = false;
                 break;

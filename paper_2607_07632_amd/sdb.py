@@ -36,7 +36,7 @@ AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
 TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3, "part": 4}
 BASELINES = {"per_operator": 0, "global_handoff": 1}
 TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global", 4: "part"}
-LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank"}
+LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank", 4: "lds_coarse"}
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
           4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
 
@@ -82,14 +82,14 @@ class SdbQuery(C.Structure):
                 ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
-                ("force_block", i32), ("force_range", i32)]
+                ("force_block", i32), ("force_range", i32), ("force_coarse", i32)]
 
 
 class SdbPlan(C.Structure):
     _fields_ = [("n_stages", i32), ("stage_kind", i32 * MAX_STAGES),
                 ("stage_index", i32 * MAX_STAGES), ("stage_pass", C.c_double * MAX_STAGES),
                 ("stage_lds", i32 * MAX_STAGES), ("stage_defer", i32 * MAX_STAGES),
-                ("stage_range", i32 * MAX_STAGES),
+                ("stage_range", i32 * MAX_STAGES), ("stage_coarse", i32 * MAX_STAGES),
                 ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
                 ("vector", i32), ("eager", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
                 ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
@@ -300,8 +300,8 @@ class StarQuery:
     list of DimTable per join (``build_dims``); ``query`` the plain-data
     description. ``force`` may hold terminal ('scalar'|'lds'|'global'|'part'),
     ipt, vector (1 / -1), order (True = keep query order), grid, lds, xcd,
-    eager, block and range (-1: no key-range probes), the sdb_query force_*
-    fields of the same names.
+    eager, block, range (-1: no key-range probes) and coarse, the sdb_query
+    force_* fields of the same names.
     """
 
     def __init__(self, fact: dict, tables: list, query: dict, force: dict | None = None):
@@ -362,6 +362,7 @@ class StarQuery:
         q.force_eager = int(force.get("eager", 0))
         q.force_block = int(force.get("block", 0))
         q.force_range = int(force.get("range", 0))
+        q.force_coarse = int(force.get("coarse", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -481,6 +482,8 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
             st["table"] = "key_range"
         elif kind == 1:
             st["table"] = LDS_NAMES.get(plan.stage_lds[s], plan.stage_lds[s])
+            if plan.stage_coarse[s]:
+                st["coarse_slots_per_bit"] = 1 << plan.stage_coarse[s]
             if plan.stage_defer[s] >= 0:
                 st["deferred_gather"] = True
         stages.append(st)

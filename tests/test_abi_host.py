@@ -38,7 +38,7 @@ def test_struct_layout_matches_binding():
     sizes = (C.c_int64 * 8)()
     assert L.sdb_struct_sizes(sizes, 8) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
-    assert L.sdb_abi_version() == 4
+    assert L.sdb_abi_version() == 5
 
 
 def test_status_strings():
@@ -296,6 +296,40 @@ def test_read_columns_validation():
     bad = (C.c_void_p * 2)(0x10000, 0x20004)
     assert L.sdb_read_columns(bad, 2, 10, 0, 0x3000, None) == 1
     assert "aligned" in L.sdb_last_error().decode()
+
+
+def test_coarse_placement_and_validation():
+    big = _fake_dim(n_rows=4_000_000, n_pass=800_000, n_slots=4_000_000)
+    big.bits = 0x80000
+    q = _query([big], [(0, 0)])
+    q.force_coarse = 2
+    p = _plan(q)
+    assert p.stage_lds[0] == 4 and p.stage_coarse[0] == 2        # 4M slots / 4 per bit = 125,000 bytes
+    st = sdb.plan_summary(p)["stages"][0]
+    assert st["table"] == "lds_coarse" and st["coarse_slots_per_bit"] == 4
+    assert p.lds_bytes >= 125_000 and p.run_scratch_bytes >= 125_000
+    q.force_coarse = 1                                          # 250,000 bytes do not fit LDS
+    p1 = _plan(q)
+    assert p1.stage_lds[0] == 0 and p1.stage_coarse[0] == 0
+    q.force_coarse = -1
+    assert _plan(q).stage_lds[0] == 0
+    for bad in (6, -2):
+        q.force_coarse = bad
+        with pytest.raises(sdb.SdbError) as e:
+            _plan(q)
+        assert e.value.name == "SDB_INVALID_ARG"
+    nobits = _fake_dim(n_rows=4_000_000, n_pass=800_000, n_slots=4_000_000)
+    qn = _query([nobits], [(0, 0)])
+    qn.force_coarse = 2
+    assert _plan(qn).stage_lds[0] == 0                          # no pass bitmap, no coarse filter
+    # plans whose coarse fields disagree are refused before any launch
+    q.force_coarse = 2
+    L = sdb.lib()
+    for lds, shift in ((0, 2), (4, 0), (4, 6)):
+        bad = sdb.SdbPlan.from_buffer_copy(p)
+        bad.stage_lds[0] = lds
+        bad.stage_coarse[0] = shift
+        assert L.sdb_run_star_query(C.byref(q), C.byref(bad), 0x1000, 0x2000, 100, None, 0, None) == 1
 
 
 def test_baseline_scratch_and_validation():

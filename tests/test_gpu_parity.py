@@ -53,6 +53,8 @@ def test_config_parity(name):
     {"block": 64, "ipt": 2, "terminal": "global"}, {"lds": 2}, {"lds": 2, "terminal": "part"},
     {"lds": 3}, {"lds": 3, "terminal": "global"}, {"lds": 3, "ipt": 1, "terminal": "part"},
     {"ipt": 1, "block": 1024, "terminal": "global"},
+    {"coarse": 1}, {"coarse": 2}, {"coarse": 3, "terminal": "global"}, {"coarse": 5, "ipt": 1, "block": 1024},
+    {"coarse": 2, "lds": -1}, {"coarse": 4, "block": 1024, "terminal": "part"},
 ])
 def test_forced_plans_agree(name, force):
     w = workload(name)
@@ -142,7 +144,8 @@ def test_random_tiny_schemas_forced(seed):
                   {"eager": 4}, {"eager": 3, "ipt": 1, "terminal": "part"}, {"eager": -1},
                   {"block": 1024, "ipt": 1}, {"block": 1024, "terminal": "part", "grid": 2}, {"lds": 2},
                   {"lds": 3}, {"lds": 3, "terminal": "part", "grid": 3},
-                  {"lds": -1, "terminal": "part"}]:
+                  {"lds": -1, "terminal": "part"}, {"lds": -1, "coarse": 1}, {"lds": -1, "coarse": 3, "ipt": 1},
+                  {"lds": -1, "coarse": 5, "vector": -1}, {"coarse": 2, "terminal": "part"}]:
         got, _ = run_gpu(w, force=force)
         assert_same(got.as_rows(), want, f"tiny {seed} {force}")
 
@@ -538,3 +541,21 @@ def test_concurrent_queries_on_two_streams():
         rows = sdb.QueryResult(k[:m, :q.n_keys].long().cpu().numpy().reshape(m, q.n_keys),
                                s[:m].cpu().numpy(), c[:m].cpu().numpy()).as_rows()
         assert_same(rows, oracle_rows(w), f"{name} concurrent")
+
+
+@pytest.mark.parametrize("shift", [1, 2, 3, 4, 5])
+def test_coarse_prefilter_tables(shift):
+    """Every dense table in device memory behind a coarse LDS bitmap of 2^shift
+    slots per bit, on random tiny schemas with gapped, offset keys and on c3."""
+    from paper_2607_07632_amd import sdb
+    for seed in (3, 8, 13, 21):
+        w = random_tiny_workload(seed + 2000, max_fact=6000, max_dim_rows=700, n_fact=5003)
+        for jd in w.query["joins"]:
+            jd["kind"] = "auto"                  # dense wherever the key range allows it
+        got, q = run_gpu(w, force={"lds": -1, "coarse": shift})
+        assert_same(got.as_rows(), oracle_rows(w), f"tiny {seed} coarse {shift}")
+    w = workload("c3_star3")
+    got, q = run_gpu(w, force={"coarse": shift, "block": 1024})
+    stages = sdb.plan_summary(q.plan_obj, w.query)["stages"]
+    assert any(st.get("table") == "lds_coarse" for st in stages) or shift == 1
+    assert_same(got.as_rows(), oracle_rows(w), f"c3 coarse {shift}")
