@@ -404,8 +404,8 @@ uint64_t coarse_bits_bytes(const sdb_dim* d, int shift) {
     return std::max<uint64_t>(16, align_up((bits + 31) / 32 * 4, 16));
 }
 bool coarse_fits_table(const sdb_dim* d) { return d->kind == SDB_TABLE_DENSE && d->bits && d->n_slots > 0; }
-// Device-memory copies of a stage's rank tables in the run scratch (256-byte aligned parts).
-uint64_t rank_scratch_part(uint64_t bytes) { return align_up(bytes, 256); }
+// A stage's part of the run scratch (rank tables, coarse bitmaps): 256-byte aligned.
+uint64_t scratch_part(uint64_t bytes) { return align_up(bytes, 256); }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -667,14 +667,14 @@ PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
 
 // Run scratch of the LDS_RANK stages' tables and the LDS_COARSE stages'
 // coarse bitmaps, in stage order; the terminal's scratch follows it.
-uint64_t rank_scratch_bytes(const sdb_query* q, const sdb_plan* plan) {
+uint64_t stage_scratch_bytes(const sdb_query* q, const sdb_plan* plan) {
     uint64_t b = 0;
     for (int s = 0; s < plan->n_stages; ++s) {
         const sdb_dim* d = plan->stage_kind[s] == 1 ? q->joins[plan->stage_index[s]].dim : nullptr;
         if (plan->stage_lds[s] == LDS_RANK)
-            b += rank_scratch_part(lds_rank_bytes(d)) + rank_scratch_part(lds_codes_bytes(d));
+            b += scratch_part(lds_rank_bytes(d)) + scratch_part(lds_codes_bytes(d));
         else if (plan->stage_lds[s] == LDS_COARSE)
-            b += rank_scratch_part(coarse_bits_bytes(d, plan->stage_coarse[s]));
+            b += scratch_part(coarse_bits_bytes(d, plan->stage_coarse[s]));
     }
     return b;
 }
@@ -1167,7 +1167,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         }
     }
     plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
-    const uint64_t rank_bytes = rank_scratch_bytes(q, plan);
+    const uint64_t stage_bytes = stage_scratch_bytes(q, plan);
 
     // per-XCD private group tables for the global terminal when enough rows survive
     const uint64_t copy_bytes = (uint64_t)kXcdCopies * plan->n_groups * 16;
@@ -1175,7 +1175,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     if (q->force_xcd == 1) xcd = term == TERM_GLOBAL;
     if (q->force_xcd == -1) xcd = false;
     plan->xcd_copies = xcd ? kXcdCopies : 0;
-    plan->run_scratch_bytes = (int64_t)rank_bytes + (xcd ? (int64_t)copy_bytes : 0);
+    plan->run_scratch_bytes = (int64_t)stage_bytes + (xcd ? (int64_t)copy_bytes : 0);
 
     if (term == TERM_PART) {
         // records are written per block: the grid is fixed now
@@ -1190,7 +1190,7 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         plan->part_cap = (int64_t)align_up((uint64_t)std::max<int64_t>(plan->part_cap, 64), 64);
         if ((uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFF0ull)
             plan->part_cap = (int64_t)(0xFFFFFFF0ull / (uint64_t)plan->grid) / 64 * 64;
-        plan->run_scratch_bytes = (int64_t)rank_bytes + (int64_t)part_layout(q, plan).total;
+        plan->run_scratch_bytes = (int64_t)stage_bytes + (int64_t)part_layout(q, plan).total;
     }
     return ok();
 }
@@ -1228,10 +1228,10 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     if (plan->xcd_copies != 0 && (plan->xcd_copies != kXcdCopies || plan->terminal != TERM_GLOBAL))
         return fail(SDB_INVALID_ARG, "bad plan xcd_copies %d", plan->xcd_copies);
     // run scratch: the rank tables, then the terminal's part
-    const uint64_t rank_bytes = rank_scratch_bytes(q, plan);
+    const uint64_t stage_bytes = stage_scratch_bytes(q, plan);
     uint64_t term_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
     if (plan->terminal == TERM_PART) term_scratch = part_layout(q, plan).total;
-    const uint64_t need_scratch = rank_bytes + term_scratch;
+    const uint64_t need_scratch = stage_bytes + term_scratch;
     if (need_scratch) {
         if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
         if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
@@ -1248,7 +1248,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     p.ring_off = (uint32_t)plan->lds_bytes;
 
     hipStream_t s = (hipStream_t)stream;
-    uint8_t* term_base = (uint8_t*)scratch + rank_bytes;
+    uint8_t* term_base = (uint8_t*)scratch + stage_bytes;
     {
         // the rank tables of LDS_RANK stages and the coarse bitmaps of
         // LDS_COARSE stages, derived from their pass bitmaps and maps
@@ -1262,7 +1262,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
                 cp.shift = (uint32_t)plan->stage_coarse[st_i];
                 cp.out = (uint32_t*)((uint8_t*)scratch + off);
                 cp.n_words = (uint32_t)(coarse_bits_bytes(d, plan->stage_coarse[st_i]) / 4);
-                off += rank_scratch_part(coarse_bits_bytes(d, plan->stage_coarse[st_i]));
+                off += scratch_part(coarse_bits_bytes(d, plan->stage_coarse[st_i]));
                 p.st[st_i].bits = cp.out;
                 if (q->n_fact > 0) SDB_HIP(launch_coarse_build(cp, s), "coarse bitmap launch");
                 continue;
@@ -1275,9 +1275,9 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
             rp.width = d->width;
             rp.nslots = (uint32_t)d->n_slots;
             rp.prefix = (uint32_t*)((uint8_t*)scratch + off);
-            off += rank_scratch_part(lds_rank_bytes(d));
+            off += scratch_part(lds_rank_bytes(d));
             rp.codes = (uint8_t*)scratch + off;
-            off += rank_scratch_part(lds_codes_bytes(d));
+            off += scratch_part(lds_codes_bytes(d));
             p.st[st_i].rank = rp.prefix;
             p.st[st_i].codes = rp.codes;
             if (q->n_fact > 0) SDB_HIP(launch_rank_build(rp, s), "rank table launch");
