@@ -1,0 +1,200 @@
+"""Properties of the planner over random queries and every combination of
+the planner overrides, on the CPU.
+
+Dimension handles are filled in by hand (no table is built), the stage order
+is the query's own (no sampling kernel) and the grid is given, so planning
+makes no GPU call. For every query the planner accepts, the plan must be
+internally consistent, and the run entry point's own validation must accept
+it: without a GPU the run then stops at its first launch with SDB_HIP_ERROR,
+never with SDB_INVALID_ARG.
+"""
+
+import ctypes as C
+
+import pytest
+from hypothesis import HealthCheck, given, settings, strategies as st
+
+from paper_2607_07632_amd import sdb
+
+OK, INVALID_ARG, UNSUPPORTED, CAPACITY, HIP_ERROR = 0, 1, 2, 3, 7
+LDS_GLOBAL, LDS_MAP, LDS_BITS, LDS_RANK, LDS_COARSE = 0, 1, 2, 3, 4
+
+
+@st.composite
+def dims(draw):
+    kind = draw(st.sampled_from([1, 2]))                    # dense, hash
+    n_rows = draw(st.one_of(st.integers(1, 3000), st.integers(1, 300_000), st.integers(1, 4_000_000)))
+    n_pass = draw(st.integers(0, n_rows))
+    n_pay = draw(st.integers(0, 2))
+    radices = tuple(draw(st.integers(1, 300)) for _ in range(n_pay))
+    h = sdb.SdbDim()
+    h.kind = kind
+    h.n_rows = n_rows
+    h.n_pass = n_pass
+    domain = 1
+    for r in radices:
+        domain *= r
+    h.n_payloads = n_pay
+    div = 1
+    for p in range(n_pay - 1, -1, -1):
+        h.payload_radix[p] = radices[p]
+        h.payload_min[p] = draw(st.integers(-1000, 1000))
+        h.payload_div[p] = div
+        div *= radices[p]
+    h.domain = domain
+    if kind == 1:
+        h.width = 1 if domain + 2 <= 0xFF else (2 if domain + 2 <= 0xFFFF else 4)
+        h.n_slots = draw(st.integers(n_rows, 2 * n_rows))
+        h.sentinel = (1 << (8 * h.width)) - 2
+        h.bits = 0x200000 if draw(st.booleans()) else None
+    else:
+        h.width = 8
+        bits = max(1, (2 * n_rows - 1).bit_length())
+        h.hash_bits = bits
+        h.n_slots = 1 << bits
+        h.sentinel = 0xFFFFFFFE
+    h.key_min = draw(st.integers(-5000, 5000))
+    h.key_max = h.key_min + (h.n_slots - 1 if kind == 1 else n_rows * 2)
+    if n_pass and draw(st.booleans()):                      # passing keys one contiguous range
+        lo = draw(st.integers(h.key_min, h.key_min + 1000))
+        h.pass_key_min, h.pass_key_max = lo, lo + n_pass - 1
+    else:
+        h.pass_key_min, h.pass_key_max = (h.key_min, h.key_min + n_pass) if n_pass else (0, -1)
+    h.map = 0x400000
+    return h
+
+
+@st.composite
+def queries(draw):
+    ds = draw(st.lists(dims(), min_size=0, max_size=4))
+    q = sdb.SdbQuery()
+    q.n_fact = draw(st.sampled_from([0, 1, 1000, 5_000_003, 600_000_000]))
+    q.n_cols = 4
+    aligned = draw(st.booleans())
+    for c in range(4):
+        q.cols[c] = 0x1000000 + c * 0x100000 + (0 if aligned else 4)
+    q.n_preds = draw(st.integers(0, 3))
+    for i in range(q.n_preds):
+        q.preds[i] = sdb.SdbPred(draw(st.integers(0, 3)), draw(st.integers(0, 6)),
+                                 draw(st.integers(-100, 100)), draw(st.integers(-100, 100)))
+    q.n_joins = len(ds)
+    for j, d in enumerate(ds):
+        q.joins[j] = sdb.SdbJoin(draw(st.integers(0, 3)), C.pointer(d))
+    keys = [(j, p) for j, d in enumerate(ds) for p in range(d.n_payloads)]
+    chosen = draw(st.lists(st.sampled_from(keys), unique=True, max_size=3)) if keys else []
+    q.n_group_keys = len(chosen)
+    for k, (j, p) in enumerate(chosen):
+        q.group_keys[k] = sdb.SdbGroupKey(j, p)
+    q.agg = sdb.SdbAgg(draw(st.integers(0, 3)), draw(st.integers(0, 3)), draw(st.integers(0, 3)))
+    q.force_terminal = draw(st.integers(0, 4))
+    q.force_ipt = draw(st.sampled_from([0, 1, 2, 4]))
+    q.force_vector = draw(st.sampled_from([0, 1, -1]))
+    q.force_order = 1
+    q.grid_blocks = draw(st.integers(1, 3000))
+    q.force_lds = draw(st.sampled_from([-1, 0, 2, 3]))
+    q.force_xcd = draw(st.sampled_from([-1, 0, 1]))
+    q.force_eager = draw(st.integers(-1, 4))
+    q.force_block = draw(st.sampled_from([0, 64, 128, 256, 512, 1024]))
+    q.force_range = draw(st.sampled_from([-1, 0, 1]))
+    q.force_coarse = draw(st.integers(-1, 5))
+    return q, ds
+
+
+def check_plan(q, p):
+    n = q.n_preds + q.n_joins
+    assert p.n_stages == n
+    seen = sorted((p.stage_kind[s], p.stage_index[s]) for s in range(n))
+    assert seen == sorted([(0, i) for i in range(q.n_preds)] + [(1, j) for j in range(q.n_joins)])
+    defers = 0
+    for s in range(n):
+        kind, idx, lds = p.stage_kind[s], p.stage_index[s], p.stage_lds[s]
+        assert lds in (LDS_GLOBAL, LDS_MAP, LDS_BITS, LDS_RANK, LDS_COARSE)
+        if lds != LDS_GLOBAL:
+            d = q.joins[idx].dim.contents
+            assert kind == 1 and d.kind == 1
+            if lds in (LDS_BITS, LDS_RANK, LDS_COARSE):
+                assert d.bits
+        assert (lds == LDS_COARSE) == (p.stage_coarse[s] != 0)
+        if lds == LDS_COARSE:
+            assert 1 <= p.stage_coarse[s] <= 5
+        if p.stage_range[s]:
+            assert kind == 1 and lds == LDS_GLOBAL and p.stage_defer[s] == -1
+            d = q.joins[idx].dim.contents
+            assert d.n_pass == 0 or d.pass_key_max - d.pass_key_min + 1 == d.n_pass
+            assert all(q.group_keys[k].join != idx for k in range(q.n_group_keys))
+        assert p.stage_defer[s] in (-1, 0)
+        if p.stage_defer[s] == 0:
+            defers += 1
+            assert lds == LDS_BITS
+    assert defers <= 1
+    assert p.terminal in (1, 2, 3, 4)
+    assert (p.terminal == 1) <= (q.n_group_keys == 0)
+    assert p.ipt in (1, 2, 4) and p.block in (64, 128, 256, 512, 1024)
+    if p.block == 1024:
+        assert p.vector == 1 and p.ipt <= 2 and p.eager == 0
+    assert 0 <= p.eager <= 4
+    assert 0 <= p.lds_bytes <= 160 * 1024
+    groups = 1
+    for k in range(q.n_group_keys):
+        groups *= p.radix[k]
+    assert p.n_groups == groups
+    assert p.run_scratch_bytes >= 0
+
+
+@settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(queries())
+def test_plans_are_consistent_and_pass_run_validation(qd):
+    q, _dims = qd                                           # the handles must outlive the calls
+    L = sdb.lib()
+    p = sdb.SdbPlan()
+    status = L.sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p))
+    assert status in (OK, INVALID_ARG, UNSUPPORTED, CAPACITY), sdb.lib().sdb_last_error()
+    if status != OK:
+        return
+    check_plan(q, p)
+    scratch = 0x10000000 if p.run_scratch_bytes else None
+    status = L.sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
+                                  scratch, int(p.run_scratch_bytes), None)
+    assert status in (OK, HIP_ERROR), (status, sdb.lib().sdb_last_error())
+
+
+@pytest.mark.parametrize("force_lds", [0, 2, 3])
+@pytest.mark.parametrize("force_block", [0, 1024])
+def test_rank_and_deferred_placements_pass_run_validation(force_lds, force_block):
+    """A c2-like query (a 200,000-slot filtered dimension whose code is a group
+    key, a small one beside it) reaches the deferred-bitmap and rank-table
+    placements the random queries above rarely draw."""
+    def dense(n, n_pass, radix, bits):
+        h = sdb.SdbDim()
+        h.kind, h.width, h.n_rows, h.n_pass, h.n_slots = 1, 1, n, n_pass, n
+        h.key_min, h.key_max, h.sentinel = 0, n - 1, 0xFE
+        h.n_payloads, h.payload_radix[0], h.payload_div[0], h.domain = 1, radix, 1, radix
+        h.pass_key_min, h.pass_key_max = 0, n_pass      # not a contiguous range
+        h.map, h.bits = 0x400000, bits
+        return h
+    sup, date = dense(200_000, 40_000, 25, 0x200000), dense(2556, 2556, 8, 0x300000)
+    q = sdb.SdbQuery()
+    q.n_fact, q.n_cols = 60_000_000, 3
+    for c in range(3):
+        q.cols[c] = 0x1000000 + c * 0x100000
+    q.n_joins = 2
+    q.joins[0], q.joins[1] = sdb.SdbJoin(0, C.pointer(sup)), sdb.SdbJoin(1, C.pointer(date))
+    q.n_group_keys = 2
+    q.group_keys[0], q.group_keys[1] = sdb.SdbGroupKey(0, 0), sdb.SdbGroupKey(1, 0)
+    q.agg = sdb.SdbAgg(0, 2, 0)
+    q.force_order, q.grid_blocks, q.force_lds, q.force_block = 1, 256, force_lds, force_block
+    q.force_terminal = 3                                      # global: the deferred gather stays possible
+    p = sdb.SdbPlan()
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p)) == OK
+    check_plan(q, p)
+    s_sup = next(s for s in range(p.n_stages) if p.stage_index[s] == 0)
+    # no lookup goes to device memory, so the planner itself takes rank tables
+    assert p.stage_lds[s_sup] == (LDS_BITS if force_lds == 2 else LDS_RANK)
+    if p.stage_lds[s_sup] == LDS_BITS:
+        assert p.stage_defer[s_sup] == 0
+    else:
+        assert p.block == 1024 and p.run_scratch_bytes > 0
+    scratch = 0x10000000 if p.run_scratch_bytes else None
+    status = sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
+                                          scratch, int(p.run_scratch_bytes), None)
+    assert status in (OK, HIP_ERROR), (status, sdb.lib().sdb_last_error())
