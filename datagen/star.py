@@ -440,7 +440,7 @@ def random_tiny_workload(seed: int, max_fact: int = 2000, max_dim_rows: int = 30
         kind = "auto"
         if allow_hash and rng.random() < 0.35:
             kind = "hash"
-        elif rng.random() < 0.2:
+        elif rng.random() < 0.2 and span <= 2 * m:      # a forced dense map needs a key range within 2m
             kind = "dense"
         jd = {"fact_key": f"fk{j}", "dim": dn, "preds": preds, "payloads": payloads, "kind": kind}
         if kind == "hash":

@@ -559,3 +559,36 @@ def test_coarse_prefilter_tables(shift):
     stages = sdb.plan_summary(q.plan_obj, w.query)["stages"]
     assert any(st.get("table") == "lds_coarse" for st in stages) or shift == 1
     assert_same(got.as_rows(), oracle_rows(w), f"c3 coarse {shift}")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_override_combinations(seed):
+    """Planner overrides drawn at random (seeded) in combination on random tiny
+    schemas: every plan the planner accepts must give the oracle's result;
+    combinations it refuses must be refused with a status, not run."""
+    from paper_2607_07632_amd import sdb
+    rng = np.random.default_rng([2607, 7632, 55, seed])
+    choices = {
+        "terminal": ["auto", "scalar", "lds", "global", "part"], "ipt": [0, 1, 2, 4], "vector": [0, 1, -1],
+        "order": [False, True], "grid": [0, 0, 1, 3, 17], "lds": [-1, 0, 2, 3], "xcd": [-1, 0, 1],
+        "eager": [-1, 0, 1, 2, 4], "block": [0, 64, 128, 256, 512, 1024], "range": [-1, 0, 1],
+        "coarse": [-1, 0, 1, 2, 5],
+    }
+    refused = ran = 0
+    for case in range(4):
+        w = random_tiny_workload(int(rng.integers(0, 10**6)), max_fact=5000, max_dim_rows=600,
+                                 n_fact=int(rng.integers(0, 5000)))
+        want = oracle_rows(w)
+        fact, dims = upload(w)
+        tables = sdb.build_dims(dims, w.dim_keys, w.query)
+        for _ in range(10):
+            force = {k: v[int(rng.integers(0, len(v)))] for k, v in choices.items()}
+            try:
+                got, _ = run_gpu(w, force=force, dev=(fact, dims), tables=tables)
+            except sdb.SdbError as e:
+                assert e.name in ("SDB_INVALID_ARG", "SDB_CAPACITY", "SDB_UNSUPPORTED"), (force, str(e))
+                refused += 1
+                continue
+            assert_same(got.as_rows(), want, f"seed {seed} case {case} {force}")
+            ran += 1
+    assert ran > 0
