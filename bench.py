@@ -230,6 +230,148 @@ def upload_fact(cfg_name: str, n: int, device) -> dict:
     return out
 
 
+def stream_read_reference(sdb, cols: list, n: int, stream, achieved: float) -> dict:
+    """A plain streaming read of the query's fact columns (sdb_read_columns),
+    best of 1-4 blocks of 512 per CU: the practical ceiling of the stream."""
+    import numpy as np
+    import torch
+    acc = torch.zeros(1, dtype=torch.int64, device=cols[0].device)
+    best = None
+    for per_cu in (1, 2, 3, 4):
+        sdb.read_columns(cols, acc, blocks_per_cu=per_cu)
+        torch.cuda.synchronize()
+        rd = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            sdb.read_columns(cols, acc, blocks_per_cu=per_cu)
+            b.record(stream)
+            b.synchronize()
+            rd.append(a.elapsed_time(b))
+        if best is None or np.mean(rd) < best[1]:
+            best = (per_cu, float(np.mean(rd)))
+    gbps = n * 4 * len(cols) / (best[1] * 1e-3) / 1e9
+    log(f"[bench] streaming read of {len(cols)} columns: {best[1]:.4f} ms, {gbps:.0f} GB/s "
+        f"({best[0]} blocks per CU)")
+    return {"ms": best[1], "GBps": gbps, "frac_of_peak": gbps / HBM_PEAK_GBPS,
+            "fused_frac_of_stream_read": achieved / gbps,
+            "what": f"sdb_read_columns over the query's {len(cols)} fact columns (128-bit loads), "
+                    f"best of 1-4 blocks of 512 per CU ({best[0]})"}
+
+
+def graph_replay_ms(q, sums, counts, plan, fin_out, stream, n_groups: int) -> float:
+    """The run and the compaction captured in one HIP graph and replayed (no
+    host launch gaps); the replay must reproduce the group count."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    scratch = q.run_scratch(plan)
+    with torch.cuda.graph(graph, stream=side):
+        q.run(sums, counts, plan=plan, scratch=scratch)
+        q.finalize(sums, counts, plan=plan, outputs=fin_out)
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    if int(fin_out[3].item()) != n_groups:
+        raise AssertionError("graph replay changed the number of groups")
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(10):
+        graph.replay()
+    b.record(stream)
+    b.synchronize()
+    ms = a.elapsed_time(b) / 10
+    log(f"[bench] run + finalize replayed from a HIP graph: {ms:.4f} ms")
+    return ms
+
+
+def end_to_end(sdb, build_tables, fact, query, force, sums, counts, fin_out) -> dict:
+    """One query end to end (builds, plan, run, compaction, copy of the groups
+    to the host), and an MD5 digest of the whole result (keys, sums, counts as
+    little-endian bytes) for comparing runs across machines, the way the paper
+    compares its outputs."""
+    import numpy as np
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    q = sdb.StarQuery(fact, build_tables(), query, force)
+    q.plan()
+    q.run(sums, counts)
+    k, s, c, nout, _ = q.finalize(sums, counts, outputs=fin_out)
+    m = int(nout.item())
+    host = (k[:m].cpu(), s[:m].cpu(), c[:m].cpu())
+    ms = 1000.0 * (time.perf_counter() - t0)
+    digest = hashlib.md5()
+    for t in host:
+        digest.update(np.ascontiguousarray(t.numpy()).tobytes())
+    return {"e2e_ms": ms, "e2e_includes": f"build + plan + run + finalize + copy of {m} groups to the host",
+            "result_md5": digest.hexdigest()}
+
+
+def mall_cold_ms(q, sums, counts, plan, stream, dev) -> float:
+    """Run time with a 1 GiB write before every run, which evicts the columns
+    from the 256 MB cache."""
+    import numpy as np
+    import torch
+    flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+    scratch = q.run_scratch(plan)
+    cold = []
+    for _ in range(5):
+        flush.fill_(7)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        q.run(sums, counts, plan=plan, scratch=scratch)
+        b.record(stream)
+        b.synchronize()
+        cold.append(a.elapsed_time(b))
+    return float(np.mean(cold))
+
+
+def copy_calibration(dev) -> None:
+    """Three device copies of exactly 1 GiB: the reference launches that scale
+    the HBM byte counters in the profiles."""
+    import torch
+    src = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log("[bench] copy calibration: 3 x 1 GiB device-to-device copies done")
+
+
+def cpu_baseline_leg(sdb, fact, wdims, query, force, build_tables, args, n, plan_info, kernel_ms) -> dict:
+    """The oracle timed on the first rows of the same workload (one thread),
+    the GPU compared with it bit for bit on those rows, and B_alg from them."""
+    import oracle
+    m = min(args.cpu_rows, n)
+    sample = {k: v[:m].cpu().numpy() for k, v in fact.items()}
+    t0 = time.perf_counter()
+    ref = oracle.star_query(sample, wdims.dims, wdims.dim_keys, query)
+    t_oracle = time.perf_counter() - t0
+    qs = sdb.StarQuery({k: v[:m] for k, v in fact.items()}, build_tables(), query, force)
+    parity = qs.execute().as_rows() == ref.as_rows()
+    b_alg = b_alg_per_row(sample, wdims.dims, wdims.dim_keys, query, plan_info)
+    log(f"[bench] oracle {m} rows in {t_oracle:.1f} s; GPU result on the sample "
+        f"{'equals' if parity else 'DIFFERS FROM'} the oracle")
+    return {
+        "cpu_baseline": {
+            "value": m / t_oracle,
+            "unit": "fact rows/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": f"first {m} of {n} fact rows of {args.config}, full dimension tables; "
+                      f"numpy oracle, one thread, {t_oracle:.1f} s",
+            "cpu": cpu_model(),
+        },
+        "parity_on_cpu_sample": parity,
+        "b_alg_bytes_per_row": b_alg,
+        "b_alg_GBps_fused": n * b_alg / (kernel_ms * 1e-3) / 1e9,
+    }
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -336,7 +478,7 @@ def main(argv=None) -> int:
         ev[3].record(stream)
         sdb.set_fused_events()
         last_fused[0] = ev[1]
-        k, s_, c_, nout, _ = q.finalize(sl["sums"], sl["counts"], plan=plan, outputs=sl["fin"], stream=stream)
+        nout = q.finalize(sl["sums"], sl["counts"], plan=plan, outputs=sl["fin"], stream=stream)[3]
         if n_out is not None:
             n_out[i].copy_(nout[0], non_blocking=True)
         sl["done"].record(stream)
@@ -438,92 +580,16 @@ def main(argv=None) -> int:
         result["hbm_traffic_GBps_fused"] = traffic / (kernel_ms_mean * 1e-3) / 1e9
         result["hbm_traffic_frac_fused"] = result["hbm_traffic_GBps_fused"] / HBM_PEAK_GBPS
 
-    # context: a plain streaming read of the same columns (the practical ceiling)
-    used_cols = [fact[c] for c in query_columns(query)]
-    acc = torch.zeros(1, dtype=torch.int64, device=dev)
-    best = None
-    for per_cu in (1, 2, 3, 4):                 # the fastest launch shape is the ceiling
-        sdb.read_columns(used_cols, acc, blocks_per_cu=per_cu)
-        torch.cuda.synchronize()
-        rd = []
-        for _ in range(5):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            sdb.read_columns(used_cols, acc, blocks_per_cu=per_cu)
-            b.record(stream)
-            b.synchronize()
-            rd.append(a.elapsed_time(b))
-        if best is None or np.mean(rd) < best[1]:
-            best = (per_cu, float(np.mean(rd)))
-    read_gbps = n * 4 * len(used_cols) / (best[1] * 1e-3) / 1e9
-    result["stream_read"] = {
-        "ms": best[1], "GBps": read_gbps, "frac_of_peak": read_gbps / HBM_PEAK_GBPS,
-        "fused_frac_of_stream_read": achieved / read_gbps,
-        "what": f"sdb_read_columns over the query's {len(used_cols)} fact columns (128-bit loads), "
-                f"best of 1-4 blocks of 512 per CU ({best[0]})",
-    }
-    log(f"[bench] streaming read of {len(used_cols)} columns: {best[1]:.4f} ms, {read_gbps:.0f} GB/s "
-        f"({best[0]} blocks per CU)")
+    result["stream_read"] = stream_read_reference(sdb, [fact[c] for c in query_columns(query)], n, stream,
+                                                  achieved)
 
-    # the run and the compaction replayed from one HIP graph (no host launch gaps)
-    side = torch.cuda.Stream()
-    side.wait_stream(stream)
-    graph = torch.cuda.CUDAGraph()
-    scratch_g = q0.run_scratch(plan)
-    with torch.cuda.graph(graph, stream=side):
-        q0.run(sums, counts, plan=plan, scratch=scratch_g)
-        q0.finalize(sums, counts, plan=plan, outputs=fin_out)
-    torch.cuda.synchronize()
-    graph.replay()
-    torch.cuda.synchronize()
-    if int(fin_out[3].item()) != n_groups_out:
-        raise AssertionError("graph replay changed the number of groups")
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    for _ in range(10):
-        graph.replay()
-    b.record(stream)
-    b.synchronize()
-    result["run_finalize_ms_graph"] = a.elapsed_time(b) / 10
-    log(f"[bench] run + finalize replayed from a HIP graph: {result['run_finalize_ms_graph']:.4f} ms")
-    del graph
+    result["run_finalize_ms_graph"] = graph_replay_ms(q0, sums, counts, plan, fin_out, stream, n_groups_out)
 
-    # end to end once: builds, plan, fused pass, compaction and the copy of the groups to the host
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    tabs = build_tables()
-    qe = sdb.StarQuery(fact, tabs, query, force)
-    qe.plan()
-    qe.run(sums, counts)
-    k, s_, c_, nout, _ = qe.finalize(sums, counts, outputs=fin_out)
-    m_out = int(nout.item())
-    host = (k[:m_out].cpu(), s_[:m_out].cpu(), c_[:m_out].cpu())
-    result["e2e_ms"] = 1000.0 * (time.perf_counter() - t0)
-    result["e2e_includes"] = f"build + plan + run + finalize + copy of {m_out} groups to the host"
-    # a digest of the whole result (keys, sums, counts as little-endian bytes), for
-    # comparing runs across machines the way the paper compares its outputs
-    digest = hashlib.md5()
-    for t in host:
-        digest.update(np.ascontiguousarray(t.numpy()).tobytes())
-    result["result_md5"] = digest.hexdigest()
-    del host
+    result.update(end_to_end(sdb, build_tables, fact, query, force, sums, counts, fin_out))
 
     if cfg.n_fact <= 100_000_000:
-        # MALL-cold runs: a 1 GiB write between runs evicts the columns from the 256 MB cache
-        flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
-        scratch_cold = q0.run_scratch(plan)
-        cold = []
-        for _ in range(5):
-            flush.fill_(7)
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            q0.run(sums, counts, plan=plan, scratch=scratch_cold)
-            b.record(stream)
-            b.synchronize()
-            cold.append(a.elapsed_time(b))
-        del flush
-        result["run_ms_mall_cold"] = float(np.mean(cold))
-        log(f"[bench] MALL-cold run {np.mean(cold):.4f} ms (warm {run_ms_mean:.4f} ms)")
+        result["run_ms_mall_cold"] = mall_cold_ms(q0, sums, counts, plan, stream, dev)
+        log(f"[bench] MALL-cold run {result['run_ms_mall_cold']:.4f} ms (warm {run_ms_mean:.4f} ms)")
 
     if args.ablation:
         ladder = ablation_ladder(sdb, fact, dims, wdims, query, stream, force)
@@ -533,41 +599,11 @@ def main(argv=None) -> int:
             log(f"[ablation] {r['rung']:58s} {r['run_ms']:8.3f} ms  {r['plan']}")
 
     if args.copy_calibration:
-        src = torch.empty(1 << 28, dtype=torch.int32, device=dev)
-        dst = torch.empty_like(src)
-        src.fill_(1)
-        torch.cuda.synchronize()
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        log("[bench] copy calibration: 3 x 1 GiB device-to-device copies done")
+        copy_calibration(dev)
 
     if not args.no_cpu:
-        import oracle
-        m = min(args.cpu_rows, n)
-        sample = {k: v[:m].cpu().numpy() for k, v in fact.items()}
-        t0 = time.perf_counter()
-        ref = oracle.star_query(sample, wdims.dims, wdims.dim_keys, query)
-        t_oracle = time.perf_counter() - t0
-        # GPU on the same rows (column views), compared bit for bit
-        qs = sdb.StarQuery({k: v[:m] for k, v in fact.items()}, build_tables(), query, force)
-        got = qs.execute()
-        parity = got.as_rows() == ref.as_rows()
-        result["cpu_baseline"] = {
-            "value": m / t_oracle,
-            "unit": "fact rows/s",
-            "cores": 1,
-            "kind": "oracle",
-            "sample": f"first {m} of {n} fact rows of {args.config}, full dimension tables; "
-                      f"numpy oracle, one thread, {t_oracle:.1f} s",
-            "cpu": cpu_model(),
-        }
-        result["parity_on_cpu_sample"] = parity
-        b_alg = b_alg_per_row(sample, wdims.dims, wdims.dim_keys, query, plan_info)
-        result["b_alg_bytes_per_row"] = b_alg
-        result["b_alg_GBps_fused"] = n * b_alg / (kernel_ms_mean * 1e-3) / 1e9
-        log(f"[bench] oracle {m} rows in {t_oracle:.1f} s; GPU result on the sample "
-            f"{'equals' if parity else 'DIFFERS FROM'} the oracle")
+        result.update(cpu_baseline_leg(sdb, fact, wdims, query, force, build_tables, args, n, plan_info,
+                                       kernel_ms_mean))
 
     print(json.dumps(result), flush=True)
     return 0
