@@ -110,11 +110,12 @@ def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_in
 
 # The plan features of the fused pass added one at a time, each rung a set of
 # planner overrides (the last rung is the planner's own choice).
-_NR = {"range": -1}     # the rungs before the key-range rewrite keep every probe a lookup
+_NR = {"range": -1, "slice": -1}     # the rungs before the key-range rewrite keep every probe a lookup, unsliced
 ABLATION_RUNGS = [
     ("kernel at a time: flags and group ids through HBM; hash tables; query order",
-     {"order": True, "baseline": "per_operator", "tables": "hash"}),
-    ("one kernel; operators hand off through HBM", {"order": True, "baseline": "global_handoff", "tables": "hash"}),
+     {"order": True, "baseline": "per_operator", "tables": "hash", "slice": -1}),
+    ("one kernel; operators hand off through HBM", {"order": True, "baseline": "global_handoff", "tables": "hash",
+                                                    "slice": -1}),
     ("+ register table; 1-row items", {"order": True, "lds": -1, "vector": -1, "ipt": 1, "terminal": "global",
                                        "xcd": -1, "block": 256, "tables": "hash"} | _NR),
     ("+ packed direct-mapped maps", {"order": True, "lds": -1, "vector": -1, "ipt": 1,
@@ -128,8 +129,9 @@ ABLATION_RUNGS = [
     ("+ sampled stage order", {"lds": 2, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256} | _NR),
     ("+ per-XCD group tables", {"lds": 2, "ipt": 2, "terminal": "global", "block": 256} | _NR),
     ("+ probes of one contiguous passing key range run as BETWEEN", {"lds": 2, "ipt": 2, "terminal": "global",
-                                                                     "block": 256, "range": 1}),
-    ("planner's choice (terminal, block size, rank tables)", {}),
+                                                                     "block": 256, "range": 1, "slice": -1}),
+    ("planner's choice (terminal, block size, rank tables)", {"slice": -1}),
+    ("+ a hash probe over 2 MiB table slices (planner's choice)", {}),
 ]
 
 

@@ -36,7 +36,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 5
+#define SDB_ABI_VERSION 6
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -192,7 +192,10 @@ typedef struct sdb_agg {
  *  force_coarse    coarse LDS pre-filters for dense tables left in device
  *                  memory (SDB_LDS_COARSE): 0: chosen by the planner; -1:
  *                  none; k in 1..SDB_MAX_COARSE_SHIFT: every such table whose
- *                  coarse bitmap of 2^k slots per bit fits in LDS */
+ *                  coarse bitmap of 2^k slots per bit fits in LDS
+ *  force_slice     the hash probe over table slices (sdb_plan.slice_bits):
+ *                  0: chosen by the planner; -1: never; 1: wherever the
+ *                  query allows it */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -215,6 +218,7 @@ typedef struct sdb_query {
     int32_t force_block;
     int32_t force_range;
     int32_t force_coarse;
+    int32_t force_slice;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -245,7 +249,19 @@ enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, 
  * key's stride 1, so ascending group ids are ascending key tuples.
  * With xcd_copies > 0 the global terminal accumulates into that many private
  * copies of the group table (one per XCD, in the run scratch) that a second
- * kernel adds into the outputs. */
+ * kernel adds into the outputs.
+ * With slice_bits > 0 the hash probe of stage slice_stage runs over table
+ * slices (the L2-resident lookup tables of Section 3.3, extended to a hash
+ * table larger than the caches): a count pass and a scatter pass, slice_grid
+ * blocks each, evaluate the fact predicates and write every passing row's
+ * probe key and aggregate value into 2^slice_bits partitions by the top
+ * slice_bits bits of the key's 32-bit hash, which also selects the table
+ * slice its home slot lies in; the fused kernel then runs the probe alone
+ * over the partitioned records, partition after partition, so the slots it
+ * reads at any time fit in L2. It needs one hash probe, all other stages fact
+ * predicates, a one-column SUM, and the columns those passes read 16-byte
+ * aligned. ipt, vector, eager (0), block, grid,
+ * lds_bytes and the terminal fields describe that fused launch. */
 typedef struct sdb_plan {
     int32_t n_stages;
     int32_t stage_kind[SDB_MAX_STAGES];
@@ -277,7 +293,13 @@ typedef struct sdb_plan {
     uint64_t stride[SDB_MAX_GROUP_KEYS];
     uint64_t n_groups;                    /* product of radices; 1 without GROUP BY */
     int64_t run_scratch_bytes;            /* device scratch sdb_run_star_query needs */
+    int32_t slice_bits;                   /* 0: no sliced probe; else 1 .. SDB_MAX_SLICE_BITS */
+    int32_t slice_stage;                  /* stage of the sliced hash probe (slice_bits > 0) */
+    int32_t slice_grid;                   /* blocks of the count and scatter passes */
+    int32_t slice_reserved;               /* 0 */
 } sdb_plan;
+/* most partitions of the sliced hash probe: 2^SDB_MAX_SLICE_BITS */
+#define SDB_MAX_SLICE_BITS 10
 
 /* ---- errors and ABI ---------------------------------------------------- */
 
@@ -346,7 +368,9 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
  * when the group table fits a block's LDS, partitioned for many survivors
  * into a large table, else global, with per-XCD copies when enough rows
  * survive); items per lane, block size, eager columns, and for the
- * partitioned terminal the grid and region sizes. Errors: INVALID_ARG,
+ * partitioned terminal the grid and region sizes; whether the hash probe
+ * runs over table slices (chosen for a table of at least 16 MiB and at
+ * least 2^24 fact rows, when the query allows it). Errors: INVALID_ARG,
  * UNSUPPORTED, CAPACITY, WORKSPACE_TOO_SMALL, HIP_ERROR. */
 SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_t scratch_bytes,
                                        void* stream, sdb_plan* plan);
@@ -356,7 +380,8 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
 /* Runs `q` with `plan` (from sdb_plan_star_query for this query and these
  * tables) as one fused probe-filter-aggregate kernel (Sections 3.2 and 4.2),
  * all queued on `stream` (asynchronous): rank tables are derived first when
- * the plan stages any, and the partitioned terminal's sort and sum passes or
+ * the plan stages any, a sliced hash probe's count and scatter passes come
+ * before the fused kernel, and the partitioned terminal's sort and sum passes or
  * the per-XCD copies' merge follow the fused kernel. Only kernels are
  * enqueued (no memset, copy or synchronization), so the call can be captured
  * in a HIP graph. The outputs are zeroed first (or, with per-XCD copies, the
@@ -376,7 +401,9 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
  * handles the caller created and owns), every later sdb_run_star_query on
  * this thread records `start` on its stream just before the fused kernel and
  * `stop` just after it (before any terminal pass), so the elapsed time
- * between them is that kernel's duration. NULL, NULL turns it off. */
+ * between them is that kernel's duration; with a sliced hash probe `start`
+ * comes before its count pass, so the time covers both passes and the
+ * kernel. NULL, NULL turns it off. */
 SDB_API sdb_status sdb_set_fused_events(void* start, void* stop);
 
 /* Measurement only: the plain streaming read the fused pass is compared

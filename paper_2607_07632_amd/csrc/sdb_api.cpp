@@ -665,6 +665,63 @@ PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
     return L;
 }
 
+// Sliced hash probe (sdb_plan.slice_bits): chosen for a hash table of at
+// least 16 MiB (random probes into it miss L2; measured on MI355X, 8-byte
+// probes run at about 54G/s into 32-256 MiB and 215G/s into 0.5-2 MiB) over
+// at least 2^24 fact rows. Slices of 2 MiB: more partitions would shorten
+// the scatter's runs of stores (measured: its time grows from 2.6 ms at 64
+// partitions to 3.8 ms at 512 for 600M rows) for little gain in the probe.
+constexpr uint64_t kSliceMinTableBytes = 16ull << 20;
+constexpr int64_t kSliceMinRows = 1ll << 24;
+constexpr int64_t kSliceMaxRows = 0xFFFFF000ll;   // record positions are 32-bit
+constexpr int kSliceLog2Bytes = 21;
+
+// The join the query allows to run over table slices, or -1: the only join,
+// into a hash table, with every other stage a fact predicate, a SUM of one
+// column (the partitioned records carry one 32-bit value), and the columns
+// the count and scatter passes read 16-byte aligned (128-bit loads).
+int slice_join(const sdb_query* q) {
+    if (q->n_joins != 1 || q->agg.kind != SDB_AGG_COL || q->n_fact > kSliceMaxRows) return -1;
+    const sdb_dim* d = q->joins[0].dim;
+    if (d->kind != SDB_TABLE_HASH || d->hash_bits < 1) return -1;
+    if (!aligned16(q->cols[q->joins[0].fact_key_col]) || !aligned16(q->cols[q->agg.a])) return -1;
+    for (int i = 0; i < q->n_preds; ++i)
+        if (!aligned16(q->cols[q->preds[i].col])) return -1;
+    return 0;
+}
+
+int slice_bits_for(const sdb_dim* d) {
+    const int want = d->hash_bits + 3 - kSliceLog2Bytes;
+    return std::max(1, std::min(want, std::min((int)d->hash_bits, SDB_MAX_SLICE_BITS)));
+}
+
+// Run-scratch layout of the sliced probe's partition passes.
+struct SliceLayout {
+    uint64_t hist, part_count, part_start, chunk_start, out_key, out_val, total;
+};
+
+SliceLayout slice_layout(const sdb_query* q, const sdb_plan* plan) {
+    SliceLayout L;
+    std::memset(&L, 0, sizeof L);
+    if (plan->slice_bits <= 0) return L;
+    const uint64_t P = 1ull << plan->slice_bits, grid = (uint64_t)plan->slice_grid;
+    const uint64_t n = (uint64_t)std::max<int64_t>(q->n_fact, 1);
+    uint64_t off = 0;
+    auto take = [&](uint64_t bytes) {
+        const uint64_t at = off;
+        off += align_up(bytes, 256);
+        return at;
+    };
+    L.hist = take(P * grid * 4);
+    L.part_count = take(P * 4);
+    L.part_start = take((P + 1) * 4);
+    L.chunk_start = take((P + 1) * 4);
+    L.out_key = take(n * 4);
+    L.out_val = take(n * 4);
+    L.total = off;
+    return L;
+}
+
 // Run scratch of the LDS_RANK stages' tables and the LDS_COARSE stages'
 // coarse bitmaps, in stage order; the terminal's scratch follows it.
 uint64_t stage_scratch_bytes(const sdb_query* q, const sdb_plan* plan) {
@@ -1003,6 +1060,13 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     st = group_layout(q, plan);
     if (st != SDB_OK) return st;
 
+    // the hash probe over table slices, where the query allows it
+    int slice_j = (q->force_slice == -1 || q->force_eager > 0 || q->n_fact == 0) ? -1 : slice_join(q);
+    if (slice_j >= 0 && q->force_slice != 1) {
+        const sdb_dim* d = q->joins[slice_j].dim;
+        if ((uint64_t)d->n_slots * 8u < kSliceMinTableBytes || q->n_fact < kSliceMinRows) slice_j = -1;
+    }
+
     // terminal
     int term;
     if (q->force_terminal != SDB_TERMINAL_AUTO) term = q->force_terminal;
@@ -1044,6 +1108,8 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         for (int s = 0; s < n; ++s)
             plan->stage_range[s] = plan->stage_kind[s] == 1 && plan->stage_lds[s] == LDS_GLOBAL &&
                                    range_eligible(q, plan->stage_index[s]);
+    for (int s = 0; s < n; ++s)
+        if (plan->stage_kind[s] == 1 && plan->stage_range[s]) slice_j = -1;   // the probe became a compare
     if (!q->force_order && n > 1) choose_order(q, plan);
     else {
         int order[SDB_MAX_STAGES];
@@ -1062,7 +1128,8 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     }
     plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
 
-    const bool aligned = columns_aligned(q, plan);
+    // (a sliced probe's fused kernel reads the partitioned records, which are aligned)
+    const bool aligned = columns_aligned(q, plan) || slice_j >= 0;
     if (q->force_vector == 1 && !aligned && q->n_fact > 0)
         return fail(SDB_INVALID_ARG, "vector loads forced but a column is not 16-byte aligned");
     plan->vector = q->force_vector == -1 ? 0 : (aligned ? 1 : 0);
@@ -1120,7 +1187,8 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     plan->eager = 0;
     if (q->force_eager > 0 && (!plan->vector || plan->ipt > 2 || plan->block == kBigBlock))
         return fail(SDB_INVALID_ARG, "eager loads need 4-row items, ipt 1 or 2 and blocks of at most %d", kMaxBlock);
-    if (plan->vector && plan->ipt <= 2 && plan->block <= kMaxBlock && q->n_fact > 0 && q->force_eager >= 0) {
+    if (plan->vector && plan->ipt <= 2 && plan->block <= kMaxBlock && q->n_fact > 0 && q->force_eager >= 0 &&
+        slice_j < 0) {
         int cols[SDB_MAX_FACT_COLS];
         double live[SDB_MAX_FACT_COLS];
         const int n_used = columns_in_use_order(q, plan, cols, live);
@@ -1192,6 +1260,14 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             plan->part_cap = (int64_t)(0xFFFFFFF0ull / (uint64_t)plan->grid) / 64 * 64;
         plan->run_scratch_bytes = (int64_t)stage_bytes + (int64_t)part_layout(q, plan).total;
     }
+    if (slice_j >= 0) {
+        plan->slice_bits = slice_bits_for(q->joins[slice_j].dim);
+        for (int s = 0; s < n; ++s)
+            if (plan->stage_kind[s] == 1) plan->slice_stage = s;
+        plan->slice_grid = (int32_t)std::min<int64_t>(
+            kSliceMaxGrid, std::max<int64_t>(1, (q->n_fact + kSliceChunk - 1) / kSliceChunk));
+        plan->run_scratch_bytes += (int64_t)slice_layout(q, plan).total;
+    }
     return ok();
 }
 
@@ -1221,7 +1297,17 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     if (plan->block == kBigBlock && (!plan->vector || plan->ipt > 2 || plan->eager > 0))
         return fail(SDB_INVALID_ARG, "blocks of %d threads need 4-row items, ipt 1 or 2 and no eager loads",
                     kBigBlock);
-    if (plan->vector && q->n_fact > 0 && !columns_aligned(q, plan))
+    const bool sliced = plan->slice_bits != 0;
+    if (sliced) {
+        const int sj = slice_join(q);
+        const int ss = plan->slice_stage;
+        if (plan->slice_bits < 1 || plan->slice_bits > SDB_MAX_SLICE_BITS || sj < 0 || ss < 0 ||
+            ss >= plan->n_stages || plan->stage_kind[ss] != 1 || plan->stage_index[ss] != sj ||
+            plan->stage_range[ss] != 0 || plan->slice_bits > q->joins[sj].dim->hash_bits || plan->slice_grid < 1 ||
+            plan->slice_grid > kSliceMaxGrid || plan->eager != 0 || plan->slice_reserved != 0)
+            return fail(SDB_INVALID_ARG, "bad sliced-probe plan");
+    }
+    if (plan->vector && q->n_fact > 0 && !sliced && !columns_aligned(q, plan))
         return fail(SDB_INVALID_ARG, "vector plan but a column is not 16-byte aligned");
     if (plan->eager < 0 || plan->eager > kMaxEager || (plan->eager > 0 && (!plan->vector || plan->ipt > 2)))
         return fail(SDB_INVALID_ARG, "bad plan eager %d (needs 4-row items and ipt 1 or 2)", plan->eager);
@@ -1231,7 +1317,8 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     const uint64_t stage_bytes = stage_scratch_bytes(q, plan);
     uint64_t term_scratch = plan->xcd_copies ? (uint64_t)plan->xcd_copies * plan->n_groups * 16 : 0;
     if (plan->terminal == TERM_PART) term_scratch = part_layout(q, plan).total;
-    const uint64_t need_scratch = stage_bytes + term_scratch;
+    const SliceLayout SL = slice_layout(q, plan);
+    const uint64_t need_scratch = stage_bytes + SL.total + term_scratch;
     if (need_scratch) {
         if (!scratch) return fail(SDB_INVALID_ARG, "null run scratch");
         if (((uintptr_t)scratch & 255u) != 0) return fail(SDB_INVALID_ARG, "run scratch is not 256-byte aligned");
@@ -1248,7 +1335,56 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     p.ring_off = (uint32_t)plan->lds_bytes;
 
     hipStream_t s = (hipStream_t)stream;
-    uint8_t* term_base = (uint8_t*)scratch + stage_bytes;
+    uint8_t* slice_base = (uint8_t*)scratch + stage_bytes;
+    uint8_t* term_base = slice_base + SL.total;
+    SliceParams sp;
+    std::memset(&sp, 0, sizeof sp);
+    if (sliced) {
+        // the count and scatter passes evaluate the predicates and write the
+        // probe keys and aggregate values partitioned by slice; the fused
+        // kernel runs the probe alone over them, up to the count they wrote
+        const int ss = plan->slice_stage;
+        for (int c = 0; c < q->n_cols; ++c) sp.cols[c] = q->cols[c];
+        sp.n = q->n_fact;
+        const int64_t per = (q->n_fact + plan->slice_grid - 1) / plan->slice_grid;
+        sp.rows_per_block = (per + kSliceChunk - 1) / kSliceChunk * kSliceChunk;
+        sp.key_col = q->joins[plan->stage_index[ss]].fact_key_col;
+        sp.val_col = q->agg.a;
+        sp.bits = plan->slice_bits;
+        for (int st_i = 0; st_i < plan->n_stages; ++st_i) {
+            if (plan->stage_kind[st_i] != 0) continue;
+            const sdb_pred& pr = q->preds[plan->stage_index[st_i]];
+            sp.pred_col[sp.n_preds] = pr.col;
+            sp.pred[sp.n_preds] = lower_pred(pr);
+            ++sp.n_preds;
+        }
+        sp.hist = (uint32_t*)(slice_base + SL.hist);
+        sp.part_count = (uint32_t*)(slice_base + SL.part_count);
+        sp.part_start = (uint32_t*)(slice_base + SL.part_start);
+        sp.chunk_start = (uint32_t*)(slice_base + SL.chunk_start);
+        sp.out_key = (int32_t*)(slice_base + SL.out_key);
+        sp.out_val = (int32_t*)(slice_base + SL.out_val);
+        StageDev hs = p.st[ss];
+        hs.col = 0;
+        hs.eg_slot = -1;
+        FusedParams p3;
+        std::memset(&p3, 0, sizeof p3);
+        p3.cols[0] = sp.out_key;
+        p3.cols[1] = sp.out_val;
+        p3.n = q->n_fact;
+        p3.n_dev = sp.part_start + (1u << plan->slice_bits);
+        p3.nstages = 1;
+        p3.st[0] = hs;
+        p3.agg_kind = SDB_AGG_COL;
+        p3.agg_a = 1;
+        p3.agg_b = 1;
+        p3.agg_a_slot = -1;
+        p3.agg_b_slot = -1;
+        p3.defer_stage = -1;
+        p3.n_groups = p.n_groups;
+        p3.ring_off = p.ring_off;
+        p = p3;
+    }
     {
         // the rank tables of LDS_RANK stages and the coarse bitmaps of
         // LDS_COARSE stages, derived from their pass bitmaps and maps
@@ -1334,6 +1470,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         }
         const bool timed = g_fused_start && g_fused_stop;
         if (timed) SDB_HIP(hipEventRecord(g_fused_start, s), "event record");
+        if (sliced) SDB_HIP(launch_slice_partition(sp, plan->slice_grid, s), "slice passes launch");
         SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, plan->eager, grid, plan->block, lds_bytes,
                              s),
                 "fused kernel launch");

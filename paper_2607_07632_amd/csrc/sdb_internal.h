@@ -65,6 +65,13 @@ constexpr uint32_t kRingEntries = 128;     // fused kernel: per-wave record ring
 constexpr uint32_t kLdsRankBudget = 98304;  // LDS for a stage's rank tables (bitmap, counts, codes)
 constexpr uint32_t kRankGroups = 4096;      // at most this many 64-slot groups (one scan block)
 
+// Sliced hash probe: fact rows partitioned by the top bits of the key's hash.
+constexpr int kSliceBlock = 1024;          // threads per block of the count and scatter passes
+constexpr int kSliceRowsPerThread = 16;    // rows a thread holds per scatter chunk
+constexpr int kSliceChunk = kSliceBlock * kSliceRowsPerThread;   // rows one block sorts in LDS at a time
+constexpr int kSliceMaxGrid = 256;         // one block per compute unit of an MI355X
+static_assert(SDB_MAX_SLICE_BITS <= 10, "scatter LDS holds 3 x 2^10 partition counters");
+
 // A literal comparison lowered to one unsigned range test over int32:
 // pass  <=>  ((uint32_t)(x - lo) <= span) != negate.
 struct RangeTest {
@@ -135,6 +142,7 @@ struct RankParams {
 struct FusedParams {
     const int32_t* cols[SDB_MAX_FACT_COLS];
     int64_t n;
+    const uint32_t* n_dev;     // non-null: rows are min(n, *n_dev) (a count another kernel wrote)
     int32_t nstages;
     int32_t agg_kind;
     int32_t agg_a;
@@ -254,6 +262,26 @@ struct PartParams {
     unsigned long long* counts;
 };
 
+// Count and scatter passes of the sliced hash probe. Block b of the grid
+// reads fact rows [b * rows_per_block, (b + 1) * rows_per_block) in both.
+struct SliceParams {
+    const int32_t* cols[SDB_MAX_FACT_COLS];
+    int64_t n;                 // fact rows
+    int64_t rows_per_block;    // a multiple of kSliceChunk; columns are 16-byte aligned
+    int32_t key_col;           // the probe's fact key column
+    int32_t val_col;           // the aggregate's column
+    int32_t n_preds;
+    int32_t bits;              // 2^bits partitions, 1 .. SDB_MAX_SLICE_BITS
+    int32_t pred_col[kMaxStages];
+    RangeTest pred[kMaxStages];
+    uint32_t* hist;            // [q * grid + b]: passing rows, then their offset within partition q
+    uint32_t* part_count;      // rows per partition
+    uint32_t* part_start;      // n_parts + 1 entries; [n_parts] = all passing rows
+    uint32_t* chunk_start;     // n_parts + 1 entries (written by the shared scan, unused)
+    int32_t* out_key;          // partitioned keys and values, all passing rows
+    int32_t* out_val;
+};
+
 // ---- launchers (sdb_kernels.hip) -----------------------------------------
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s);
@@ -286,5 +314,7 @@ hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t
                             unsigned long long* sums, unsigned long long* counts, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s);
 hipError_t launch_part_passes(const PartParams& pp, hipStream_t s);
+// count pass, per-partition offsets, scatter pass over `grid` blocks
+hipError_t launch_slice_partition(const SliceParams& sp, int grid, hipStream_t s);
 
 }  // namespace sdb

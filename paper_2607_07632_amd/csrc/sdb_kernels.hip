@@ -1107,7 +1107,9 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
     }
     __syncthreads();
 
-    const int64_t n_items = p.n / W;
+    int64_t n_rows = p.n;
+    if (p.n_dev) n_rows = min(n_rows, (int64_t)*p.n_dev);
+    const int64_t n_items = n_rows / W;
     const int64_t tile = (int64_t)blockDim.x * IPT;
     const int64_t n_tiles = (n_items + tile - 1) / tile;
     for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
@@ -1125,7 +1127,7 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
         // the last n mod W rows, one per lane, by the last block
         if (blockIdx.x == gridDim.x - 1) {
             int64_t row[1] = {n_items * W + (int64_t)threadIdx.x};
-            bool al1[1][1] = {{row[0] < p.n}};
+            bool al1[1][1] = {{row[0] < n_rows}};
             process_items<1, 1, TERM, false>(p, lds, row, al1, ts);
         }
     }
@@ -1747,6 +1749,223 @@ hipError_t launch_part_passes(const PartParams& pp, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(part_merge_kernel, dim3(fill_grid(pp.n_groups)), dim3(256), 0, s, pp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// sliced hash probe: fact rows partitioned by the top bits of the key's hash
+// ---------------------------------------------------------------------------
+
+// Partition of key k: the top `bits` bits of its 32-bit multiplicative hash,
+// which are also the top bits of its home slot in a table of at least 2^bits
+// slots, so partition q probes only slice q of the table (and the slots
+// that linear probing runs into past its end).
+__device__ __forceinline__ uint32_t slice_of(int32_t k, int bits) {
+    return ((uint32_t)k * 0x9E3779B1u) >> (32 - bits);
+}
+
+// Rows r .. r + 3 of a column (r a multiple of 4, the column 16-byte
+// aligned): one 128-bit load, or row by row below r1 in a last partial group.
+__device__ __forceinline__ void slice_load4(const int32_t* col, int64_t r, int64_t r1, int32_t* x) {
+    if (r + 3 < r1) {
+        const v4i v = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(col + r));
+        x[0] = v.x;
+        x[1] = v.y;
+        x[2] = v.z;
+        x[3] = v.w;
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = r + j < r1 ? __builtin_nontemporal_load(col + r + j) : 0;
+    }
+}
+
+// A thread's rows of the chunk at c0: kSliceRowsPerThread / 4 groups of 4,
+// group i at c0 + 4 * (i * kSliceBlock + threadIdx.x). Which of them lie below
+// r1 and pass every fact predicate, and their keys (0 for the others).
+__device__ __forceinline__ void slice_load_keys(const SliceParams& sp, int64_t c0, int64_t r1,
+                                                int32_t (&k)[kSliceRowsPerThread],
+                                                bool (&ok)[kSliceRowsPerThread]) {
+    constexpr int G = kSliceRowsPerThread / 4;
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+        const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ok[4 * i + j] = r + j < r1;
+    }
+    for (int pi = 0; pi < sp.n_preds; ++pi) {
+        const int32_t* col = sp.cols[sp.pred_col[pi]];
+        const RangeTest t = sp.pred[pi];
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
+            if (!(ok[4 * i] || ok[4 * i + 1] || ok[4 * i + 2] || ok[4 * i + 3])) continue;
+            int32_t x[4];
+            slice_load4(col, r, r1, x);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) ok[4 * i + j] = ok[4 * i + j] && range_pass(t, x[j]);
+        }
+    }
+    const int32_t* key = sp.cols[sp.key_col];
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+        const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
+        int32_t x[4] = {0, 0, 0, 0};
+        if (ok[4 * i] || ok[4 * i + 1] || ok[4 * i + 2] || ok[4 * i + 3]) slice_load4(key, r, r1, x);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) k[4 * i + j] = ok[4 * i + j] ? x[j] : 0;
+    }
+}
+
+// Count pass: block b's passing rows per partition, into hist[q * grid + b].
+// Lanes count into four interleaved copies of the histogram (by lane mod 4),
+// so fewer lanes of one LDS atomic instruction hit the same counter.
+__global__ void __launch_bounds__(kSliceBlock) slice_count_kernel(SliceParams sp) {
+    __shared__ uint32_t lh[4 << SDB_MAX_SLICE_BITS];
+    const uint32_t P = 1u << sp.bits;
+    for (uint32_t q = threadIdx.x; q < 4u * P; q += blockDim.x) lh[q] = 0u;
+    __syncthreads();
+    uint32_t* mine = lh + (threadIdx.x & 3u);
+    const int64_t r0 = (int64_t)blockIdx.x * sp.rows_per_block;
+    const int64_t r1 = min(sp.n, r0 + sp.rows_per_block);
+    for (int64_t c0 = r0; c0 < r1; c0 += kSliceChunk) {
+        int32_t k[kSliceRowsPerThread];
+        bool ok[kSliceRowsPerThread];
+        slice_load_keys(sp, c0, r1, k, ok);
+#pragma unroll
+        for (int i = 0; i < kSliceRowsPerThread; ++i)
+            if (ok[i]) atomicAdd(&mine[4u * slice_of(k[i], sp.bits)], 1u);
+    }
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < P; q += blockDim.x)
+        sp.hist[(uint64_t)q * gridDim.x + blockIdx.x] = lh[4u * q] + lh[4u * q + 1u] + lh[4u * q + 2u] + lh[4u * q + 3u];
+}
+
+// Exclusive scan of n values by the whole block (blockDim.x a multiple of
+// 64, at most 1024): out[i] = carry + sum of in[0..i); in and out distinct.
+// Every thread must call it; returns the sum of in[0..n).
+__device__ uint32_t block_scan_any(const uint32_t* in, uint32_t* out, uint32_t n, uint32_t carry,
+                                   uint32_t* wtmp) {
+    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const uint32_t per = (n + blockDim.x - 1u) / blockDim.x;
+    const uint32_t b0 = threadIdx.x * per;
+    uint32_t loc = 0;
+    for (uint32_t k = 0; k < per; ++k)
+        if (b0 + k < n) loc += in[b0 + k];
+    uint32_t x = loc;
+    for (uint32_t off = 1; off < 64u; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63u) wtmp[wave] = x;
+    __syncthreads();
+    uint32_t before = 0, total = 0;
+    for (uint32_t w = 0; w < nw; ++w) {
+        const uint32_t t = wtmp[w];
+        if (w < wave) before += t;
+        total += t;
+    }
+    uint32_t run = carry + before + x - loc;
+    for (uint32_t k = 0; k < per; ++k)
+        if (b0 + k < n) {
+            out[b0 + k] = run;
+            run += in[b0 + k];
+        }
+    __syncthreads();
+    return total;
+}
+
+// Scatter pass: block b reads its rows again, kSliceChunk at a time, sorts
+// each chunk's passing rows by partition in LDS (counting sort) and writes
+// every partition's run of keys and values after the ones block b wrote
+// before (hist holds block b's first offset within each partition).
+__global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams sp) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    __shared__ uint32_t wtmp[kSliceBlock / 64];
+    int32_t* skey = reinterpret_cast<int32_t*>(smem);
+    int32_t* sval = skey + kSliceChunk;
+    const uint32_t P = 1u << sp.bits;
+    uint32_t* lcnt = reinterpret_cast<uint32_t*>(sval + kSliceChunk);
+    uint32_t* lstart = lcnt + P;
+    uint32_t* lcur = lstart + P;
+    for (uint32_t q = threadIdx.x; q < P; q += blockDim.x) {
+        lcur[q] = sp.part_start[q] + sp.hist[(uint64_t)q * gridDim.x + blockIdx.x];
+        lcnt[q] = 0u;
+    }
+    __syncthreads();
+    const int64_t r0 = (int64_t)blockIdx.x * sp.rows_per_block;
+    const int64_t r1 = min(sp.n, r0 + sp.rows_per_block);
+    const int32_t* val = sp.cols[sp.val_col];
+    for (int64_t c0 = r0; c0 < r1; c0 += kSliceChunk) {
+        int32_t k[kSliceRowsPerThread], v[kSliceRowsPerThread];
+        bool ok[kSliceRowsPerThread];
+        uint32_t rk[kSliceRowsPerThread];
+        slice_load_keys(sp, c0, r1, k, ok);
+#pragma unroll
+        for (int i = 0; i < kSliceRowsPerThread / 4; ++i) {
+            const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
+            int32_t x[4] = {0, 0, 0, 0};
+            if (ok[4 * i] || ok[4 * i + 1] || ok[4 * i + 2] || ok[4 * i + 3]) slice_load4(val, r, r1, x);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[4 * i + j] = x[j];
+        }
+#pragma unroll
+        for (int i = 0; i < kSliceRowsPerThread; ++i) {
+            rk[i] = 0u;
+            if (ok[i]) rk[i] = atomicAdd(&lcnt[slice_of(k[i], sp.bits)], 1u);
+        }
+        __syncthreads();
+        const uint32_t cn = block_scan_any(lcnt, lstart, P, 0u, wtmp);
+#pragma unroll
+        for (int i = 0; i < kSliceRowsPerThread; ++i)
+            if (ok[i]) {
+                const uint32_t pos = lstart[slice_of(k[i], sp.bits)] + rk[i];
+                skey[pos] = k[i];
+                sval[pos] = v[i];
+            }
+        __syncthreads();
+        for (uint32_t i = threadIdx.x; i < cn; i += blockDim.x) {
+            const int32_t key = skey[i];
+            const uint32_t q = slice_of(key, sp.bits);
+            const uint64_t dest = (uint64_t)lcur[q] + (i - lstart[q]);
+            if (dest < (uint64_t)sp.n) {   // always: both passes count the same rows
+                sp.out_key[dest] = key;
+                sp.out_val[dest] = sval[i];
+            }
+        }
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < P; q += blockDim.x) {
+            lcur[q] += lcnt[q];
+            lcnt[q] = 0u;
+        }
+        __syncthreads();
+    }
+}
+
+size_t slice_scatter_lds_bytes(uint32_t n_parts) {
+    return (size_t)kSliceChunk * 8u + (size_t)n_parts * 12u;
+}
+
+hipError_t launch_slice_partition(const SliceParams& sp, int grid, hipStream_t s) {
+    if (sp.bits < 1 || sp.bits > SDB_MAX_SLICE_BITS || grid < 1) return hipErrorInvalidValue;
+    const uint32_t P = 1u << sp.bits;
+    hipLaunchKernelGGL(slice_count_kernel, dim3(grid), dim3(kSliceBlock), 0, s, sp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    PartParams pp;
+    std::memset(&pp, 0, sizeof pp);
+    pp.n_parts = P;
+    pp.n_regions = (uint32_t)grid;
+    pp.part_hist = sp.hist;
+    pp.part_count = sp.part_count;
+    pp.part_start = sp.part_start;
+    pp.chunk_start = sp.chunk_start;
+    hipLaunchKernelGGL(part_offsets_kernel, dim3(P), dim3(256), 0, s, pp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, pp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(slice_scatter_kernel, dim3(grid), dim3(kSliceBlock), slice_scatter_lds_bytes(P), s, sp);
     return hipGetLastError();
 }
 

@@ -82,7 +82,8 @@ class SdbQuery(C.Structure):
                 ("agg", SdbAgg), ("force_terminal", i32), ("force_ipt", i32),
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
-                ("force_block", i32), ("force_range", i32), ("force_coarse", i32)]
+                ("force_block", i32), ("force_range", i32), ("force_coarse", i32),
+                ("force_slice", i32)]
 
 
 class SdbPlan(C.Structure):
@@ -95,7 +96,8 @@ class SdbPlan(C.Structure):
                 ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
                 ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
-                ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64)]
+                ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64),
+                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("slice_reserved", i32)]
 
 
 STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan]
@@ -300,8 +302,9 @@ class StarQuery:
     list of DimTable per join (``build_dims``); ``query`` the plain-data
     description. ``force`` may hold terminal ('scalar'|'lds'|'global'|'part'),
     ipt, vector (1 / -1), order (True = keep query order), grid, lds, xcd,
-    eager, block, range (-1: no key-range probes) and coarse, the sdb_query
-    force_* fields of the same names.
+    eager, block, range (-1: no key-range probes), coarse and slice (-1: no
+    sliced hash probe, 1: wherever allowed), the sdb_query force_* fields of
+    the same names.
     """
 
     def __init__(self, fact: dict, tables: list, query: dict, force: dict | None = None):
@@ -363,6 +366,7 @@ class StarQuery:
         q.force_block = int(force.get("block", 0))
         q.force_range = int(force.get("range", 0))
         q.force_coarse = int(force.get("coarse", 0))
+        q.force_slice = int(force.get("slice", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -486,11 +490,14 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
                 st["coarse_slots_per_bit"] = 1 << plan.stage_coarse[s]
             if plan.stage_defer[s] >= 0:
                 st["deferred_gather"] = True
+            if plan.slice_bits and s == plan.slice_stage:
+                st["table_slices"] = 1 << plan.slice_bits
         stages.append(st)
     return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
             "ipt": plan.ipt, "vector": plan.vector, "eager": plan.eager, "block": plan.block, "grid": plan.grid,
             "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
             "n_parts": plan.n_parts, "part_cap": int(plan.part_cap),
+            "slice_bits": plan.slice_bits, "slice_grid": plan.slice_grid,
             "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}

@@ -38,7 +38,7 @@ def test_struct_layout_matches_binding():
     sizes = (C.c_int64 * 8)()
     assert L.sdb_struct_sizes(sizes, 8) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
-    assert L.sdb_abi_version() == 5
+    assert L.sdb_abi_version() == 6
 
 
 def test_status_strings():

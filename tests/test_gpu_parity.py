@@ -87,11 +87,78 @@ def test_baselines_small_and_tiny_schemas(n, mode):
 @pytest.mark.parametrize("force", [
     {"ipt": 2, "block": 512}, {"ipt": 2, "block": 1024}, {"ipt": 4}, {"vector": -1}, {"terminal": "global"},
     {"terminal": "global", "xcd": -1}, {"eager": 2, "ipt": 1, "block": 512}, {"grid": 3}, {"order": True},
+    {"slice": 1}, {"slice": 1, "terminal": "global"}, {"slice": 1, "terminal": "global", "xcd": -1},
+    {"slice": 1, "vector": -1}, {"slice": 1, "grid": 3}, {"slice": 1, "ipt": 2, "block": 512},
+    {"slice": 1, "ipt": 4, "block": 256}, {"slice": 1, "terminal": "part", "grid": 5},
 ])
 def test_c5_forced_plans_agree(force):
     w = workload("c5_hash_stress")
-    got, _ = run_gpu(w, force=force)
+    got, q = run_gpu(w, force=force)
+    assert bool(q.plan_obj.slice_bits) == bool(force.get("slice"))
     assert_same(got.as_rows(), oracle_rows(w), f"c5 {force}")
+
+
+def _sliceable(w, load_factor=0.5):
+    """w's query narrowed to the shape a sliced hash probe serves: its first
+    join only, as a hash table, group keys from that join, SUM of one column
+    (the fact predicates stay)."""
+    import copy
+    q = copy.deepcopy(w.query)
+    j = dict(q["joins"][0], kind="hash", load_factor=load_factor)
+    q["joins"] = [j]
+    q["group_by"] = [g for g in q["group_by"] if g[0] == j["dim"]]
+    q["agg"] = {"kind": "col", "a": q["agg"]["a"], "b": None}
+    return datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys, q)
+
+
+# row counts around the passes' 16,384-row chunks, up to many blocks
+@pytest.mark.parametrize("n", [0, 1, 5, 16_383, 16_384, 16_385, 70_001, 400_003])
+def test_sliced_probe_on_random_tiny_schemas(n):
+    """Sliced probes (forced) over random one-join schemas with fact
+    predicates, negative keys and values, misses and filtered rows: the
+    oracle's groups, sums and counts exactly."""
+    from paper_2607_07632_amd import sdb
+    done = 0
+    for seed in range(40):
+        w0 = random_tiny_workload(1000 + seed, n_fact=n, max_dim_rows=3000)
+        if not w0.query["joins"]:
+            continue
+        w = _sliceable(w0, load_factor=(0.5, 0.25, 0.9)[seed % 3])
+        for force in ({"slice": 1}, {"slice": 1, "terminal": "global"}, {"slice": 1, "order": True}):
+            got, q = run_gpu(w, force=force)
+            assert q.plan_obj.slice_bits > 0 or n == 0, (seed, force)
+            assert_same(got.as_rows(), oracle_rows(w), f"seed {seed} n {n} {force}")
+        done += 1
+        if done == 3:
+            break
+    assert done == 3
+
+
+def test_sliced_probe_at_every_slice_count():
+    """The partition count follows the table size (slices of 2 MiB, at
+    least 2): one-join schemas with 2^9 ... 2^24 dimension rows (keys with
+    gaps and negative values, half filtered out) give 1 ... 8 slice bits,
+    each with the oracle's result."""
+    rng = np.random.default_rng([2607, 7632, 61])
+    n = 300_007
+    seen = set()
+    for m, lf in ((1 << 9, 0.5), (1 << 18, 0.5), (1 << 19, 0.5), (1 << 20, 0.5), (1 << 22, 0.5),
+                  (1 << 24, 0.25)):
+        keys = (rng.permutation(2 * m)[:m] - m).astype(np.int32)
+        dims = {"big": {"key": keys, "flag": rng.integers(0, 2, m, dtype=np.int32),
+                        "attr": rng.integers(0, 1000, m, dtype=np.int32)}}
+        fact = {"key": rng.integers(-m - 10, m + 10, n, dtype=np.int32),
+                "value": rng.integers(-10**6, 10**6, n, dtype=np.int32)}
+        query = {"fact_preds": [{"col": "value", "op": "ge", "lo": -900_000, "hi": None}],
+                 "joins": [{"fact_key": "key", "dim": "big", "preds": [{"col": "flag", "op": "eq", "lo": 1, "hi": None}],
+                            "payloads": ["attr"], "kind": "hash", "load_factor": lf}],
+                 "group_by": [["big", "attr"]], "agg": {"kind": "col", "a": "value", "b": None}}
+        w = datagen.Workload(f"one hash join, {m} rows", n, fact, dims, {"big": "key"}, query)
+        got, sq = run_gpu(w, force={"slice": 1})
+        bits = sq.plan_obj.slice_bits
+        seen.add(bits)
+        assert_same(got.as_rows(), oracle_rows(w), f"{m} dimension rows, {bits} slice bits")
+    assert seen == {1, 2, 3, 5, 8}, seen
 
 
 def test_c1_forced_plans_agree():
@@ -463,8 +530,8 @@ def test_read_columns_sums_every_value(n_cols):
             assert int(out.item()) == want, (n_cols, n, per_cu)
 
 
-@pytest.mark.parametrize("name", list(SIZES))
-def test_graph_replay_of_run_and_finalize(name):
+@pytest.mark.parametrize("name,force", [(n, None) for n in SIZES] + [("c5_hash_stress", {"slice": 1})])
+def test_graph_replay_of_run_and_finalize(name, force):
     """The run and the compaction enqueue only kernels (no memset, copy or
     synchronization), so they can be captured in a HIP graph: every replay,
     with eager work scribbling over the outputs in between, must give the
@@ -473,8 +540,9 @@ def test_graph_replay_of_run_and_finalize(name):
     from paper_2607_07632_amd import sdb
     w = workload(name)
     fact, dims = upload(w)
-    q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query)
+    q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query, force)
     plan = q.plan()
+    assert bool(plan.slice_bits) == bool(force)
     sums, counts = q.alloc_outputs(plan)
     scratch = q.run_scratch(plan)
     outs = q.finalize(sums, counts, plan=plan)
@@ -572,7 +640,7 @@ def test_random_override_combinations(seed):
         "terminal": ["auto", "scalar", "lds", "global", "part"], "ipt": [0, 1, 2, 4], "vector": [0, 1, -1],
         "order": [False, True], "grid": [0, 0, 1, 3, 17], "lds": [-1, 0, 2, 3], "xcd": [-1, 0, 1],
         "eager": [-1, 0, 1, 2, 4], "block": [0, 64, 128, 256, 512, 1024], "range": [-1, 0, 1],
-        "coarse": [-1, 0, 1, 2, 5],
+        "coarse": [-1, 0, 1, 2, 5], "slice": [-1, 0, 1],
     }
     refused = ran = 0
     for case in range(4):

@@ -97,6 +97,7 @@ def queries(draw):
     q.force_block = draw(st.sampled_from([0, 64, 128, 256, 512, 1024]))
     q.force_range = draw(st.sampled_from([-1, 0, 1]))
     q.force_coarse = draw(st.integers(-1, 5))
+    q.force_slice = draw(st.sampled_from([-1, 0, 1, 1]))
     return q, ds
 
 
@@ -139,6 +140,24 @@ def check_plan(q, p):
         groups *= p.radix[k]
     assert p.n_groups == groups
     assert p.run_scratch_bytes >= 0
+    # the sliced hash probe: only the query shape it supports, and wherever
+    # that shape is forced
+    join_probe = [s for s in range(n) if p.stage_kind[s] == 1 and not p.stage_range[s]]
+    read = [q.joins[0].fact_key_col, q.agg.a] + [q.preds[i].col for i in range(q.n_preds)] if q.n_joins else []
+    sliceable = (q.n_joins == 1 and len(join_probe) == 1 and q.joins[0].dim.contents.kind == 2 and
+                 q.agg.kind == 0 and 0 < q.n_fact <= 0xFFFFF000 and q.force_eager <= 0 and
+                 all(q.cols[c] % 16 == 0 for c in read))
+    if p.slice_bits:
+        assert sliceable and q.force_slice != -1
+        s = p.slice_stage
+        d = q.joins[0].dim.contents
+        assert s == join_probe[0] and 1 <= p.slice_bits <= min(10, d.hash_bits)
+        assert 1 <= p.slice_grid <= 256 and p.eager == 0 and p.stage_lds[s] == LDS_GLOBAL
+        # partition counts and offsets, and one key and value per fact row
+        assert p.run_scratch_bytes >= 8 * q.n_fact + 4 * p.slice_grid * (1 << p.slice_bits)
+    else:
+        assert not (sliceable and q.force_slice == 1)
+    assert p.slice_reserved == 0
 
 
 @settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.too_slow])
@@ -198,3 +217,80 @@ def test_rank_and_deferred_placements_pass_run_validation(force_lds, force_block
     status = sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
                                           scratch, int(p.run_scratch_bytes), None)
     assert status in (OK, HIP_ERROR), (status, sdb.lib().sdb_last_error())
+
+
+def _c5_like(n_fact, hash_bits=25, n_preds=1, agg_kind=0, aligned=True):
+    """One hash join with its payload as the group key (a 2^hash_bits-slot
+    table), an optional fact predicate, SUM of one column."""
+    d = sdb.SdbDim()
+    d.kind, d.width, d.n_rows = 2, 8, 1 << (hash_bits - 1)
+    d.n_pass, d.hash_bits, d.n_slots, d.sentinel = 1 << (hash_bits - 2), hash_bits, 1 << hash_bits, 0xFFFFFFFE
+    d.key_min, d.key_max = 0, (1 << (hash_bits - 1)) - 1
+    d.pass_key_min, d.pass_key_max = 0, 5                  # passing keys are not one range
+    d.n_payloads, d.payload_radix[0], d.payload_div[0], d.domain = 1, 65536, 1, 65536
+    d.map = 0x400000
+    q = sdb.SdbQuery()
+    q.n_fact, q.n_cols = n_fact, 3
+    for c in range(3):
+        q.cols[c] = 0x1000000 + c * 0x100000 + (0 if aligned else 4)
+    q.n_preds = n_preds
+    for i in range(n_preds):
+        q.preds[i] = sdb.SdbPred(2, 5, 1, 100)               # col 2 BETWEEN 1 AND 100
+    q.n_joins = 1
+    q.joins[0] = sdb.SdbJoin(0, C.pointer(d))
+    q.n_group_keys = 1
+    q.group_keys[0] = sdb.SdbGroupKey(0, 0)
+    q.agg = sdb.SdbAgg(agg_kind, 1, 2)
+    q.force_order, q.grid_blocks = 1, 256
+    return q, d
+
+
+def _run_status(q, p):
+    scratch = 0x10000000 if p.run_scratch_bytes else None
+    return sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
+                                        scratch, int(p.run_scratch_bytes), None)
+
+
+@pytest.mark.parametrize("force_slice,n_fact,hash_bits,agg_kind,aligned,sliced", [
+    (0, 600_000_000, 25, 0, True, True),      # c5's shape: a 256 MiB table, 600M rows
+    (0, 600_000_000, 20, 0, True, False),     # an 8 MiB table: probes mostly hit L2 anyway
+    (0, 1_000_000, 25, 0, True, False),       # too few rows to pay for the passes
+    (1, 1_000_000, 12, 0, True, True),        # forced on a small case
+    (1, 600_000_000, 25, 2, True, False),     # revenue - cost: records would need 64-bit values
+    (1, 600_000_000, 25, 0, False, False),    # the passes load 128 bits at a time
+    (-1, 600_000_000, 25, 0, True, False),
+])
+def test_sliced_probe_choice(force_slice, n_fact, hash_bits, agg_kind, aligned, sliced):
+    q, _d = _c5_like(n_fact, hash_bits, agg_kind=agg_kind, aligned=aligned)
+    q.force_slice = force_slice
+    p = sdb.SdbPlan()
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p)) == OK, sdb.lib().sdb_last_error()
+    check_plan(q, p)
+    assert bool(p.slice_bits) == sliced
+    if sliced:
+        assert p.stage_kind[p.slice_stage] == 1
+        # 2 MiB slices of the table
+        assert p.slice_bits == max(1, min(hash_bits + 3 - 21, hash_bits, 10))
+        assert p.vector == 1
+        assert p.slice_grid == min(256, -(-n_fact // 16384))
+    assert _run_status(q, p) in (OK, HIP_ERROR), sdb.lib().sdb_last_error()
+
+
+def test_sliced_plan_validation():
+    q, _d = _c5_like(600_000_000)
+    p = sdb.SdbPlan()
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p)) == OK
+    assert p.slice_bits == 7
+    good = bytes(p)
+    for field, value in [("slice_bits", 11), ("slice_bits", -1), ("slice_stage", 0), ("slice_stage", 5),
+                         ("slice_grid", 0), ("slice_grid", 257), ("slice_reserved", 1), ("eager", 1)]:
+        bad = sdb.SdbPlan.from_buffer_copy(good)
+        setattr(bad, field, value)
+        assert _run_status(q, bad) == INVALID_ARG, (field, value)
+    # a plan for one query is not valid for one the slices cannot serve
+    q2, _d2 = _c5_like(600_000_000, agg_kind=2)
+    assert _run_status(q2, sdb.SdbPlan.from_buffer_copy(good)) == INVALID_ARG
+    # too little scratch for the partitioned records
+    short = sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
+                                         0x10000000, int(p.run_scratch_bytes) - 256, None)
+    assert short == 4                                       # SDB_WORKSPACE_TOO_SMALL
