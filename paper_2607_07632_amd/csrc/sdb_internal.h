@@ -143,6 +143,8 @@ struct FusedParams {
     const int32_t* cols[SDB_MAX_FACT_COLS];
     int64_t n;
     const uint32_t* n_dev;     // non-null: rows are min(n, *n_dev) (a count another kernel wrote)
+    const int32_t* tile_map;   // non-null: loop index t runs tile tile_map[t] (< 0: none), t < n_vtiles
+    int64_t n_vtiles;
     int32_t nstages;
     int32_t agg_kind;
     int32_t agg_a;
@@ -280,6 +282,12 @@ struct SliceParams {
     uint32_t* chunk_start;     // n_parts + 1 entries (written by the shared scan, unused)
     int32_t* out_key;          // partitioned keys and values, all passing rows
     int32_t* out_val;
+    // tile order of the fused launch over them: its tiles of tile_rows rows;
+    // XCD x (x = q mod 8) walks the tiles whose first row lies in partition q
+    int64_t tile_rows;
+    uint32_t* tile_base;       // n_parts entries: rank of partition q's first tile among its XCD's tiles
+    int32_t* tile_map;         // n_vtiles entries: [8 * rank + x] = tile, -1 where XCD x has fewer tiles
+    int64_t n_vtiles;
 };
 
 // ---- launchers (sdb_kernels.hip) -----------------------------------------

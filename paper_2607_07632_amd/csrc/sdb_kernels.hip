@@ -1112,12 +1112,18 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
     const int64_t n_items = n_rows / W;
     const int64_t tile = (int64_t)blockDim.x * IPT;
     const int64_t n_tiles = (n_items + tile - 1) / tile;
-    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const int64_t n_loop = p.tile_map ? p.n_vtiles : n_tiles;
+    for (int64_t t = blockIdx.x; t < n_loop; t += gridDim.x) {
+        int64_t tt = t;
+        if (p.tile_map) {   // the sliced probe's XCD-aware tile order
+            tt = p.tile_map[t];
+            if (tt < 0) continue;
+        }
         int64_t item[IPT];
         bool al[IPT][W];
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
-            item[j] = t * tile + (int64_t)j * blockDim.x + threadIdx.x;
+            item[j] = tt * tile + (int64_t)j * blockDim.x + threadIdx.x;
 #pragma unroll
             for (int r = 0; r < W; ++r) al[j][r] = item[j] < n_items;
         }
@@ -1941,6 +1947,49 @@ __global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams 
     }
 }
 
+// The tile order of the fused launch over the partitioned rows. Loop index t
+// runs on block t mod grid, which the dispatcher places on XCD t mod 8 (the
+// grids here are multiples of 8); giving XCD x only the tiles whose first row
+// lies in a partition q with q mod 8 == x means each XCD's L2 holds the table
+// slices of its own partitions, and each slice is probed by one XCD's 32 CUs
+// for eight times as long, so the blocks drift apart by fewer slices.
+// One thread: the rank of each partition's first tile among its XCD's tiles.
+__global__ void slice_tile_base_kernel(SliceParams sp) {
+    if (blockIdx.x != 0 || threadIdx.x != 0) return;
+    const uint32_t P = 1u << sp.bits;
+    const uint64_t T = (uint64_t)sp.tile_rows;
+    uint64_t run[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (uint32_t q = 0; q < P; ++q) {
+        const uint64_t a = ((uint64_t)sp.part_start[q] + T - 1) / T;
+        const uint64_t b = ((uint64_t)sp.part_start[q + 1] + T - 1) / T;
+        sp.tile_base[q] = (uint32_t)run[q & 7u];
+        run[q & 7u] += b - a;
+    }
+}
+
+// One thread per tile j (first row j * tile_rows below the passing-row count):
+// its partition q (binary search of the partition starts), then its slot
+// 8 * rank + (q mod 8) in the map (filled with -1 before).
+__global__ void __launch_bounds__(256) slice_tile_map_kernel(SliceParams sp) {
+    const uint32_t P = 1u << sp.bits;
+    const uint64_t T = (uint64_t)sp.tile_rows;
+    const uint64_t total = sp.part_start[P];
+    const uint64_t n_phys = (total + T - 1) / T;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_phys; j += stride) {
+        const uint64_t row = j * T;
+        uint32_t lo = 0, hi = P;   // last partition whose start is <= row
+        while (hi - lo > 1u) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if ((uint64_t)sp.part_start[mid] <= row) lo = mid;
+            else hi = mid;
+        }
+        const uint64_t first = ((uint64_t)sp.part_start[lo] + T - 1) / T;
+        const uint64_t v = 8u * ((uint64_t)sp.tile_base[lo] + (j - first)) + (lo & 7u);
+        if (v < (uint64_t)sp.n_vtiles) sp.tile_map[v] = (int32_t)j;
+    }
+}
+
 size_t slice_scatter_lds_bytes(uint32_t n_parts) {
     return (size_t)kSliceChunk * 8u + (size_t)n_parts * 12u;
 }
@@ -1966,6 +2015,18 @@ hipError_t launch_slice_partition(const SliceParams& sp, int grid, hipStream_t s
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(slice_scatter_kernel, dim3(grid), dim3(kSliceBlock), slice_scatter_lds_bytes(P), s, sp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (sp.tile_map) {
+        e = launch_fill_u32(reinterpret_cast<uint32_t*>(sp.tile_map), (uint64_t)sp.n_vtiles, 0xFFFFFFFFu, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(slice_tile_base_kernel, dim3(1), dim3(64), 0, s, sp);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const uint64_t phys = (uint64_t)sp.n_vtiles / 8u;
+        const int g = (int)std::min<uint64_t>(1024u, std::max<uint64_t>(1u, (phys + 255u) / 256u));
+        hipLaunchKernelGGL(slice_tile_map_kernel, dim3(g), dim3(256), 0, s, sp);
+    }
     return hipGetLastError();
 }
 
