@@ -257,8 +257,11 @@ enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, 
  * probe key and aggregate value into 2^slice_bits partitions by the top
  * slice_bits bits of the key's 32-bit hash, which also selects the table
  * slice its home slot lies in; the fused kernel then runs the probe alone
- * over the partitioned records, partition after partition, so the slots it
- * reads at any time fit in L2. It needs one hash probe, all other stages fact
+ * over the partitioned records, each XCD taking the partitions q with
+ * q mod 8 equal to its index in turn (a tile map built after the count pass
+ * orders the kernel's tiles so; results do not depend on that order), so
+ * the slots one XCD reads at any time fit in its L2. The run scratch then
+ * holds 8 bytes per fact row for the partitioned keys and values. It needs one hash probe, all other stages fact
  * predicates, a one-column SUM, and the columns those passes read 16-byte
  * aligned. ipt, vector, eager (0), block, grid,
  * lds_bytes and the terminal fields describe that fused launch. */
