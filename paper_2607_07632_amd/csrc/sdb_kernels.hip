@@ -709,9 +709,13 @@ __device__ __forceinline__ void part_flush(const FusedParams& p, TermState<TERM_
         }
         const uint32_t pos = base + lane;
         if (pos < p.part_cap) {
-            ts.rgid[pos] = g;
-            if (p.rec_wide) static_cast<long long*>(ts.rval)[pos] = v;
-            else static_cast<int32_t*>(ts.rval)[pos] = (int32_t)v;
+            // non-temporal: the records are read back only by the scatter pass,
+            // so they should not take L2 lines from the lookup tables
+            // (measured: c5 13.85 -> 13.68 ms per run; the same hint on the
+            // scatter passes' stores made them slower)
+            __builtin_nontemporal_store(g, ts.rgid + pos);
+            if (p.rec_wide) __builtin_nontemporal_store((long long)v, static_cast<long long*>(ts.rval) + pos);
+            else __builtin_nontemporal_store((int32_t)v, static_cast<int32_t*>(ts.rval) + pos);
             atomicAdd(&ts.lhist[g >> p.part_shift], 1u);
         } else {
             atomicAdd(&p.sums[g], (unsigned long long)v);
