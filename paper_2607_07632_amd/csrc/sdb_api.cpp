@@ -1386,6 +1386,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         StageDev hs = p.st[ss];
         hs.col = 0;
         hs.eg_slot = -1;
+        hs.op = OP_HASH_PAIR;   // its slots are mostly in L2: fewer requests pay
         FusedParams p3;
         std::memset(&p3, 0, sizeof p3);
         p3.cols[0] = sp.out_key;

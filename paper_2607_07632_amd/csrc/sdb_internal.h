@@ -43,7 +43,8 @@ enum StageOp : int32_t {
     OP_LDS_RANK4 = 12,
     OP_COARSE1 = 13,    // coarse pass bitmap in LDS, then the device map, 1/2/4-byte codes
     OP_COARSE2 = 14,
-    OP_COARSE4 = 15
+    OP_COARSE4 = 15,
+    OP_HASH_PAIR = 16   // OP_HASH reading the home slot and the next with one 16-byte load
 };
 // How a table's code becomes part of the group id.
 enum GroupMode : int32_t { GK_NONE = 0, GK_ONE = 1, GK_GENERAL = 2 };

@@ -26,6 +26,8 @@ namespace sdb {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+typedef u64x2 __attribute__((aligned(8))) u64x2_a8;   // two adjacent 8-byte slots
 
 // ---------------------------------------------------------------------------
 // small helpers
@@ -900,7 +902,13 @@ __device__ __forceinline__ void stage_coarse(const StageDev& S, const unsigned c
     add_group<W, IPT>(S, c, gid);
 }
 
-template <int W, int IPT>
+// PAIR: the home slot and the next one come from one 16-byte load at 8-byte
+// alignment (global loads on gfx950 need 4-byte alignment only): one memory
+// request instead of two. Measured on c5, it pays when the slots are in L2,
+// as with the sliced probe (13.67 -> 13.15 ms per run), and not when they
+// come from HBM (16.13 -> 16.22 ms). The table's last slot, whose successor
+// is slot 0, still takes two loads, so no load reaches past the table.
+template <int W, int IPT, bool PAIR>
 __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)[IPT][W], bool (&al)[IPT][W],
                                            uint32_t (&gid)[IPT][W]) {
     // open addressing: first slots of two items in flight, then resolve
@@ -919,8 +927,14 @@ __device__ __forceinline__ void stage_hash(const StageDev& S, const int32_t (&x)
                 sn[jj][r] = 0ull;
                 if (al[j0 + jj][r]) {
                     // the home slot and the next one (mostly the same cache line)
-                    sl[jj][r] = tab[h[jj][r]];
-                    sn[jj][r] = tab[(h[jj][r] + 1u) & S.hmask];
+                    if (PAIR && h[jj][r] != S.hmask) {
+                        const u64x2 pr = *reinterpret_cast<const u64x2_a8*>(tab + h[jj][r]);
+                        sl[jj][r] = pr.x;
+                        sn[jj][r] = pr.y;
+                    } else {
+                        sl[jj][r] = tab[h[jj][r]];
+                        sn[jj][r] = tab[(h[jj][r] + 1u) & S.hmask];
+                    }
                 }
             }
 #pragma unroll
@@ -994,7 +1008,8 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
             case OP_MAP1: stage_map<W, IPT, 1, false>(S, lds, x, al, gid); break;
             case OP_MAP2: stage_map<W, IPT, 2, false>(S, lds, x, al, gid); break;
             case OP_MAP4: stage_map<W, IPT, 4, false>(S, lds, x, al, gid); break;
-            case OP_HASH: stage_hash<W, IPT>(S, x, al, gid); break;
+            case OP_HASH: stage_hash<W, IPT, false>(S, x, al, gid); break;
+            case OP_HASH_PAIR: stage_hash<W, IPT, true>(S, x, al, gid); break;
             case OP_LDS_RANK1: stage_rank<W, IPT, 1>(S, lds, x, al, gid); break;
             case OP_LDS_RANK2: stage_rank<W, IPT, 2>(S, lds, x, al, gid); break;
             case OP_LDS_RANK4: stage_rank<W, IPT, 4>(S, lds, x, al, gid); break;
