@@ -38,7 +38,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 6
+#define SDB_ABI_VERSION 7
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -197,7 +197,10 @@ typedef struct sdb_agg {
  *                  coarse bitmap of 2^k slots per bit fits in LDS
  *  force_slice     the hash probe over table slices (sdb_plan.slice_bits):
  *                  0: chosen by the planner; -1: never; 1: wherever the
- *                  query allows it */
+ *                  query allows it
+ *  force_unroll    the fused kernel with its stage loop written out
+ *                  (sdb_plan.unroll): 0: wherever the plan allows it; -1:
+ *                  never */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -221,6 +224,8 @@ typedef struct sdb_query {
     int32_t force_range;
     int32_t force_coarse;
     int32_t force_slice;
+    int32_t force_unroll;
+    int32_t reserved_;                    /* 0 */
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -301,7 +306,12 @@ typedef struct sdb_plan {
     int32_t slice_bits;                   /* 0: no sliced probe; else 1 .. SDB_MAX_SLICE_BITS */
     int32_t slice_stage;                  /* stage of the sliced hash probe (slice_bits > 0) */
     int32_t slice_grid;                   /* blocks of the count and scatter passes */
-    int32_t slice_reserved;               /* 0 */
+    int32_t unroll;                       /* 1: the fused kernel's instance with its stage loop
+                                             written out four times (stage parameters stay in
+                                             scalar registers across tiles); allowed for plans of
+                                             at most 4 stages, 4-row items, ipt 2, blocks of 512
+                                             or 1024, no eager loads and no hash-table probe;
+                                             0 otherwise */
 } sdb_plan;
 /* most partitions of the sliced hash probe: 2^SDB_MAX_SLICE_BITS */
 #define SDB_MAX_SLICE_BITS 10

@@ -15,6 +15,7 @@ constexpr int kMaxEager = SDB_MAX_EAGER;
 constexpr int kBlock = 256;              // default threads per block of the fused kernel
 constexpr int kMaxBlock = 512;           // launch bound of the fused kernel
 constexpr int kBigBlock = 1024;          // launch bound of its big-block instances (4-row items, IPT 1 or 2)
+constexpr int kUnrollStages = 4;         // stage copies of the fused kernel's unrolled instances
 constexpr int kLdsGroupLimit = 2048;     // LDS terminal: sums + counts of G <= 2048 groups (32 KB)
 constexpr int kLdsStageBudget = 32768;   // LDS bytes per block for staged dimension tables
 constexpr int kXcdCopies = 8;            // XCDs of an MI355X: private group-table copies
@@ -303,9 +304,12 @@ hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
                          unsigned long long* pass_counts, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if
 // the instance does not exist.
-int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, size_t lds_bytes);
-hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
-                        size_t lds_bytes, hipStream_t s);
+// `unroll`: the instance whose stage loop is written out kUnrollStages times
+// (plans of at most that many stages, 4-row items, 2 per lane, blocks of
+// kMaxBlock or kBigBlock, no eager loads).
+int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, int unroll, size_t lds_bytes);
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int unroll, int grid,
+                        int block, size_t lds_bytes, hipStream_t s);
 hipError_t launch_rank_build(const RankParams& rp, hipStream_t s);
 // kernel-at-a-time run of the stages and aggregate of p (device tables only)
 hipError_t launch_unfused(const FusedParams& p, uint8_t* flags, uint32_t* gid, hipStream_t s);

@@ -977,9 +977,42 @@ __device__ __forceinline__ bool wave_has_live(const bool (&al)[IPT][W]) {
     return __any(any) != 0;
 }
 
+// One stage of the plan for the current items: fetch its column, then apply
+// its predicate or lookup.
+template <int W, int IPT, bool EG>
+__device__ __forceinline__ void run_stage(const FusedParams& p, const unsigned char* lds, const StageDev& S,
+                                          const int64_t (&item)[IPT], bool (&al)[IPT][W], uint32_t (&gid)[IPT][W],
+                                          uint32_t (&didx)[IPT][W], const int32_t (&eg)[kMaxEager][IPT][W]) {
+    int32_t x[IPT][W];
+    fetch_column<W, IPT, EG>(p, S.col, S.eg_slot, item, al, eg, x);
+    switch (S.op) {
+        case OP_PRED:
+            SDB_ROWS(j, r) al[j][r] = al[j][r] && range_pass(S.test, x[j][r]);
+            break;
+        case OP_LDS_BITS: stage_bits<W, IPT>(S, lds, x, al, gid, didx); break;
+        case OP_LDS_MAP1: stage_map<W, IPT, 1, true>(S, lds, x, al, gid); break;
+        case OP_LDS_MAP2: stage_map<W, IPT, 2, true>(S, lds, x, al, gid); break;
+        case OP_LDS_MAP4: stage_map<W, IPT, 4, true>(S, lds, x, al, gid); break;
+        case OP_MAP1: stage_map<W, IPT, 1, false>(S, lds, x, al, gid); break;
+        case OP_MAP2: stage_map<W, IPT, 2, false>(S, lds, x, al, gid); break;
+        case OP_MAP4: stage_map<W, IPT, 4, false>(S, lds, x, al, gid); break;
+        case OP_HASH: stage_hash<W, IPT, false>(S, x, al, gid); break;
+        case OP_HASH_PAIR: stage_hash<W, IPT, true>(S, x, al, gid); break;
+        case OP_LDS_RANK1: stage_rank<W, IPT, 1>(S, lds, x, al, gid); break;
+        case OP_LDS_RANK2: stage_rank<W, IPT, 2>(S, lds, x, al, gid); break;
+        case OP_LDS_RANK4: stage_rank<W, IPT, 4>(S, lds, x, al, gid); break;
+        case OP_COARSE1: stage_coarse<W, IPT, 1>(S, lds, x, al, gid); break;
+        case OP_COARSE2: stage_coarse<W, IPT, 2>(S, lds, x, al, gid); break;
+        case OP_COARSE4: stage_coarse<W, IPT, 4>(S, lds, x, al, gid); break;
+        default:   // OP_NEVER
+            SDB_ROWS(j, r) al[j][r] = false;
+            break;
+    }
+}
+
 // Runs every stage and the terminal for IPT items of W rows each. All lanes
 // of the wave must call this together (the early exit is a wave-wide vote).
-template <int W, int IPT, int TERM, bool EG>
+template <int W, int IPT, int TERM, bool EG, int UNR = 0>
 __device__ __forceinline__ void process_items(const FusedParams& p, const unsigned char* lds,
                                               const int64_t (&item)[IPT], bool (&al)[IPT][W],
                                               TermState<TERM>& ts) {
@@ -992,33 +1025,19 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
     int32_t eg[kMaxEager][IPT][W];
     if constexpr (EG) load_eager<W, IPT>(p, item, al, eg);
 
-    for (int s = 0; s < p.nstages; ++s) {
-        if (!wave_has_live<W, IPT>(al)) return;     // no live row left in the wave
-        const StageDev& S = p.st[s];
-        int32_t x[IPT][W];
-        fetch_column<W, IPT, EG>(p, S.col, S.eg_slot, item, al, eg, x);
-        switch (S.op) {
-            case OP_PRED:
-                SDB_ROWS(j, r) al[j][r] = al[j][r] && range_pass(S.test, x[j][r]);
-                break;
-            case OP_LDS_BITS: stage_bits<W, IPT>(S, lds, x, al, gid, didx); break;
-            case OP_LDS_MAP1: stage_map<W, IPT, 1, true>(S, lds, x, al, gid); break;
-            case OP_LDS_MAP2: stage_map<W, IPT, 2, true>(S, lds, x, al, gid); break;
-            case OP_LDS_MAP4: stage_map<W, IPT, 4, true>(S, lds, x, al, gid); break;
-            case OP_MAP1: stage_map<W, IPT, 1, false>(S, lds, x, al, gid); break;
-            case OP_MAP2: stage_map<W, IPT, 2, false>(S, lds, x, al, gid); break;
-            case OP_MAP4: stage_map<W, IPT, 4, false>(S, lds, x, al, gid); break;
-            case OP_HASH: stage_hash<W, IPT, false>(S, x, al, gid); break;
-            case OP_HASH_PAIR: stage_hash<W, IPT, true>(S, x, al, gid); break;
-            case OP_LDS_RANK1: stage_rank<W, IPT, 1>(S, lds, x, al, gid); break;
-            case OP_LDS_RANK2: stage_rank<W, IPT, 2>(S, lds, x, al, gid); break;
-            case OP_LDS_RANK4: stage_rank<W, IPT, 4>(S, lds, x, al, gid); break;
-            case OP_COARSE1: stage_coarse<W, IPT, 1>(S, lds, x, al, gid); break;
-            case OP_COARSE2: stage_coarse<W, IPT, 2>(S, lds, x, al, gid); break;
-            case OP_COARSE4: stage_coarse<W, IPT, 4>(S, lds, x, al, gid); break;
-            default:   // OP_NEVER
-                SDB_ROWS(j, r) al[j][r] = false;
-                break;
+    if constexpr (UNR > 0) {
+        // the stage loop written out UNR times: each copy's stage parameters
+        // stay in scalar registers across tiles instead of being reloaded
+#pragma unroll
+        for (int s = 0; s < UNR; ++s) {
+            if (s >= p.nstages) break;
+            if (!wave_has_live<W, IPT>(al)) return;
+            run_stage<W, IPT, EG>(p, lds, p.st[s], item, al, gid, didx, eg);
+        }
+    } else {
+        for (int s = 0; s < p.nstages; ++s) {
+            if (!wave_has_live<W, IPT>(al)) return;
+            run_stage<W, IPT, EG>(p, lds, p.st[s], item, al, gid, didx, eg);
         }
     }
     if (!wave_has_live<W, IPT>(al)) return;
@@ -1079,7 +1098,7 @@ __device__ __forceinline__ void process_items(const FusedParams& p, const unsign
 // The kernel reads its parameters in place from the kernel-argument segment
 // (constant memory, scalar loads); indexing the by-value copy with a runtime
 // stage number could otherwise make the compiler copy it to scratch.
-template <int W, int IPT, int TERM, bool EG, int LB>
+template <int W, int IPT, int TERM, bool EG, int LB, int UNR = 0>
 __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args) {
     (void)kernel_args;
     const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -1146,7 +1165,7 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
 #pragma unroll
             for (int r = 0; r < W; ++r) al[j][r] = item[j] < n_items;
         }
-        process_items<W, IPT, TERM, EG>(p, lds, item, al, ts);
+        process_items<W, IPT, TERM, EG, UNR>(p, lds, item, al, ts);
     }
     if constexpr (W > 1) {
         // the last n mod W rows, one per lane, by the last block
@@ -1221,15 +1240,31 @@ hipError_t launch_xcd_merge(const unsigned long long* xtab, int copies, uint64_t
     return hipGetLastError();
 }
 
-template <int W, int IPT, int TERM, bool EG, int LB = kMaxBlock>
+template <int W, int IPT, int TERM, bool EG, int LB = kMaxBlock, int UNR = 0>
 static const void* fused_fn() {
-    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM, EG, LB>);
+    return reinterpret_cast<const void*>(&star_fused_kernel<W, IPT, TERM, EG, LB, UNR>);
 }
 
 // Instances: 4-row or 1-row items, 1/2/4 items per lane, every terminal;
 // eager column loads for 4-row items with 1 or 2 items per lane; blocks of
-// kBigBlock threads for 4-row items with 1 or 2 items per lane.
-static const void* pick_fused(int vector, int ipt, int terminal, int eager, int block) {
+// kBigBlock threads for 4-row items with 1 or 2 items per lane; the stage
+// loop written out kUnrollStages times for 4-row items, 2 items per lane,
+// blocks of kMaxBlock or kBigBlock and no eager loads.
+static const void* pick_fused(int vector, int ipt, int terminal, int eager, int block, int unroll) {
+    if (unroll) {
+        if (!vector || ipt != 2 || eager > 0) return nullptr;
+#define SDB_PICK_UNR(LBv)                                                                           \
+    if (block == LBv) {                                                                             \
+        if (terminal == TERM_SCALAR) return fused_fn<4, 2, TERM_SCALAR, false, LBv, kUnrollStages>(); \
+        if (terminal == TERM_LDS) return fused_fn<4, 2, TERM_LDS, false, LBv, kUnrollStages>();       \
+        if (terminal == TERM_GLOBAL) return fused_fn<4, 2, TERM_GLOBAL, false, LBv, kUnrollStages>(); \
+        if (terminal == TERM_PART) return fused_fn<4, 2, TERM_PART, false, LBv, kUnrollStages>();     \
+    }
+        SDB_PICK_UNR(kMaxBlock)
+        SDB_PICK_UNR(kBigBlock)
+#undef SDB_PICK_UNR
+        return nullptr;
+    }
 #define SDB_PICK(Wv, I, EGv, LBv)                                                        \
     if (ipt == I) {                                                                      \
         if (terminal == TERM_SCALAR) return fused_fn<Wv, I, TERM_SCALAR, EGv, LBv>();    \
@@ -1261,8 +1296,8 @@ static const void* pick_fused(int vector, int ipt, int terminal, int eager, int 
     return nullptr;
 }
 
-int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, size_t lds_bytes) {
-    const void* fn = pick_fused(vector, ipt, terminal, eager, block);
+int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block, int unroll, size_t lds_bytes) {
+    const void* fn = pick_fused(vector, ipt, terminal, eager, block, unroll);
     if (!fn) return -1;
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, block, lds_bytes) != hipSuccess)
@@ -1270,9 +1305,10 @@ int fused_blocks_per_cu(int vector, int ipt, int terminal, int eager, int block,
     return blocks;
 }
 
-hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int grid, int block,
-                        size_t lds_bytes, hipStream_t s) {
-    const void* fn = pick_fused(vector, ipt, terminal, eager, block);
+hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal, int eager, int unroll, int grid,
+                        int block, size_t lds_bytes, hipStream_t s) {
+    if (unroll && p.nstages > kUnrollStages) return hipErrorInvalidValue;
+    const void* fn = pick_fused(vector, ipt, terminal, eager, block, unroll);
     if (!fn) return hipErrorInvalidValue;
     void* args[] = {const_cast<FusedParams*>(&p)};
     return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);

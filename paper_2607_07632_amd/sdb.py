@@ -83,7 +83,7 @@ class SdbQuery(C.Structure):
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
                 ("force_block", i32), ("force_range", i32), ("force_coarse", i32),
-                ("force_slice", i32)]
+                ("force_slice", i32), ("force_unroll", i32), ("reserved_", i32)]
 
 
 class SdbPlan(C.Structure):
@@ -97,7 +97,7 @@ class SdbPlan(C.Structure):
                 ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
                 ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64),
-                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("slice_reserved", i32)]
+                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("unroll", i32)]
 
 
 STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan]
@@ -367,6 +367,7 @@ class StarQuery:
         q.force_range = int(force.get("range", 0))
         q.force_coarse = int(force.get("coarse", 0))
         q.force_slice = int(force.get("slice", 0))
+        q.force_unroll = int(force.get("unroll", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -497,7 +498,7 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
             "ipt": plan.ipt, "vector": plan.vector, "eager": plan.eager, "block": plan.block, "grid": plan.grid,
             "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
             "n_parts": plan.n_parts, "part_cap": int(plan.part_cap),
-            "slice_bits": plan.slice_bits, "slice_grid": plan.slice_grid,
+            "slice_bits": plan.slice_bits, "slice_grid": plan.slice_grid, "unroll": plan.unroll,
             "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}

@@ -38,7 +38,7 @@ def test_struct_layout_matches_binding():
     sizes = (C.c_int64 * 8)()
     assert L.sdb_struct_sizes(sizes, 8) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
-    assert L.sdb_abi_version() == 6
+    assert L.sdb_abi_version() == 7
 
 
 def test_status_strings():
@@ -235,6 +235,31 @@ def test_run_rejects_mismatched_plan_before_any_launch():
     p5 = sdb.SdbPlan.from_buffer_copy(p)
     p5.xcd_copies = 8                                     # copies need the global terminal
     assert L.sdb_run_star_query(C.byref(q), C.byref(p5), 0x1000, 0x2000, 100, None, 0, None) == 1
+    # the unrolled stage loop: only for the instance it exists for
+    p6 = sdb.SdbPlan.from_buffer_copy(p)
+    p6.unroll = 2
+    assert L.sdb_run_star_query(C.byref(q), C.byref(p6), 0x1000, 0x2000, 100, None, 0, None) == 1
+    if p.unroll:
+        p7 = sdb.SdbPlan.from_buffer_copy(p)
+        p7.ipt = 1                                        # no unrolled instance with one item per lane
+        assert L.sdb_run_star_query(C.byref(q), C.byref(p7), 0x1000, 0x2000, 100, None, 0, None) == 1
+
+
+def test_unroll_choice_and_validation():
+    d = _fake_dim()
+    q = _query([d], [(0, 0)])
+    assert _plan(q).unroll == 1                            # one dense probe, 4-row items, ipt 2, blocks of 512
+    q.force_unroll = -1
+    assert _plan(q).unroll == 0
+    q.force_ipt = 1
+    q.force_unroll = 0
+    assert _plan(q).unroll == 0                            # no unrolled instance for ipt 1
+    L = sdb.lib()
+    p = sdb.SdbPlan()
+    for field, bad in [("force_unroll", 1), ("force_unroll", -2), ("reserved_", 1)]:
+        qb = _query([d], [(0, 0)])
+        setattr(qb, field, bad)
+        assert L.sdb_plan_star_query(C.byref(qb), None, 0, None, C.byref(p)) == 1, (field, bad)
 
 
 def test_probe_as_key_range():

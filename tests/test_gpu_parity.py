@@ -63,6 +63,26 @@ def test_forced_plans_agree(name, force):
     assert_same(got.as_rows(), want, f"{name} {force}")
 
 
+@pytest.mark.parametrize("name", ["c1_scalar_scan", "c2_join_group", "c3_star3"])
+@pytest.mark.parametrize("terminal", ["auto", "scalar", "lds", "global", "part"])
+def test_unrolled_stage_loop_agrees(name, terminal):
+    # the instance with the stage loop written out against the loop, per terminal
+    if terminal == "scalar" and name != "c1_scalar_scan":
+        pytest.skip("scalar terminal needs a query without GROUP BY")
+    if terminal == "lds" and name == "c3_star3":
+        pytest.skip("375,000 groups do not fit the LDS terminal")
+    w = workload(name)
+    want = oracle_rows(w)
+    force = {} if terminal == "auto" else {"terminal": terminal}
+    got_u, qu = run_gpu(w, force=force)
+    got_l, ql = run_gpu(w, force={**force, "unroll": -1})
+    assert ql.plan_obj.unroll == 0
+    if terminal == "auto":
+        assert qu.plan_obj.unroll == 1
+    assert_same(got_u.as_rows(), want, f"{name} {terminal} unrolled")
+    assert_same(got_l.as_rows(), want, f"{name} {terminal} loop")
+
+
 @pytest.mark.parametrize("mode", ["per_operator", "global_handoff"])
 @pytest.mark.parametrize("name", list(SIZES))
 def test_baselines_agree(name, mode):

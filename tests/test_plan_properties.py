@@ -98,6 +98,7 @@ def queries(draw):
     q.force_range = draw(st.sampled_from([-1, 0, 1]))
     q.force_coarse = draw(st.integers(-1, 5))
     q.force_slice = draw(st.sampled_from([-1, 0, 1, 1]))
+    q.force_unroll = draw(st.sampled_from([-1, 0, 0]))
     return q, ds
 
 
@@ -157,7 +158,12 @@ def check_plan(q, p):
         assert p.run_scratch_bytes >= 8 * q.n_fact + 4 * p.slice_grid * (1 << p.slice_bits)
     else:
         assert not (sliceable and q.force_slice == 1)
-    assert p.slice_reserved == 0
+    # the unrolled stage loop: exactly where its instance exists and no hash
+    # table is probed, unless turned off
+    hash_probe = any(q.joins[p.stage_index[s]].dim.contents.kind == 2 for s in join_probe)
+    can_unroll = (p.vector == 1 and p.ipt == 2 and p.eager == 0 and p.block in (512, 1024) and n <= 4 and
+                  not p.slice_bits and not hash_probe)
+    assert p.unroll == (1 if can_unroll and q.force_unroll != -1 else 0)
 
 
 @settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.too_slow])
@@ -283,7 +289,7 @@ def test_sliced_plan_validation():
     assert p.slice_bits == 7
     good = bytes(p)
     for field, value in [("slice_bits", 11), ("slice_bits", -1), ("slice_stage", 0), ("slice_stage", 5),
-                         ("slice_grid", 0), ("slice_grid", 257), ("slice_reserved", 1), ("eager", 1)]:
+                         ("slice_grid", 0), ("slice_grid", 257), ("unroll", 1), ("eager", 1)]:
         bad = sdb.SdbPlan.from_buffer_copy(good)
         setattr(bad, field, value)
         assert _run_status(q, bad) == INVALID_ARG, (field, value)
