@@ -130,7 +130,8 @@ ABLATION_RUNGS = [
     ("+ per-XCD group tables", {"lds": 2, "ipt": 2, "terminal": "global", "block": 256} | _NR),
     ("+ probes of one contiguous passing key range run as BETWEEN", {"lds": 2, "ipt": 2, "terminal": "global",
                                                                      "block": 256, "range": 1, "slice": -1}),
-    ("planner's choice (terminal, block size, rank tables)", {"slice": -1}),
+    ("planner's choice (terminal, block size, rank tables)", {"slice": -1, "unroll": -1}),
+    ("+ stage loop written out (plans without a hash probe)", {"slice": -1}),
     ("+ a hash probe over 2 MiB table slices (planner's choice)", {}),
 ]
 
