@@ -15,5 +15,4 @@ from .star import (  # noqa: F401
     OracleResult,
     star_query,
     eval_pred,
-    checksum61,
 )

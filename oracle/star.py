@@ -35,10 +35,6 @@ from dataclasses import dataclass
 
 import numpy as np
 
-P61 = (1 << 61) - 1
-_MIX = 0x9E3779B97F4A7C15
-
-
 class DuplicateKeyError(ValueError):
     """A dimension table holds the same key in more than one row."""
 
@@ -178,19 +174,3 @@ def star_query(fact: dict, dims: dict, dim_keys: dict, query: dict) -> OracleRes
     counts = np.bincount(inverse, minlength=uniq.shape[0]).astype(np.int64)
     return OracleResult(uniq.astype(np.int64), sums.view(np.int64), counts, int(rows.size))
 
-
-def checksum61(result: OracleResult) -> int:
-    """One 64-bit summary of a result, for logs only (parity compares whole tables).
-
-    The paper reduces a grouped result to a key-binding per-group checksum
-    modulo 2**61-1 without defining it (Section 2.2); this reading packs each
-    key tuple into 32-bit fields, mixes it, and weights the group's sum by it.
-    """
-    c = 0
-    for k, s, _ in result.as_rows():
-        pack = 0
-        for i, x in enumerate(k):
-            pack = (pack + ((x & 0xFFFFFFFF) << (32 * i))) % P61
-        w = (pack * _MIX + 1) % P61
-        c = (c + w * (s % P61)) % P61
-    return c
