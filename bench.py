@@ -12,11 +12,18 @@ date_key, revenue), customer 3M / supplier 200k / date 2556 rows, SUM(revenue)
 GROUP BY (customer city, supplier city, year).
 
 Prints one JSON line. `value` = fact rows per second of the whole step.
-`roofline` rates the fused kernel: fact-column bytes (4 bytes x distinct fact
-columns x rows) over its mean duration, timed with HIP events that the library
-records on the kernel's stream right around its launch (`run_ms` also covers
-the output fill and any terminal passes). `cpu_baseline` times the CPU oracle (numpy, one thread) on the first
-rows of the same workload; the GPU result on those rows is compared with it.
+`roofline` rates the fused kernel on B_alg, the fact-column bytes the method
+must move at 128-byte line granularity (4 bytes per column times the fraction
+of lines holding a row still live where the plan first reads that column,
+measured on the first rows of the same data), over its mean duration timed
+with HIP events that the library records on the kernel's stream right around
+its launch; `frac_b_dense` rates it on all fact-column bytes, and
+`frac_run_window` rates the whole run (output fill, fused kernel, terminal
+passes). `cpu_baseline` times the CPU oracle over the whole fact table on one
+worker process per host core (at most 16), and the full GPU result is compared
+with it group by group. `configs` holds a compact record of each other
+workload (run and kernel times, roofline fractions, oracle parity over its
+whole fact table).
 """
 
 from __future__ import annotations
@@ -345,34 +352,136 @@ def copy_calibration(dev) -> None:
     log("[bench] copy calibration: 3 x 1 GiB device-to-device copies done")
 
 
-def cpu_baseline_leg(sdb, fact, wdims, query, force, build_tables, args, n, plan_info, kernel_ms) -> dict:
-    """The oracle timed on the first rows of the same workload (one thread),
-    the GPU compared with it bit for bit on those rows, and B_alg from them."""
-    import oracle
-    m = min(args.cpu_rows, n)
-    sample = {k: v[:m].cpu().numpy() for k, v in fact.items()}
-    t0 = time.perf_counter()
-    ref = oracle.star_query(sample, wdims.dims, wdims.dim_keys, query)
-    t_oracle = time.perf_counter() - t0
-    qs = sdb.StarQuery({k: v[:m] for k, v in fact.items()}, build_tables(), query, force)
-    parity = qs.execute().as_rows() == ref.as_rows()
-    b_alg = b_alg_per_row(sample, wdims.dims, wdims.dim_keys, query, plan_info)
-    log(f"[bench] oracle {m} rows in {t_oracle:.1f} s; GPU result on the sample "
-        f"{'equals' if parity else 'DIFFERS FROM'} the oracle")
+def host_sample(fact: dict, rows: int) -> dict:
+    """The first ``rows`` rows of every device column, on the host."""
+    return {k: v[:rows].cpu().numpy() for k, v in fact.items()}
+
+
+def device_column_sums(fact: dict) -> dict:
+    import torch
+    return {k: int(v.sum(dtype=torch.int64).item()) for k, v in fact.items()}
+
+
+def cpu_baseline_leg(cfg_name: str, n: int, gpu_rows: list, fact: dict) -> dict:
+    """The oracle over all n fact rows, one row range per worker process (one
+    per host core, at most 16), the oracle phases started together once every
+    worker has generated its rows; the full GPU result compared with it group
+    by group, and the workers' column sums with the device columns'."""
+    from oracle import ranges
+    workers = ranges.worker_count()
+    res, col_sums, info = ranges.run_timed(cfg_name, n, workers)
+    same_rows = col_sums == device_column_sums(fact)
+    parity = same_rows and gpu_rows == res.as_rows()
+    per_core = n / sum(info["worker_oracle_s"])
+    log(f"[bench] oracle over all {n} rows on {info['workers']} processes: {info['wall_s']:.1f} s "
+        f"(merge {info['merge_s']:.1f} s); the full GPU result {'equals' if parity else 'DIFFERS FROM'} it")
     return {
         "cpu_baseline": {
-            "value": m / t_oracle,
+            "value": n / info["wall_s"],
             "unit": "fact rows/s",
-            "cores": 1,
+            "cores": info["workers"],
             "kind": "oracle",
-            "sample": f"first {m} of {n} fact rows of {args.config}, full dimension tables; "
-                      f"numpy oracle, one thread, {t_oracle:.1f} s",
+            "sample": f"all {n} fact rows of {cfg_name} and its full dimension tables: the numpy oracle "
+                      f"on {info['workers']} row ranges, one worker process each, merged group by group; "
+                      f"{info['wall_s']:.1f} s wall clock from the first range's start to the merge's end "
+                      f"(generation excluded)",
             "cpu": cpu_model(),
+            "host_cores_in_affinity": len(os.sched_getaffinity(0)),
+            "rows_per_s_per_core": per_core,
         },
-        "parity_on_cpu_sample": parity,
-        "b_alg_bytes_per_row": b_alg,
-        "b_alg_GBps_fused": n * b_alg / (kernel_ms * 1e-3) / 1e9,
+        "parity_full_table": parity,
+        "parity_detail": {"groups": len(gpu_rows), "oracle_groups": len(res.sums),
+                          "oracle_live_rows": int(res.n_live), "oracle_saw_device_rows": same_rows},
     }
+
+
+def config_record(sdb, name: str, ex, dev, runs: int = 10, balg_rows: int = 16_000_000,
+                  parity_rows: int = 1 << 27) -> dict:
+    """One workload measured compactly: table builds, the run window and the
+    fused kernel (HIP events), roofline fractions on B_alg and B_dense, and the
+    GPU result against the oracle over the first min(N, parity_rows) fact rows
+    (the whole table for c1 and c2; the full-size tests compare all 600M rows
+    of c4 and c5)."""
+    import numpy as np
+    import torch
+    import datagen
+    from datagen.star import CHUNK, CONFIGS
+    cfg = CONFIGS[name]
+    n = cfg.n_fact
+    log(f"[bench] {name}: {n} fact rows")
+    fact = upload_fact(name, n, dev)
+    w = datagen.make_workload(name, n_fact=0)
+    dims = {d: {c: torch.from_numpy(a).to(dev) for c, a in t.items()} for d, t in w.dims.items()}
+    query = w.query
+    stream = torch.cuda.current_stream()
+    build_ms = []
+    for _ in range(4):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        tabs = sdb.build_dims(dims, w.dim_keys, query)
+        torch.cuda.synchronize()
+        build_ms.append(1000.0 * (time.perf_counter() - t0))
+    q = sdb.StarQuery(fact, tabs, query)
+    plan = q.plan()
+    sums, counts = q.alloc_outputs(plan)
+    scratch = q.run_scratch(plan)
+    for _ in range(2):
+        q.run(sums, counts, plan=plan, scratch=scratch)
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(runs)]
+    torch.cuda.synchronize()
+    for ev in evs:
+        sdb.set_fused_events(ev[0], ev[1])
+        ev[2].record(stream)
+        q.run(sums, counts, plan=plan, scratch=scratch)
+        ev[3].record(stream)
+    sdb.set_fused_events()
+    torch.cuda.synchronize()
+    kernel_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    run_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    got = q.execute(replan=False).as_rows()
+    info = sdb.plan_summary(plan, query)
+    b_dense = 4 * int(q.q.n_cols)
+    b_alg = b_alg_per_row(host_sample(fact, min(n, balg_rows)), w.dims, w.dim_keys, query, info)
+    parity = same_rows = None
+    m = min(n, parity_rows)
+    if ex is not None:
+        from oracle import ranges
+        t0 = time.perf_counter()
+        head = {k: v[:m] for k, v in fact.items()}
+        got_m = got if m == n else sdb.StarQuery(head, tabs, query).execute().as_rows()
+        want, col_sums = ranges.run(name, m, ex, 2 * CHUNK)
+        same_rows = col_sums == device_column_sums(head)
+        parity = same_rows and got_m == want.as_rows()
+        log(f"[bench] {name}: oracle over the first {m} rows in {time.perf_counter() - t0:.1f} s: "
+            f"{'equal' if parity else 'DIFFERENT'}")
+    log(f"[bench] {name}: fused {kernel_ms:.4f} ms, run {run_ms:.4f} ms, builds {min(build_ms):.3f} ms")
+    rec = {
+        "workload": f"{name}: {cfg.describe}",
+        "fact_rows": n,
+        "plan": info,
+        "runs": runs,
+        "fused_kernel_ms": kernel_ms,
+        "run_ms": run_ms,
+        "build_ms_min": min(build_ms),
+        "run_rows_per_s": n / (run_ms * 1e-3),
+        "b_dense_bytes_per_row": b_dense,
+        "b_alg_bytes_per_row": b_alg,
+        "frac_b_alg_fused": n * b_alg / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "frac_b_alg_run_window": n * b_alg / (run_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "frac_b_dense_fused": n * b_dense / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "groups": len(got),
+        "oracle_parity": parity,
+        "oracle_parity_rows": m if ex is not None else 0,
+        "oracle_saw_device_rows": same_rows,
+    }
+    if plan.slice_bits:
+        rec["fused_window_covers"] = "count pass + scatter pass + fused kernel (hash probe over table slices)"
+    if any(sdb.dim_info(t)["kind"] == "hash" for t in tabs):
+        rec["probes_per_s_run"] = n / (run_ms * 1e-3)
+        rec["build_reported_separately"] = True
+    del fact, q, sums, counts, scratch, tabs
+    torch.cuda.empty_cache()
+    return rec
 
 
 def main(argv=None) -> int:
@@ -382,8 +491,11 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c3_star3")
     ap.add_argument("--rows", type=int, default=None, help="fact rows (default: the workload's size)")
-    ap.add_argument("--cpu-rows", type=int, default=40_000_000, help="oracle sample rows")
-    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
+    ap.add_argument("--balg-rows", type=int, default=40_000_000,
+                    help="first fact rows on which B_alg (line-granular algorithmic bytes) is measured")
+    ap.add_argument("--no-cpu", action="store_true",
+                    help="skip the oracle leg (CPU baseline and every comparison with the oracle)")
+    ap.add_argument("--no-configs", action="store_true", help="skip the compact records of the other workloads")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (scale for HBM byte counters)")
     ap.add_argument("--force", default="", help="planner overrides, e.g. ipt=4,vector=1,terminal=global")
@@ -395,6 +507,11 @@ def main(argv=None) -> int:
         print(f"bench.py runs on one GPU only: the path needs no collective, and --gpus {args.gpus} "
               "is not supported (see the sharding plan in the design notes)", file=sys.stderr)
         return 2
+
+    if not args.no_cpu:
+        # the oracle's worker processes fork from a server started before any GPU call
+        from oracle import ranges
+        ranges.start_forkserver()
 
     import numpy as np
     import torch
@@ -526,9 +643,12 @@ def main(argv=None) -> int:
     rows_per_s = n / (t_total / max(args.steps, 1))
     fact_cols = int(q0.q.n_cols)
     b_dense_per_row = 4 * fact_cols
-    achieved = n * b_dense_per_row / (kernel_ms_mean * 1e-3) / 1e9
     traffic = traffic_from_profile(args.config)
     plan_info = sdb.plan_summary(plan, query)
+    balg_rows = min(n, args.balg_rows)
+    b_alg = b_alg_per_row(host_sample(fact, balg_rows), wdims.dims, wdims.dim_keys, query, plan_info)
+    achieved = n * b_alg / (kernel_ms_mean * 1e-3) / 1e9
+    achieved_dense = n * b_dense_per_row / (kernel_ms_mean * 1e-3) / 1e9
     log(f"[bench] plan {json.dumps(plan_info)}")
     log(f"[bench] fused kernel mean {kernel_ms_mean:.4f} ms (min {min(kernel_ms):.4f}, "
         f"max {max(kernel_ms):.4f}); run {run_ms_mean:.4f} ms; step {ms_per_step:.4f} ms; groups {n_groups_out}")
@@ -573,9 +693,16 @@ def main(argv=None) -> int:
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
-            "bytes_basis": f"{b_dense_per_row} B/row fact-column bytes x {n} rows per launch",
+            "bytes_basis": f"B_alg {b_alg:.4f} B/row (4 B per fact column x fraction of 128-byte lines holding "
+                           f"a row live where the plan first reads the column, measured on the first "
+                           f"{balg_rows} rows) x {n} rows per launch",
+            "frac_b_dense": achieved_dense / HBM_PEAK_GBPS,
+            "b_dense_basis": f"{b_dense_per_row} B/row: every byte of the {fact_cols} fact columns",
+            "frac_run_window": n * b_alg / (run_ms_mean * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "run_window": "output fill + fused kernel + terminal passes (t_query), B_alg basis",
         },
         "cpu_baseline": None,
+        "b_alg_bytes_per_row": b_alg,
     }
     if traffic:
         # measured HBM bytes per launch (profiles/) over the kernel's time: the
@@ -605,8 +732,27 @@ def main(argv=None) -> int:
         copy_calibration(dev)
 
     if not args.no_cpu:
-        result.update(cpu_baseline_leg(sdb, fact, wdims, query, force, build_tables, args, n, plan_info,
-                                       kernel_ms_mean))
+        q0.run(sums, counts, plan=plan)
+        k, s_, c, nout, _ = q0.finalize(sums, counts, plan=plan, outputs=fin_out)
+        torch.cuda.synchronize()
+        m = int(nout.item())
+        keys = k[:m, :q0.n_keys].to(torch.int64).cpu().numpy()
+        gpu_rows = sdb.QueryResult(keys.reshape(m, q0.n_keys), s_[:m].cpu().numpy(), c[:m].cpu().numpy()).as_rows()
+        result.update(cpu_baseline_leg(args.config, n, gpu_rows, fact))
+
+    if not args.no_configs and args.rows is None and args.config == "c3_star3":
+        del fact, slots, sums, counts, fin_out, q0
+        torch.cuda.empty_cache()
+        ex = None
+        if not args.no_cpu:
+            from oracle import ranges
+            ex = ranges.pool(ranges.worker_count())
+        try:
+            result["configs"] = [config_record(sdb, name, ex, dev)
+                                 for name in ("c1_scalar_scan", "c2_join_group", "c4_star4_zipf", "c5_hash_stress")]
+        finally:
+            if ex is not None:
+                ex.shutdown()
 
     print(json.dumps(result), flush=True)
     return 0

@@ -38,7 +38,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 7
+#define SDB_ABI_VERSION 8
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -151,6 +151,33 @@ typedef struct sdb_dim {
     void* stats;                  /* device, inside the workspace */
     void* bits;                   /* DENSE: device pass bitmap inside the workspace; HASH: NULL */
 } sdb_dim;
+
+/* What a built lookup table holds, as sdb_dim_info reports it: the layout the
+ * build chose (Section 4.3: the key-range check picks a direct-mapped map or
+ * falls back to a hash table) and the ranges the plan derives group radices
+ * from (Section 4.3: the group table is sized from the payload domains). */
+typedef struct sdb_dim_summary {
+    int32_t kind;                 /* SDB_TABLE_DENSE or SDB_TABLE_HASH */
+    int32_t width;                /* bytes per map entry (1, 2, 4) or per hash slot (8) */
+    int64_t n_rows;
+    int64_t n_pass;               /* rows that pass the dimension predicates */
+    int32_t key_min;              /* over all rows (0 and -1 when there are none) */
+    int32_t key_max;
+    int32_t pass_key_min;         /* over passing rows (0 and -1 when none pass) */
+    int32_t pass_key_max;
+    int32_t pass_keys_contiguous; /* 1: the passing keys are exactly pass_key_min..pass_key_max
+                                     (the table can be probed as a key range) */
+    int32_t n_payloads;
+    uint64_t n_slots;             /* map entries (key range) or hash slots */
+    uint64_t table_bytes;         /* device bytes the lookup table occupies in the workspace:
+                                     map plus pass bitmap, or hash slots */
+    double occupancy;             /* n_rows / n_slots (a hash table's load factor); 0 without slots */
+    int32_t payload_min[SDB_MAX_PAYLOADS];     /* over passing rows */
+    int32_t payload_max[SDB_MAX_PAYLOADS];     /* payload_min + radix - 1 */
+    uint32_t payload_radix[SDB_MAX_PAYLOADS];
+    int32_t reserved_;
+    uint64_t domain;              /* product of the payload radices: distinct codes */
+} sdb_dim_summary;
 
 typedef struct sdb_join {
     int32_t fact_key_col;         /* index into sdb_query.cols[] */
@@ -329,8 +356,9 @@ SDB_API const char* sdb_status_string(int32_t status);
 SDB_API int32_t sdb_abi_version(void);
 
 /* Writes sizeof of sdb_pred, sdb_dim_desc, sdb_dim, sdb_join, sdb_group_key,
- * sdb_agg, sdb_query, sdb_plan (in that order) to sizes[0..n-1], n <= 8, so a
- * binding can check its struct layout. Host only. */
+ * sdb_agg, sdb_query, sdb_plan, sdb_dim_summary (in that order) to
+ * sizes[0..n-1], n <= 9, so a binding can check its struct layout. Host
+ * only. */
 SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n);
 
 /* ---- dimension build (separate from the fused pass, Section 4.2) ------- */
@@ -365,6 +393,15 @@ SDB_API sdb_status sdb_build_dim(const sdb_dim_desc* desc, void* workspace,
  * outputs are then undefined. Errors: as sdb_build_dim. */
 SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, void* const* workspaces,
                                   const int64_t* workspace_bytes, void* stream, sdb_dim* outs);
+
+/* Host only. Describes the table `dim` (a handle sdb_build_dim or
+ * sdb_build_dims filled) in `out` (host): its layout, key ranges, pass count
+ * and payload domains, without touching the device (Sections 3.3 and 4.3:
+ * the direct-mapped or hash layout a build chose, and the domains the group
+ * table is sized from). Errors: INVALID_ARG (null pointer, or a handle whose
+ * fields contradict each other: unknown kind, a width or slot count the
+ * kind does not allow, a pass count above the row count, a missing map). */
+SDB_API sdb_status sdb_dim_info(const sdb_dim* dim, sdb_dim_summary* out);
 
 /* ---- planning ----------------------------------------------------------- */
 

@@ -930,11 +930,12 @@ SDB_API const char* sdb_status_string(int32_t s) {
 SDB_API int32_t sdb_abi_version(void) { return SDB_ABI_VERSION; }
 
 SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n) {
-    if (!sizes || n < 0 || n > 8) return fail(SDB_INVALID_ARG, "sizes must hold 0..8 entries");
-    const int64_t all[8] = {(int64_t)sizeof(sdb_pred),  (int64_t)sizeof(sdb_dim_desc),
+    if (!sizes || n < 0 || n > 9) return fail(SDB_INVALID_ARG, "sizes must hold 0..9 entries");
+    const int64_t all[9] = {(int64_t)sizeof(sdb_pred),  (int64_t)sizeof(sdb_dim_desc),
                             (int64_t)sizeof(sdb_dim),   (int64_t)sizeof(sdb_join),
                             (int64_t)sizeof(sdb_group_key), (int64_t)sizeof(sdb_agg),
-                            (int64_t)sizeof(sdb_query), (int64_t)sizeof(sdb_plan)};
+                            (int64_t)sizeof(sdb_query), (int64_t)sizeof(sdb_plan),
+                            (int64_t)sizeof(sdb_dim_summary)};
     for (int i = 0; i < n; ++i) sizes[i] = all[i];
     return ok();
 }
@@ -1080,6 +1081,60 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
                         d, (unsigned long long)fin.occupied, (long long)descs[d].n_rows);
         if (fin.dup) return fail(SDB_HIP_ERROR, "dimension %d: build inconsistency (flag %u)", d, fin.dup);
     }
+    return ok();
+}
+
+SDB_API sdb_status sdb_dim_info(const sdb_dim* dim, sdb_dim_summary* out) {
+    if (!dim || !out) return fail(SDB_INVALID_ARG, "null argument");
+    const sdb_dim& d = *dim;
+    if (d.kind != SDB_TABLE_DENSE && d.kind != SDB_TABLE_HASH)
+        return fail(SDB_INVALID_ARG, "handle kind %d is neither DENSE nor HASH", d.kind);
+    if (d.n_rows < 0 || d.n_pass < 0 || d.n_pass > d.n_rows)
+        return fail(SDB_INVALID_ARG, "handle counts %lld passing of %lld rows", (long long)d.n_pass,
+                    (long long)d.n_rows);
+    if (d.n_payloads < 0 || d.n_payloads > SDB_MAX_PAYLOADS)
+        return fail(SDB_INVALID_ARG, "handle has %d payloads", d.n_payloads);
+    uint64_t table_bytes = 0;
+    if (d.kind == SDB_TABLE_DENSE) {
+        if (d.width != 1 && d.width != 2 && d.width != 4)
+            return fail(SDB_INVALID_ARG, "dense handle with entry width %d", d.width);
+        const uint64_t range = d.n_rows > 0 ? (uint64_t)((int64_t)d.key_max - (int64_t)d.key_min + 1) : 0;
+        if (d.n_slots != range) return fail(SDB_INVALID_ARG, "dense handle: %llu slots for a key range of %llu",
+                                            (unsigned long long)d.n_slots, (unsigned long long)range);
+        if (d.n_slots > 0 && (!d.map || !d.bits)) return fail(SDB_INVALID_ARG, "dense handle without its map");
+        table_bytes = dense_bytes(d.n_slots, d.width);
+    } else {
+        if (d.width != 8 || d.hash_bits < 1 || d.hash_bits > 32 || d.n_slots != (1ull << d.hash_bits))
+            return fail(SDB_INVALID_ARG, "hash handle: width %d, %llu slots, hash_bits %d", d.width,
+                        (unsigned long long)d.n_slots, d.hash_bits);
+        if (!d.map) return fail(SDB_INVALID_ARG, "hash handle without its slots");
+        table_bytes = d.n_slots * 8ull;
+    }
+    sdb_dim_summary o;
+    std::memset(&o, 0, sizeof o);
+    o.kind = d.kind;
+    o.width = d.width;
+    o.n_rows = d.n_rows;
+    o.n_pass = d.n_pass;
+    o.key_min = d.key_min;
+    o.key_max = d.key_max;
+    o.pass_key_min = d.pass_key_min;
+    o.pass_key_max = d.pass_key_max;
+    o.pass_keys_contiguous =
+        d.n_pass > 0 && (int64_t)d.pass_key_max - (int64_t)d.pass_key_min + 1 == d.n_pass ? 1 : 0;
+    o.n_payloads = d.n_payloads;
+    o.n_slots = d.n_slots;
+    o.table_bytes = table_bytes;
+    o.occupancy = d.n_slots > 0 ? (double)d.n_rows / (double)d.n_slots : 0.0;
+    uint64_t domain = 1;
+    for (int p = 0; p < d.n_payloads; ++p) {
+        o.payload_min[p] = d.payload_min[p];
+        o.payload_radix[p] = d.payload_radix[p];
+        o.payload_max[p] = (int32_t)((int64_t)d.payload_min[p] + (int64_t)d.payload_radix[p] - 1);
+        domain *= d.payload_radix[p];
+    }
+    o.domain = domain;
+    *out = o;
     return ok();
 }
 

@@ -62,6 +62,15 @@ class SdbDim(C.Structure):
                 ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp), ("bits", vp)]
 
 
+class SdbDimSummary(C.Structure):
+    _fields_ = [("kind", i32), ("width", i32), ("n_rows", i64), ("n_pass", i64),
+                ("key_min", i32), ("key_max", i32), ("pass_key_min", i32), ("pass_key_max", i32),
+                ("pass_keys_contiguous", i32), ("n_payloads", i32), ("n_slots", u64), ("table_bytes", u64),
+                ("occupancy", C.c_double), ("payload_min", i32 * MAX_PAYLOADS),
+                ("payload_max", i32 * MAX_PAYLOADS), ("payload_radix", u32 * MAX_PAYLOADS),
+                ("reserved_", i32), ("domain", u64)]
+
+
 class SdbJoin(C.Structure):
     _fields_ = [("fact_key_col", i32), ("dim", C.POINTER(SdbDim))]
 
@@ -100,7 +109,7 @@ class SdbPlan(C.Structure):
                 ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("unroll", i32)]
 
 
-STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan]
+STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan, SdbDimSummary]
 
 # exported symbol -> (restype, argtypes)
 SIGNATURES = {
@@ -111,6 +120,7 @@ SIGNATURES = {
     "sdb_dim_required_bytes": (i32, [C.POINTER(SdbDimDesc), C.POINTER(i64)]),
     "sdb_build_dim": (i32, [C.POINTER(SdbDimDesc), vp, i64, vp, C.POINTER(SdbDim)]),
     "sdb_build_dims": (i32, [i32, C.POINTER(SdbDimDesc), C.POINTER(vp), C.POINTER(i64), vp, C.POINTER(SdbDim)]),
+    "sdb_dim_info": (i32, [C.POINTER(SdbDim), C.POINTER(SdbDimSummary)]),
     "sdb_set_fused_events": (i32, [vp, vp]),
     "sdb_read_columns": (i32, [C.POINTER(vp), i32, i64, i32, vp, vp]),
     "sdb_baseline_scratch_bytes": (i32, [i64, C.POINTER(i64)]),
@@ -171,6 +181,27 @@ def _ptr(t) -> int | None:
     return None if t is None else (t.data_ptr() or None)
 
 
+def check_column(t, what: str, n: int | None = None, device=None, dtype: str = "int32") -> None:
+    """Raises ValueError unless ``t`` is a one-dimensional contiguous torch
+    tensor of ``dtype`` on the GPU (on ``device`` and of ``n`` elements when
+    given): the library reads it through a raw device pointer as a dense array."""
+    import torch
+    want = {"int32": torch.int32, "int64": torch.int64, "uint8": torch.uint8}[dtype]
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what} must be a torch tensor, not {type(t).__name__}")
+    if t.dtype != want:
+        raise ValueError(f"{what} must be {dtype}, not {t.dtype}")
+    if t.dim() != 1 or not t.is_contiguous():
+        raise ValueError(f"{what} must be a one-dimensional contiguous tensor "
+                         f"(shape {tuple(t.shape)}, strides {t.stride()})")
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be on the GPU, not {t.device}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{what} is on {t.device}, the other inputs on {device}")
+    if n is not None and t.numel() != n:
+        raise ValueError(f"{what} has {t.numel()} elements, {n} expected")
+
+
 def _pred(p: dict, col_index: dict) -> SdbPred:
     if p["op"] not in OPS:
         raise ValueError(f"unknown predicate op {p['op']!r}")
@@ -206,10 +237,10 @@ def dim_desc(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
     """The C descriptor of one dimension: ``key`` and the values of ``cols``
     are int32 device tensors of equal length; ``preds`` are predicate dicts
     naming columns of ``cols``; ``payloads`` name the columns to gather."""
-    import torch
     names = list(cols)
     if len(names) > MAX_DIM_COLS:
         raise ValueError("too many dimension columns")
+    check_column(key, "dimension key")
     idx = {n: i for i, n in enumerate(names)}
     d = SdbDimDesc()
     d.key = _ptr(key)
@@ -217,8 +248,7 @@ def dim_desc(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
     d.n_cols = len(names)
     for i, n in enumerate(names):
         t = cols[n]
-        if t.dtype != torch.int32 or not t.is_cuda or t.numel() != key.numel():
-            raise ValueError(f"dimension column {n!r} must be int32 on the GPU with {key.numel()} rows")
+        check_column(t, f"dimension column {n!r}", key.numel(), key.device)
         d.cols[i] = _ptr(t)
     if len(preds) > MAX_DIM_PREDS or len(payloads) > MAX_PAYLOADS:
         raise ValueError("too many dimension predicates or payloads")
@@ -241,10 +271,25 @@ def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
     need = dim_required_bytes(d)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=key.device)
+    check_column(workspace, "dimension workspace", device=key.device, dtype="uint8")
     h = SdbDim()
     _check(lib().sdb_build_dim(C.byref(d), _ptr(workspace), workspace.numel(),
                                _stream_handle(stream), C.byref(h)))
     return DimTable(h, d, workspace, [key] + list(cols.values()))
+
+
+def dim_info(table) -> dict:
+    """sdb_dim_info of a built table (a DimTable or an SdbDim handle), as a dict."""
+    h = table.handle if isinstance(table, DimTable) else table
+    o = SdbDimSummary()
+    _check(lib().sdb_dim_info(C.byref(h), C.byref(o)))
+    k = o.n_payloads
+    return {"kind": {1: "dense", 2: "hash"}[o.kind], "width": o.width, "n_rows": o.n_rows, "n_pass": o.n_pass,
+            "key_min": o.key_min, "key_max": o.key_max, "pass_key_min": o.pass_key_min,
+            "pass_key_max": o.pass_key_max, "pass_keys_contiguous": bool(o.pass_keys_contiguous),
+            "n_slots": int(o.n_slots), "table_bytes": int(o.table_bytes), "occupancy": o.occupancy,
+            "payload_min": list(o.payload_min[:k]), "payload_max": list(o.payload_max[:k]),
+            "payload_radix": [int(x) for x in o.payload_radix[:k]], "domain": int(o.domain)}
 
 
 def _join_inputs(dims: dict, dim_keys: dict, jd: dict):
@@ -272,6 +317,10 @@ def build_dims(dims: dict, dim_keys: dict, query: dict, stream=None, workspaces=
     if workspaces is None:
         workspaces = [torch.empty(dim_required_bytes(descs[i]), dtype=torch.uint8, device=inputs[i][0].device)
                       for i in range(len(joins))]
+    if len(workspaces) != len(joins):
+        raise ValueError(f"{len(workspaces)} workspaces for {len(joins)} joins")
+    for i, w in enumerate(workspaces):
+        check_column(w, f"workspace of join {i}", device=inputs[i][0].device, dtype="uint8")
     ws_ptrs = (C.c_void_p * len(joins))(*[_ptr(w) for w in workspaces])
     ws_bytes = (C.c_int64 * len(joins))(*[w.numel() for w in workspaces])
     outs = (SdbDim * len(joins))()
@@ -325,15 +374,15 @@ class StarQuery:
         idx = {n: i for i, n in enumerate(names)}
         q = SdbQuery()
         n = None
+        dev = None
         for i, name in enumerate(names):
             t = fact[name]
-            if t.dtype != torch.int32 or not t.is_cuda:
-                raise ValueError(f"fact column {name!r} must be an int32 GPU tensor")
-            if n is None:
-                n = t.numel()
-            elif t.numel() != n:
-                raise ValueError("fact columns differ in length")
+            check_column(t, f"fact column {name!r}", n, dev)
+            n, dev = t.numel(), t.device
             q.cols[i] = _ptr(t)
+        for j, tab in enumerate(tables):
+            if dev is not None and tab.workspace.device != dev:
+                raise ValueError(f"the table of join {j} is on {tab.workspace.device}, the fact columns on {dev}")
         q.n_fact = int(n or 0)
         q.n_cols = len(names)
         preds = query.get("fact_preds", [])
@@ -424,14 +473,24 @@ class StarQuery:
         plan = plan or self.plan_obj
         if scratch is None:
             scratch = self.baseline_scratch(sums.device)
+        self._check_outputs(sums, counts, scratch)
         _check(lib().sdb_run_star_query_baseline(C.byref(self.q), C.byref(plan), BASELINES[mode], _ptr(sums),
                                                  _ptr(counts), sums.numel(), _ptr(scratch), scratch.numel(),
                                                  _stream_handle(stream)))
+
+    def _check_outputs(self, sums, counts, scratch) -> None:
+        dev = next(iter(self.fact.values())).device if self.fact else None
+        check_column(sums, "sums", device=dev, dtype="int64")
+        if counts is not None:
+            check_column(counts, "counts", sums.numel(), dev, dtype="int64")
+        if scratch is not None:
+            check_column(scratch, "run scratch", device=dev, dtype="uint8")
 
     def run(self, sums, counts, plan: SdbPlan | None = None, stream=None, scratch=None) -> None:
         plan = plan or self.plan_obj
         if scratch is None:
             scratch = self.run_scratch(plan)
+        self._check_outputs(sums, counts, scratch)
         nbytes = 0 if scratch is None else scratch.numel()
         _check(lib().sdb_run_star_query(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
                                         sums.numel(), _ptr(scratch), nbytes, _stream_handle(stream)))

@@ -35,10 +35,11 @@ def test_library_exports_every_declared_symbol():
 
 def test_struct_layout_matches_binding():
     L = sdb.lib()
-    sizes = (C.c_int64 * 8)()
-    assert L.sdb_struct_sizes(sizes, 8) == 0
+    sizes = (C.c_int64 * 9)()
+    assert L.sdb_struct_sizes(sizes, 9) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
-    assert L.sdb_abi_version() == 7
+    assert L.sdb_struct_sizes(sizes, 10) == 1
+    assert L.sdb_abi_version() == 8
 
 
 def test_status_strings():
@@ -99,7 +100,7 @@ def test_dim_descriptor_validation(mutate, status):
 
 
 def _fake_dim(kind=1, width=1, n_rows=200_000, n_pass=40_000, radices=(25,), mins=(0,),
-              key_min=0, n_slots=200_000, bits=0, pass_range=(0, 0)):
+              key_min=0, n_slots=200_000, bits=0, pass_range=(0, 0), with_bitmap=False):
     h = sdb.SdbDim()
     h.kind = kind
     h.width = width
@@ -120,7 +121,67 @@ def _fake_dim(kind=1, width=1, n_rows=200_000, n_pass=40_000, radices=(25,), min
         div *= radices[p]
     h.domain = div
     h.map = 0x40000
+    h.bits = 0x80000 if with_bitmap else None
     return h
+
+
+def test_dim_info_reports_the_handle():
+    """sdb_dim_info through the ABI, on handles filled on the host."""
+    info = sdb.dim_info(_fake_dim(radices=(25, 7), mins=(3, -2), n_slots=200_000, pass_range=(10, 40_009),
+                                  with_bitmap=True))
+    assert info["kind"] == "dense" and info["width"] == 1 and info["n_slots"] == 200_000
+    assert info["table_bytes"] == 200_192 + 25_088       # map and pass bitmap, each padded to 256 bytes
+    assert info["payload_min"] == [3, -2] and info["payload_max"] == [27, 4]
+    assert info["payload_radix"] == [25, 7] and info["domain"] == 175
+    assert info["pass_keys_contiguous"] and info["occupancy"] == 1.0
+    gap = sdb.dim_info(_fake_dim(pass_range=(0, 40_000), with_bitmap=True))   # 40,001 keys, 40,000 passing
+    assert not gap["pass_keys_contiguous"]
+    h = sdb.dim_info(_fake_dim(kind=2, width=8, n_rows=1 << 24, n_pass=1 << 23, bits=25, radices=(65536,)))
+    assert h["kind"] == "hash" and h["n_slots"] == 1 << 25 and h["table_bytes"] == 1 << 28
+    assert h["occupancy"] == 0.5 and h["payload_max"] == [65535]
+
+
+@pytest.mark.parametrize("field,value", [("kind", 0), ("kind", 3), ("width", 3), ("n_pass", 200_001),
+                                         ("n_rows", -1), ("n_payloads", 4), ("n_slots", 7), ("map", None),
+                                         ("bits", None)])
+def test_dim_info_rejects_inconsistent_handles(field, value):
+    h = _fake_dim(with_bitmap=True)
+    sdb.dim_info(h)
+    setattr(h, field, value)
+    with pytest.raises(sdb.SdbError) as e:
+        sdb.dim_info(h)
+    assert e.value.name == "SDB_INVALID_ARG"
+    hh = _fake_dim(kind=2, width=8, n_rows=1000, n_pass=10, bits=11)
+    hh.n_slots = 1000                                             # not 2^hash_bits
+    with pytest.raises(sdb.SdbError):
+        sdb.dim_info(hh)
+
+
+def test_binding_rejects_unreadable_columns_before_any_library_call(monkeypatch):
+    """int64, strided, two-dimensional and host tensors are refused with a
+    ValueError by the binding; the library is never reached."""
+    import torch
+
+    def no_library():
+        raise AssertionError("the binding called the library")
+
+    monkeypatch.setattr(sdb, "lib", no_library)
+    good = torch.arange(100, dtype=torch.int32)
+    cases = [(torch.arange(100, dtype=torch.int64), "int32"),
+             (torch.arange(200, dtype=torch.int32)[::2], "contiguous"),
+             (torch.arange(200, dtype=torch.int32).reshape(100, 2)[:, 0], "contiguous"),
+             (torch.arange(100, dtype=torch.int32).reshape(10, 10), "one-dimensional"),
+             (good, "GPU")]
+    for bad, msg in cases:
+        with pytest.raises(ValueError, match=msg):
+            sdb.dim_desc(bad, {"a": good}, [], [])
+        with pytest.raises(ValueError, match=msg):
+            sdb.build_dim(bad, {"a": good}, [], [])
+        q = {"fact_preds": [], "joins": [], "group_by": [], "agg": {"kind": "col", "a": "v", "b": None}}
+        with pytest.raises(ValueError, match=msg):
+            sdb.StarQuery({"v": bad}, [], q)
+    with pytest.raises(ValueError, match="must be a torch tensor"):
+        sdb.dim_desc([1, 2, 3], {}, [], [])
 
 
 def _query(dims, group_keys, n_fact=1000, n_preds=0, align=True):

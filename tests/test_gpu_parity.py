@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import datagen
+import oracle
 from datagen.star import random_tiny_workload
 from gpu_util import assert_same, oracle_rows, require_gpu, run_gpu, upload
 
@@ -25,6 +26,7 @@ SIZES = {"c1_scalar_scan": None, "c2_join_group": 4_000_003, "c3_star3": 4_000_0
          "c4_star4_zipf": 4_000_002, "c5_hash_stress": 2_000_003}
 
 _cache = {}
+_want = {}
 
 
 def workload(name):
@@ -33,10 +35,17 @@ def workload(name):
     return _cache[name]
 
 
+def want_rows(name):
+    """The oracle's result of workload(name), computed once per session."""
+    if name not in _want:
+        _want[name] = oracle_rows(workload(name))
+    return _want[name]
+
+
 @pytest.mark.parametrize("name", list(SIZES))
 def test_config_parity(name):
     w = workload(name)
-    want = oracle_rows(w)
+    want = want_rows(name)
     got, q = run_gpu(w)
     print(name, w.n_fact, "rows;", len(want), "groups;", q.plan_obj.terminal, q.plan_obj.ipt)
     assert_same(got.as_rows(), want, name)
@@ -58,21 +67,24 @@ def test_config_parity(name):
 ])
 def test_forced_plans_agree(name, force):
     w = workload(name)
-    want = oracle_rows(w)
+    want = want_rows(name)
     got, _ = run_gpu(w, force=force)
     assert_same(got.as_rows(), want, f"{name} {force}")
 
 
-@pytest.mark.parametrize("name", ["c1_scalar_scan", "c2_join_group", "c3_star3"])
-@pytest.mark.parametrize("terminal", ["auto", "scalar", "lds", "global", "part"])
+# every terminal a workload's query admits: the scalar terminal needs a query
+# without GROUP BY, and c3's 375,000 groups do not fit the LDS terminal
+_UNROLL_CASES = [(name, terminal) for name in ["c1_scalar_scan", "c2_join_group", "c3_star3"]
+                 for terminal in ["auto", "scalar", "lds", "global", "part"]
+                 if not (terminal == "scalar" and name != "c1_scalar_scan")
+                 and not (terminal == "lds" and name == "c3_star3")]
+
+
+@pytest.mark.parametrize("name,terminal", _UNROLL_CASES)
 def test_unrolled_stage_loop_agrees(name, terminal):
     # the instance with the stage loop written out against the loop, per terminal
-    if terminal == "scalar" and name != "c1_scalar_scan":
-        pytest.skip("scalar terminal needs a query without GROUP BY")
-    if terminal == "lds" and name == "c3_star3":
-        pytest.skip("375,000 groups do not fit the LDS terminal")
     w = workload(name)
-    want = oracle_rows(w)
+    want = want_rows(name)
     force = {} if terminal == "auto" else {"terminal": terminal}
     got_u, qu = run_gpu(w, force=force)
     got_l, ql = run_gpu(w, force={**force, "unroll": -1})
@@ -90,7 +102,7 @@ def test_baselines_agree(name, mode):
     w = workload(name)
     fact, dims = upload(w)
     q = sdb.StarQuery(fact, sdb.build_dims(dims, w.dim_keys, w.query), w.query)
-    assert_same(q.execute(baseline=mode).as_rows(), oracle_rows(w), f"{name} {mode}")
+    assert_same(q.execute(baseline=mode).as_rows(), want_rows(name), f"{name} {mode}")
 
 
 @pytest.mark.parametrize("mode", ["per_operator", "global_handoff"])
@@ -115,7 +127,7 @@ def test_c5_forced_plans_agree(force):
     w = workload("c5_hash_stress")
     got, q = run_gpu(w, force=force)
     assert bool(q.plan_obj.slice_bits) == bool(force.get("slice"))
-    assert_same(got.as_rows(), oracle_rows(w), f"c5 {force}")
+    assert_same(got.as_rows(), want_rows("c5_hash_stress"), f"c5 {force}")
 
 
 def _sliceable(w, load_factor=0.5):
@@ -183,7 +195,7 @@ def test_sliced_probe_at_every_slice_count():
 
 def test_c1_forced_plans_agree():
     w = workload("c1_scalar_scan")
-    want = oracle_rows(w)
+    want = want_rows("c1_scalar_scan")
     for force in [{"ipt": 1}, {"ipt": 2}, {"ipt": 4}, {"vector": -1}, {"order": True},
                   {"terminal": "global"}, {"terminal": "lds"}, {"grid": 3}]:
         got, _ = run_gpu(w, force=force)
@@ -351,10 +363,67 @@ def test_build_statistics_match_numpy():
     assert np.array_equal(unpacked, ok)
 
 
+@pytest.mark.parametrize("name", ["c3_star3", "c4_star4_zipf", "c5_hash_stress", "c1_scalar_scan"])
+def test_dim_info_of_built_tables(name):
+    """sdb_dim_info through the ABI against numpy over the dimension columns."""
+    import torch
+    from paper_2607_07632_amd import sdb
+    w = datagen.make_workload(name, n_fact=10)
+    dev = {d: {c: torch.from_numpy(a).cuda() for c, a in t.items()} for d, t in w.dims.items()}
+    tables = sdb.build_dims(dev, w.dim_keys, w.query)
+    for jd, tab in zip(w.query["joins"], tables):
+        t = w.dims[jd["dim"]]
+        keys = t[w.dim_keys[jd["dim"]]].astype(np.int64)
+        ok = np.ones(keys.size, dtype=bool)
+        for p in jd["preds"]:
+            ok &= oracle.eval_pred(t[p["col"]], p)
+        info = sdb.dim_info(tab)
+        assert info["n_rows"] == keys.size and info["n_pass"] == int(ok.sum())
+        assert (info["key_min"], info["key_max"]) == (keys.min(), keys.max())
+        assert (info["pass_key_min"], info["pass_key_max"]) == (keys[ok].min(), keys[ok].max())
+        assert info["pass_keys_contiguous"] == (keys[ok].max() - keys[ok].min() + 1 == ok.sum())
+        for i, col in enumerate(jd["payloads"]):
+            assert info["payload_min"][i] == t[col][ok].min() and info["payload_max"][i] == t[col][ok].max()
+        assert info["domain"] == int(np.prod([t[c][ok].max() - t[c][ok].min() + 1 for c in jd["payloads"]]))
+        if jd.get("kind") == "hash":
+            assert info["kind"] == "hash" and info["n_slots"] == 1 << 25 and info["table_bytes"] == 1 << 28
+            assert info["occupancy"] == 0.5
+        else:
+            assert info["kind"] == "dense" and info["n_slots"] == keys.max() - keys.min() + 1
+            assert info["table_bytes"] <= tab.workspace.numel() - 256
+            assert info["width"] == (1 if info["domain"] <= 0xFE else 2 if info["domain"] <= 0xFFFE else 4)
+
+
+def test_binding_rejects_unreadable_device_columns():
+    """Device tensors the library cannot read as dense int32 arrays are refused
+    by the binding with a ValueError before any launch."""
+    import torch
+    from paper_2607_07632_amd import sdb
+    key = torch.arange(100, dtype=torch.int32, device="cuda")
+    good = torch.zeros(100, dtype=torch.int32, device="cuda")
+    for bad, msg in [(torch.zeros(200, dtype=torch.int32, device="cuda")[::2], "contiguous"),
+                     (torch.zeros(100, 2, dtype=torch.int32, device="cuda")[:, 1], "contiguous"),
+                     (torch.zeros(100, dtype=torch.int64, device="cuda"), "int32"),
+                     (good.cpu(), "GPU"), (good[:99], "elements")]:
+        with pytest.raises(ValueError, match=msg):
+            sdb.build_dim(key, {"a": bad}, [], ["a"])
+        q = {"fact_preds": [], "joins": [], "group_by": [], "agg": {"kind": "add", "a": "x", "b": "y"}}
+        with pytest.raises(ValueError, match=msg):
+            sdb.StarQuery({"x": good, "y": bad}, [], q)
+    q = {"fact_preds": [], "joins": [], "group_by": [], "agg": {"kind": "col", "a": "x", "b": None}}
+    sq = sdb.StarQuery({"x": good}, [], q)
+    plan = sq.plan()
+    sums, counts = sq.alloc_outputs(plan)
+    with pytest.raises(ValueError, match="int64"):
+        sq.run(sums.int(), counts, plan=plan)
+    with pytest.raises(ValueError, match="elements"):
+        sq.run(sums, torch.zeros(2, dtype=torch.int64, device="cuda"), plan=plan)
+
+
 @pytest.mark.parametrize("name", ["c2_join_group", "c3_star3", "c4_star4_zipf", "c5_hash_stress", "c1_scalar_scan"])
 def test_partitioned_terminal(name):
     w = workload(name)
-    want = oracle_rows(w)
+    want = want_rows(name)
     got, q = run_gpu(w, force={"terminal": "part"})
     assert q.plan_obj.terminal == 4
     assert_same(got.as_rows(), want, f"{name} part")
@@ -380,7 +449,7 @@ def test_partitioned_terminal_region_overflow(cap):
     m = int(n.item())
     rows = [(tuple(int(x) for x in kk), int(ss), int(cc))
             for kk, ss, cc in zip(k[:m].cpu().numpy(), s[:m].cpu().numpy(), c[:m].cpu().numpy())]
-    assert_same(rows, oracle_rows(w), f"overflow cap {cap}")
+    assert_same(rows, want_rows("c3_star3"), f"overflow cap {cap}")
 
 
 @pytest.mark.parametrize("seed", [3, 11, 29, 41])
@@ -455,7 +524,7 @@ def test_fused_events_bracket_the_kernel():
     m = int(n.item())
     rows = [(tuple(int(x) for x in kk), int(ss), int(cc))
             for kk, ss, cc in zip(k[:m].cpu().numpy(), s[:m].cpu().numpy(), c[:m].cpu().numpy())]
-    assert_same(rows, oracle_rows(w), "timed run")
+    assert_same(rows, want_rows("c3_star3"), "timed run")
 
 
 def _range_workload(seed, n=50_003, empty_join=False):
@@ -530,7 +599,7 @@ def test_c1_date_join_as_key_range():
         got, q = run_gpu(w, force=force)
         tables = {st["name"]: st.get("table") for st in sdb.plan_summary(q.plan_obj, w.query)["stages"]}
         assert tables["date"] == table
-        assert_same(got.as_rows(), oracle_rows(w), f"c1 {force}")
+        assert_same(got.as_rows(), want_rows("c1_scalar_scan"), f"c1 {force}")
 
 
 @pytest.mark.parametrize("n_cols", [1, 3, 4, 5, 9])
@@ -573,7 +642,7 @@ def test_graph_replay_of_run_and_finalize(name, force):
     want = [t[:m].clone() for t in outs[:3]]
     got_rows = sdb.QueryResult(want[0][:, :q.n_keys].long().cpu().numpy().reshape(m, q.n_keys),
                                want[1].cpu().numpy(), want[2].cpu().numpy()).as_rows()
-    assert_same(got_rows, oracle_rows(w), f"{name} eager")
+    assert_same(got_rows, want_rows(name), f"{name} eager")
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
