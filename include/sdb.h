@@ -449,6 +449,31 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan,
                                       int64_t n_groups_capacity, void* scratch,
                                       int64_t scratch_bytes, void* stream);
 
+/* Size of the fixed run scratch of sdb_run_star_query_noalloc: 64 MiB per
+ * device, held from the library's first use of that device until the
+ * process ends. */
+#define SDB_NOALLOC_SCRATCH_BYTES (64ll << 20)
+
+/* For callers that cannot allocate device memory (code under HIP stream
+ * capture, tight serving loops, harnesses that forbid hipMalloc): as
+ * sdb_run_star_query, with the run scratch taken from a fixed array of
+ * SDB_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs
+ * on, instead of a caller buffer. The caller still owns the outputs. The
+ * call allocates nothing: no hipMalloc, hipFree or allocating library call
+ * (its first call on a device looks the array's device address up once).
+ * The array belongs to the device, not to the call: every call on a device
+ * uses the same array, so calls whose work overlaps on one device (two
+ * streams, or two host threads) race and give undefined results; calls one
+ * after another on one stream are safe, each clearing what it needs.
+ * Plans whose run_scratch_bytes exceed the array (the partitioned terminal
+ * or the sliced hash probe at large row counts, per-XCD copies of more than
+ * 4 Mi groups) are refused with SDB_WORKSPACE_TOO_SMALL before any launch;
+ * plan such a query with force_terminal = SDB_TERMINAL_GLOBAL, force_xcd =
+ * -1 and force_slice = -1, which leaves only the small rank and coarse
+ * tables in the scratch. Errors: as sdb_run_star_query. */
+SDB_API sdb_status sdb_run_star_query_noalloc(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
+                                              int64_t* counts, int64_t n_groups_capacity, void* stream);
+
 /* Measurement hook, host only. With both events non-NULL (hipEvent_t
  * handles the caller created and owns), every later sdb_run_star_query on
  * this thread records `start` on its stream just before the fused kernel and

@@ -1618,6 +1618,21 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
     return ok();
 }
 
+SDB_API sdb_status sdb_run_star_query_noalloc(const sdb_query* q, const sdb_plan* plan, int64_t* sums,
+                                              int64_t* counts, int64_t n_groups_capacity, void* stream) {
+    sdb_status st = check_run(q, plan, sums, counts, n_groups_capacity);
+    if (st != SDB_OK) return st;
+    if (plan->run_scratch_bytes < 0 || (uint64_t)plan->run_scratch_bytes > kNoallocScratchBytes)
+        return fail(SDB_WORKSPACE_TOO_SMALL,
+                    "the plan needs %lld bytes of run scratch; the fixed scratch of the allocation-free run holds "
+                    "%llu (plan with the global terminal, no per-XCD copies and no table slices)",
+                    (long long)plan->run_scratch_bytes, (unsigned long long)kNoallocScratchBytes);
+    void* fixed = nullptr;
+    SDB_HIP(noalloc_scratch(&fixed), "fixed run scratch address");
+    return sdb_run_star_query(q, plan, sums, counts, n_groups_capacity, fixed, (int64_t)kNoallocScratchBytes,
+                              stream);
+}
+
 SDB_API sdb_status sdb_baseline_scratch_bytes(int64_t n_fact, int64_t* bytes) {
     if (!bytes) return fail(SDB_INVALID_ARG, "null argument");
     if (n_fact < 0) return fail(SDB_INVALID_ARG, "negative n_fact");

@@ -330,4 +330,10 @@ hipError_t launch_part_passes(const PartParams& pp, hipStream_t s);
 // count pass, per-partition offsets, scatter pass over `grid` blocks
 hipError_t launch_slice_partition(const SliceParams& sp, int grid, hipStream_t s);
 
+// the fixed run scratch of sdb_run_star_query_noalloc: its device address on
+// the calling thread's current device
+constexpr int kNoallocMaxDevices = 64;
+constexpr uint64_t kNoallocScratchBytes = (uint64_t)SDB_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch(void** out);
+
 }  // namespace sdb

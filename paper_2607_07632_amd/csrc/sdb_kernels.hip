@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <cstring>
 #include <climits>
+#include <mutex>
 
 #include "sdb_internal.h"
 
@@ -2178,6 +2179,36 @@ hipError_t launch_finalize(const FinalizeParams& fp, hipStream_t s) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fin_scatter_kernel, dim3((unsigned)fp.n_blocks), dim3(kFinBlock), 0, s, fp);
     return hipGetLastError();
+}
+
+// ---- fixed device scratch for sdb_run_star_query_noalloc ------------------
+//
+// Callers that cannot allocate device memory (code under stream capture,
+// serving loops, harnesses that forbid hipMalloc) run a query with this
+// file-scope array as its run scratch. Every device the library runs on holds
+// its own copy from the code object's load until the process ends. In host
+// code the array's name is only a host-side stand-in: its device address comes
+// from hipGetSymbolAddress, taken once per device with that device current.
+
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+hipError_t noalloc_scratch(void** out) {
+    static std::mutex mu;
+    static void* per_device[kNoallocMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kNoallocMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!per_device[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p || ((uintptr_t)p & 255u) != 0) return hipErrorInvalidSymbol;
+        per_device[dev] = p;
+    }
+    *out = per_device[dev];
+    return hipSuccess;
 }
 
 }  // namespace sdb

@@ -29,6 +29,7 @@ MAX_JOINS = 6
 MAX_GROUP_KEYS = 4
 MAX_STAGES = MAX_FACT_PREDS + MAX_JOINS
 PLAN_SCRATCH_BYTES = 256
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 OPS = {"eq": 0, "ne": 1, "lt": 2, "le": 3, "gt": 4, "ge": 5, "between": 6}
 TABLES = {"auto": 0, "dense": 1, "hash": 2}
@@ -128,6 +129,7 @@ SIGNATURES = {
                                           vp]),
     "sdb_plan_star_query": (i32, [C.POINTER(SdbQuery), vp, i64, vp, C.POINTER(SdbPlan)]),
     "sdb_run_star_query": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp, i64, vp]),
+    "sdb_run_star_query_noalloc": (i32, [C.POINTER(SdbQuery), C.POINTER(SdbPlan), vp, vp, i64, vp]),
     "sdb_finalize_scratch_bytes": (i32, [C.POINTER(SdbPlan), C.POINTER(i64)]),
     "sdb_finalize_groups": (i32, [C.POINTER(SdbPlan), vp, vp, vp, vp, vp, i64, vp, vp, i64, vp]),
 }
@@ -494,6 +496,14 @@ class StarQuery:
         nbytes = 0 if scratch is None else scratch.numel()
         _check(lib().sdb_run_star_query(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
                                         sums.numel(), _ptr(scratch), nbytes, _stream_handle(stream)))
+
+    def run_noalloc(self, sums, counts, plan: SdbPlan | None = None, stream=None) -> None:
+        """sdb_run_star_query_noalloc: the run with the library's fixed device
+        scratch (NOALLOC_SCRATCH_BYTES per device) instead of a caller buffer."""
+        plan = plan or self.plan_obj
+        self._check_outputs(sums, counts, None)
+        _check(lib().sdb_run_star_query_noalloc(C.byref(self.q), C.byref(plan), _ptr(sums), _ptr(counts),
+                                                sums.numel(), _stream_handle(stream)))
 
     def finalize(self, sums, counts, plan: SdbPlan | None = None, stream=None, outputs=None):
         """Device compaction; returns (keys, sums, counts, n) device tensors (n: int64[1])."""
