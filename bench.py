@@ -42,7 +42,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_07632_amd", "csrc", "sdb_kernels.hip")
+# the fused kernel's source: its template and the device helpers it uses
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_07632_amd", "csrc", f) for f in ("sdb_fused.h", "sdb_device.h")]
 
 
 def log(*a):
@@ -50,7 +51,10 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def traffic_from_profile(workload: str):

@@ -19,7 +19,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsdb.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["sdb_api.cpp", "sdb_kernels.hip"]
+# the fused pass's instances are spread over several files so they compile in parallel
+SOURCES = ["sdb_api.cpp", "sdb_kernels.hip", "sdb_fused_vec.hip", "sdb_fused_rows.hip", "sdb_fused_eager.hip",
+           "sdb_fused_big.hip", "sdb_fused_unroll.hip", "sdb_fused_unroll_big.hip"]
 
 COMMON = [
     "--offload-arch=gfx950",
