@@ -121,7 +121,8 @@ def b_alg_per_row(sample: dict, dims: dict, dim_keys: dict, query: dict, plan_in
 
 # The plan features of the fused pass added one at a time, each rung a set of
 # planner overrides (the last rung is the planner's own choice).
-_NR = {"range": -1, "slice": -1}     # the rungs before the key-range rewrite keep every probe a lookup, unsliced
+# the rungs before the key-range rewrite keep every probe a lookup, unsliced, without LDS windows
+_NR = {"range": -1, "slice": -1, "window": -1}
 ABLATION_RUNGS = [
     ("kernel at a time: flags and group ids through HBM; hash tables; query order",
      {"order": True, "baseline": "per_operator", "tables": "hash", "slice": -1}),
@@ -140,9 +141,11 @@ ABLATION_RUNGS = [
     ("+ sampled stage order", {"lds": 2, "ipt": 2, "terminal": "global", "xcd": -1, "block": 256} | _NR),
     ("+ per-XCD group tables", {"lds": 2, "ipt": 2, "terminal": "global", "block": 256} | _NR),
     ("+ probes of one contiguous passing key range run as BETWEEN", {"lds": 2, "ipt": 2, "terminal": "global",
-                                                                     "block": 256, "range": 1, "slice": -1}),
-    ("planner's choice (terminal, block size, rank tables)", {"slice": -1, "unroll": -1}),
-    ("+ stage loop written out (plans without a hash probe)", {"slice": -1}),
+                                                                     "block": 256, "range": 1, "slice": -1,
+                                                                     "window": -1}),
+    ("planner's choice (terminal, block size, rank tables)", {"slice": -1, "unroll": -1, "window": -1}),
+    ("+ stage loop written out (plans without a hash probe)", {"slice": -1, "window": -1}),
+    ("+ LDS window over the busiest device-memory map", {"slice": -1}),
     ("+ a hash probe over 2 MiB table slices (planner's choice)", {}),
 ]
 

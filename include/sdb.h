@@ -16,7 +16,7 @@
  *    stay valid until the work queued on the stream has finished. The library
  *    allocates no device memory and keeps no global mutable state besides a
  *    per-thread error string, the per-thread measurement events of
- *    sdb_set_fused_events, a per-device properties cache and a 4 KB pinned
+ *    sdb_set_fused_events, a per-device properties cache and a 96 KB pinned
  *    host buffer per calling thread (allocated on the first build or sampled
  *    plan, kept while the thread lives) for the small reads those calls
  *    synchronize on; calls on different streams may run concurrently.
@@ -38,7 +38,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 8
+#define SDB_ABI_VERSION 9
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -82,7 +82,7 @@ enum { SDB_TERMINAL_AUTO = 0, SDB_TERMINAL_SCALAR = 1, SDB_TERMINAL_LDS = 2,
 #define SDB_MAX_JOINS 6
 #define SDB_MAX_GROUP_KEYS 4
 #define SDB_MAX_STAGES (SDB_MAX_FACT_PREDS + SDB_MAX_JOINS)
-#define SDB_PLAN_SCRATCH_BYTES 256
+#define SDB_PLAN_SCRATCH_BYTES 81920
 /* fact columns the fused kernel can load eagerly (sdb_plan.eager) */
 #define SDB_MAX_EAGER 4
 
@@ -227,7 +227,12 @@ typedef struct sdb_agg {
  *                  query allows it
  *  force_unroll    the fused kernel with its stage loop written out
  *                  (sdb_plan.unroll): 0: wherever the plan allows it; -1:
- *                  never */
+ *                  never
+ *  force_window    LDS windows (SDB_LDS_WINDOW): 0: the planner's choice
+ *                  (none: measured on MI355X, a window does not pay); -1:
+ *                  none; 1: the largest window that fits without lowering
+ *                  the blocks per CU, for the dense device-memory stage it
+ *                  serves most; k >= 2: the same with at most 128 * k slots */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -252,7 +257,7 @@ typedef struct sdb_query {
     int32_t force_coarse;
     int32_t force_slice;
     int32_t force_unroll;
-    int32_t reserved_;                    /* 0 */
+    int32_t force_window;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -272,8 +277,16 @@ typedef struct sdb_query {
  *          j * 2^stage_coarse[s] ... holds a passing key (sdb_run_star_query
  *          derives it from the pass bitmap in its run scratch). A row whose
  *          bit is clear dies without touching device memory; the others
- *          gather their code from the map as with GLOBAL. */
-enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, SDB_LDS_COARSE = 4 };
+ *          gather their code from the map as with GLOBAL;
+ *  WINDOW  the pass bitmap of slots stage_window_lo[s] ...
+ *          stage_window_lo[s] + stage_window_slots[s] - 1 sits in LDS (a
+ *          window of the key range, placed where the sampled keys are
+ *          densest): a row whose key falls in it and whose bit is clear
+ *          dies without touching device memory; every other row gathers its
+ *          code from the device map as with GLOBAL (a passing row in the
+ *          window only for its group key). */
+enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, SDB_LDS_COARSE = 4,
+       SDB_LDS_WINDOW = 5 };
 /* log2 of the slots one coarse bit covers: 1 ... SDB_MAX_COARSE_SHIFT */
 #define SDB_MAX_COARSE_SHIFT 5
 
@@ -303,14 +316,22 @@ typedef struct sdb_plan {
     int32_t n_stages;
     int32_t stage_kind[SDB_MAX_STAGES];
     int32_t stage_index[SDB_MAX_STAGES];
-    double stage_pass[SDB_MAX_STAGES];    /* pass fraction on the sample, or the estimate used */
+    double stage_pass[SDB_MAX_STAGES];    /* pass fraction on the sample among the sampled rows that
+                                             pass every earlier stage (conditional), or the estimate
+                                             used (the dimension's pass fraction) without a sample */
+    double stage_pass_alone[SDB_MAX_STAGES];  /* the stage's pass fraction on the sample by itself */
     int32_t stage_lds[SDB_MAX_STAGES];    /* SDB_LDS_* */
-    int32_t stage_defer[SDB_MAX_STAGES];  /* deferred-gather slot (0 or 1), or -1 */
+    int32_t stage_defer[SDB_MAX_STAGES];  /* 0: an LDS_BITS stage whose code is gathered after all
+                                             stages; -1 otherwise */
     int32_t stage_range[SDB_MAX_STAGES];  /* 1: a probe run as `fact key BETWEEN pass_key_min AND
                                              pass_key_max` (its dimension's passing keys are exactly
                                              that range and it feeds no group key; Section 3.2's
                                              date-range scan, generalized); 0 otherwise */
     int32_t stage_coarse[SDB_MAX_STAGES]; /* SDB_LDS_COARSE: log2 of the slots per coarse bit; else 0 */
+    int32_t stage_window_lo[SDB_MAX_STAGES];    /* SDB_LDS_WINDOW: first slot (a multiple of 128); else 0 */
+    int32_t stage_window_slots[SDB_MAX_STAGES]; /* SDB_LDS_WINDOW: slots (a multiple of 128); else 0 */
+    double stage_window_cover[SDB_MAX_STAGES];  /* SDB_LDS_WINDOW: sampled fraction of the stage's fact
+                                                   keys that fall in the window; else 0 */
     int64_t sampled_rows;                 /* 0 when no sample was taken */
     double est_cost;                      /* cost model value of the chosen order */
     int32_t terminal;
@@ -405,25 +426,37 @@ SDB_API sdb_status sdb_dim_info(const sdb_dim* dim, sdb_dim_summary* out);
 
 /* ---- planning ----------------------------------------------------------- */
 
-/* Plans `q` (host) into `plan` (host). Unless q->force_order is set, a
- * sampling kernel evaluates every stage on its own over every
- * ceil(n_fact / 65536)-th fact row; this needs `scratch` (device,
+/* Plans `q` (host) into `plan` (host): the runtime choices of Section 4.3
+ * (key-range checks, the group table sized from the payload domains, the
+ * terminal by group count) and the stage order of Section 4.2's fact-spine
+ * lowering. Unless q->force_order is set, a sampling kernel evaluates every
+ * stage over every ceil(n_fact / 65536)-th fact row and records, per sampled
+ * row, which stages it passes (a histogram over the 2^stages pass patterns)
+ * and, when a window is forced, per dense-table stage a 256-bucket histogram
+ * of its fact keys over the table's key range; this needs `scratch` (device,
  * >= SDB_PLAN_SCRATCH_BYTES) and synchronizes `stream` once. With
  * force_order set, scratch and stream are unused, no GPU call is made and
- * the stages keep query order (predicates, then joins). The plan fixes:
+ * the stages keep query order (predicates, then joins), with the
+ * dimensions' pass fractions taken as independent estimates. The plan fixes:
  * which small dense tables are staged in LDS (whole maps, pass bitmaps or
  * rank tables) and which probes run as key ranges; the stage order with the
  * least modelled cost (fact columns streamed at 128-byte line granularity
- * plus each stage's lookups for the rows that reach it; every order is tried
- * up to 7 stages, a greedy rank beyond); group radices and strides from the
- * built tables' payload ranges; the terminal (scalar without GROUP BY, LDS
- * when the group table fits a block's LDS, partitioned for many survivors
- * into a large table, else global, with per-XCD copies when enough rows
- * survive); items per lane, block size, eager columns, and for the
- * partitioned terminal the grid and region sizes; whether the hash probe
- * runs over table slices (chosen for a table of at least 16 MiB and at
- * least 2^24 fact rows, when the query allows it). Errors: INVALID_ARG,
- * UNSUPPORTED, CAPACITY, WORKSPACE_TOO_SMALL, HIP_ERROR. */
+ * plus each stage's lookups for the rows that reach it, the rows reaching a
+ * stage counted exactly from the sampled pass patterns, so correlated
+ * predicates are priced as measured; every order is tried up to 7 stages, a
+ * greedy rank on conditional pass fractions beyond); when forced, an LDS
+ * window for the dense device-memory stage whose sampled keys it serves
+ * most (4-row items then run in blocks of 1024); group radices and strides
+ * from the built
+ * tables' payload ranges; the terminal (scalar without GROUP BY, LDS when
+ * the group table fits a block's LDS, partitioned when at least a million
+ * rows survive, 16 or more per group, else global, with per-XCD copies when
+ * enough rows survive);
+ * items per lane, block size, eager columns, and for the partitioned
+ * terminal the grid and region sizes; whether the hash probe runs over
+ * table slices (chosen for a table of at least 16 MiB and at least 2^24 fact
+ * rows, when the query allows it). Errors: INVALID_ARG, UNSUPPORTED,
+ * CAPACITY, WORKSPACE_TOO_SMALL, HIP_ERROR. */
 SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_t scratch_bytes,
                                        void* stream, sdb_plan* plan);
 

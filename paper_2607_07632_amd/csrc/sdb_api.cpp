@@ -57,9 +57,13 @@ sdb_status hip_fail(hipError_t e, const char* what) {
 // host thread, allocated on first use and kept while the thread lives (calls
 // on one thread never overlap: each synchronizes before it returns); if the
 // allocation fails the reads go to the caller's stack as before.
-constexpr size_t kStagingBytes = 4096;
+constexpr size_t kStagingBytes = 96 * 1024;
+// planner scratch: pass-pattern histogram, then the per-stage key histograms
+constexpr size_t kPatternBytes = sizeof(uint32_t) << kMaxStages;
+constexpr size_t kKeyHistBytes = sizeof(uint32_t) * kMaxStages * kKeyBuckets;
 static_assert(sizeof(DimStats) * SDB_MAX_JOINS <= kStagingBytes, "statistics staging");
-static_assert(sizeof(unsigned long long) * kMaxStages <= kStagingBytes, "sample staging");
+static_assert(kPatternBytes + kKeyHistBytes <= kStagingBytes, "sample staging");
+static_assert(kPatternBytes + kKeyHistBytes <= SDB_PLAN_SCRATCH_BYTES, "planner scratch");
 thread_local void* t_staging = nullptr;
 thread_local bool t_staging_failed = false;
 
@@ -290,7 +294,8 @@ sdb_status check_query(const sdb_query* q) {
         return fail(SDB_INVALID_ARG, "force_eager %d is not in -1..%d", q->force_eager, kMaxEager);
     if (q->force_unroll < -1 || q->force_unroll > 0)
         return fail(SDB_INVALID_ARG, "force_unroll %d is not -1 or 0", q->force_unroll);
-    if (q->reserved_ != 0) return fail(SDB_INVALID_ARG, "sdb_query.reserved_ must be 0");
+    if (q->force_window < -1 || q->force_window > (1 << 24))
+        return fail(SDB_INVALID_ARG, "force_window %d is not in -1..2^24", q->force_window);
     return SDB_OK;
 }
 
@@ -412,6 +417,11 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
             S.lds_mode = plan->stage_lds[pos];
             S.defer = plan->stage_defer[pos];
             S.coarse_shift = plan->stage_coarse[pos];
+            if (S.lds_mode == LDS_WINDOW) {
+                S.win_lo = (uint32_t)plan->stage_window_lo[pos];
+                S.win_slots = (uint32_t)plan->stage_window_slots[pos];
+                S.bits = static_cast<const uint32_t*>(d->bits) + S.win_lo / 32u;   // the staged words
+            }
         }
     }
     S.gk_mode = S.n_gk == 0 ? GK_NONE
@@ -422,6 +432,7 @@ StageDev make_stage(const sdb_query* q, const sdb_plan* plan, int kind, int inde
     else if (S.lds_mode == LDS_BITS) S.op = OP_LDS_BITS;
     else if (S.lds_mode == LDS_RANK) S.op = OP_LDS_RANK1 + wsel;
     else if (S.lds_mode == LDS_COARSE) S.op = OP_COARSE1 + wsel;
+    else if (S.lds_mode == LDS_WINDOW) S.op = OP_WINDOW1 + wsel;
     else if (S.lds_mode == LDS_MAP) S.op = OP_LDS_MAP1 + wsel;
     else S.op = OP_MAP1 + wsel;
     return S;
@@ -478,16 +489,59 @@ double stage_cost(const sdb_query* q, const sdb_plan* plan, int s) {
 // Fraction of 128-byte lines (32 int32 rows) holding at least one live row.
 double line_fraction(double f) { return 1.0 - std::pow(1.0 - std::min(std::max(f, 0.0), 1.0), 32.0); }
 
+// What the planner's sampling kernel measured: for every subset m of the
+// stages (bit i = the stage at query position i), the fraction of sampled
+// rows that pass every stage in m, and each dense stage's key histogram.
+struct Sample {
+    bool have = false;
+    int n = 0;
+    double rows = 0.0;
+    std::vector<double> joint;      // 2^n entries
+    std::vector<uint32_t> keys;     // kMaxStages x kKeyBuckets
+    double frac(uint32_t m) const { return rows > 0.0 ? joint[m] / rows : 0.0; }
+};
+
+// Joint pass counts from the pass-pattern histogram: the rows passing every
+// stage in m are those whose pattern contains m (a sum over supersets).
+void joint_from_patterns(const uint32_t* hist, int n, double rows, Sample* smp) {
+    smp->have = true;
+    smp->n = n;
+    smp->rows = rows;
+    smp->joint.assign((size_t)1 << n, 0.0);
+    for (size_t m = 0; m < smp->joint.size(); ++m) smp->joint[m] = (double)hist[m];
+    for (int b = 0; b < n; ++b)
+        for (size_t m = 0; m < smp->joint.size(); ++m)
+            if (!(m & ((size_t)1 << b))) smp->joint[m] += smp->joint[m | ((size_t)1 << b)];
+}
+
+// Fraction of rows that pass the stages at positions order[0 .. k-1]: measured
+// jointly when there is a sample, else the product of the per-stage estimates.
+struct Reach {
+    const sdb_plan* plan;
+    const Sample* smp;
+    const int* bit;     // query position of the stage at each plan position
+    double of(const int* order, int k) const {
+        if (smp && smp->have) {
+            uint32_t m = 0;
+            for (int i = 0; i < k; ++i) m |= 1u << bit[order[i]];
+            return smp->frac(m);
+        }
+        double f = 1.0;
+        for (int i = 0; i < k; ++i) f *= plan->stage_pass[order[i]];
+        return f;
+    }
+};
+
 // Modeled cost of running the stages in `order`: column streaming at line
 // granularity plus lookups for the rows that reach each stage, then the
 // aggregate columns and deferred gathers for the survivors.
-double order_cost(const sdb_query* q, const sdb_plan* plan, const int* order, int n) {
-    double f = 1.0, cost = 0.0;
+double order_cost(const sdb_query* q, const sdb_plan* plan, const int* order, int n, const Reach& reach) {
+    double cost = 0.0;
     for (int i = 0; i < n; ++i) {
-        const int s = order[i];
-        cost += line_fraction(f) + f * stage_cost(q, plan, s);
-        f *= plan->stage_pass[s];
+        const double f = reach.of(order, i);
+        cost += line_fraction(f) + f * stage_cost(q, plan, order[i]);
     }
+    const double f = reach.of(order, n);
     const int agg_cols = q->agg.kind == SDB_AGG_COL ? 1 : 2;
     cost += agg_cols * line_fraction(f);
     for (int s = 0; s < n; ++s)
@@ -500,39 +554,66 @@ double order_cost(const sdb_query* q, const sdb_plan* plan, const int* order, in
     return cost;
 }
 
-// Cheapest order under order_cost: exhaustive up to 7 stages, else greedy by
-// the rank (1 - pass) / cost of each stage taken alone.
-void choose_order(const sdb_query* q, sdb_plan* plan) {
+// Cheapest order under order_cost: exhaustive up to 7 stages, else greedy:
+// next the stage with the best (1 - conditional pass) / cost among those
+// left, given the stages already chosen. Permutes the plan's stage arrays
+// and `bit` alike, and leaves in stage_pass each stage's pass fraction given
+// the stages before it (measured jointly when there is a sample).
+void choose_order(const sdb_query* q, sdb_plan* plan, int* bit, const Sample* smp) {
     const int n = plan->n_stages;
+    const Reach reach{plan, smp, bit};
     std::vector<int> order(n), best;
     for (int i = 0; i < n; ++i) order[i] = i;
     double best_cost = 0.0;
     if (n <= 7) {
-        best_cost = order_cost(q, plan, order.data(), n);
+        best_cost = order_cost(q, plan, order.data(), n, reach);
         best = order;
         while (std::next_permutation(order.begin(), order.end())) {
-            const double c = order_cost(q, plan, order.data(), n);
+            const double c = order_cost(q, plan, order.data(), n, reach);
             if (c < best_cost - 1e-12) {
                 best_cost = c;
                 best = order;
             }
         }
     } else {
-        std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-            const double cx = 1.0 + stage_cost(q, plan, x);
-            const double cy = 1.0 + stage_cost(q, plan, y);
-            return (1.0 - plan->stage_pass[x]) / cx > (1.0 - plan->stage_pass[y]) / cy;
-        });
-        best = order;
-        best_cost = order_cost(q, plan, best.data(), n);
+        std::vector<bool> used(n, false);
+        for (int i = 0; i < n; ++i) {
+            const double before = reach.of(best.data(), i);
+            int pick = -1;
+            double pick_rank = -1.0;
+            for (int s = 0; s < n; ++s) {
+                if (used[s]) continue;
+                best.push_back(s);
+                const double after = reach.of(best.data(), i + 1);
+                best.pop_back();
+                const double pass = before > 0.0 ? after / before : plan->stage_pass[s];
+                const double rank = (1.0 - pass) / (1.0 + stage_cost(q, plan, s));
+                if (rank > pick_rank + 1e-12) {
+                    pick_rank = rank;
+                    pick = s;
+                }
+            }
+            used[pick] = true;
+            best.push_back(pick);
+        }
+        best_cost = order_cost(q, plan, best.data(), n, reach);
     }
     const sdb_plan tmp = *plan;
+    int tmp_bit[SDB_MAX_STAGES];
+    for (int i = 0; i < n; ++i) tmp_bit[i] = bit[i];
+    std::vector<double> cond(n);
+    for (int i = 0; i < n; ++i) {
+        const double before = reach.of(best.data(), i), after = reach.of(best.data(), i + 1);
+        cond[i] = before > 0.0 ? after / before : tmp.stage_pass[best[i]];
+    }
     for (int i = 0; i < n; ++i) {
         plan->stage_kind[i] = tmp.stage_kind[best[i]];
         plan->stage_index[i] = tmp.stage_index[best[i]];
-        plan->stage_pass[i] = tmp.stage_pass[best[i]];
+        plan->stage_pass[i] = smp && smp->have ? cond[i] : tmp.stage_pass[best[i]];
+        plan->stage_pass_alone[i] = tmp.stage_pass_alone[best[i]];
         plan->stage_lds[i] = tmp.stage_lds[best[i]];
         plan->stage_range[i] = tmp.stage_range[best[i]];
+        bit[i] = tmp_bit[best[i]];
     }
     plan->est_cost = best_cost;
 }
@@ -576,6 +657,7 @@ uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
         const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
         const uint64_t bytes = plan->stage_lds[s] == LDS_MAP      ? lds_map_bytes(d)
                                : plan->stage_lds[s] == LDS_COARSE ? coarse_bits_bytes(d, plan->stage_coarse[s])
+                               : plan->stage_lds[s] == LDS_WINDOW ? (uint64_t)plan->stage_window_slots[s] / 8u
                                                                   : lds_bits_bytes(d);
         if (p) {
             p->st[s].lds_off = (uint32_t)off;
@@ -670,9 +752,8 @@ constexpr int kDefaultIpt = 2;
 constexpr bool kAutoEager = false;
 // a 128-byte line holds 32 rows: at 2% live rows about half its lines are still read
 constexpr double kEagerMinLive = 0.02;
-// group tables from this size on (16 bytes a group, 8 XCD copies: 8 MiB) go
-// to the partitioned terminal when at least a million rows survive
-constexpr uint64_t kPartMinGroups = 65536;
+// the partitioned terminal: at least a million survivors, and this many per group
+constexpr double kPartMinPerGroup = 16.0;
 
 // Partitioned-terminal records carry 64-bit values only when the aggregate
 // combines two columns; a single int32 column's values fit 32 bits.
@@ -843,6 +924,97 @@ sdb_status choose_grid(const sdb_query* q, const sdb_plan* plan, int* grid_out) 
 
 // Checks shared by both run entry points: the query, the plan's stage list
 // and deferred gathers, the group layout and the output capacity.
+// LDS windows are a forced placement only: measured on MI355X they do not
+// pay. On c3 a window over 29% of the customer keys spares 28M of the fused
+// kernel's 211M L2 requests but leaves the kernel within 1% (2.219 against
+// 2.229 ms) and the run and step slower; on c4 a window over 96% of the Zipf
+// part keys, sized to keep 32 waves per CU, spares 30M of 90M requests and
+// runs 5% slower (1.720 against 1.640 ms): c4 is bound by each wave's chain of
+// dependent loads, not by the number of requests. The automatic rule below
+// (a window that spares the gathers of at least 2% of all fact rows, on at
+// least 2^24 rows) is kept for hardware where that trade differs.
+constexpr bool kWindowAuto = false;
+constexpr double kWindowMinGain = 0.02;
+constexpr int64_t kWindowMinRows = 1ll << 24;
+
+// Sampled fraction of a dense stage's fact keys inside slots [lo, lo + len):
+// whole buckets count fully, a partly covered bucket by its covered share.
+double window_cover(const uint32_t* hist, uint64_t nslots, uint64_t lo, uint64_t len) {
+    double in = 0.0, all = 0.0;
+    for (int b = 0; b < kKeyBuckets; ++b) {
+        const uint64_t b0 = (uint64_t)b * nslots / kKeyBuckets, b1 = (uint64_t)(b + 1) * nslots / kKeyBuckets;
+        all += hist[b];
+        if (b1 <= b0) continue;
+        const uint64_t o0 = std::max(b0, lo), o1 = std::min(b1, lo + len);
+        if (o1 > o0) in += hist[b] * (double)(o1 - o0) / (double)(b1 - b0);
+    }
+    return all > 0.0 ? in / all : 0.0;
+}
+
+// LDS window (SDB_LDS_WINDOW) for the dense device-memory stage whose rows it
+// serves most: window length from the LDS a block can take without lowering
+// the blocks per CU its registers allow (measured on c4: a window that halves
+// the waves per CU makes the kernel 60% slower although it spares 96% of the
+// part-map gathers), start where the sampled keys are densest. Returns the
+// stage or -1.
+int place_window(const sdb_query* q, sdb_plan* plan, const Sample& smp, const int* bit, int64_t n_fact) {
+    if (q->force_window == -1 || q->force_lds == -1) return -1;
+    const Reach reach{plan, &smp, bit};
+    int order[SDB_MAX_STAGES];
+    for (int i = 0; i < plan->n_stages; ++i) order[i] = i;
+    const uint64_t used = lds_layout(q, plan, nullptr) + ring_lds_bytes(q, plan);
+    int per_cu = fused_blocks_per_cu(plan->vector, plan->ipt, plan->terminal, plan->eager, plan->block,
+                                     unroll_allowed(q, plan) && q->force_unroll != -1 ? 1 : 0, (size_t)used);
+    if (per_cu < 1) per_cu = 1;
+    const uint64_t per_block = (uint64_t)kLdsUsable / (uint64_t)per_cu / 2048u * 2048u;
+    if (used + 2048u >= per_block) return -1;
+    const uint64_t lds_left = per_block - used - 2048u;   // a granule of slack
+    int best = -1;
+    double best_gain = 0.0, best_cover = 0.0;
+    uint64_t best_lo = 0, best_len = 0;
+    for (int s = 0; s < plan->n_stages; ++s) {
+        if (plan->stage_kind[s] != 1 || plan->stage_lds[s] != LDS_GLOBAL || plan->stage_range[s]) continue;
+        const sdb_dim* d = q->joins[plan->stage_index[s]].dim;
+        if (d->kind != SDB_TABLE_DENSE || !d->bits || d->n_slots == 0 || d->n_slots > 0xFFFFFFFFull) continue;
+        const uint64_t padded = align_up(d->n_slots, 128);
+        uint64_t len = std::min<uint64_t>(padded, lds_left * 8u / 128u * 128u);
+        if (q->force_window >= 2) len = std::min<uint64_t>(len, 128ull * (uint64_t)q->force_window);
+        if (len < 128) continue;
+        uint64_t lo = 0;
+        double cover = (double)std::min<uint64_t>(len, d->n_slots) / (double)d->n_slots;
+        if (smp.have) {
+            const uint32_t* hist = &smp.keys[(size_t)bit[s] * kKeyBuckets];
+            cover = -1.0;
+            for (int b = 0; b <= kKeyBuckets; ++b) {
+                // windows starting at a bucket edge, and the one ending at the last slot
+                uint64_t cand = b < kKeyBuckets ? (uint64_t)b * d->n_slots / kKeyBuckets / 128 * 128
+                                                : padded - len;
+                cand = std::min(cand, padded - len);
+                const double c = window_cover(hist, d->n_slots, cand, len);
+                if (c > cover + 1e-12) {
+                    cover = c;
+                    lo = cand;
+                }
+            }
+        }
+        const double gain = reach.of(order, s) * cover;   // rows whose gather the window saves
+        if (gain > best_gain) {
+            best_gain = gain;
+            best = s;
+            best_cover = cover;
+            best_lo = lo;
+            best_len = len;
+        }
+    }
+    if (best < 0) return -1;
+    if (q->force_window == 0 && (!kWindowAuto || best_gain < kWindowMinGain || n_fact < kWindowMinRows)) return -1;
+    plan->stage_lds[best] = LDS_WINDOW;
+    plan->stage_window_lo[best] = (int32_t)best_lo;
+    plan->stage_window_slots[best] = (int32_t)best_len;
+    plan->stage_window_cover[best] = best_cover;
+    return best;
+}
+
 sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, int64_t* counts,
                      int64_t n_groups_capacity) {
     sdb_status st = check_query(q);
@@ -864,9 +1036,10 @@ sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, in
             if (lm != LDS_GLOBAL) {
                 if (k != 1 || q->joins[i].dim->kind != SDB_TABLE_DENSE)
                     return fail(SDB_INVALID_ARG, "plan stage %d: LDS placement needs a dense table", s);
-                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK && lm != LDS_COARSE)
+                if (lm != LDS_MAP && lm != LDS_BITS && lm != LDS_RANK && lm != LDS_COARSE && lm != LDS_WINDOW)
                     return fail(SDB_INVALID_ARG, "plan stage %d: bad LDS mode", s);
-                if ((lm == LDS_BITS || lm == LDS_RANK || lm == LDS_COARSE) && !q->joins[i].dim->bits)
+                if ((lm == LDS_BITS || lm == LDS_RANK || lm == LDS_COARSE || lm == LDS_WINDOW) &&
+                    !q->joins[i].dim->bits)
                     return fail(SDB_INVALID_ARG, "plan stage %d: table has no bitmap", s);
                 if (lm == LDS_RANK && !rank_fits(q->joins[i].dim))
                     return fail(SDB_INVALID_ARG, "plan stage %d: rank tables do not fit LDS", s);
@@ -875,6 +1048,19 @@ sdb_status check_run(const sdb_query* q, const sdb_plan* plan, int64_t* sums, in
                 if (plan->stage_defer[s] != 0 || lm != LDS_BITS)
                     return fail(SDB_INVALID_ARG, "plan stage %d: bad deferred gather", s);
                 ++n_defer;
+            }
+            if (lm == LDS_WINDOW) {
+                const uint64_t lo = (uint64_t)(uint32_t)plan->stage_window_lo[s];
+                const uint64_t len = (uint64_t)(uint32_t)plan->stage_window_slots[s];
+                const uint64_t padded = align_up(q->joins[i].dim->n_slots, 128);
+                if (plan->stage_window_lo[s] < 0 || plan->stage_window_slots[s] <= 0 || lo % 128 || len % 128 ||
+                    lo + len > padded)
+                    return fail(SDB_INVALID_ARG, "plan stage %d: window of %lld slots at %lld outside the table's "
+                                "%llu slots (or not whole 128-slot groups)", s,
+                                (long long)plan->stage_window_slots[s], (long long)plan->stage_window_lo[s],
+                                (unsigned long long)q->joins[i].dim->n_slots);
+            } else if (plan->stage_window_lo[s] != 0 || plan->stage_window_slots[s] != 0) {
+                return fail(SDB_INVALID_ARG, "plan stage %d: window fields without a window", s);
             }
             if (plan->stage_range[s] != 0) {
                 if (plan->stage_range[s] != 1 || k != 1 || lm != LDS_GLOBAL || plan->stage_defer[s] != -1 ||
@@ -1169,6 +1355,10 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         ++n;
     }
     plan->n_stages = n;
+    for (int s = 0; s < n; ++s) plan->stage_pass_alone[s] = plan->stage_pass[s];
+    int bit[SDB_MAX_STAGES];   // query position of the stage at each plan position
+    for (int s = 0; s < n; ++s) bit[s] = s;
+    Sample smp;
     for (int s = 0; s < SDB_MAX_STAGES; ++s) plan->stage_defer[s] = -1;
     if (q->force_range == 1)
         for (int s = 0; s < n; ++s)
@@ -1206,16 +1396,29 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
                         (long long)scratch_bytes, SDB_PLAN_SCRATCH_BYTES);
         hipStream_t s = (hipStream_t)stream;
         FusedParams fp = fused_params(q, plan, false);
+        // key histograms only where a window may be placed (windows are forced, never automatic)
+        for (int i = 0; i < n; ++i) fp.st[i].sample_hist = q->force_window > 0 && q->force_lds != -1;
         const int64_t step = (q->n_fact + 65535) / 65536;
         const int64_t n_sample = (q->n_fact + step - 1) / step;
-        unsigned long long* dcounts = (unsigned long long*)scratch;
-        SDB_HIP(launch_sample(fp, step, n_sample, dcounts, s), "sample launch");
-        unsigned long long hc_stack[kMaxStages];
-        unsigned long long* hc = host_staging() ? static_cast<unsigned long long*>(host_staging()) : hc_stack;
-        SDB_HIP(hipMemcpyAsync(hc, dcounts, sizeof(unsigned long long) * kMaxStages, hipMemcpyDeviceToHost, s),
-                "sample copy");
+        uint32_t* dpattern = (uint32_t*)scratch;
+        uint32_t* dkeys = (uint32_t*)((uint8_t*)scratch + kPatternBytes);
+        SDB_HIP(launch_sample(fp, step, n_sample, dpattern, dkeys, s), "sample launch");
+        std::vector<uint8_t> fallback;
+        uint8_t* host = static_cast<uint8_t*>(host_staging());
+        if (!host) {
+            fallback.resize(kPatternBytes + kKeyHistBytes);
+            host = fallback.data();
+        }
+        const size_t pattern_bytes = sizeof(uint32_t) << n;
+        SDB_HIP(hipMemcpyAsync(host, dpattern, pattern_bytes, hipMemcpyDeviceToHost, s), "sample copy");
+        SDB_HIP(hipMemcpyAsync(host + kPatternBytes, dkeys, sizeof(uint32_t) * kKeyBuckets * (size_t)n,
+                               hipMemcpyDeviceToHost, s), "sample copy");
         SDB_HIP(hipStreamSynchronize(s), "sample sync");
-        for (int i = 0; i < n; ++i) plan->stage_pass[i] = (double)hc[i] / (double)n_sample;
+        joint_from_patterns(reinterpret_cast<const uint32_t*>(host), n, (double)n_sample, &smp);
+        const uint32_t* keys = reinterpret_cast<const uint32_t*>(host + kPatternBytes);
+        smp.keys.assign((size_t)kMaxStages * kKeyBuckets, 0u);
+        std::copy(keys, keys + (size_t)kKeyBuckets * n, smp.keys.begin());
+        for (int i = 0; i < n; ++i) plan->stage_pass[i] = plan->stage_pass_alone[i] = smp.frac(1u << i);
         plan->sampled_rows = n_sample;
     }
 
@@ -1229,11 +1432,12 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
                                    range_eligible(q, plan->stage_index[s]);
     for (int s = 0; s < n; ++s)
         if (plan->stage_kind[s] == 1 && plan->stage_range[s]) slice_j = -1;   // the probe became a compare
-    if (!q->force_order && n > 1) choose_order(q, plan);
-    else {
+    if (!q->force_order && n > 1) {
+        choose_order(q, plan, bit, &smp);
+    } else {
         int order[SDB_MAX_STAGES];
         for (int i = 0; i < n; ++i) order[i] = i;
-        plan->est_cost = order_cost(q, plan, order, n);
+        plan->est_cost = order_cost(q, plan, order, n, Reach{plan, &smp, bit});
     }
     // the first LDS-bitmap stage that carries group keys gathers its code after all stages
     for (int s = 0; s < n; ++s) {
@@ -1264,12 +1468,12 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         while (shift < kPartMaxShift && (1ull << shift) < plan->n_groups) ++shift;
         const uint64_t parts = (plan->n_groups + (1ull << shift) - 1) >> shift;
         const bool fits = parts <= (uint64_t)kPartMaxParts;
-        // chosen automatically for many survivors into a group table too large
-        // for the L2s to hold its per-XCD copies, or many survivors per group
-        const bool big_table = plan->n_groups >= kPartMinGroups;
+        // chosen automatically for many survivors per group (measured: c3,
+        // 55 per group, 2.47 against 2.76 ms with per-XCD atomics; c4, about
+        // 6 per group, 2.52 against 1.63 ms the other way round)
         bool part = term == TERM_PART ||
                     (q->force_terminal == SDB_TERMINAL_AUTO && fits && q->n_fact > 0 && survivors >= 1.0e6 &&
-                     (big_table || survivors >= 512.0 * (double)plan->n_groups));
+                     survivors >= kPartMinPerGroup * (double)plan->n_groups);
         if (part && !fits)
             return fail(SDB_CAPACITY, "partitioned terminal needs at most %d partitions of %d groups",
                         kPartMaxParts, 1 << kPartMaxShift);
@@ -1321,6 +1525,20 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             while (k < n_used && k < kMaxEager && live[k] >= kEagerMinLive) ++k;
         }
         plan->eager = k;
+    }
+
+    // An LDS window for the dense device-memory stage it helps most; with it a
+    // block's LDS leaves room for one block per CU, so 4-row items run in
+    // blocks of 1024 (16 waves per CU).
+    if (plan->vector && plan->ipt <= 2 && plan->eager == 0 && slice_j < 0 &&
+        (q->force_block == 0 || q->force_block == kBigBlock)) {
+        const int block_before = plan->block;
+        plan->block = kBigBlock;
+        plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
+        if (place_window(q, plan, smp, bit, q->n_fact) < 0) plan->block = block_before;
+    } else if (q->force_window > 0 && slice_j < 0) {
+        plan->lds_bytes = (int32_t)lds_layout(q, plan, nullptr);
+        place_window(q, plan, smp, bit, q->n_fact);
     }
 
     // LDS rank tables instead of the deferred gather of a bitmap stage's code.

@@ -267,6 +267,32 @@ __device__ __forceinline__ void stage_coarse(const StageDev& S, const unsigned c
     add_group<W, IPT>(S, c, gid);
 }
 
+// Pass bitmap of a window of the key range in LDS, the device map behind it:
+// a row whose slot falls in the window and whose bit is clear dies without a
+// device-memory gather; every other live row gathers its code (for a row in
+// the window that passed, only for its group key). One gather instruction
+// serves both; rows that do not gather read slot 0, a line every such lane
+// shares.
+template <int W, int IPT, int WB>
+__device__ __forceinline__ void stage_window(const StageDev& S, const unsigned char* lds, const int32_t (&x)[IPT][W],
+                                             bool (&al)[IPT][W], uint32_t (&gid)[IPT][W]) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(lds + S.lds_off);
+    uint32_t c[IPT][W];
+    SDB_ROWS(j, r) {
+        const uint32_t idx = (uint32_t)(x[j][r] - S.kmin);
+        const bool ok = al[j][r] && idx < S.nslots;
+        const uint32_t w = idx - S.win_lo;
+        const bool inw = w < S.win_slots;
+        const uint32_t wi = inw ? w : 0u;
+        const bool bit = ((words[wi >> 5] >> (wi & 31u)) & 1u) != 0u;
+        const bool need = ok && (bit || !inw);
+        c[j][r] = ld_code<WB>(S.map, need ? idx : 0u);
+        al[j][r] = need;
+    }
+    SDB_ROWS(j, r) al[j][r] = al[j][r] && c[j][r] < S.sentinel;
+    add_group<W, IPT>(S, c, gid);
+}
+
 // PAIR: the home slot and the next one come from one 16-byte load at 8-byte
 // alignment (global loads on gfx950 need 4-byte alignment only): one memory
 // request instead of two. Measured on c5, it pays when the slots are in L2,
@@ -369,6 +395,9 @@ __device__ __forceinline__ void run_stage(const FusedParams& p, const unsigned c
         case OP_COARSE1: stage_coarse<W, IPT, 1>(S, lds, x, al, gid); break;
         case OP_COARSE2: stage_coarse<W, IPT, 2>(S, lds, x, al, gid); break;
         case OP_COARSE4: stage_coarse<W, IPT, 4>(S, lds, x, al, gid); break;
+        case OP_WINDOW1: stage_window<W, IPT, 1>(S, lds, x, al, gid); break;
+        case OP_WINDOW2: stage_window<W, IPT, 2>(S, lds, x, al, gid); break;
+        case OP_WINDOW4: stage_window<W, IPT, 4>(S, lds, x, al, gid); break;
         default:   // OP_NEVER
             SDB_ROWS(j, r) al[j][r] = false;
             break;

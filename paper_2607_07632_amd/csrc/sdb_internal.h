@@ -45,7 +45,10 @@ enum StageOp : int32_t {
     OP_COARSE1 = 13,    // coarse pass bitmap in LDS, then the device map, 1/2/4-byte codes
     OP_COARSE2 = 14,
     OP_COARSE4 = 15,
-    OP_HASH_PAIR = 16   // OP_HASH reading the home slot and the next with one 16-byte load
+    OP_HASH_PAIR = 16,  // OP_HASH reading the home slot and the next with one 16-byte load
+    OP_WINDOW1 = 17,    // pass bitmap of a key window in LDS, the device map outside it, 1/2/4-byte codes
+    OP_WINDOW2 = 18,
+    OP_WINDOW4 = 19
 };
 // How a table's code becomes part of the group id.
 enum GroupMode : int32_t { GK_NONE = 0, GK_ONE = 1, GK_GENERAL = 2 };
@@ -54,7 +57,8 @@ enum LdsMode : int32_t {
     LDS_MAP = SDB_LDS_MAP,
     LDS_BITS = SDB_LDS_BITS,
     LDS_RANK = SDB_LDS_RANK,
-    LDS_COARSE = SDB_LDS_COARSE
+    LDS_COARSE = SDB_LDS_COARSE,
+    LDS_WINDOW = SDB_LDS_WINDOW
 };
 enum Terminal : int32_t { TERM_SCALAR = 1, TERM_LDS = 2, TERM_GLOBAL = 3, TERM_PART = 4 };
 
@@ -118,8 +122,16 @@ struct StageDev {
     // which then points at the coarse bitmap in the run scratch) covers
     // slots [j << coarse_shift, (j + 1) << coarse_shift)
     int32_t coarse_shift;
-    int32_t pad_;
+    // LDS_WINDOW: the staged bitmap (at lds_off, staged from `bits`, which then
+    // points at the window's first word) covers slots [win_lo, win_lo + win_slots)
+    uint32_t win_lo;
+    uint32_t win_slots;
+    int32_t sample_hist;   // planner sampling: 1 = histogram this dense stage's keys
 };
+// sampling: key histogram buckets per dense stage; pass-pattern bins a block
+// counts in LDS (plans of up to 12 stages)
+constexpr int kKeyBuckets = 256;
+constexpr int kSamplePatternsLds = 4096;
 
 // Derives a coarse pass bitmap (LDS_COARSE) from a dense table's pass bitmap.
 struct CoarseParams {
@@ -300,8 +312,10 @@ hipError_t launch_zero_pair(unsigned long long* a, unsigned long long* b, uint64
 hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s);
 // table fill, then dense scatter + pass bitmap or hash inserts, of every table
 hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s);
-hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
-                         unsigned long long* pass_counts, hipStream_t s);
+// Planner sampling: pass-pattern histogram (2^nstages uint32) and per-stage
+// key histograms (kMaxStages x kKeyBuckets uint32), both zeroed first.
+hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, uint32_t* pattern_hist,
+                         uint32_t* key_hist, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if
 // the instance does not exist.
 // `unroll`: the instance whose stage loop is written out kUnrollStages times

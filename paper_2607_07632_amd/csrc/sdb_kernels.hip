@@ -519,44 +519,59 @@ hipError_t launch_rank_build(const RankParams& rp, hipStream_t s) {
 // plan sampling: pass count of every stage on its own over a strided sample
 // ---------------------------------------------------------------------------
 
+// Every sampled row (row k * step) is evaluated against every stage on its
+// own; the pattern of stages it passes (bit s for stage s) is counted in
+// pattern_hist, and for a dense-table stage the bucket of its key in the
+// table's key range (kKeyBuckets equal buckets) in key_hist[s].
 __global__ void __launch_bounds__(256) sample_kernel(FusedParams kernel_args, int64_t step, int64_t n_sample,
-                                                     unsigned long long* pass_counts) {
+                                                     uint32_t* pattern_hist, uint32_t* key_hist) {
     (void)kernel_args;
     const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
-    __shared__ unsigned int cnt[kMaxStages];
-    if (threadIdx.x < kMaxStages) cnt[threadIdx.x] = 0u;
+    // block-private histograms in LDS (the few pass patterns of a small plan
+    // would otherwise draw every sampled row's atomic onto a handful of words)
+    __shared__ uint32_t kh[kMaxStages * kKeyBuckets];
+    __shared__ uint32_t ph[kSamplePatternsLds];
+    const uint32_t n_patterns = 1u << p.nstages;
+    const bool lds_patterns = n_patterns <= (uint32_t)kSamplePatternsLds;
+    for (int i = threadIdx.x; i < p.nstages * kKeyBuckets; i += blockDim.x) kh[i] = 0u;
+    for (uint32_t i = threadIdx.x; lds_patterns && i < n_patterns; i += blockDim.x) ph[i] = 0u;
     __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    // every lane runs the same number of iterations so the wave-wide votes below are complete
-    const int64_t n_iter = (n_sample + stride - 1) / stride;
-    for (int64_t it = 0; it < n_iter; ++it) {
-        const int64_t k = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-        const bool valid = k < n_sample;
-        const int64_t row = valid ? k * step : 0;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n_sample; k += stride) {
+        const int64_t row = k * step;
+        uint32_t pattern = 0u;
         for (int s = 0; s < p.nstages; ++s) {
             const StageDev& S = p.st[s];
-            bool pass = false;
-            if (valid) pass = stage_pass_one(S, p.cols[S.col][row]);
-            const unsigned long long m = __ballot(pass);
-            if ((threadIdx.x & 63) == 0 && m) atomicAdd(&cnt[s], (unsigned int)__popcll(m));
+            const int32_t x = p.cols[S.col][row];
+            if (stage_pass_one(S, x)) pattern |= 1u << s;
+            if (S.sample_hist && S.kind == ST_DENSE && S.nslots > 0u) {
+                const uint32_t idx = (uint32_t)(x - S.kmin);
+                if (idx < S.nslots)
+                    atomicAdd(&kh[s * kKeyBuckets + (uint32_t)((uint64_t)idx * kKeyBuckets / S.nslots)], 1u);
+            }
         }
+        if (lds_patterns) atomicAdd(&ph[pattern], 1u);
+        else atomicAdd(&pattern_hist[pattern], 1u);
     }
     __syncthreads();
-    if (threadIdx.x < p.nstages && cnt[threadIdx.x])
-        atomicAdd(&pass_counts[threadIdx.x], (unsigned long long)cnt[threadIdx.x]);
+    for (int i = threadIdx.x; i < p.nstages * kKeyBuckets; i += blockDim.x)
+        if (kh[i]) atomicAdd(&key_hist[i], kh[i]);
+    for (uint32_t i = threadIdx.x; lds_patterns && i < n_patterns; i += blockDim.x)
+        if (ph[i]) atomicAdd(&pattern_hist[i], ph[i]);
 }
 
-hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample,
-                         unsigned long long* pass_counts, hipStream_t s) {
-    hipLaunchKernelGGL(fill_u64_kernel, dim3(1), dim3(64), 0, s, pass_counts, (uint64_t)kMaxStages);
-    hipError_t e = hipGetLastError();
+hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, uint32_t* pattern_hist,
+                         uint32_t* key_hist, hipStream_t s) {
+    if (p.nstages < 0 || p.nstages > kMaxStages) return hipErrorInvalidValue;
+    hipError_t e = launch_fill_u32(pattern_hist, 1ull << p.nstages, 0u, s);
+    if (e != hipSuccess) return e;
+    e = launch_fill_u32(key_hist, (uint64_t)kMaxStages * kKeyBuckets, 0u, s);
     if (e != hipSuccess || n_sample == 0 || p.nstages == 0) return e;
     int64_t g = (n_sample + 255) / 256;
     if (g > 256) g = 256;
-    hipLaunchKernelGGL(sample_kernel, dim3((int)g), dim3(256), 0, s, p, step, n_sample, pass_counts);
+    hipLaunchKernelGGL(sample_kernel, dim3((int)g), dim3(256), 0, s, p, step, n_sample, pattern_hist, key_hist);
     return hipGetLastError();
 }
-
 
 // Adds the per-XCD copies into the outputs (which it overwrites).
 __global__ void __launch_bounds__(256) xcd_merge_kernel(const unsigned long long* xtab, int copies,
@@ -619,6 +634,7 @@ hipError_t launch_fused(const FusedParams& p, int vector, int ipt, int terminal,
     void* args[] = {const_cast<FusedParams*>(&p)};
     return hipLaunchKernel(fn, dim3(grid), dim3(block), args, lds_bytes, s);
 }
+
 
 // ---------------------------------------------------------------------------
 // kernel-at-a-time execution: one kernel per operator, flags and group ids in

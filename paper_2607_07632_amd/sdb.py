@@ -28,7 +28,7 @@ MAX_FACT_PREDS = 8
 MAX_JOINS = 6
 MAX_GROUP_KEYS = 4
 MAX_STAGES = MAX_FACT_PREDS + MAX_JOINS
-PLAN_SCRATCH_BYTES = 256
+PLAN_SCRATCH_BYTES = 81920
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
 OPS = {"eq": 0, "ne": 1, "lt": 2, "le": 3, "gt": 4, "ge": 5, "between": 6}
@@ -37,7 +37,7 @@ AGGS = {"col": 0, "mul": 1, "sub": 2, "add": 3}
 TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3, "part": 4}
 BASELINES = {"per_operator": 0, "global_handoff": 1}
 TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global", 4: "part"}
-LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank", 4: "lds_coarse"}
+LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank", 4: "lds_coarse", 5: "lds_window"}
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
           4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
 
@@ -93,14 +93,17 @@ class SdbQuery(C.Structure):
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
                 ("force_block", i32), ("force_range", i32), ("force_coarse", i32),
-                ("force_slice", i32), ("force_unroll", i32), ("reserved_", i32)]
+                ("force_slice", i32), ("force_unroll", i32), ("force_window", i32)]
 
 
 class SdbPlan(C.Structure):
     _fields_ = [("n_stages", i32), ("stage_kind", i32 * MAX_STAGES),
                 ("stage_index", i32 * MAX_STAGES), ("stage_pass", C.c_double * MAX_STAGES),
+                ("stage_pass_alone", C.c_double * MAX_STAGES),
                 ("stage_lds", i32 * MAX_STAGES), ("stage_defer", i32 * MAX_STAGES),
                 ("stage_range", i32 * MAX_STAGES), ("stage_coarse", i32 * MAX_STAGES),
+                ("stage_window_lo", i32 * MAX_STAGES), ("stage_window_slots", i32 * MAX_STAGES),
+                ("stage_window_cover", C.c_double * MAX_STAGES),
                 ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
                 ("vector", i32), ("eager", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
                 ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
@@ -353,9 +356,10 @@ class StarQuery:
     list of DimTable per join (``build_dims``); ``query`` the plain-data
     description. ``force`` may hold terminal ('scalar'|'lds'|'global'|'part'),
     ipt, vector (1 / -1), order (True = keep query order), grid, lds, xcd,
-    eager, block, range (-1: no key-range probes), coarse and slice (-1: no
-    sliced hash probe, 1: wherever allowed), the sdb_query force_* fields of
-    the same names.
+    eager, block, range (-1: no key-range probes), coarse, slice (-1: no
+    sliced hash probe, 1: wherever allowed), unroll and window (-1: no LDS
+    window, 1: the largest that fits, k >= 2: at most 128 k slots), the
+    sdb_query force_* fields of the same names.
     """
 
     def __init__(self, fact: dict, tables: list, query: dict, force: dict | None = None):
@@ -419,6 +423,7 @@ class StarQuery:
         q.force_coarse = int(force.get("coarse", 0))
         q.force_slice = int(force.get("slice", 0))
         q.force_unroll = int(force.get("unroll", 0))
+        q.force_window = int(force.get("window", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -551,13 +556,16 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
         if query is not None:
             name = (query["fact_preds"][i]["col"] if kind == 0 else query["joins"][i]["dim"])
         st = {"kind": "pred" if kind == 0 else "probe", "index": i, "name": name,
-              "pass": round(plan.stage_pass[s], 6)}
+              "pass": round(plan.stage_pass[s], 6), "pass_alone": round(plan.stage_pass_alone[s], 6)}
         if kind == 1 and plan.stage_range[s]:
             st["table"] = "key_range"
         elif kind == 1:
             st["table"] = LDS_NAMES.get(plan.stage_lds[s], plan.stage_lds[s])
             if plan.stage_coarse[s]:
                 st["coarse_slots_per_bit"] = 1 << plan.stage_coarse[s]
+            if plan.stage_lds[s] == 5:
+                st["window"] = [int(plan.stage_window_lo[s]), int(plan.stage_window_slots[s])]
+                st["window_cover"] = round(plan.stage_window_cover[s], 6)
             if plan.stage_defer[s] >= 0:
                 st["deferred_gather"] = True
             if plan.slice_bits and s == plan.slice_stage:

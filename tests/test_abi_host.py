@@ -39,7 +39,7 @@ def test_struct_layout_matches_binding():
     assert L.sdb_struct_sizes(sizes, 9) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
     assert L.sdb_struct_sizes(sizes, 10) == 1
-    assert L.sdb_abi_version() == 8
+    assert L.sdb_abi_version() == 9
 
 
 def test_status_strings():
@@ -317,7 +317,7 @@ def test_unroll_choice_and_validation():
     assert _plan(q).unroll == 0                            # no unrolled instance for ipt 1
     L = sdb.lib()
     p = sdb.SdbPlan()
-    for field, bad in [("force_unroll", 1), ("force_unroll", -2), ("reserved_", 1)]:
+    for field, bad in [("force_unroll", 1), ("force_unroll", -2), ("force_window", -2)]:
         qb = _query([d], [(0, 0)])
         setattr(qb, field, bad)
         assert L.sdb_plan_star_query(C.byref(qb), None, 0, None, C.byref(p)) == 1, (field, bad)
@@ -510,3 +510,55 @@ def test_plan_block_and_items_per_lane():
     with pytest.raises(sdb.SdbError) as e:
         _plan(qq)
     assert e.value.name == "SDB_INVALID_ARG"
+
+
+def test_window_placement_and_validation():
+    """LDS windows (SDB_LDS_WINDOW) on the host: the planner's choice under the
+    overrides, its LDS and block size, and the run's refusal of inconsistent
+    window fields before any launch."""
+    big = _fake_dim(n_rows=3_000_000, n_pass=600_000, n_slots=3_000_000, with_bitmap=True)
+    q = _query([big], [(0, 0)])
+    q.force_window = 1
+    p = _plan(q)
+    assert p.stage_lds[0] == 5 and p.stage_defer[0] == -1 and p.block == 1024
+    lo, slots = p.stage_window_lo[0], p.stage_window_slots[0]
+    assert lo == 0 and slots % 128 == 0 and 500_000 < slots < 1_300_000
+    assert abs(p.stage_window_cover[0] - slots / 3_000_000) < 1e-9     # no sample: the share of the key range
+    assert p.terminal == 2 and p.lds_bytes == 16 * p.n_groups + slots // 8 <= 152 * 1024   # LDS group table first
+    assert sdb.plan_summary(p)["stages"][0]["window"] == [0, slots]
+    q.force_window = 4
+    p4 = _plan(q)
+    assert p4.stage_window_slots[0] == 512 and p4.lds_bytes == 16 * p4.n_groups + 64
+    q.force_window = -1
+    assert _plan(q).stage_lds[0] == 0
+    q.force_window = 0                                   # 1,000 fact rows: too few for the staging copy
+    assert _plan(q).stage_lds[0] == 0
+    mid = _fake_dim(n_rows=300_000, n_pass=60_000, n_slots=300_000, with_bitmap=True)   # bitmap over 32 KB
+    qm = _query([mid], [(0, 0)])
+    qm.force_window = 1
+    pm = _plan(qm)
+    assert pm.stage_lds[0] == 5 and pm.stage_window_slots[0] == 300_032 and pm.stage_window_lo[0] == 0
+    assert pm.stage_window_cover[0] == 1.0
+    qm.force_lds = -1                                    # no LDS staging at all: no window either
+    assert _plan(qm).stage_lds[0] == 0
+    small = _fake_dim(n_rows=1000, n_pass=500, n_slots=1000, with_bitmap=True)
+    qs = _query([small], [(0, 0)])
+    qs.force_window = 1
+    assert _plan(qs).stage_lds[0] == 1                   # a small map sits in LDS whole
+    nobits = _fake_dim(n_rows=3_000_000, n_pass=600_000, n_slots=3_000_000)
+    qn = _query([nobits], [(0, 0)])
+    qn.force_window = 1
+    assert _plan(qn).stage_lds[0] == 0                   # no pass bitmap, no window
+    L = sdb.lib()
+    q.force_window = 4
+    for field, value in [("stage_window_lo", 64), ("stage_window_lo", -128), ("stage_window_slots", 100),
+                         ("stage_window_slots", 0), ("stage_window_lo", 3_000_064), ("stage_defer", 1),
+                         ("stage_defer", 0), ("stage_lds", 0)]:
+        pb = sdb.SdbPlan.from_buffer_copy(p4)
+        getattr(pb, field)[0] = value
+        assert L.sdb_run_star_query(C.byref(q), C.byref(pb), 0x1000, 0x2000, 1 << 20, None, 0, None) == 1, \
+            (field, value)
+    filt = _query([big], [])                             # a filter-only table gets its window too
+    filt.force_window = 4
+    pf = _plan(filt)
+    assert pf.stage_lds[0] == 5 and pf.stage_defer[0] == -1

@@ -363,6 +363,120 @@ def test_build_statistics_match_numpy():
     assert np.array_equal(unpacked, ok)
 
 
+def _stage_masks(w, rows):
+    """Pass mask of every stage (query order: predicates, then joins) on the
+    given fact rows, by direct indexing (dimension keys are row numbers here)."""
+    masks = []
+    for p in w.query["fact_preds"]:
+        masks.append(oracle.eval_pred(w.fact[p["col"]][rows], p))
+    for jd in w.query["joins"]:
+        t = w.dims[jd["dim"]]
+        keys = t[w.dim_keys[jd["dim"]]].astype(np.int64)
+        assert np.array_equal(keys, np.arange(keys.size))
+        ok = np.ones(keys.size, dtype=bool)
+        for p in jd["preds"]:
+            ok &= oracle.eval_pred(t[p["col"]], p)
+        fk = w.fact[jd["fact_key"]][rows].astype(np.int64)
+        inr = (fk >= 0) & (fk < keys.size)
+        masks.append(inr & ok[np.clip(fk, 0, keys.size - 1)])
+    return masks
+
+
+@pytest.mark.parametrize("name", ["c1_scalar_scan", "c3_star3", "c4_star4_zipf"])
+def test_plan_pass_fractions_are_the_sampled_conditional_fractions(name):
+    """Each stage's pass fraction in the plan is the fraction of sampled rows
+    passing it among those passing every earlier stage, exactly as counted
+    on the sampled rows."""
+    w = workload(name)
+    _, q = run_gpu(w)
+    p = q.plan_obj
+    n = w.n_fact
+    step = (n + 65535) // 65536
+    rows = np.arange(0, n, step)
+    assert p.sampled_rows == rows.size
+    masks = _stage_masks(w, rows)
+    n_preds = len(w.query["fact_preds"])
+    live = np.ones(rows.size, dtype=bool)
+    for s in range(p.n_stages):
+        m = masks[p.stage_index[s] + (n_preds if p.stage_kind[s] == 1 else 0)]
+        assert abs(p.stage_pass_alone[s] - m.mean()) < 1e-12
+        want = (live & m).sum() / live.sum() if live.sum() else None
+        if want is not None:
+            assert abs(p.stage_pass[s] - want) < 1e-12, (s, p.stage_pass[s], want)
+        live &= m
+
+
+def test_correlated_predicates_are_priced_jointly():
+    """Two predicates on one column that each pass most rows but jointly few
+    (qty < 30 and qty >= 28): the plan's second stage passes about 2/29 of the
+    rows the first leaves, not the marginal product; results are exact."""
+    w0 = workload("c1_scalar_scan")
+    q = {**w0.query, "fact_preds": [{"col": "qty", "op": "lt", "lo": 30, "hi": None},
+                                    {"col": "qty", "op": "ge", "lo": 28, "hi": None},
+                                    {"col": "disc", "op": "between", "lo": 2, "hi": 4}]}
+    w = datagen.Workload("c1 correlated", w0.n_fact, w0.fact, w0.dims, w0.dim_keys, q)
+    got, sq = run_gpu(w)
+    p = sq.plan_obj
+    f = 1.0
+    for s in range(p.n_stages):
+        f *= p.stage_pass[s]
+    qty = w.fact["qty"]
+    live = ((qty < 30) & (qty >= 28) & (w.fact["disc"] >= 2) & (w.fact["disc"] <= 4) &
+            (w.dims["date"]["year"][w.fact["date_key"]] == 1994))
+    assert abs(f - live.mean()) < 0.002                   # joint estimate within sampling error
+    alone = 1.0
+    for s in range(p.n_stages):
+        alone *= p.stage_pass_alone[s]
+    assert alone > 3 * f                                  # the independence estimate would be far off
+    assert_same(got.as_rows(), oracle_rows(w), "correlated predicates")
+
+
+_WINDOW_FORCES = [{"window": 1}, {"window": 7}, {"window": 64, "terminal": "part"},
+                  {"window": 1, "terminal": "global"}, {"window": 2, "ipt": 1}, {"window": 1, "vector": -1},
+                  {"window": 300, "eager": 2}, {"window": 1, "lds": 3}, {"window": 1, "unroll": -1},
+                  {"window": 1, "block": 512}, {"window": 9, "order": True}]
+
+
+@pytest.mark.parametrize("name", ["c3_star3", "c4_star4_zipf"])
+@pytest.mark.parametrize("force", _WINDOW_FORCES)
+def test_lds_window_plans_agree(name, force):
+    """LDS windows over the device-memory dense tables (c3's customer map, c4's
+    part and customer maps): rows inside and outside the window, deferred
+    codes, every terminal and item shape, against the oracle."""
+    w = workload(name)
+    got, q = run_gpu(w, force=force)
+    windows = [s for s in range(q.plan_obj.n_stages) if q.plan_obj.stage_lds[s] == 5]
+    assert len(windows) == 1, f"{name} {force}: no window placed"
+    assert_same(got.as_rows(), want_rows(name), f"{name} {force}")
+
+
+def test_lds_window_follows_the_sampled_keys():
+    """Fact keys concentrated in the upper third of the customer key range:
+    the sampled key histogram moves the window there; results stay exact."""
+    w0 = workload("c3_star3")
+    fact = dict(w0.fact)
+    fact["cust_key"] = (2_000_000 + w0.fact["cust_key"] % 1_000_000).astype(np.int32)
+    w = datagen.Workload("c3 keys in the upper third", w0.n_fact, fact, w0.dims, w0.dim_keys, w0.query)
+    got, q = run_gpu(w, force={"window": 1})
+    p = q.plan_obj
+    s = next(s for s in range(p.n_stages) if p.stage_lds[s] == 5)
+    lo, slots = p.stage_window_lo[s], p.stage_window_slots[s]
+    assert lo < 3_000_000 and lo + slots > 2_000_000
+    assert p.stage_window_cover[s] >= min(1.0, slots / 1_000_000) - 0.02
+    assert_same(got.as_rows(), oracle_rows(w), "keys in the upper third")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_lds_window_on_random_schemas(seed):
+    """Random schemas with dimensions large enough that their pass bitmaps are
+    not staged whole: windows of several sizes, against the oracle."""
+    w = random_tiny_workload(seed + 5000, max_fact=60_000, max_dim_rows=400_000, n_fact=50_003)
+    want = oracle_rows(w)
+    for win in (1, 3, 40):
+        got, _ = run_gpu(w, force={"window": win})
+        assert_same(got.as_rows(), want, f"seed {seed} window {win}")
+
+
 @pytest.mark.parametrize("name", ["c3_star3", "c4_star4_zipf", "c5_hash_stress", "c1_scalar_scan"])
 def test_dim_info_of_built_tables(name):
     """sdb_dim_info through the ABI against numpy over the dimension columns."""

@@ -17,7 +17,7 @@ from hypothesis import HealthCheck, given, settings, strategies as st
 from paper_2607_07632_amd import sdb
 
 OK, INVALID_ARG, UNSUPPORTED, CAPACITY, HIP_ERROR = 0, 1, 2, 3, 7
-LDS_GLOBAL, LDS_MAP, LDS_BITS, LDS_RANK, LDS_COARSE = 0, 1, 2, 3, 4
+LDS_GLOBAL, LDS_MAP, LDS_BITS, LDS_RANK, LDS_COARSE, LDS_WINDOW = 0, 1, 2, 3, 4, 5
 
 
 @st.composite
@@ -99,6 +99,7 @@ def queries(draw):
     q.force_coarse = draw(st.integers(-1, 5))
     q.force_slice = draw(st.sampled_from([-1, 0, 1, 1]))
     q.force_unroll = draw(st.sampled_from([-1, 0, 0]))
+    q.force_window = draw(st.sampled_from([-1, 0, 0, 1, 2, 7]))
     return q, ds
 
 
@@ -110,12 +111,24 @@ def check_plan(q, p):
     defers = 0
     for s in range(n):
         kind, idx, lds = p.stage_kind[s], p.stage_index[s], p.stage_lds[s]
-        assert lds in (LDS_GLOBAL, LDS_MAP, LDS_BITS, LDS_RANK, LDS_COARSE)
+        assert lds in (LDS_GLOBAL, LDS_MAP, LDS_BITS, LDS_RANK, LDS_COARSE, LDS_WINDOW)
         if lds != LDS_GLOBAL:
             d = q.joins[idx].dim.contents
             assert kind == 1 and d.kind == 1
-            if lds in (LDS_BITS, LDS_RANK, LDS_COARSE):
+            if lds in (LDS_BITS, LDS_RANK, LDS_COARSE, LDS_WINDOW):
                 assert d.bits
+        if lds == LDS_WINDOW:
+            d = q.joins[idx].dim.contents
+            lo, slots = p.stage_window_lo[s], p.stage_window_slots[s]
+            assert lo % 128 == 0 and slots % 128 == 0 and slots > 0 and lo >= 0
+            assert lo + slots <= (d.n_slots + 127) // 128 * 128
+            assert q.force_window != -1 and q.force_lds != -1
+            if q.force_window >= 2:
+                assert slots <= 128 * q.force_window
+            assert 0.0 <= p.stage_window_cover[s] <= 1.0
+            assert p.stage_defer[s] == -1
+        else:
+            assert p.stage_window_lo[s] == 0 and p.stage_window_slots[s] == 0
         assert (lds == LDS_COARSE) == (p.stage_coarse[s] != 0)
         if lds == LDS_COARSE:
             assert 1 <= p.stage_coarse[s] <= 5
@@ -129,6 +142,7 @@ def check_plan(q, p):
             defers += 1
             assert lds == LDS_BITS
     assert defers <= 1
+    assert sum(p.stage_lds[s] == LDS_WINDOW for s in range(n)) <= 1
     assert p.terminal in (1, 2, 3, 4)
     assert (p.terminal == 1) <= (q.n_group_keys == 0)
     assert p.ipt in (1, 2, 4) and p.block in (64, 128, 256, 512, 1024)
