@@ -21,6 +21,9 @@ Generation recipe (stated once, used everywhere):
   frequent key.
 * ``index`` is the row number (dense primary keys, as in the benchmark the
   paper uses); ``perm n`` is one seeded permutation of ``0..n-1``.
+* ``ramp lo hi n`` gives row ``i`` of an ``n``-row column the value
+  ``lo + i * (hi - lo + 1) // n``: rows sorted by that column, each value
+  holding an equal run of rows (a fact table clustered by date).
 * The date dimension has one row per day ``d`` in ``0..2555`` with
   ``year = 1992 + d // 365`` (integer floor). That formula gives eight years,
   the last (1999) holding day 2555 only.
@@ -51,6 +54,7 @@ N_DAYS = 2556
 class Col:
     name: str
     dist: tuple          # ("uniform", lo, hi) | ("zipf", n, s) | ("index",) | ("perm", n) | ("year_of_day",)
+                         # | ("ramp", lo, hi, n)
     stream: int = 0
 
 
@@ -214,6 +218,16 @@ _register(Config(
     "SUM(value) GROUP BY attr through a 2^25-slot open-addressing table",
 ))
 
+_c3 = CONFIGS["c3_star3"]
+_register(Config(
+    6, "c3d_star3_date_sorted", FULL_ROWS,
+    tuple(Col("date_key", ("ramp", 0, N_DAYS - 1, FULL_ROWS)) if c.name == "date_key" else c for c in _c3.fact_cols),
+    _c3.dims,
+    _c3.query,
+    "c3's query over fact rows sorted by date (each day an equal run of rows): the date filter's pass "
+    "fraction changes along the table",
+))
+
 CONFIG_ORDER = ["c1_scalar_scan", "c2_join_group", "c3_star3", "c4_star4_zipf", "c5_hash_stress"]
 
 
@@ -247,6 +261,11 @@ def _chunk_values(config_id: int, col: Col, chunk: int, lo_row: int, hi_row: int
         base = chunk * CHUNK
         d = np.arange(base + lo_row, base + hi_row, dtype=np.int64)
         return (1992 + d // 365).astype(np.int32)
+    if kind == "ramp":
+        _, lo, hi, n_total = col.dist
+        base = chunk * CHUNK
+        i = np.arange(base + lo_row, base + hi_row, dtype=np.int64)
+        return (lo + i * (hi - lo + 1) // n_total).astype(np.int32)
     rng = _rng(config_id, col.stream, chunk)
     if kind == "uniform":
         _, lo, hi = col.dist

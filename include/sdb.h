@@ -82,6 +82,8 @@ enum { SDB_TERMINAL_AUTO = 0, SDB_TERMINAL_SCALAR = 1, SDB_TERMINAL_LDS = 2,
 #define SDB_MAX_JOINS 6
 #define SDB_MAX_GROUP_KEYS 4
 #define SDB_MAX_STAGES (SDB_MAX_FACT_PREDS + SDB_MAX_JOINS)
+/* row ranges of a plan whose stage order changes along the fact table */
+#define SDB_MAX_SEGMENTS 8
 #define SDB_PLAN_SCRATCH_BYTES 81920
 /* fact columns the fused kernel can load eagerly (sdb_plan.eager) */
 #define SDB_MAX_EAGER 4
@@ -102,9 +104,15 @@ typedef struct sdb_pred {
  *  preds[]      conjunctive filter on the dimension rows (Section 3.3)
  *  payload_cols attributes to gather for passing rows (group keys), 0..3
  *  kind         SDB_TABLE_*; AUTO picks DENSE when the key range is at most
- *               max(2 * n_rows, 1024) slots, else HASH (the paper checks the
- *               key range at run time and falls back to a hash table, 4.3)
- *  load_factor  HASH only; 0 means 0.5 (the paper's double-sized table) */
+ *               max(2 * n_rows, 1024) slots, or when the dense table fits
+ *               dense_budget_bytes, else HASH (the paper checks the key range
+ *               at run time and falls back to a hash table, 4.3)
+ *  load_factor  HASH only; 0 means 0.5 (the paper's double-sized table)
+ *  dense_budget_bytes  the memory budget of that runtime choice: a dense
+ *               table (packed map plus pass bitmap) of at most this many
+ *               bytes is built whatever its key range (one load per probe
+ *               instead of a hash chain, paid for in memory); 0: the key-range
+ *               rule alone. sdb_dim_required_bytes grows to hold it. */
 typedef struct sdb_dim_desc {
     const int32_t* key;
     int64_t n_rows;
@@ -116,6 +124,7 @@ typedef struct sdb_dim_desc {
     int32_t payload_cols[SDB_MAX_PAYLOADS];
     int32_t kind;
     double load_factor;
+    int64_t dense_budget_bytes;
 } sdb_dim_desc;
 
 /* A built lookup table: a plain handle into the caller's workspace.
@@ -228,6 +237,10 @@ typedef struct sdb_agg {
  *  force_unroll    the fused kernel with its stage loop written out
  *                  (sdb_plan.unroll): 0: wherever the plan allows it; -1:
  *                  never
+ *  force_segments  stage orders per row range (sdb_plan.n_segments): 0: the
+ *                  planner's choice; -1: one order for the whole table; 1:
+ *                  a range gets an order of its own wherever its sampled
+ *                  rows favour one, however small the modelled gain
  *  force_window    LDS windows (SDB_LDS_WINDOW): 0: the planner's choice
  *                  (none: measured on MI355X, a window does not pay); -1:
  *                  none; 1: the largest window that fits without lowering
@@ -258,6 +271,8 @@ typedef struct sdb_query {
     int32_t force_slice;
     int32_t force_unroll;
     int32_t force_window;
+    int32_t force_segments;
+    int32_t reserved_;                    /* 0 */
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -360,6 +375,17 @@ typedef struct sdb_plan {
                                              at most 4 stages, 4-row items, ipt 2, blocks of 512
                                              or 1024, no eager loads and no hash-table probe;
                                              0 otherwise */
+    int32_t n_segments;                   /* 1, or 2 .. SDB_MAX_SEGMENTS row ranges that run the
+                                             stages in orders of their own (mid-scan reordering:
+                                             the sample is split by row range, each range's order
+                                             is chosen on its own pass patterns, and neighbours
+                                             with equal orders are merged); the fused kernel is
+                                             launched once per segment over its rows, every
+                                             launch adding into the same terminal */
+    int32_t segment_order[SDB_MAX_SEGMENTS][SDB_MAX_STAGES];   /* segment g runs the plan's stages
+                                             (positions 0 .. n_stages - 1) in this order */
+    int64_t segment_start[SDB_MAX_SEGMENTS + 1];   /* first fact row of each segment (multiples of
+                                             4096); segment_start[n_segments] = n_fact */
 } sdb_plan;
 /* most partitions of the sliced hash probe: 2^SDB_MAX_SLICE_BITS */
 #define SDB_MAX_SLICE_BITS 10
@@ -386,8 +412,9 @@ SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n);
 
 /* Host only. Workspace bytes sdb_build_dim needs for `desc`: 256 bytes of
  * statistics, then the lookup table sized by an upper bound (a DENSE map of
- * max(2 * n_rows, 1024) 4-byte slots plus its pass bitmap, and/or a HASH
- * table of next_pow2(n_rows / load_factor) 8-byte slots). */
+ * max(2 * n_rows, 1024) 4-byte slots plus its pass bitmap, or
+ * dense_budget_bytes plus 512 bytes of alignment when that is larger, and/or
+ * a HASH table of next_pow2(n_rows / load_factor) 8-byte slots). */
 SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* bytes);
 
 /* Builds the lookup table for `desc` into `workspace` (device, 256-byte

@@ -150,6 +150,10 @@ sdb_status device_info(DeviceInfo* out) {
 
 constexpr uint64_t kStatsBytes = 256;
 
+// dense tables within a memory budget: key ranges up to 2^31 slots
+constexpr int64_t kMaxDenseBudget = 1ll << 36;
+constexpr uint64_t kMaxDenseSlots = 1ull << 31;
+
 uint64_t dense_slot_limit(int64_t n_rows) {
     return std::max<uint64_t>(2 * (uint64_t)n_rows, (uint64_t)kDenseSlack);
 }
@@ -192,6 +196,9 @@ sdb_status check_dim_desc(const sdb_dim_desc* d) {
             return fail(SDB_INVALID_ARG, "payload %d names column %d of %d", p, d->payload_cols[p], d->n_cols);
     if (d->kind < SDB_TABLE_AUTO || d->kind > SDB_TABLE_HASH)
         return fail(SDB_INVALID_ARG, "bad table kind %d", d->kind);
+    if (d->dense_budget_bytes < 0 || d->dense_budget_bytes > kMaxDenseBudget)
+        return fail(SDB_INVALID_ARG, "dense_budget_bytes %lld outside 0..%lld", (long long)d->dense_budget_bytes,
+                    (long long)kMaxDenseBudget);
     if (d->kind != SDB_TABLE_DENSE) {
         const double lf = effective_lf(d);
         if (!(lf > 0.0 && lf <= 0.9)) return fail(SDB_INVALID_ARG, "load factor %g outside (0, 0.9]", lf);
@@ -203,7 +210,10 @@ sdb_status check_dim_desc(const sdb_dim_desc* d) {
 
 uint64_t required_bytes(const sdb_dim_desc* d) {
     uint64_t table = 0;
-    if (d->kind != SDB_TABLE_HASH) table = std::max(table, dense_bytes(dense_slot_limit(d->n_rows), 4));
+    if (d->kind != SDB_TABLE_HASH) {
+        table = std::max(table, dense_bytes(dense_slot_limit(d->n_rows), 4));
+        if (d->dense_budget_bytes > 0) table = std::max(table, (uint64_t)d->dense_budget_bytes + 512u);
+    }
     if (d->kind != SDB_TABLE_DENSE) table = std::max(table, hash_capacity(d->n_rows, effective_lf(d)) * 8);
     return kStatsBytes + table;
 }
@@ -296,6 +306,9 @@ sdb_status check_query(const sdb_query* q) {
         return fail(SDB_INVALID_ARG, "force_unroll %d is not -1 or 0", q->force_unroll);
     if (q->force_window < -1 || q->force_window > (1 << 24))
         return fail(SDB_INVALID_ARG, "force_window %d is not in -1..2^24", q->force_window);
+    if (q->force_segments < -1 || q->force_segments > 1)
+        return fail(SDB_INVALID_ARG, "force_segments %d is not -1, 0 or 1", q->force_segments);
+    if (q->reserved_ != 0) return fail(SDB_INVALID_ARG, "sdb_query.reserved_ must be 0");
     return SDB_OK;
 }
 
@@ -618,6 +631,70 @@ void choose_order(const sdb_query* q, sdb_plan* plan, int* bit, const Sample* sm
     plan->est_cost = best_cost;
 }
 
+// Mid-scan reordering: each run of sampled rows (range) gets the order with
+// the least modelled cost on its own pass patterns; neighbouring ranges with
+// equal orders merge into one segment. Kept when the modelled cost over all
+// ranges drops by at least kSegmentMinGain against the table's single order
+// (any drop when forced), on tables of at least kSegmentMinRows rows, in at
+// most SDB_MAX_SEGMENTS segments. Segment starts are the first sampled row of
+// each range, rounded down to a multiple of kSegmentAlign rows.
+constexpr double kSegmentMinGain = 0.03;
+constexpr int64_t kSegmentMinRows = 1ll << 24;
+constexpr int64_t kSegmentAlign = 4096;
+
+void choose_segments(const sdb_query* q, sdb_plan* plan, const int* bit, const std::vector<Sample>& ranges,
+                     int64_t step, int64_t n_sample, std::vector<double>* seg_survivors) {
+    const int n = plan->n_stages, R = (int)ranges.size();
+    if (n > 7 || R < 2) return;
+    std::vector<std::vector<int>> best(R);
+    double base = 0.0, tuned = 0.0;
+    std::vector<int> ident(n);
+    for (int i = 0; i < n; ++i) ident[i] = i;
+    for (int r = 0; r < R; ++r) {
+        const Reach reach{plan, &ranges[r], bit};
+        std::vector<int> order = ident;
+        const double c0 = order_cost(q, plan, order.data(), n, reach);
+        double bc = c0;
+        best[r] = order;
+        while (std::next_permutation(order.begin(), order.end())) {
+            const double c = order_cost(q, plan, order.data(), n, reach);
+            if (c < bc - 1e-12) {
+                bc = c;
+                best[r] = order;
+            }
+        }
+        base += c0;
+        tuned += bc;
+    }
+    // merge neighbours with equal orders
+    std::vector<int> first;   // first range of each segment
+    for (int r = 0; r < R; ++r)
+        if (r == 0 || best[r] != best[r - 1]) first.push_back(r);
+    const int segs = (int)first.size();
+    const bool forced = q->force_segments == 1;
+    if (segs < 2 || segs > SDB_MAX_SEGMENTS) return;
+    if (!forced && (q->n_fact < kSegmentMinRows || base <= 0.0 || (base - tuned) / base < kSegmentMinGain)) return;
+    int64_t start[SDB_MAX_SEGMENTS + 1];
+    for (int g = 0; g < segs; ++g) {
+        const int64_t k = ((int64_t)first[g] * n_sample + R - 1) / R;   // first sampled row of the range
+        start[g] = g == 0 ? 0 : std::min<int64_t>(k * step, q->n_fact) / kSegmentAlign * kSegmentAlign;
+    }
+    start[segs] = q->n_fact;
+    for (int g = 1; g <= segs; ++g)
+        if (start[g] <= start[g - 1]) return;   // a range too short for its own segment
+    plan->n_segments = segs;
+    for (int g = 0; g < segs; ++g)
+        for (int i = 0; i < n; ++i) plan->segment_order[g][i] = best[first[g]][i];
+    for (int g = 0; g <= segs; ++g) plan->segment_start[g] = start[g];
+    // survivors per segment: each range's sampled fraction passing every stage
+    const uint32_t all = (uint32_t)((1ull << n) - 1);
+    seg_survivors->assign(segs, 0.0);
+    for (int r = 0, g = 0; r < R; ++r) {
+        if (g + 1 < segs && r >= first[g + 1]) ++g;
+        (*seg_survivors)[g] += ranges[r].frac(all) * (double)q->n_fact / R;
+    }
+}
+
 // LDS placement: dense tables, smallest first, as the whole map when it fits
 // the remaining budget, else as the pass bitmap, else left in device memory.
 void place_lds(const sdb_query* q, sdb_plan* plan, uint64_t budget) {
@@ -767,7 +844,8 @@ struct PartLayout {
 
 PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
     PartLayout L;
-    const uint64_t grid = (uint64_t)plan->grid, P = (uint64_t)plan->n_parts;
+    // one region per block of every launch (a segmented plan launches once per segment)
+    const uint64_t grid = (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments), P = (uint64_t)plan->n_parts;
     const uint64_t recs = grid * (uint64_t)plan->part_cap;
     const uint64_t vbytes = records_wide(q) ? 8 : 4;
     // aggregation work items: at most one partial chunk per partition plus full chunks
@@ -1201,11 +1279,17 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
         out->domain = domain;
 
         const uint64_t range = n > 0 ? (uint64_t)((int64_t)out->key_max - (int64_t)out->key_min + 1) : 0;
+        // the runtime dense-or-hash choice: by key range, or by the memory budget
+        const int code_width = domain <= 0xFEull ? 1 : (domain <= 0xFFFEull ? 2 : 4);
+        const bool in_budget = desc->dense_budget_bytes > 0 && range <= kMaxDenseSlots &&
+                               dense_bytes(range, code_width) <= (uint64_t)desc->dense_budget_bytes;
+        const bool dense_ok = range <= dense_slot_limit(n) || in_budget;
         int kind = desc->kind;
-        if (kind == SDB_TABLE_AUTO) kind = range <= dense_slot_limit(n) ? SDB_TABLE_DENSE : SDB_TABLE_HASH;
-        if (kind == SDB_TABLE_DENSE && range > dense_slot_limit(n))
-            return fail(SDB_KEY_RANGE, "dimension %d: key range %llu exceeds the dense limit %llu", d,
-                        (unsigned long long)range, (unsigned long long)dense_slot_limit(n));
+        if (kind == SDB_TABLE_AUTO) kind = dense_ok ? SDB_TABLE_DENSE : SDB_TABLE_HASH;
+        if (kind == SDB_TABLE_DENSE && !dense_ok)
+            return fail(SDB_KEY_RANGE, "dimension %d: key range %llu exceeds the dense limit %llu and the dense "
+                        "budget of %lld bytes", d, (unsigned long long)range,
+                        (unsigned long long)dense_slot_limit(n), (long long)desc->dense_budget_bytes);
         kinds[d] = kind;
         out->kind = kind;
         out->stats = workspaces[d];
@@ -1359,6 +1443,9 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     int bit[SDB_MAX_STAGES];   // query position of the stage at each plan position
     for (int s = 0; s < n; ++s) bit[s] = s;
     Sample smp;
+    std::vector<Sample> range_smp;   // per run of sampled rows (segmented plans)
+    int n_ranges = 1;
+    int64_t sample_step = 0, sample_n = 0;
     for (int s = 0; s < SDB_MAX_STAGES; ++s) plan->stage_defer[s] = -1;
     if (q->force_range == 1)
         for (int s = 0; s < n; ++s)
@@ -1402,19 +1489,36 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         const int64_t n_sample = (q->n_fact + step - 1) / step;
         uint32_t* dpattern = (uint32_t*)scratch;
         uint32_t* dkeys = (uint32_t*)((uint8_t*)scratch + kPatternBytes);
-        SDB_HIP(launch_sample(fp, step, n_sample, dpattern, dkeys, s), "sample launch");
+        // the sampled rows split into runs of rows for per-range stage orders
+        n_ranges = (q->force_segments != -1 && n <= kSampleRangeStages && n_sample >= 64 * kSampleRanges)
+                       ? kSampleRanges : 1;
+        SDB_HIP(launch_sample(fp, step, n_sample, n_ranges, dpattern, dkeys, s), "sample launch");
         std::vector<uint8_t> fallback;
         uint8_t* host = static_cast<uint8_t*>(host_staging());
         if (!host) {
             fallback.resize(kPatternBytes + kKeyHistBytes);
             host = fallback.data();
         }
-        const size_t pattern_bytes = sizeof(uint32_t) << n;
+        const size_t pattern_bytes = (sizeof(uint32_t) << n) * (size_t)n_ranges;
         SDB_HIP(hipMemcpyAsync(host, dpattern, pattern_bytes, hipMemcpyDeviceToHost, s), "sample copy");
         SDB_HIP(hipMemcpyAsync(host + kPatternBytes, dkeys, sizeof(uint32_t) * kKeyBuckets * (size_t)n,
                                hipMemcpyDeviceToHost, s), "sample copy");
         SDB_HIP(hipStreamSynchronize(s), "sample sync");
-        joint_from_patterns(reinterpret_cast<const uint32_t*>(host), n, (double)n_sample, &smp);
+        const uint32_t* ph = reinterpret_cast<const uint32_t*>(host);
+        std::vector<uint32_t> whole((size_t)1 << n, 0u);
+        range_smp.resize(n_ranges);
+        for (int r = 0; r < n_ranges; ++r) {
+            const uint32_t* h = ph + ((size_t)r << n);
+            double rows = 0.0;
+            for (size_t m = 0; m < whole.size(); ++m) {
+                whole[m] += h[m];
+                rows += h[m];
+            }
+            if (n_ranges > 1) joint_from_patterns(h, n, rows, &range_smp[r]);
+        }
+        joint_from_patterns(whole.data(), n, (double)n_sample, &smp);
+        sample_step = step;
+        sample_n = n_sample;
         const uint32_t* keys = reinterpret_cast<const uint32_t*>(host + kPatternBytes);
         smp.keys.assign((size_t)kMaxStages * kKeyBuckets, 0u);
         std::copy(keys, keys + (size_t)kKeyBuckets * n, smp.keys.begin());
@@ -1439,6 +1543,14 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
         for (int i = 0; i < n; ++i) order[i] = i;
         plan->est_cost = order_cost(q, plan, order, n, Reach{plan, &smp, bit});
     }
+    // stage orders of their own for runs of rows that favour one
+    plan->n_segments = 1;
+    for (int i = 0; i < n; ++i) plan->segment_order[0][i] = i;
+    plan->segment_start[0] = 0;
+    plan->segment_start[1] = q->n_fact;
+    std::vector<double> seg_survivors;
+    if (n_ranges > 1 && slice_j < 0 && q->force_eager <= 0)
+        choose_segments(q, plan, bit, range_smp, sample_step, sample_n, &seg_survivors);
     // the first LDS-bitmap stage that carries group keys gathers its code after all stages
     for (int s = 0; s < n; ++s) {
         if (plan->stage_kind[s] != 1 || plan->stage_lds[s] != LDS_BITS) continue;
@@ -1594,11 +1706,22 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             if (st != SDB_OK) return st;
             plan->grid = grid;
         }
-        const double cap_total = std::min((double)q->n_fact, 1.5 * survivors + 256.0 * plan->grid);
+        // records per block: 1.5 x the survivors the busiest launch (segment) expects
+        double seg_rows = (double)q->n_fact, seg_surv = survivors;
+        if (plan->n_segments > 1) {
+            seg_rows = 0.0;
+            seg_surv = 0.0;
+            for (int g = 0; g < plan->n_segments; ++g) {
+                seg_rows = std::max(seg_rows, (double)(plan->segment_start[g + 1] - plan->segment_start[g]));
+                seg_surv = std::max(seg_surv, seg_survivors[g]);
+            }
+        }
+        const double cap_total = std::min(seg_rows, 1.5 * seg_surv + 256.0 * plan->grid);
         plan->part_cap = (int64_t)std::ceil(cap_total / plan->grid);
         plan->part_cap = (int64_t)align_up((uint64_t)std::max<int64_t>(plan->part_cap, 64), 64);
-        if ((uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFF0ull)
-            plan->part_cap = (int64_t)(0xFFFFFFF0ull / (uint64_t)plan->grid) / 64 * 64;
+        const uint64_t regions = (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments);
+        if ((uint64_t)plan->part_cap * regions > 0xFFFFFFF0ull)
+            plan->part_cap = (int64_t)(0xFFFFFFF0ull / regions) / 64 * 64;
         plan->run_scratch_bytes = (int64_t)stage_bytes + (int64_t)part_layout(q, plan).total;
     }
     if (slice_j >= 0) {
@@ -1623,8 +1746,30 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         if (plan->grid <= 0 || plan->part_cap <= 0 || plan->part_shift < 0 || plan->part_shift > kPartMaxShift ||
             plan->n_parts <= 0 || plan->n_parts > kPartMaxParts ||
             (uint64_t)plan->n_parts != ((plan->n_groups + (1ull << plan->part_shift) - 1) >> plan->part_shift) ||
-            (uint64_t)plan->part_cap * (uint64_t)plan->grid > 0xFFFFFFFFull)
+            (uint64_t)plan->part_cap * (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments) >
+                0xFFFFFFFFull)
             return fail(SDB_INVALID_ARG, "bad partitioned-terminal plan");
+    }
+    if (plan->n_segments < 0 || plan->n_segments > SDB_MAX_SEGMENTS)
+        return fail(SDB_INVALID_ARG, "bad plan n_segments %d", plan->n_segments);
+    if (plan->n_segments > 1) {
+        if (plan->eager != 0 || plan->slice_bits != 0)
+            return fail(SDB_INVALID_ARG, "a segmented plan needs no eager loads and no table slices");
+        if (plan->segment_start[0] != 0 || plan->segment_start[plan->n_segments] != q->n_fact)
+            return fail(SDB_INVALID_ARG, "plan segments do not cover the fact rows");
+        for (int g = 0; g < plan->n_segments; ++g) {
+            const int64_t a = plan->segment_start[g], b = plan->segment_start[g + 1];
+            if (b <= a || a % kSegmentAlign != 0)
+                return fail(SDB_INVALID_ARG, "plan segment %d: rows %lld .. %lld (starts are increasing "
+                            "multiples of %lld)", g, (long long)a, (long long)b, (long long)kSegmentAlign);
+            bool seen[SDB_MAX_STAGES] = {false};
+            for (int i = 0; i < plan->n_stages; ++i) {
+                const int o = plan->segment_order[g][i];
+                if (o < 0 || o >= plan->n_stages || seen[o])
+                    return fail(SDB_INVALID_ARG, "plan segment %d: the order is not a permutation of the stages", g);
+                seen[o] = true;
+            }
+        }
     }
     if (plan->terminal == TERM_SCALAR && q->n_group_keys > 0)
         return fail(SDB_INVALID_ARG, "scalar terminal on a grouped query");
@@ -1797,7 +1942,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         pp.n_groups = plan->n_groups;
         pp.part_shift = plan->part_shift;
         pp.n_parts = (uint32_t)plan->n_parts;
-        pp.n_regions = (uint32_t)plan->grid;
+        pp.n_regions = (uint32_t)((uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments));
         pp.part_cap = (uint32_t)plan->part_cap;
         pp.region_count = p.region_count;
         pp.rec_gid = p.rec_gid;
@@ -1823,9 +1968,27 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         const bool timed = g_fused_start && g_fused_stop;
         if (timed) SDB_HIP(hipEventRecord(g_fused_start, s), "event record");
         if (sliced) SDB_HIP(launch_slice_partition(sp, plan->slice_grid, s), "slice passes launch");
-        SDB_HIP(launch_fused(p, plan->vector, plan->ipt, plan->terminal, plan->eager, plan->unroll, grid,
-                             plan->block, lds_bytes, s),
-                "fused kernel launch");
+        const int segs = std::max(1, plan->n_segments);
+        p.n_regions = (uint32_t)((uint64_t)grid * (uint64_t)segs);
+        for (int g = 0; g < segs; ++g) {
+            // segment g: its rows, its stage order, its own block regions
+            FusedParams pg = p;
+            if (segs > 1) {
+                const int64_t a = plan->segment_start[g], b = plan->segment_start[g + 1];
+                for (int c = 0; c < q->n_cols; ++c) pg.cols[c] = q->cols[c] + a;
+                pg.n = b - a;
+                pg.defer_stage = -1;
+                for (int i = 0; i < plan->n_stages; ++i) {
+                    const int o = plan->segment_order[g][i];
+                    pg.st[i] = p.st[o];
+                    if (o == p.defer_stage) pg.defer_stage = i;
+                }
+                pg.region_base = (uint32_t)((uint64_t)g * (uint64_t)grid);
+            }
+            SDB_HIP(launch_fused(pg, plan->vector, plan->ipt, plan->terminal, plan->eager, plan->unroll, grid,
+                                 plan->block, lds_bytes, s),
+                    "fused kernel launch");
+        }
         if (timed) SDB_HIP(hipEventRecord(g_fused_stop, s), "event record");
         if (plan->terminal == TERM_PART) SDB_HIP(launch_part_passes(pp, s), "partition passes launch");
     }

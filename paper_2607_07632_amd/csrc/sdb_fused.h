@@ -518,8 +518,9 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
         ts.ring_val = lds + p.ring_off + (size_t)wave * kRing * 8u;
         ts.ring_gid = reinterpret_cast<uint32_t*>(lds + p.ring_off + (blockDim.x >> 6) * kRing * 8u) +
                       (size_t)wave * kRing;
-        ts.rgid = p.rec_gid + (uint64_t)blockIdx.x * p.part_cap;
-        ts.rval = static_cast<unsigned char*>(p.rec_val) + (uint64_t)blockIdx.x * p.part_cap * vbytes;
+        const uint64_t region = (uint64_t)p.region_base + blockIdx.x;   // launches of a segmented plan
+        ts.rgid = p.rec_gid + region * p.part_cap;
+        ts.rval = static_cast<unsigned char*>(p.rec_val) + region * p.part_cap * vbytes;
     }
     // stage the LDS-resident dimension tables (16-byte copies; sources are padded)
     for (int s = 0; s < p.nstages; ++s) {
@@ -602,10 +603,11 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
     } else if constexpr (TERM == TERM_PART) {
         if (ts.pend) part_flush(p, ts, ts.pend);
         __syncthreads();
-        if (threadIdx.x == 0) p.region_count[blockIdx.x] = min(*ts.lfill, p.part_cap);
+        const uint32_t region = p.region_base + blockIdx.x;
+        if (threadIdx.x == 0) p.region_count[region] = min(*ts.lfill, p.part_cap);
         // this block's column of the partition x block histogram
         for (uint32_t q = threadIdx.x; q < p.n_parts; q += blockDim.x)
-            p.part_hist[(uint64_t)q * gridDim.x + blockIdx.x] = ts.lhist[q];
+            p.part_hist[(uint64_t)q * p.n_regions + region] = ts.lhist[q];
     }
 }
 

@@ -132,6 +132,9 @@ struct StageDev {
 // counts in LDS (plans of up to 12 stages)
 constexpr int kKeyBuckets = 256;
 constexpr int kSamplePatternsLds = 4096;
+// sampled row ranges for segmented plans (plans of up to kSampleRangeStages stages)
+constexpr int kSampleRanges = 16;
+constexpr int kSampleRangeStages = 10;
 
 // Derives a coarse pass bitmap (LDS_COARSE) from a dense table's pass bitmap.
 struct CoarseParams {
@@ -174,7 +177,9 @@ struct FusedParams {
     uint32_t* region_count;    // records each block wrote
     uint32_t* rec_gid;
     void* rec_val;             // int64 values if rec_wide, else int32
-    uint32_t* part_hist;       // records per (partition, block): [q * gridDim.x + block]
+    uint32_t* part_hist;       // records per (partition, region): [q * n_regions + region]
+    uint32_t region_base;      // region of block 0 (a segmented plan launches once per segment)
+    uint32_t n_regions;        // regions of all launches
     uint32_t part_cap;
     int32_t part_shift;
     uint32_t n_parts;
@@ -312,10 +317,11 @@ hipError_t launch_zero_pair(unsigned long long* a, unsigned long long* b, uint64
 hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s);
 // table fill, then dense scatter + pass bitmap or hash inserts, of every table
 hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s);
-// Planner sampling: pass-pattern histogram (2^nstages uint32) and per-stage
-// key histograms (kMaxStages x kKeyBuckets uint32), both zeroed first.
-hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, uint32_t* pattern_hist,
-                         uint32_t* key_hist, hipStream_t s);
+// Planner sampling: pass-pattern histograms (n_ranges x 2^nstages uint32: the
+// sampled rows split into n_ranges equal runs) and per-stage key histograms
+// (kMaxStages x kKeyBuckets uint32), both zeroed first.
+hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, int32_t n_ranges,
+                         uint32_t* pattern_hist, uint32_t* key_hist, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if
 // the instance does not exist.
 // `unroll`: the instance whose stage loop is written out kUnrollStages times

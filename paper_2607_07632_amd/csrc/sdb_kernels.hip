@@ -524,14 +524,14 @@ hipError_t launch_rank_build(const RankParams& rp, hipStream_t s) {
 // pattern_hist, and for a dense-table stage the bucket of its key in the
 // table's key range (kKeyBuckets equal buckets) in key_hist[s].
 __global__ void __launch_bounds__(256) sample_kernel(FusedParams kernel_args, int64_t step, int64_t n_sample,
-                                                     uint32_t* pattern_hist, uint32_t* key_hist) {
+                                                     int32_t n_ranges, uint32_t* pattern_hist, uint32_t* key_hist) {
     (void)kernel_args;
     const FusedParams& p = *(const FusedParams*)__builtin_amdgcn_kernarg_segment_ptr();
     // block-private histograms in LDS (the few pass patterns of a small plan
     // would otherwise draw every sampled row's atomic onto a handful of words)
     __shared__ uint32_t kh[kMaxStages * kKeyBuckets];
     __shared__ uint32_t ph[kSamplePatternsLds];
-    const uint32_t n_patterns = 1u << p.nstages;
+    const uint32_t n_patterns = (uint32_t)n_ranges << p.nstages;
     const bool lds_patterns = n_patterns <= (uint32_t)kSamplePatternsLds;
     for (int i = threadIdx.x; i < p.nstages * kKeyBuckets; i += blockDim.x) kh[i] = 0u;
     for (uint32_t i = threadIdx.x; lds_patterns && i < n_patterns; i += blockDim.x) ph[i] = 0u;
@@ -550,8 +550,9 @@ __global__ void __launch_bounds__(256) sample_kernel(FusedParams kernel_args, in
                     atomicAdd(&kh[s * kKeyBuckets + (uint32_t)((uint64_t)idx * kKeyBuckets / S.nslots)], 1u);
             }
         }
-        if (lds_patterns) atomicAdd(&ph[pattern], 1u);
-        else atomicAdd(&pattern_hist[pattern], 1u);
+        const uint32_t bin = (uint32_t)(k * n_ranges / n_sample) << p.nstages | pattern;
+        if (lds_patterns) atomicAdd(&ph[bin], 1u);
+        else atomicAdd(&pattern_hist[bin], 1u);
     }
     __syncthreads();
     for (int i = threadIdx.x; i < p.nstages * kKeyBuckets; i += blockDim.x)
@@ -560,16 +561,18 @@ __global__ void __launch_bounds__(256) sample_kernel(FusedParams kernel_args, in
         if (ph[i]) atomicAdd(&pattern_hist[i], ph[i]);
 }
 
-hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, uint32_t* pattern_hist,
-                         uint32_t* key_hist, hipStream_t s) {
-    if (p.nstages < 0 || p.nstages > kMaxStages) return hipErrorInvalidValue;
-    hipError_t e = launch_fill_u32(pattern_hist, 1ull << p.nstages, 0u, s);
+hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, int32_t n_ranges,
+                         uint32_t* pattern_hist, uint32_t* key_hist, hipStream_t s) {
+    if (p.nstages < 0 || p.nstages > kMaxStages || n_ranges < 1 || ((uint64_t)n_ranges << p.nstages) > (1ull << kMaxStages))
+        return hipErrorInvalidValue;
+    hipError_t e = launch_fill_u32(pattern_hist, (uint64_t)n_ranges << p.nstages, 0u, s);
     if (e != hipSuccess) return e;
     e = launch_fill_u32(key_hist, (uint64_t)kMaxStages * kKeyBuckets, 0u, s);
     if (e != hipSuccess || n_sample == 0 || p.nstages == 0) return e;
     int64_t g = (n_sample + 255) / 256;
     if (g > 256) g = 256;
-    hipLaunchKernelGGL(sample_kernel, dim3((int)g), dim3(256), 0, s, p, step, n_sample, pattern_hist, key_hist);
+    hipLaunchKernelGGL(sample_kernel, dim3((int)g), dim3(256), 0, s, p, step, n_sample, n_ranges, pattern_hist,
+                       key_hist);
     return hipGetLastError();
 }
 

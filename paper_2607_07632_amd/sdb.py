@@ -28,6 +28,7 @@ MAX_FACT_PREDS = 8
 MAX_JOINS = 6
 MAX_GROUP_KEYS = 4
 MAX_STAGES = MAX_FACT_PREDS + MAX_JOINS
+MAX_SEGMENTS = 8
 PLAN_SCRATCH_BYTES = 81920
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -51,7 +52,8 @@ class SdbPred(C.Structure):
 class SdbDimDesc(C.Structure):
     _fields_ = [("key", vp), ("n_rows", i64), ("n_cols", i32), ("cols", vp * MAX_DIM_COLS),
                 ("n_preds", i32), ("preds", SdbPred * MAX_DIM_PREDS), ("n_payloads", i32),
-                ("payload_cols", i32 * MAX_PAYLOADS), ("kind", i32), ("load_factor", C.c_double)]
+                ("payload_cols", i32 * MAX_PAYLOADS), ("kind", i32), ("load_factor", C.c_double),
+                ("dense_budget_bytes", i64)]
 
 
 class SdbDim(C.Structure):
@@ -93,7 +95,8 @@ class SdbQuery(C.Structure):
                 ("force_vector", i32), ("force_order", i32), ("grid_blocks", i32),
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
                 ("force_block", i32), ("force_range", i32), ("force_coarse", i32),
-                ("force_slice", i32), ("force_unroll", i32), ("force_window", i32)]
+                ("force_slice", i32), ("force_unroll", i32), ("force_window", i32), ("force_segments", i32),
+                ("reserved_", i32)]
 
 
 class SdbPlan(C.Structure):
@@ -110,7 +113,9 @@ class SdbPlan(C.Structure):
                 ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
                 ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64),
-                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("unroll", i32)]
+                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("unroll", i32),
+                ("n_segments", i32), ("segment_order", (i32 * MAX_STAGES) * MAX_SEGMENTS),
+                ("segment_start", i64 * (MAX_SEGMENTS + 1))]
 
 
 STRUCTS = [SdbPred, SdbDimDesc, SdbDim, SdbJoin, SdbGroupKey, SdbAgg, SdbQuery, SdbPlan, SdbDimSummary]
@@ -238,10 +243,12 @@ def dim_required_bytes(desc: SdbDimDesc) -> int:
 
 
 def dim_desc(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
-             load_factor: float = 0.0) -> SdbDimDesc:
+             load_factor: float = 0.0, dense_budget_bytes: int = 0) -> SdbDimDesc:
     """The C descriptor of one dimension: ``key`` and the values of ``cols``
     are int32 device tensors of equal length; ``preds`` are predicate dicts
-    naming columns of ``cols``; ``payloads`` name the columns to gather."""
+    naming columns of ``cols``; ``payloads`` name the columns to gather;
+    ``dense_budget_bytes`` lets a dense table of that size be built whatever
+    its key range."""
     names = list(cols)
     if len(names) > MAX_DIM_COLS:
         raise ValueError("too many dimension columns")
@@ -265,14 +272,15 @@ def dim_desc(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
         d.payload_cols[i] = idx[p]
     d.kind = TABLES[kind]
     d.load_factor = float(load_factor or 0.0)
+    d.dense_budget_bytes = int(dense_budget_bytes or 0)
     return d
 
 
 def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
-              load_factor: float = 0.0, stream=None, workspace=None) -> DimTable:
+              load_factor: float = 0.0, stream=None, workspace=None, dense_budget_bytes: int = 0) -> DimTable:
     """Builds the lookup table of one dimension (arguments as dim_desc)."""
     import torch
-    d = dim_desc(key, cols, preds, payloads, kind, load_factor)
+    d = dim_desc(key, cols, preds, payloads, kind, load_factor, dense_budget_bytes)
     need = dim_required_bytes(d)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=key.device)
@@ -303,7 +311,7 @@ def _join_inputs(dims: dict, dim_keys: dict, jd: dict):
     for n in [p["col"] for p in jd.get("preds", [])] + list(jd.get("payloads", [])):
         cols.setdefault(n, t[n])
     return (t[dim_keys[jd["dim"]]], cols, jd.get("preds", []), list(jd.get("payloads", [])),
-            jd.get("kind", "auto"), jd.get("load_factor", 0.0))
+            jd.get("kind", "auto"), jd.get("load_factor", 0.0), jd.get("dense_budget_bytes", 0))
 
 
 def build_dims(dims: dict, dim_keys: dict, query: dict, stream=None, workspaces=None) -> list:
@@ -359,7 +367,9 @@ class StarQuery:
     eager, block, range (-1: no key-range probes), coarse, slice (-1: no
     sliced hash probe, 1: wherever allowed), unroll and window (-1: no LDS
     window, 1: the largest that fits, k >= 2: at most 128 k slots), the
-    sdb_query force_* fields of the same names.
+    sdb_query force_* fields of the same names, and segments (-1: one stage
+    order for the whole table, 1: an order per row range wherever the
+    sampled rows favour one).
     """
 
     def __init__(self, fact: dict, tables: list, query: dict, force: dict | None = None):
@@ -424,6 +434,7 @@ class StarQuery:
         q.force_slice = int(force.get("slice", 0))
         q.force_unroll = int(force.get("unroll", 0))
         q.force_window = int(force.get("window", 0))
+        q.force_segments = int(force.get("segments", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -576,6 +587,9 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
             "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
             "n_parts": plan.n_parts, "part_cap": int(plan.part_cap),
             "slice_bits": plan.slice_bits, "slice_grid": plan.slice_grid, "unroll": plan.unroll,
+            "segments": [{"rows": [int(plan.segment_start[g]), int(plan.segment_start[g + 1])],
+                          "order": [int(plan.segment_order[g][i]) for i in range(plan.n_stages)]}
+                         for g in range(plan.n_segments)] if plan.n_segments > 1 else None,
             "est_cost": round(plan.est_cost, 4),
             "n_groups": int(plan.n_groups), "sampled_rows": int(plan.sampled_rows),
             "radix": [int(plan.radix[k]) for k in range(plan.n_group_keys)]}

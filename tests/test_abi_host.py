@@ -8,6 +8,7 @@ import re
 
 import pytest
 
+from conftest import GPU_PRESENT
 from paper_2607_07632_amd import sdb
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -71,6 +72,16 @@ def test_required_bytes_bounds():
     assert a == max(dense, h)
     big = sdb.dim_required_bytes(_desc(1 << 24, "hash", lf=0.5))
     assert big == 256 + (1 << 25) * 8            # 256 MiB table at load factor 0.5
+    budget = _desc(1000, "auto")
+    budget.dense_budget_bytes = 1 << 20
+    assert sdb.dim_required_bytes(budget) == 256 + (1 << 20) + 512      # room for a dense table of the budget
+    budget.kind = sdb.TABLES["hash"]
+    assert sdb.dim_required_bytes(budget) == h                          # a hash table ignores it
+    for bad in (-1, 1 << 40):
+        budget.dense_budget_bytes = bad
+        with pytest.raises(sdb.SdbError) as e:
+            sdb.dim_required_bytes(budget)
+        assert e.value.name == "SDB_INVALID_ARG"
 
 
 @pytest.mark.parametrize("mutate,status", [
@@ -562,3 +573,43 @@ def test_window_placement_and_validation():
     filt.force_window = 4
     pf = _plan(filt)
     assert pf.stage_lds[0] == 5 and pf.stage_defer[0] == -1
+
+
+def test_segment_validation():
+    """A plan with stage orders per row range: the run checks the segments
+    (cover the rows, start at multiples of 4096, each order a permutation,
+    no eager loads) before any launch."""
+    a = _fake_dim(n_rows=200_000, n_pass=40_000, n_slots=200_000)
+    b = _fake_dim(n_rows=200_000, n_pass=100_000, n_slots=200_000)
+    q = _query([a, b], [(0, 0)], n_fact=100_000)
+    q.force_order = 1
+    p = _plan(q)
+    assert p.n_segments == 1 and p.segment_start[0] == 0 and p.segment_start[1] == 100_000
+    assert list(p.segment_order[0][:2]) == [0, 1]
+    L = sdb.lib()
+
+    def status(pl):
+        return L.sdb_run_star_query(C.byref(q), C.byref(pl), 0x1000, 0x2000, 1 << 20, 0x100000,
+                                    1 << 30, None)
+
+    good = sdb.SdbPlan.from_buffer_copy(p)
+    good.n_segments = 2
+    good.segment_start[1], good.segment_start[2] = 8192, 100_000
+    good.segment_order[1][0], good.segment_order[1][1] = 1, 0
+    if not GPU_PRESENT:
+        assert status(good) != 1, sdb.lib().sdb_last_error()    # valid: the launch itself fails without a GPU
+    assert sdb.plan_summary(good)["segments"][1] == {"rows": [8192, 100_000], "order": [1, 0]}
+    for mutate in [lambda x: x.segment_start.__setitem__(1, 8000),        # not a multiple of 4096
+                   lambda x: x.segment_start.__setitem__(2, 99_999),      # does not reach n_fact
+                   lambda x: x.segment_start.__setitem__(1, 0),           # empty segment
+                   lambda x: x.segment_order[1].__setitem__(0, 0),        # not a permutation
+                   lambda x: x.segment_order[1].__setitem__(1, 5),
+                   lambda x: setattr(x, "n_segments", 9),
+                   lambda x: setattr(x, "eager", 1)]:
+        bad = sdb.SdbPlan.from_buffer_copy(good)
+        mutate(bad)
+        assert status(bad) == 1
+    for field, value in [("force_segments", 2), ("force_segments", -2), ("reserved_", 1)]:
+        qb = sdb.SdbQuery.from_buffer_copy(q)
+        setattr(qb, field, value)
+        assert L.sdb_plan_star_query(C.byref(qb), None, 0, None, C.byref(sdb.SdbPlan())) == 1

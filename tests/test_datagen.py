@@ -26,6 +26,21 @@ def test_value_ranges(name):
             assert v.min() >= col.dist[1] and v.max() <= col.dist[2]
         if col.dist[0] == "zipf":
             assert v.min() >= 0 and v.max() < col.dist[1]
+        if col.dist[0] == "ramp":
+            assert np.all(np.diff(v) >= 0) and v[0] == col.dist[1]
+
+
+def test_date_sorted_variant():
+    """The date-sorted c3 variant: every day holds an equal run of rows (up to
+    one row), in ascending order; the other columns follow c3's recipe with
+    seeds of their own."""
+    n = 600_000_000
+    ends = datagen.fact_column("c3d_star3_date_sorted", "date_key", n - 5, n)
+    assert list(ends) == [2555] * 5
+    mid = datagen.fact_column("c3d_star3_date_sorted", "date_key", 300_000_000 - 2, 300_000_000 + 2)
+    assert list(mid) == [1277, 1277, 1278, 1278]            # 2556 days: row 3e8 starts day 1278
+    a = datagen.fact_column("c3d_star3_date_sorted", "cust_key", 0, 100_000)
+    assert a.min() >= 0 and a.max() <= 2_999_999 and np.unique(a).size > 95_000
 
 
 def test_date_dimension_recipe():

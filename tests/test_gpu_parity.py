@@ -431,6 +431,91 @@ def test_correlated_predicates_are_priced_jointly():
     assert_same(got.as_rows(), oracle_rows(w), "correlated predicates")
 
 
+def _sparse_key_workload(seed=7, m=100_000, spread=7, n=400_003):
+    """One dimension whose m keys spread over spread * m values (beyond the
+    dense key-range limit of 2m), fact keys mostly hits, some misses."""
+    rng = np.random.default_rng(seed)
+    keys = (spread * rng.permutation(m) + 13).astype(np.int32)
+    dim = {"k": keys, "region": rng.integers(0, 5, m).astype(np.int32),
+           "attr": rng.integers(0, 200, m).astype(np.int32)}
+    hit = keys[rng.integers(0, m, n)]
+    miss = rng.integers(0, spread * m + 30, n).astype(np.int32)
+    fact = {"fk": np.where(rng.random(n) < 0.9, hit, miss).astype(np.int32),
+            "v": rng.integers(-1000, 1_000_000, n).astype(np.int32)}
+    q = {"fact_preds": [], "joins": [{"fact_key": "fk", "dim": "d", "preds": [{"col": "region", "op": "eq",
+                                                                               "lo": 2, "hi": None}],
+                                      "payloads": ["attr"], "kind": "auto"}],
+         "group_by": [["d", "attr"]], "agg": {"kind": "col", "a": "v", "b": None}}
+    return datagen.Workload("sparse keys", n, fact, {"d": dim}, {"d": "k"}, q)
+
+
+def test_dense_table_within_a_memory_budget():
+    """Keys spread over 7x the rows: the key-range rule alone builds a hash
+    table; a memory budget that holds the dense table (700,000 one-byte slots
+    and the pass bitmap) builds it dense instead; a smaller budget does not;
+    DENSE forced beyond both limits is refused. Every result equals the oracle."""
+    from paper_2607_07632_amd import sdb
+    w = _sparse_key_workload()
+    want = oracle_rows(w)
+    fact, dims = upload(w)
+    for budget, kind in [(0, "hash"), (1 << 20, "dense"), (600_000, "hash")]:
+        w.query["joins"][0]["dense_budget_bytes"] = budget
+        tables = sdb.build_dims(dims, w.dim_keys, w.query)
+        assert tables[0].kind == kind, (budget, tables[0].kind)
+        info = sdb.dim_info(tables[0])
+        if kind == "dense":
+            assert info["n_slots"] == 7 * 99_999 + 1 and info["table_bytes"] <= budget
+        got = sdb.StarQuery(fact, tables, w.query).execute()
+        assert_same(got.as_rows(), want, f"budget {budget}")
+    w.query["joins"][0]["kind"] = "dense"
+    w.query["joins"][0]["dense_budget_bytes"] = 600_000
+    with pytest.raises(sdb.SdbError) as e:
+        sdb.build_dims(dims, w.dim_keys, w.query)
+    assert e.value.name == "SDB_KEY_RANGE"
+
+
+def _sorted_by(w, col):
+    """The workload with its fact rows reordered by one column (the result of
+    the query does not depend on row order)."""
+    order = np.argsort(w.fact[col], kind="stable")
+    fact = {k: np.ascontiguousarray(v[order]) for k, v in w.fact.items()}
+    return datagen.Workload(f"{w.name} sorted by {col}", w.n_fact, fact, w.dims, w.dim_keys, w.query)
+
+
+_SEGMENT_FORCES = [{"segments": 1}, {"segments": 1, "terminal": "global"}, {"segments": 1, "terminal": "part"},
+                   {"segments": 1, "terminal": "part", "grid": 7}, {"segments": 1, "ipt": 1},
+                   {"segments": 1, "vector": -1}, {"segments": 1, "terminal": "global", "xcd": 1},
+                   {"segments": 1, "block": 1024}, {"segments": 1, "unroll": -1}, {"segments": 1, "lds": -1}]
+
+
+@pytest.mark.parametrize("force", _SEGMENT_FORCES)
+def test_segmented_plans_on_date_sorted_rows(force):
+    """c3's rows sorted by date: the rows of 1998 and 1999 fail the date filter,
+    so the planner gives their row range an order that tests the date first;
+    each segment is its own launch into one terminal. The result equals c3's."""
+    w = _sorted_by(workload("c3_star3"), "date_key")
+    got, q = run_gpu(w, force=force)
+    p = q.plan_obj
+    assert p.n_segments >= 2, force
+    assert p.segment_start[0] == 0 and p.segment_start[p.n_segments] == w.n_fact
+    date = next(s for s in range(p.n_stages) if p.stage_kind[s] == 1 and w.query["joins"][p.stage_index[s]]["dim"]
+                == "date")
+    assert p.segment_order[p.n_segments - 1][0] == date          # the last rows test the date first
+    assert_same(got.as_rows(), want_rows("c3_star3"), f"date-sorted {force}")
+
+
+@pytest.mark.parametrize("name", ["c1_scalar_scan", "c2_join_group", "c4_star4_zipf"])
+def test_segmented_plans_other_terminals(name):
+    """Segments on date-sorted rows of the scalar (c1), LDS (c2) and global
+    (c4) terminals, and no segments when they are turned off."""
+    w = _sorted_by(workload(name), "date_key")
+    got, q = run_gpu(w, force={"segments": 1})
+    assert_same(got.as_rows(), want_rows(name), f"{name} date-sorted, segments")
+    off, q2 = run_gpu(w, force={"segments": -1})
+    assert q2.plan_obj.n_segments == 1
+    assert_same(off.as_rows(), want_rows(name), f"{name} date-sorted, one order")
+
+
 _WINDOW_FORCES = [{"window": 1}, {"window": 7}, {"window": 64, "terminal": "part"},
                   {"window": 1, "terminal": "global"}, {"window": 2, "ipt": 1}, {"window": 1, "vector": -1},
                   {"window": 300, "eager": 2}, {"window": 1, "lds": 3}, {"window": 1, "unroll": -1},

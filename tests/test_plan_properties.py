@@ -14,6 +14,7 @@ import ctypes as C
 import pytest
 from hypothesis import HealthCheck, given, settings, strategies as st
 
+from conftest import GPU_PRESENT
 from paper_2607_07632_amd import sdb
 
 OK, INVALID_ARG, UNSUPPORTED, CAPACITY, HIP_ERROR = 0, 1, 2, 3, 7
@@ -191,6 +192,8 @@ def test_plans_are_consistent_and_pass_run_validation(qd):
     if status != OK:
         return
     check_plan(q, p)
+    if GPU_PRESENT:
+        return
     scratch = 0x10000000 if p.run_scratch_bytes else None
     status = L.sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
                                   scratch, int(p.run_scratch_bytes), None)
@@ -233,6 +236,8 @@ def test_rank_and_deferred_placements_pass_run_validation(force_lds, force_block
         assert p.stage_defer[s_sup] == 0
     else:
         assert p.block == 1024 and p.run_scratch_bytes > 0
+    if GPU_PRESENT:
+        return
     scratch = 0x10000000 if p.run_scratch_bytes else None
     status = sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
                                           scratch, int(p.run_scratch_bytes), None)
@@ -293,7 +298,8 @@ def test_sliced_probe_choice(force_slice, n_fact, hash_bits, agg_kind, aligned, 
         assert p.slice_bits == max(1, min(hash_bits + 3 - 21, hash_bits, 10))
         assert p.vector == 1
         assert p.slice_grid == min(256, -(-n_fact // 16384))
-    assert _run_status(q, p) in (OK, HIP_ERROR), sdb.lib().sdb_last_error()
+    if not GPU_PRESENT:
+        assert _run_status(q, p) in (OK, HIP_ERROR), sdb.lib().sdb_last_error()
 
 
 def test_sliced_plan_validation():
