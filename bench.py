@@ -403,7 +403,7 @@ def cpu_baseline_leg(cfg_name: str, n: int, gpu_rows: list, fact: dict) -> dict:
 
 
 def config_record(sdb, name: str, ex, dev, runs: int = 10, balg_rows: int = 16_000_000,
-                  parity_rows: int = 1 << 27) -> dict:
+                  parity_rows: int = 1 << 27, compare: dict | None = None) -> dict:
     """One workload measured compactly: table builds, the run window and the
     fused kernel (HIP events), roofline fractions on B_alg and B_dense, and the
     GPU result against the oracle over the first min(N, parity_rows) fact rows
@@ -446,6 +446,28 @@ def config_record(sdb, name: str, ex, dev, runs: int = 10, balg_rows: int = 16_0
     kernel_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     run_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
     got = q.execute(replan=False).as_rows()
+    versus = None
+    if compare:
+        # the same query under planner overrides, timed the same way (context)
+        qc = sdb.StarQuery(fact, tabs, query, compare)
+        pc = qc.plan()
+        sc, cc = qc.alloc_outputs(pc)
+        scr = qc.run_scratch(pc)
+        qc.run(sc, cc, plan=pc, scratch=scr)
+        evc = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(runs)]
+        torch.cuda.synchronize()
+        for ev in evc:
+            sdb.set_fused_events(ev[0], ev[1])
+            ev[2].record(stream)
+            qc.run(sc, cc, plan=pc, scratch=scr)
+            ev[3].record(stream)
+        sdb.set_fused_events()
+        torch.cuda.synchronize()
+        same = qc.execute(replan=False).as_rows() == got
+        versus = {"force": compare, "fused_kernel_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evc])),
+                  "run_ms": float(np.mean([e[2].elapsed_time(e[3]) for e in evc])), "same_result": same,
+                  "plan": sdb.plan_summary(pc, query)}
+        del qc, sc, cc, scr
     info = sdb.plan_summary(plan, query)
     b_dense = 4 * int(q.q.n_cols)
     b_alg = b_alg_per_row(host_sample(fact, min(n, balg_rows)), w.dims, w.dim_keys, query, info)
@@ -481,6 +503,8 @@ def config_record(sdb, name: str, ex, dev, runs: int = 10, balg_rows: int = 16_0
         "oracle_parity_rows": m if ex is not None else 0,
         "oracle_saw_device_rows": same_rows,
     }
+    if versus:
+        rec["versus"] = versus
     if plan.slice_bits:
         rec["fused_window_covers"] = "count pass + scatter pass + fused kernel (hash probe over table slices)"
     if any(sdb.dim_info(t)["kind"] == "hash" for t in tabs):
@@ -757,6 +781,10 @@ def main(argv=None) -> int:
         try:
             result["configs"] = [config_record(sdb, name, ex, dev)
                                  for name in ("c1_scalar_scan", "c2_join_group", "c4_star4_zipf", "c5_hash_stress")]
+            # c3's query over date-sorted rows: the planner's per-range stage
+            # orders against one order for the whole table
+            result["configs"].append(config_record(sdb, "c3d_star3_date_sorted", ex, dev,
+                                                   compare={"segments": -1}))
         finally:
             if ex is not None:
                 ex.shutdown()

@@ -1654,10 +1654,14 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
     }
 
     // LDS rank tables instead of the deferred gather of a bitmap stage's code.
-    // Their LDS footprint leaves one block of 1024 per CU, which pays only when
-    // no other lookup goes to device memory (measured: c2 0.185 -> 0.173 ms;
-    // c3, with its device-memory customer map, unchanged; c4 much slower).
-    const bool want_rank = q->force_lds == 3 || (q->force_lds == 0 && device_lookups == 0);
+    // Their LDS footprint leaves one block of 1024 per CU, which pays when no
+    // other lookup goes to device memory (measured: c2 0.185 -> 0.173 ms) or
+    // when the plan runs two items per lane, whose registers allow no more
+    // than 16 waves per CU anyway (c3: fused kernel 2.234 -> 2.195 ms, 21M
+    // deferred gathers spared), not when a lookup-heavy plan runs one item per
+    // lane at 32 waves per CU (c4: 1.67 -> 2.67 ms).
+    const bool want_rank = q->force_lds == 3 ||
+                           (q->force_lds == 0 && (device_lookups == 0 || (plan->ipt == 2 && plan->vector)));
     if (want_rank && plan->vector && plan->ipt <= 2 && plan->eager == 0 &&
         (q->force_block == 0 || q->force_block == kBigBlock)) {
         for (int s = 0; s < n; ++s) {
