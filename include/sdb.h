@@ -323,9 +323,10 @@ enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, 
  * q mod 8 equal to its index in turn (a tile map built after the count pass
  * orders the kernel's tiles so; results do not depend on that order), so
  * the slots one XCD reads at any time fit in its L2. The run scratch then
- * holds 8 bytes per fact row for the partitioned keys and values. It needs one hash probe, all other stages fact
- * predicates, a one-column SUM, and the columns those passes read 16-byte
- * aligned. ipt, vector, eager (0), block, grid,
+ * holds 8 bytes per fact row for the partitioned keys and values (12 for a
+ * two-column aggregate, whose both operands travel with the key). It needs
+ * one hash probe, all other stages fact predicates, and the columns those
+ * passes read 16-byte aligned. ipt, vector, eager (0), block, grid,
  * lds_bytes and the terminal fields describe that fused launch. */
 typedef struct sdb_plan {
     int32_t n_stages;

@@ -888,10 +888,11 @@ constexpr int kSliceLog2Bytes = 21;
 // column (the partitioned records carry one 32-bit value), and the columns
 // the count and scatter passes read 16-byte aligned (128-bit loads).
 int slice_join(const sdb_query* q) {
-    if (q->n_joins != 1 || q->agg.kind != SDB_AGG_COL || q->n_fact > kSliceMaxRows) return -1;
+    if (q->n_joins != 1 || q->n_fact > kSliceMaxRows) return -1;
     const sdb_dim* d = q->joins[0].dim;
     if (d->kind != SDB_TABLE_HASH || d->hash_bits < 1) return -1;
     if (!aligned16(q->cols[q->joins[0].fact_key_col]) || !aligned16(q->cols[q->agg.a])) return -1;
+    if (q->agg.kind != SDB_AGG_COL && !aligned16(q->cols[q->agg.b])) return -1;
     for (int i = 0; i < q->n_preds; ++i)
         if (!aligned16(q->cols[q->preds[i].col])) return -1;
     return 0;
@@ -904,7 +905,7 @@ int slice_bits_for(const sdb_dim* d) {
 
 // Run-scratch layout of the sliced probe's partition passes.
 struct SliceLayout {
-    uint64_t hist, part_count, part_start, chunk_start, out_key, out_val, tile_base, tile_map, total;
+    uint64_t hist, part_count, part_start, chunk_start, out_key, out_val, out_val2, tile_base, tile_map, total;
     int64_t tile_rows, n_vtiles;
 };
 
@@ -933,6 +934,7 @@ SliceLayout slice_layout(const sdb_query* q, const sdb_plan* plan) {
     L.chunk_start = take((P + 1) * 4);
     L.out_key = take(n * 4);
     L.out_val = take(n * 4);
+    L.out_val2 = q->agg.kind != SDB_AGG_COL ? take(n * 4) : 0;
     L.tile_rows = std::max<int64_t>(1, slice_tile_rows(plan));
     L.n_vtiles = 8 * ((int64_t)((n + (uint64_t)L.tile_rows - 1) / (uint64_t)L.tile_rows) + 1);
     L.tile_base = take(P * 4);
@@ -1844,6 +1846,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         sp.rows_per_block = (per + kSliceChunk - 1) / kSliceChunk * kSliceChunk;
         sp.key_col = q->joins[plan->stage_index[ss]].fact_key_col;
         sp.val_col = q->agg.a;
+        sp.val2_col = q->agg.kind != SDB_AGG_COL ? q->agg.b : -1;
         sp.bits = plan->slice_bits;
         for (int st_i = 0; st_i < plan->n_stages; ++st_i) {
             if (plan->stage_kind[st_i] != 0) continue;
@@ -1858,6 +1861,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         sp.chunk_start = (uint32_t*)(slice_base + SL.chunk_start);
         sp.out_key = (int32_t*)(slice_base + SL.out_key);
         sp.out_val = (int32_t*)(slice_base + SL.out_val);
+        sp.out_val2 = sp.val2_col >= 0 ? (int32_t*)(slice_base + SL.out_val2) : nullptr;
         sp.tile_rows = SL.tile_rows;
         sp.tile_base = (uint32_t*)(slice_base + SL.tile_base);
         sp.tile_map = (int32_t*)(slice_base + SL.tile_map);
@@ -1870,15 +1874,16 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         std::memset(&p3, 0, sizeof p3);
         p3.cols[0] = sp.out_key;
         p3.cols[1] = sp.out_val;
+        p3.cols[2] = sp.out_val2;   // two-column aggregates only
         p3.n = q->n_fact;
         p3.n_dev = sp.part_start + (1u << plan->slice_bits);
         p3.tile_map = sp.tile_map;
         p3.n_vtiles = sp.n_vtiles;
         p3.nstages = 1;
         p3.st[0] = hs;
-        p3.agg_kind = SDB_AGG_COL;
+        p3.agg_kind = q->agg.kind;
         p3.agg_a = 1;
-        p3.agg_b = 1;
+        p3.agg_b = sp.val2_col >= 0 ? 2 : 1;
         p3.agg_a_slot = -1;
         p3.agg_b_slot = -1;
         p3.defer_stage = -1;

@@ -290,7 +290,8 @@ struct SliceParams {
     int64_t n;                 // fact rows
     int64_t rows_per_block;    // a multiple of kSliceChunk; columns are 16-byte aligned
     int32_t key_col;           // the probe's fact key column
-    int32_t val_col;           // the aggregate's column
+    int32_t val_col;           // the aggregate's (first) column
+    int32_t val2_col;          // its second column (MUL, SUB, ADD), or -1
     int32_t n_preds;
     int32_t bits;              // 2^bits partitions, 1 .. SDB_MAX_SLICE_BITS
     int32_t pred_col[kMaxStages];
@@ -301,6 +302,7 @@ struct SliceParams {
     uint32_t* chunk_start;     // n_parts + 1 entries (written by the shared scan, unused)
     int32_t* out_key;          // partitioned keys and values, all passing rows
     int32_t* out_val;
+    int32_t* out_val2;         // val2_col >= 0: the second operands
     // tile order of the fused launch over them: its tiles of tile_rows rows;
     // XCD x (x = q mod 8) walks the tiles whose first row lies in partition q
     int64_t tile_rows;

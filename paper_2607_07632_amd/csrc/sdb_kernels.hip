@@ -1168,10 +1168,10 @@ __device__ __forceinline__ void slice_load4(const int32_t* col, int64_t r, int64
 // A thread's rows of the chunk at c0: kSliceRowsPerThread / 4 groups of 4,
 // group i at c0 + 4 * (i * kSliceBlock + threadIdx.x). Which of them lie below
 // r1 and pass every fact predicate, and their keys (0 for the others).
-__device__ __forceinline__ void slice_load_keys(const SliceParams& sp, int64_t c0, int64_t r1,
-                                                int32_t (&k)[kSliceRowsPerThread],
-                                                bool (&ok)[kSliceRowsPerThread]) {
-    constexpr int G = kSliceRowsPerThread / 4;
+template <int RPT>
+__device__ __forceinline__ void slice_load_keys(const SliceParams& sp, int64_t c0, int64_t r1, int32_t (&k)[RPT],
+                                                bool (&ok)[RPT]) {
+    constexpr int G = RPT / 4;
 #pragma unroll
     for (int i = 0; i < G; ++i) {
         const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
@@ -1216,7 +1216,7 @@ __global__ void __launch_bounds__(kSliceBlock) slice_count_kernel(SliceParams sp
     for (int64_t c0 = r0; c0 < r1; c0 += kSliceChunk) {
         int32_t k[kSliceRowsPerThread];
         bool ok[kSliceRowsPerThread];
-        slice_load_keys(sp, c0, r1, k, ok);
+        slice_load_keys<kSliceRowsPerThread>(sp, c0, r1, k, ok);
 #pragma unroll
         for (int i = 0; i < kSliceRowsPerThread; ++i)
             if (ok[i]) atomicAdd(&mine[4u * slice_of(k[i], sp.bits)], 1u);
@@ -1260,17 +1260,22 @@ __device__ uint32_t block_scan_any(const uint32_t* in, uint32_t* out, uint32_t n
     return total;
 }
 
-// Scatter pass: block b reads its rows again, kSliceChunk at a time, sorts
-// each chunk's passing rows by partition in LDS (counting sort) and writes
-// every partition's run of keys and values after the ones block b wrote
-// before (hist holds block b's first offset within each partition).
+// Scatter pass: block b reads its rows again, RPT * kSliceBlock at a time,
+// sorts each chunk's passing rows by partition in LDS (counting sort) and
+// writes every partition's run of keys and values (TWO: both operands of a
+// two-column aggregate, in chunks half as long so they fit LDS) after the ones
+// block b wrote before (hist holds block b's first offset within each
+// partition).
+template <int RPT, bool TWO>
 __global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams sp) {
+    constexpr int CHUNK = RPT * kSliceBlock;
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     __shared__ uint32_t wtmp[kSliceBlock / 64];
     int32_t* skey = reinterpret_cast<int32_t*>(smem);
-    int32_t* sval = skey + kSliceChunk;
+    int32_t* sval = skey + CHUNK;
+    int32_t* sval2 = sval + CHUNK;            // TWO only
     const uint32_t P = 1u << sp.bits;
-    uint32_t* lcnt = reinterpret_cast<uint32_t*>(sval + kSliceChunk);
+    uint32_t* lcnt = reinterpret_cast<uint32_t*>(sval + (TWO ? 2 : 1) * CHUNK);
     uint32_t* lstart = lcnt + P;
     uint32_t* lcur = lstart + P;
     for (uint32_t q = threadIdx.x; q < P; q += blockDim.x) {
@@ -1281,32 +1286,39 @@ __global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams 
     const int64_t r0 = (int64_t)blockIdx.x * sp.rows_per_block;
     const int64_t r1 = min(sp.n, r0 + sp.rows_per_block);
     const int32_t* val = sp.cols[sp.val_col];
-    for (int64_t c0 = r0; c0 < r1; c0 += kSliceChunk) {
-        int32_t k[kSliceRowsPerThread], v[kSliceRowsPerThread];
-        bool ok[kSliceRowsPerThread];
-        uint32_t rk[kSliceRowsPerThread];
-        slice_load_keys(sp, c0, r1, k, ok);
+    const int32_t* val2 = sp.cols[TWO ? sp.val2_col : sp.val_col];
+    for (int64_t c0 = r0; c0 < r1; c0 += CHUNK) {
+        int32_t k[RPT], v[RPT], v2[RPT];
+        bool ok[RPT];
+        uint32_t rk[RPT];
+        slice_load_keys<RPT>(sp, c0, r1, k, ok);
 #pragma unroll
-        for (int i = 0; i < kSliceRowsPerThread / 4; ++i) {
+        for (int i = 0; i < RPT / 4; ++i) {
             const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
-            int32_t x[4] = {0, 0, 0, 0};
-            if (ok[4 * i] || ok[4 * i + 1] || ok[4 * i + 2] || ok[4 * i + 3]) slice_load4(val, r, r1, x);
+            int32_t x[4] = {0, 0, 0, 0}, y[4] = {0, 0, 0, 0};
+            const bool any = ok[4 * i] || ok[4 * i + 1] || ok[4 * i + 2] || ok[4 * i + 3];
+            if (any) slice_load4(val, r, r1, x);
+            if (TWO && any) slice_load4(val2, r, r1, y);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) v[4 * i + j] = x[j];
+            for (int j = 0; j < 4; ++j) {
+                v[4 * i + j] = x[j];
+                v2[4 * i + j] = y[j];
+            }
         }
 #pragma unroll
-        for (int i = 0; i < kSliceRowsPerThread; ++i) {
+        for (int i = 0; i < RPT; ++i) {
             rk[i] = 0u;
             if (ok[i]) rk[i] = atomicAdd(&lcnt[slice_of(k[i], sp.bits)], 1u);
         }
         __syncthreads();
         const uint32_t cn = block_scan_any(lcnt, lstart, P, 0u, wtmp);
 #pragma unroll
-        for (int i = 0; i < kSliceRowsPerThread; ++i)
+        for (int i = 0; i < RPT; ++i)
             if (ok[i]) {
                 const uint32_t pos = lstart[slice_of(k[i], sp.bits)] + rk[i];
                 skey[pos] = k[i];
                 sval[pos] = v[i];
+                if (TWO) sval2[pos] = v2[i];
             }
         __syncthreads();
         for (uint32_t i = threadIdx.x; i < cn; i += blockDim.x) {
@@ -1316,6 +1328,7 @@ __global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams 
             if (dest < (uint64_t)sp.n) {   // always: both passes count the same rows
                 sp.out_key[dest] = key;
                 sp.out_val[dest] = sval[i];
+                if (TWO) sp.out_val2[dest] = sval2[i];
             }
         }
         __syncthreads();
@@ -1370,8 +1383,12 @@ __global__ void __launch_bounds__(256) slice_tile_map_kernel(SliceParams sp) {
     }
 }
 
-size_t slice_scatter_lds_bytes(uint32_t n_parts) {
-    return (size_t)kSliceChunk * 8u + (size_t)n_parts * 12u;
+// rows per thread of the scatter chunk: half as many with two value columns
+constexpr int kSliceRowsPerThreadTwo = kSliceRowsPerThread / 2;
+
+size_t slice_scatter_lds_bytes(uint32_t n_parts, bool two) {
+    const size_t chunk = (size_t)kSliceBlock * (two ? kSliceRowsPerThreadTwo : kSliceRowsPerThread);
+    return chunk * 4u * (two ? 3u : 2u) + (size_t)n_parts * 12u;
 }
 
 hipError_t launch_slice_partition(const SliceParams& sp, int grid, hipStream_t s) {
@@ -1394,7 +1411,12 @@ hipError_t launch_slice_partition(const SliceParams& sp, int grid, hipStream_t s
     hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, pp);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(slice_scatter_kernel, dim3(grid), dim3(kSliceBlock), slice_scatter_lds_bytes(P), s, sp);
+    if (sp.val2_col >= 0)
+        hipLaunchKernelGGL((slice_scatter_kernel<kSliceRowsPerThreadTwo, true>), dim3(grid), dim3(kSliceBlock),
+                           slice_scatter_lds_bytes(P, true), s, sp);
+    else
+        hipLaunchKernelGGL((slice_scatter_kernel<kSliceRowsPerThread, false>), dim3(grid), dim3(kSliceBlock),
+                           slice_scatter_lds_bytes(P, false), s, sp);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (sp.tile_map) {

@@ -130,17 +130,54 @@ def test_c5_forced_plans_agree(force):
     assert_same(got.as_rows(), want_rows("c5_hash_stress"), f"c5 {force}")
 
 
-def _sliceable(w, load_factor=0.5):
+def _sliceable(w, load_factor=0.5, keep_agg=False):
     """w's query narrowed to the shape a sliced hash probe serves: its first
-    join only, as a hash table, group keys from that join, SUM of one column
-    (the fact predicates stay)."""
+    join only, as a hash table, group keys from that join, and (unless
+    keep_agg) SUM of one column (the fact predicates stay)."""
     import copy
     q = copy.deepcopy(w.query)
     j = dict(q["joins"][0], kind="hash", load_factor=load_factor)
     q["joins"] = [j]
     q["group_by"] = [g for g in q["group_by"] if g[0] == j["dim"]]
-    q["agg"] = {"kind": "col", "a": q["agg"]["a"], "b": None}
+    if not keep_agg:
+        q["agg"] = {"kind": "col", "a": q["agg"]["a"], "b": None}
     return datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys, q)
+
+
+@pytest.mark.parametrize("n", [1, 16_385, 70_001, 400_003])
+@pytest.mark.parametrize("kind", ["mul", "sub", "add"])
+def test_sliced_probe_with_two_column_aggregates(n, kind):
+    """Sliced probes whose aggregate combines two columns (both operands travel
+    with the key through the scatter pass): random one-join schemas, every
+    terminal shape, against the oracle."""
+    done = 0
+    for seed in range(60):
+        w0 = random_tiny_workload(3000 + seed, n_fact=n, max_dim_rows=3000)
+        if not w0.query["joins"] or len(w0.fact) < 3:
+            continue
+        w = _sliceable(w0, load_factor=(0.5, 0.25, 0.9)[seed % 3], keep_agg=True)
+        vals = [c for c in w.fact if c.startswith("v")]
+        w.query["agg"] = {"kind": kind, "a": vals[0], "b": vals[-1]}
+        want = oracle_rows(w)
+        for force in ({"slice": 1}, {"slice": 1, "terminal": "global"}, {"slice": 1, "terminal": "part"}):
+            got, q = run_gpu(w, force=force)
+            assert q.plan_obj.slice_bits > 0, (seed, force)
+            assert_same(got.as_rows(), want, f"seed {seed} n {n} {kind} {force}")
+        done += 1
+        if done == 2:
+            break
+    assert done == 2
+
+
+def test_sliced_probe_c5_with_a_difference():
+    """c5's shape with SUM(value - key) through the sliced probe, both
+    operands in the partitioned records (64-bit record values)."""
+    w0 = workload("c5_hash_stress")
+    w = datagen.Workload("c5 difference", w0.n_fact, w0.fact, w0.dims, w0.dim_keys,
+                         {**w0.query, "agg": {"kind": "sub", "a": "value", "b": "key"}})
+    got, q = run_gpu(w, force={"slice": 1})
+    assert q.plan_obj.slice_bits > 0
+    assert_same(got.as_rows(), oracle_rows(w), "c5 value - key, sliced")
 
 
 # row counts around the passes' 16,384-row chunks, up to many blocks

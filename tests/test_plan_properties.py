@@ -159,9 +159,10 @@ def check_plan(q, p):
     # the sliced hash probe: only the query shape it supports, and wherever
     # that shape is forced
     join_probe = [s for s in range(n) if p.stage_kind[s] == 1 and not p.stage_range[s]]
-    read = [q.joins[0].fact_key_col, q.agg.a] + [q.preds[i].col for i in range(q.n_preds)] if q.n_joins else []
+    read = ([q.joins[0].fact_key_col, q.agg.a] + ([q.agg.b] if q.agg.kind else []) +
+            [q.preds[i].col for i in range(q.n_preds)]) if q.n_joins else []
     sliceable = (q.n_joins == 1 and len(join_probe) == 1 and q.joins[0].dim.contents.kind == 2 and
-                 q.agg.kind == 0 and 0 < q.n_fact <= 0xFFFFF000 and q.force_eager <= 0 and
+                 0 < q.n_fact <= 0xFFFFF000 and q.force_eager <= 0 and
                  all(q.cols[c] % 16 == 0 for c in read))
     if p.slice_bits:
         assert sliceable and q.force_slice != -1
@@ -169,8 +170,9 @@ def check_plan(q, p):
         d = q.joins[0].dim.contents
         assert s == join_probe[0] and 1 <= p.slice_bits <= min(10, d.hash_bits)
         assert 1 <= p.slice_grid <= 256 and p.eager == 0 and p.stage_lds[s] == LDS_GLOBAL
-        # partition counts and offsets, and one key and value per fact row
-        assert p.run_scratch_bytes >= 8 * q.n_fact + 4 * p.slice_grid * (1 << p.slice_bits)
+        # partition counts and offsets, and one key and value (two for a two-column aggregate) per fact row
+        per_row = 12 if q.agg.kind else 8
+        assert p.run_scratch_bytes >= per_row * q.n_fact + 4 * p.slice_grid * (1 << p.slice_bits)
     else:
         assert not (sliceable and q.force_slice == 1)
     # the unrolled stage loop: exactly where its instance exists and no hash
@@ -281,7 +283,8 @@ def _run_status(q, p):
     (0, 600_000_000, 20, 0, True, False),     # an 8 MiB table: probes mostly hit L2 anyway
     (0, 1_000_000, 25, 0, True, False),       # too few rows to pay for the passes
     (1, 1_000_000, 12, 0, True, True),        # forced on a small case
-    (1, 600_000_000, 25, 2, True, False),     # revenue - cost: records would need 64-bit values
+    (1, 600_000_000, 25, 2, True, True),      # revenue - cost: both operands travel with the key
+    (0, 600_000_000, 25, 1, True, True),      # a product, chosen by the planner
     (1, 600_000_000, 25, 0, False, False),    # the passes load 128 bits at a time
     (-1, 600_000_000, 25, 0, True, False),
 ])
@@ -313,9 +316,12 @@ def test_sliced_plan_validation():
         bad = sdb.SdbPlan.from_buffer_copy(good)
         setattr(bad, field, value)
         assert _run_status(q, bad) == INVALID_ARG, (field, value)
-    # a plan for one query is not valid for one the slices cannot serve
-    q2, _d2 = _c5_like(600_000_000, agg_kind=2)
+    # a plan for one query is not valid for one the slices cannot serve (unaligned columns)
+    q2, _d2 = _c5_like(600_000_000, aligned=False)
     assert _run_status(q2, sdb.SdbPlan.from_buffer_copy(good)) == INVALID_ARG
+    # nor, for want of scratch, for a two-column aggregate, whose second operands travel too
+    q3, _d3 = _c5_like(600_000_000, agg_kind=2)
+    assert _run_status(q3, sdb.SdbPlan.from_buffer_copy(good)) == 4
     # too little scratch for the partitioned records
     short = sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
                                          0x10000000, int(p.run_scratch_bytes) - 256, None)
