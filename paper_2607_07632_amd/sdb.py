@@ -277,7 +277,7 @@ def dim_desc(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
 
 
 def build_dim(key, cols: dict, preds: list, payloads: list, kind: str = "auto",
-              load_factor: float = 0.0, stream=None, workspace=None, dense_budget_bytes: int = 0) -> DimTable:
+              load_factor: float = 0.0, dense_budget_bytes: int = 0, stream=None, workspace=None) -> DimTable:
     """Builds the lookup table of one dimension (arguments as dim_desc)."""
     import torch
     d = dim_desc(key, cols, preds, payloads, kind, load_factor, dense_budget_bytes)
