@@ -948,7 +948,9 @@ def test_coarse_prefilter_tables(shift):
         got, q = run_gpu(w, force={"lds": -1, "coarse": shift})
         assert_same(got.as_rows(), oracle_rows(w), f"tiny {seed} coarse {shift}")
     w = workload("c3_star3")
-    got, q = run_gpu(w, force={"coarse": shift, "block": 1024})
+    # supplier as a plain LDS bitmap (not rank tables), so that the customer
+    # map's coarse bitmap fits LDS from 4 slots per bit on
+    got, q = run_gpu(w, force={"coarse": shift, "block": 1024, "lds": 2})
     stages = sdb.plan_summary(q.plan_obj, w.query)["stages"]
     assert any(st.get("table") == "lds_coarse" for st in stages) or shift == 1
     assert_same(got.as_rows(), oracle_rows(w), f"c3 coarse {shift}")

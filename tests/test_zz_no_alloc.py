@@ -31,7 +31,7 @@ CASES = [
     ("c2_join_group", 4_000_003, 999_999, {"lds": 3}, True),                          # LDS rank tables
     ("c3_star3", 2_000_001, 700_001, {"terminal": "part"}, True),                      # partitioned terminal
     ("c5_hash_stress", 2_000_003, 600_001, {"slice": 1}, True),                        # sliced hash probe
-    ("c3_star3", 4_000_001, 1_500_007, {"terminal": "global", "xcd": -1}, False),
+    ("c3_star3", 4_000_001, 1_500_007, {"terminal": "global", "xcd": -1, "lds": 2}, False),   # LDS bitmaps, no rank tables
     ("c1_scalar_scan", None, 100_001, None, False),
 ]
 
