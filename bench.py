@@ -42,6 +42,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+ONE_CORE_ROWS = 8_000_000        # rows of the one-core oracle timings (c1 whole, c2 and c3 a head)
 # the fused kernel's source: its template and the device helpers it uses
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_07632_amd", "csrc", f) for f in ("sdb_fused.h", "sdb_device.h")]
 
@@ -146,7 +147,8 @@ ABLATION_RUNGS = [
     ("planner's choice (terminal, block size, rank tables)", {"slice": -1, "unroll": -1, "window": -1}),
     ("+ stage loop written out (plans without a hash probe)", {"slice": -1, "window": -1}),
     ("+ LDS window over the busiest device-memory map", {"slice": -1}),
-    ("+ a hash probe over 2 MiB table slices (planner's choice)", {}),
+    ("+ a hash probe over 2 MiB table slices", {"prefilter": -1}),
+    ("+ rows the table's pass filter rejects dropped before the slicing (planner's choice)", {}),
 ]
 
 
@@ -369,6 +371,16 @@ def device_column_sums(fact: dict) -> dict:
     return {k: int(v.sum(dtype=torch.int64).item()) for k, v in fact.items()}
 
 
+def one_core_oracle(cfg_name: str, rows: int) -> dict:
+    """The oracle in this process, on one core, over the first ``rows`` fact
+    rows (generation excluded from the time)."""
+    from oracle import ranges
+    _, _, secs = ranges.range_task(cfg_name, 0, rows)
+    log(f"[bench] {cfg_name}: oracle on one core over the first {rows} rows: {secs:.1f} s")
+    return {"value": rows / secs, "unit": "fact rows/s", "cores": 1, "kind": "oracle", "rows": rows,
+            "secs": secs, "sample": f"the first {rows} fact rows of {cfg_name}, one process, generation excluded"}
+
+
 def cpu_baseline_leg(cfg_name: str, n: int, gpu_rows: list, fact: dict) -> dict:
     """The oracle over all n fact rows, one row range per worker process (one
     per host core, at most 16), the oracle phases started together once every
@@ -396,6 +408,7 @@ def cpu_baseline_leg(cfg_name: str, n: int, gpu_rows: list, fact: dict) -> dict:
             "host_cores_in_affinity": len(os.sched_getaffinity(0)),
             "rows_per_s_per_core": per_core,
         },
+        "cpu_oracle_one_core": one_core_oracle(cfg_name, min(n, ONE_CORE_ROWS)),
         "parity_full_table": parity,
         "parity_detail": {"groups": len(gpu_rows), "oracle_groups": len(res.sums),
                           "oracle_live_rows": int(res.n_live), "oracle_saw_device_rows": same_rows},
@@ -505,6 +518,8 @@ def config_record(sdb, name: str, ex, dev, runs: int = 10, balg_rows: int = 16_0
     }
     if versus:
         rec["versus"] = versus
+    if ex is not None and name in ("c1_scalar_scan", "c2_join_group"):
+        rec["cpu_oracle_one_core"] = one_core_oracle(name, min(n, ONE_CORE_ROWS))
     if plan.slice_bits:
         rec["fused_window_covers"] = "count pass + scatter pass + fused kernel (hash probe over table slices)"
     if any(sdb.dim_info(t)["kind"] == "hash" for t in tabs):

@@ -38,7 +38,7 @@ extern "C" {
 
 #define SDB_API __attribute__((visibility("default")))
 
-#define SDB_ABI_VERSION 9
+#define SDB_ABI_VERSION 10
 
 typedef enum sdb_status {
     SDB_OK = 0,
@@ -61,6 +61,10 @@ enum { SDB_OP_EQ = 0, SDB_OP_NE = 1, SDB_OP_LT = 2, SDB_OP_LE = 3,
 /* Dimension lookup-table layouts (Section 3.3: a direct-mapped table indexed
  * by a dense primary key, or a double-sized open-addressing hash table). */
 enum { SDB_TABLE_AUTO = 0, SDB_TABLE_DENSE = 1, SDB_TABLE_HASH = 2 };
+/* pass filter of a hash table's keys (sdb_dim.filter_kind) */
+enum { SDB_FILTER_NONE = 0, SDB_FILTER_BITMAP = 1, SDB_FILTER_BLOOM = 2 };
+/* most bytes a hash table's pass filter takes in its workspace */
+#define SDB_MAX_FILTER_BYTES (4ll << 20)
 
 /* Aggregate expressions over fact columns a and b, computed in int64. */
 enum { SDB_AGG_COL = 0, SDB_AGG_MUL = 1, SDB_AGG_SUB = 2, SDB_AGG_ADD = 3 };
@@ -138,7 +142,22 @@ typedef struct sdb_dim_desc {
  *  HASH:  n_slots = 2^hash_bits 8-byte slots {low 32 bits: key, high 32
  *         bits: code + 1, or 0xFFFFFFFF for a filtered row}; a slot with high
  *         half 0 is empty. Slot of key k starts at (k * 0x9E3779B1 mod 2^32)
- *         >> (32 - hash_bits) (Fibonacci hashing) and probes linearly. */
+ *         >> (32 - hash_bits) (Fibonacci hashing) and probes linearly.
+ *         Beside the slots, a pass filter of filter_bits bits (32-bit words at
+ *         `filter`) that holds every passing row's key, so a fact key it
+ *         rejects cannot pass the join (Section 3.3's filtered build, turned
+ *         into a test that needs no probe):
+ *           SDB_FILTER_BITMAP: bit (key - key_min) is set iff a passing row
+ *             holds that key (filter_bits = key range), exact;
+ *           SDB_FILTER_BLOOM: a blocked Bloom filter for key ranges too wide
+ *             for a bitmap: m = (k ^ k >> 16) * 0x85EBCA6B, m ^= m >> 13,
+ *             m *= 0xC2B2AE35, m ^= m >> 16 (mod 2^32: the 32-bit finalizer
+ *             of MurmurHash3); word
+ *             m mod (filter_bits / 32) holds bits t >> 27, (t >> 22) & 31 and
+ *             (t >> 17) & 31 of t = rotl(m, 16) * 0x9E3779B1, all set for a
+ *             passing key (false positives, no false negatives).
+ *         The filter takes at most SDB_MAX_FILTER_BYTES (8 bits per row up to
+ *         that); SDB_FILTER_NONE on handles that carry none. */
 typedef struct sdb_dim {
     int32_t kind;                 /* SDB_TABLE_DENSE or SDB_TABLE_HASH */
     int32_t width;                /* DENSE: 1, 2 or 4 bytes per entry; HASH: 8 */
@@ -159,6 +178,10 @@ typedef struct sdb_dim {
     void* map;                    /* device, inside the workspace */
     void* stats;                  /* device, inside the workspace */
     void* bits;                   /* DENSE: device pass bitmap inside the workspace; HASH: NULL */
+    void* filter;                 /* HASH: device pass filter inside the workspace; DENSE: NULL */
+    uint64_t filter_bits;         /* bits of the filter (a multiple of 32 for BLOOM) */
+    int32_t filter_kind;          /* SDB_FILTER_* */
+    int32_t reserved_;            /* 0 */
 } sdb_dim;
 
 /* What a built lookup table holds, as sdb_dim_info reports it: the layout the
@@ -184,8 +207,9 @@ typedef struct sdb_dim_summary {
     int32_t payload_min[SDB_MAX_PAYLOADS];     /* over passing rows */
     int32_t payload_max[SDB_MAX_PAYLOADS];     /* payload_min + radix - 1 */
     uint32_t payload_radix[SDB_MAX_PAYLOADS];
-    int32_t reserved_;
+    int32_t filter_kind;          /* HASH: SDB_FILTER_* of its pass filter; DENSE: SDB_FILTER_NONE */
     uint64_t domain;              /* product of the payload radices: distinct codes */
+    uint64_t filter_bytes;        /* device bytes of that filter (not part of table_bytes) */
 } sdb_dim_summary;
 
 typedef struct sdb_join {
@@ -245,7 +269,10 @@ typedef struct sdb_agg {
  *                  (none: measured on MI355X, a window does not pay); -1:
  *                  none; 1: the largest window that fits without lowering
  *                  the blocks per CU, for the dense device-memory stage it
- *                  serves most; k >= 2: the same with at most 128 * k slots */
+ *                  serves most; k >= 2: the same with at most 128 * k slots
+ *  force_prefilter the sliced hash probe's pre-filter (sdb_plan.slice_prefilter):
+ *                  0: the planner's choice; -1: never; 1: whenever the plan
+ *                  slices a hash probe into a table with a pass filter */
 typedef struct sdb_query {
     int64_t n_fact;
     int32_t n_cols;
@@ -272,7 +299,7 @@ typedef struct sdb_query {
     int32_t force_unroll;
     int32_t force_window;
     int32_t force_segments;
-    int32_t reserved_;                    /* 0 */
+    int32_t force_prefilter;
 } sdb_query;
 
 /* Where a probe looks its table up (sdb_plan.stage_lds):
@@ -324,7 +351,14 @@ enum { SDB_LDS_GLOBAL = 0, SDB_LDS_MAP = 1, SDB_LDS_BITS = 2, SDB_LDS_RANK = 3, 
  * orders the kernel's tiles so; results do not depend on that order), so
  * the slots one XCD reads at any time fit in its L2. The run scratch then
  * holds 8 bytes per fact row for the partitioned keys and values (12 for a
- * two-column aggregate, whose both operands travel with the key). It needs
+ * two-column aggregate, whose both operands travel with the key). With
+ * slice_prefilter the count pass also drops rows whose key the table's pass
+ * filter rejects and records which rows it keeps (one byte per 4 rows in the
+ * run scratch), so the scatter pass writes and the fused kernel probes only
+ * rows that can pass the join; the planner takes it when the join's sampled
+ * pass fraction, with the filter's false positives added, is at most 0.7
+ * (each dropped row saves a scatter write and a probe, each row costs one
+ * L2-resident filter read). It needs
  * one hash probe, all other stages fact predicates, and the columns those
  * passes read 16-byte aligned. ipt, vector, eager (0), block, grid,
  * lds_bytes and the terminal fields describe that fused launch. */
@@ -370,6 +404,11 @@ typedef struct sdb_plan {
     int32_t slice_bits;                   /* 0: no sliced probe; else 1 .. SDB_MAX_SLICE_BITS */
     int32_t slice_stage;                  /* stage of the sliced hash probe (slice_bits > 0) */
     int32_t slice_grid;                   /* blocks of the count and scatter passes */
+    int32_t slice_prefilter;              /* 1: the count pass also tests each row's key against the
+                                             table's pass filter and keeps only rows it lets through
+                                             (one bit per row for the scatter pass), so rows that
+                                             cannot pass the join are neither partitioned nor
+                                             probed; 0 otherwise */
     int32_t unroll;                       /* 1: the fused kernel's instance with its stage loop
                                              written out four times (stage parameters stay in
                                              scalar registers across tiles); allowed for plans of
@@ -415,7 +454,9 @@ SDB_API sdb_status sdb_struct_sizes(int64_t* sizes, int32_t n);
  * statistics, then the lookup table sized by an upper bound (a DENSE map of
  * max(2 * n_rows, 1024) 4-byte slots plus its pass bitmap, or
  * dense_budget_bytes plus 512 bytes of alignment when that is larger, and/or
- * a HASH table of next_pow2(n_rows / load_factor) 8-byte slots). */
+ * a HASH table of next_pow2(n_rows / load_factor) 8-byte slots, padded to
+ * 256 bytes, and its pass filter of min(max(next_pow2(n_rows), 256),
+ * SDB_MAX_FILTER_BYTES) bytes). */
 SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* bytes);
 
 /* Builds the lookup table for `desc` into `workspace` (device, 256-byte
@@ -424,7 +465,9 @@ SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* byt
  * count, payload ranges), then the direct-mapped map (Section 3.3: one code
  * per key, the sentinel for a filtered row, all ones for an absent key; 1, 2
  * or 4 bytes by payload domain) and its pass bitmap, or the open-addressing
- * table (64-bit compare-and-swap inserts). Synchronizes the stream twice (to
+ * table (64-bit compare-and-swap inserts) and its pass filter (a bitmap over
+ * the key range when that fits the filter's bytes, else the Bloom filter).
+ * Synchronizes the stream twice (to
  * read the statistics, then the duplicate-key check: a dense map must end
  * with one occupied slot per row).
  * Errors: INVALID_ARG, UNSUPPORTED (payload domain >= 2^32 - 2), KEY_RANGE,

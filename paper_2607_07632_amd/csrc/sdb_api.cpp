@@ -173,6 +173,56 @@ uint64_t hash_capacity(int64_t n_rows, double lf) {
     return std::max<uint64_t>(next_pow2(need), 2);
 }
 
+// Bytes of a hash table's pass filter: 8 bits per row, a power of two from
+// 256 bytes to SDB_MAX_FILTER_BYTES (an L2 holds the largest with room to
+// spare for the stream that probes it).
+uint64_t filter_bytes(int64_t n_rows) {
+    return std::min<uint64_t>((uint64_t)SDB_MAX_FILTER_BYTES, std::max<uint64_t>(256, next_pow2((uint64_t)n_rows)));
+}
+
+// Why a handle's pass filter fields contradict its kind or key range, or ""
+// when they agree.
+std::string filter_problem(const sdb_dim* d) {
+    char buf[160];
+    if (d->reserved_ != 0) return "sdb_dim.reserved_ must be 0";
+    if (d->filter_kind == SDB_FILTER_NONE) return "";
+    if (d->kind != SDB_TABLE_HASH) return "only a hash table carries a pass filter";
+    if (d->filter_kind != SDB_FILTER_BITMAP && d->filter_kind != SDB_FILTER_BLOOM) {
+        snprintf(buf, sizeof buf, "bad pass filter kind %d", d->filter_kind);
+        return buf;
+    }
+    if (!d->filter) return "pass filter without its words";
+    const uint64_t b = d->filter_bits, max_bits = (uint64_t)SDB_MAX_FILTER_BYTES * 8;
+    if (d->filter_kind == SDB_FILTER_BITMAP) {
+        const uint64_t range = d->n_rows > 0 ? (uint64_t)((int64_t)d->key_max - (int64_t)d->key_min + 1) : 0;
+        if (b == 0 || b != range || b > max_bits) {
+            snprintf(buf, sizeof buf, "pass filter bitmap of %llu bits for a key range of %llu",
+                     (unsigned long long)b, (unsigned long long)range);
+            return buf;
+        }
+    } else if (b < 32 || b % 32 != 0 || ((b / 32) & (b / 32 - 1)) != 0 || b > max_bits) {
+        snprintf(buf, sizeof buf, "pass filter (Bloom) of %llu bits is not 32 x a power of two up to %llu",
+                 (unsigned long long)b, (unsigned long long)max_bits);
+        return buf;
+    }
+    return "";
+}
+
+// Fraction of keys outside the filter's set that a Bloom filter of `bits`
+// bits holding `n_keys` keys lets through: each key sets 3 bits of one
+// 32-bit word; a word holds Poisson(n_keys / words) keys.
+double bloom_false_positive(uint64_t bits, int64_t n_keys) {
+    const double words = (double)(bits / 32), lambda = (double)n_keys / std::max(words, 1.0);
+    double fp = 0.0, pmf = std::exp(-lambda);
+    const int jmax = (int)(lambda + 12.0 * std::sqrt(lambda + 1.0) + 24.0);
+    for (int j = 0; j <= jmax; ++j) {
+        const double set = 1.0 - std::pow(31.0 / 32.0, 3.0 * j);
+        fp += pmf * set * set * set;
+        pmf *= lambda / (double)(j + 1);
+    }
+    return std::min(1.0, fp);
+}
+
 sdb_status check_dim_desc(const sdb_dim_desc* d) {
     if (!d) return fail(SDB_INVALID_ARG, "null dimension descriptor");
     if (d->n_rows < 0) return fail(SDB_INVALID_ARG, "negative n_rows");
@@ -214,7 +264,8 @@ uint64_t required_bytes(const sdb_dim_desc* d) {
         table = std::max(table, dense_bytes(dense_slot_limit(d->n_rows), 4));
         if (d->dense_budget_bytes > 0) table = std::max(table, (uint64_t)d->dense_budget_bytes + 512u);
     }
-    if (d->kind != SDB_TABLE_DENSE) table = std::max(table, hash_capacity(d->n_rows, effective_lf(d)) * 8);
+    if (d->kind != SDB_TABLE_DENSE)
+        table = std::max(table, align_up(hash_capacity(d->n_rows, effective_lf(d)) * 8, 256) + filter_bytes(d->n_rows));
     return kStatsBytes + table;
 }
 
@@ -266,6 +317,8 @@ sdb_status check_query(const sdb_query* q) {
         if (jn.dim->kind == SDB_TABLE_HASH &&
             (jn.dim->hash_bits < 1 || jn.dim->hash_bits > 31 || jn.dim->n_slots != (1ull << jn.dim->hash_bits)))
             return fail(SDB_INVALID_ARG, "join %d: bad hash table geometry", j);
+        const std::string fp = filter_problem(jn.dim);
+        if (!fp.empty()) return fail(SDB_INVALID_ARG, "join %d: %s", j, fp.c_str());
     }
     if (q->n_group_keys < 0 || q->n_group_keys > SDB_MAX_GROUP_KEYS)
         return fail(SDB_UNSUPPORTED, "n_group_keys %d outside 0..%d", q->n_group_keys, SDB_MAX_GROUP_KEYS);
@@ -308,7 +361,8 @@ sdb_status check_query(const sdb_query* q) {
         return fail(SDB_INVALID_ARG, "force_window %d is not in -1..2^24", q->force_window);
     if (q->force_segments < -1 || q->force_segments > 1)
         return fail(SDB_INVALID_ARG, "force_segments %d is not -1, 0 or 1", q->force_segments);
-    if (q->reserved_ != 0) return fail(SDB_INVALID_ARG, "sdb_query.reserved_ must be 0");
+    if (q->force_prefilter < -1 || q->force_prefilter > 1)
+        return fail(SDB_INVALID_ARG, "force_prefilter %d is not -1, 0 or 1", q->force_prefilter);
     return SDB_OK;
 }
 
@@ -882,6 +936,12 @@ constexpr uint64_t kSliceMinTableBytes = 16ull << 20;
 constexpr int64_t kSliceMinRows = 1ll << 24;
 constexpr int64_t kSliceMaxRows = 0xFFFFF000ll;   // record positions are 32-bit
 constexpr int kSliceLog2Bytes = 21;
+// The pre-filter pays when at most this fraction of the rows gets through it.
+// Measured on c5 (600M rows, half of them dropped): the filter reads add 2.3
+// ms to the count pass, and the dropped rows save 0.9 ms of the scatter pass
+// and 3.1 ms of the probe, so a row costs about 0.28 of what a dropped row
+// saves.
+constexpr double kPrefilterMaxKept = 0.7;
 
 // The join the query allows to run over table slices, or -1: the only join,
 // into a hash table, with every other stage a fact predicate, a SUM of one
@@ -905,7 +965,7 @@ int slice_bits_for(const sdb_dim* d) {
 
 // Run-scratch layout of the sliced probe's partition passes.
 struct SliceLayout {
-    uint64_t hist, part_count, part_start, chunk_start, out_key, out_val, out_val2, tile_base, tile_map, total;
+    uint64_t hist, part_count, part_start, chunk_start, out_key, out_val, out_val2, keep, tile_base, tile_map, total;
     int64_t tile_rows, n_vtiles;
 };
 
@@ -935,6 +995,7 @@ SliceLayout slice_layout(const sdb_query* q, const sdb_plan* plan) {
     L.out_key = take(n * 4);
     L.out_val = take(n * 4);
     L.out_val2 = q->agg.kind != SDB_AGG_COL ? take(n * 4) : 0;
+    L.keep = plan->slice_prefilter ? take((n + 3) / 4) : 0;
     L.tile_rows = std::max<int64_t>(1, slice_tile_rows(plan));
     L.n_vtiles = 8 * ((int64_t)((n + (uint64_t)L.tile_rows - 1) / (uint64_t)L.tile_rows) + 1);
     L.tile_base = take(P * 4);
@@ -1335,7 +1396,18 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
             bp[d].hshift = 32 - bits;
             bp[d].dense = 0;
             bp[d].fill_value = 0u;
-            bp[d].fill_words = cap * 2;
+            // the pass filter after the slots: a bitmap over the key range when
+            // it fits the filter's bytes, else the Bloom filter over all of them
+            const uint64_t slot_bytes = align_up(cap * 8, 256), fbytes = filter_bytes(n);
+            uint32_t* filt = (uint32_t*)(table + slot_bytes);
+            const bool bitmap = range > 0 && range <= fbytes * 8;
+            out->filter = filt;
+            out->filter_kind = bitmap ? SDB_FILTER_BITMAP : SDB_FILTER_BLOOM;
+            out->filter_bits = bitmap ? range : fbytes * 8;
+            bp[d].filt = filt;
+            bp[d].filt_kind = out->filter_kind;
+            bp[d].filt_bits = out->filter_bits;
+            bp[d].fill_words = (slot_bytes + fbytes) / 4;
         }
     }
 
@@ -1382,6 +1454,8 @@ SDB_API sdb_status sdb_dim_info(const sdb_dim* dim, sdb_dim_summary* out) {
         if (!d.map) return fail(SDB_INVALID_ARG, "hash handle without its slots");
         table_bytes = d.n_slots * 8ull;
     }
+    const std::string fp = filter_problem(&d);
+    if (!fp.empty()) return fail(SDB_INVALID_ARG, "%s", fp.c_str());
     sdb_dim_summary o;
     std::memset(&o, 0, sizeof o);
     o.kind = d.kind;
@@ -1398,6 +1472,8 @@ SDB_API sdb_status sdb_dim_info(const sdb_dim* dim, sdb_dim_summary* out) {
     o.n_slots = d.n_slots;
     o.table_bytes = table_bytes;
     o.occupancy = d.n_slots > 0 ? (double)d.n_rows / (double)d.n_slots : 0.0;
+    o.filter_kind = d.filter_kind;
+    o.filter_bytes = d.filter_kind != SDB_FILTER_NONE ? (d.filter_bits + 31) / 32 * 4 : 0;
     uint64_t domain = 1;
     for (int p = 0; p < d.n_payloads; ++p) {
         o.payload_min[p] = d.payload_min[p];
@@ -1736,6 +1812,16 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             if (plan->stage_kind[s] == 1) plan->slice_stage = s;
         plan->slice_grid = (int32_t)std::min<int64_t>(
             kSliceMaxGrid, std::max<int64_t>(1, (q->n_fact + kSliceChunk - 1) / kSliceChunk));
+        // pre-filter by the table's pass filter when enough rows would drop:
+        // each row costs one filter read in the count pass, each dropped row
+        // saves its scatter write and its probe
+        const sdb_dim* d = q->joins[slice_j].dim;
+        if (d->filter_kind != SDB_FILTER_NONE && q->force_prefilter != -1) {
+            const int ss = plan->slice_stage;
+            const double p = plan->sampled_rows > 0 ? plan->stage_pass_alone[ss] : plan->stage_pass[ss];
+            const double fp = d->filter_kind == SDB_FILTER_BLOOM ? bloom_false_positive(d->filter_bits, d->n_pass) : 0.0;
+            plan->slice_prefilter = (q->force_prefilter == 1 || p + (1.0 - p) * fp <= kPrefilterMaxKept) ? 1 : 0;
+        }
         plan->run_scratch_bytes += (int64_t)slice_layout(q, plan).total;
     }
     return ok();
@@ -1799,6 +1885,11 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
             plan->slice_grid > kSliceMaxGrid || plan->eager != 0)
             return fail(SDB_INVALID_ARG, "bad sliced-probe plan");
     }
+    if (plan->slice_prefilter != 0 &&
+        (plan->slice_prefilter != 1 || !sliced ||
+         q->joins[plan->stage_index[plan->slice_stage]].dim->filter_kind == SDB_FILTER_NONE))
+        return fail(SDB_INVALID_ARG, "slice_prefilter %d needs a sliced probe into a table with a pass filter",
+                    plan->slice_prefilter);
     if (plan->unroll != 0 && (plan->unroll != 1 || !unroll_allowed(q, plan)))
         return fail(SDB_INVALID_ARG, "bad plan unroll %d (needs at most %d stages, 4-row items, ipt 2, blocks of "
                     "%d or %d, no eager loads, no hash probe and no table slices)", plan->unroll, kUnrollStages,
@@ -1862,6 +1953,14 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         sp.out_key = (int32_t*)(slice_base + SL.out_key);
         sp.out_val = (int32_t*)(slice_base + SL.out_val);
         sp.out_val2 = sp.val2_col >= 0 ? (int32_t*)(slice_base + SL.out_val2) : nullptr;
+        if (plan->slice_prefilter) {
+            const sdb_dim* fd = q->joins[plan->stage_index[ss]].dim;
+            sp.filt = (const uint32_t*)fd->filter;
+            sp.filt_bits = fd->filter_bits;
+            sp.filt_kind = fd->filter_kind;
+            sp.filt_key_min = fd->key_min;
+            sp.keep = slice_base + SL.keep;
+        }
         sp.tile_rows = SL.tile_rows;
         sp.tile_base = (uint32_t*)(slice_base + SL.tile_base);
         sp.tile_map = (int32_t*)(slice_base + SL.tile_map);

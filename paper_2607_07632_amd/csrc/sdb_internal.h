@@ -233,6 +233,11 @@ struct BuildParams {
     int32_t dense;             // 1: dense map (scatter + bitmap), 0: hash table (inserts)
     uint32_t fill_value;       // the table's initial word value (all ones dense, 0 hash)
     uint64_t fill_words;       // 32-bit words of the table to fill before the scatter / inserts
+                               // (a hash table's pass filter follows its slots and is filled too)
+    uint32_t* filt;            // hash: pass filter words (SDB_FILTER_*), or null
+    uint64_t filt_bits;
+    int32_t filt_kind;
+    int32_t pad2_;
 };
 
 // Every table of one sdb_build_dims call; kernels take table blockIdx.y.
@@ -309,6 +314,14 @@ struct SliceParams {
     uint32_t* tile_base;       // n_parts entries: rank of partition q's first tile among its XCD's tiles
     int32_t* tile_map;         // n_vtiles entries: [8 * rank + x] = tile, -1 where XCD x has fewer tiles
     int64_t n_vtiles;
+    // pre-filter: rows whose key the table's pass filter rejects are dropped
+    // by the count pass, which writes one byte per 4-row group (bit j: row
+    // 4 g + j kept) for the scatter pass; filt null: no pre-filter
+    const uint32_t* filt;
+    uint64_t filt_bits;
+    int32_t filt_kind;
+    int32_t filt_key_min;
+    uint8_t* keep;             // ceil(n / 4) bytes
 };
 
 // ---- launchers (sdb_kernels.hip) -----------------------------------------

@@ -326,7 +326,38 @@ __global__ void __launch_bounds__(256) dense_bits_kernel(BuildBatch kernel_args)
     }
 }
 
-// Open addressing, linear probing, 8-byte slots {key, code + 1 | 0xFFFFFFFF}.
+// Pass filter of a hash table's keys. SDB_FILTER_BITMAP: bit k - key_min of
+// the key range. SDB_FILTER_BLOOM: three bits of one 32-bit word, the word
+// and the bits from two mixes of the key (a blocked Bloom filter: one word
+// read per test).
+// The key mix is MurmurHash3's 32-bit finalizer.
+__device__ __forceinline__ uint32_t filter_mix(int32_t k) {
+    uint32_t m = (uint32_t)k;
+    m = (m ^ (m >> 16)) * 0x85EBCA6Bu;
+    m ^= m >> 13;
+    m *= 0xC2B2AE35u;
+    return m ^ (m >> 16);
+}
+
+// Word index and bit mask of key k in a filter of `nbits` bits; false when a
+// bitmap's key range does not hold k.
+__device__ __forceinline__ bool filter_slot(int32_t kind, uint64_t nbits, int32_t kmin, int32_t k, uint32_t& word,
+                                            uint32_t& mask) {
+    if (kind == SDB_FILTER_BITMAP) {
+        const uint32_t idx = (uint32_t)k - (uint32_t)kmin;
+        word = idx >> 5;
+        mask = 1u << (idx & 31u);
+        return (uint64_t)idx < nbits;
+    }
+    const uint32_t m = filter_mix(k);
+    const uint32_t t = ((m << 16) | (m >> 16)) * 0x9E3779B1u;
+    word = m & (uint32_t)((nbits >> 5) - 1u);
+    mask = (1u << (t >> 27)) | (1u << ((t >> 22) & 31u)) | (1u << ((t >> 17) & 31u));
+    return true;
+}
+
+// Open addressing, linear probing, 8-byte slots {key, code + 1 | 0xFFFFFFFF};
+// a passing row's key also goes into the table's pass filter.
 __global__ void __launch_bounds__(256) hash_insert_kernel(BuildBatch kernel_args) {
     SDB_BATCH_TABLE;
     if (bp.dense) return;
@@ -336,6 +367,9 @@ __global__ void __launch_bounds__(256) hash_insert_kernel(BuildBatch kernel_args
         const int32_t k = bp.key[i];
         const uint32_t enc = dim_row_passes(bp, i) ? dim_row_code(bp, i) + 1u : 0xFFFFFFFFu;
         const unsigned long long slot = ((unsigned long long)enc << 32) | (uint32_t)k;
+        uint32_t fw, fm;
+        if (bp.filt && enc != 0xFFFFFFFFu && filter_slot(bp.filt_kind, bp.filt_bits, bp.kmin, k, fw, fm))
+            atomicOr(&bp.filt[fw], fm);
         uint32_t h = ((uint32_t)k * 0x9E3779B1u) >> bp.hshift & bp.hmask;
         bool placed = false;
         for (uint64_t it = 0; it < bp.nslots; ++it) {
@@ -1202,6 +1236,47 @@ __device__ __forceinline__ void slice_load_keys(const SliceParams& sp, int64_t c
     }
 }
 
+// The pre-filter of the count pass: drops the rows whose key the table's
+// pass filter rejects, and records for each of the thread's 4-row groups
+// below r1 which of its rows stay (bit j: row 4 g + j), for the scatter pass.
+template <int RPT>
+__device__ __forceinline__ void slice_prefilter(const SliceParams& sp, int64_t c0, int64_t r1, const int32_t (&k)[RPT],
+                                                bool (&ok)[RPT]) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+        uint32_t w, m;
+        if (ok[i]) ok[i] = filter_slot(sp.filt_kind, sp.filt_bits, sp.filt_key_min, k[i], w, m) &&
+                           (sp.filt[w] & m) == m;
+    }
+#pragma unroll
+    for (int i = 0; i < RPT / 4; ++i) {
+        const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
+        if (r < r1)
+            sp.keep[r >> 2] = (uint8_t)((ok[4 * i] ? 1u : 0u) | (ok[4 * i + 1] ? 2u : 0u) | (ok[4 * i + 2] ? 4u : 0u) |
+                                        (ok[4 * i + 3] ? 8u : 0u));
+    }
+}
+
+// The scatter pass's rows after a pre-filter: which of the thread's rows the
+// count pass kept, and their keys (0 for the others).
+template <int RPT>
+__device__ __forceinline__ void slice_load_kept(const SliceParams& sp, int64_t c0, int64_t r1, int32_t (&k)[RPT],
+                                                bool (&ok)[RPT]) {
+    const int32_t* key = sp.cols[sp.key_col];
+#pragma unroll
+    for (int i = 0; i < RPT / 4; ++i) {
+        const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);
+        const uint32_t kb = r < r1 ? sp.keep[r >> 2] : 0u;
+        int32_t x[4] = {0, 0, 0, 0};
+        if (kb) slice_load4(key, r, r1, x);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            ok[4 * i + j] = ((kb >> j) & 1u) != 0u;
+            k[4 * i + j] = ok[4 * i + j] ? x[j] : 0;
+        }
+    }
+}
+
 // Count pass: block b's passing rows per partition, into hist[q * grid + b].
 // Lanes count into four interleaved copies of the histogram (by lane mod 4),
 // so fewer lanes of one LDS atomic instruction hit the same counter.
@@ -1217,6 +1292,7 @@ __global__ void __launch_bounds__(kSliceBlock) slice_count_kernel(SliceParams sp
         int32_t k[kSliceRowsPerThread];
         bool ok[kSliceRowsPerThread];
         slice_load_keys<kSliceRowsPerThread>(sp, c0, r1, k, ok);
+        if (sp.filt) slice_prefilter<kSliceRowsPerThread>(sp, c0, r1, k, ok);
 #pragma unroll
         for (int i = 0; i < kSliceRowsPerThread; ++i)
             if (ok[i]) atomicAdd(&mine[4u * slice_of(k[i], sp.bits)], 1u);
@@ -1265,7 +1341,8 @@ __device__ uint32_t block_scan_any(const uint32_t* in, uint32_t* out, uint32_t n
 // writes every partition's run of keys and values (TWO: both operands of a
 // two-column aggregate, in chunks half as long so they fit LDS) after the ones
 // block b wrote before (hist holds block b's first offset within each
-// partition).
+// partition). With a pre-filter the passing rows are the ones the count pass
+// kept, read from its per-group bytes instead of testing the predicates again.
 template <int RPT, bool TWO>
 __global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams sp) {
     constexpr int CHUNK = RPT * kSliceBlock;
@@ -1291,7 +1368,8 @@ __global__ void __launch_bounds__(kSliceBlock) slice_scatter_kernel(SliceParams 
         int32_t k[RPT], v[RPT], v2[RPT];
         bool ok[RPT];
         uint32_t rk[RPT];
-        slice_load_keys<RPT>(sp, c0, r1, k, ok);
+        if (sp.keep) slice_load_kept<RPT>(sp, c0, r1, k, ok);
+        else slice_load_keys<RPT>(sp, c0, r1, k, ok);
 #pragma unroll
         for (int i = 0; i < RPT / 4; ++i) {
             const int64_t r = c0 + 4 * ((int64_t)i * kSliceBlock + threadIdx.x);

@@ -39,6 +39,8 @@ TERMINALS = {"auto": 0, "scalar": 1, "lds": 2, "global": 3, "part": 4}
 BASELINES = {"per_operator": 0, "global_handoff": 1}
 TERMINAL_NAMES = {1: "scalar", 2: "lds", 3: "global", 4: "part"}
 LDS_NAMES = {0: "global", 1: "lds_map", 2: "lds_bits", 3: "lds_rank", 4: "lds_coarse", 5: "lds_window"}
+FILTER_NAMES = {0: None, 1: "bitmap", 2: "bloom"}
+MAX_FILTER_BYTES = 4 << 20
 STATUS = {0: "SDB_OK", 1: "SDB_INVALID_ARG", 2: "SDB_UNSUPPORTED", 3: "SDB_CAPACITY",
           4: "SDB_WORKSPACE_TOO_SMALL", 5: "SDB_DUP_KEY", 6: "SDB_KEY_RANGE", 7: "SDB_HIP_ERROR"}
 
@@ -62,7 +64,8 @@ class SdbDim(C.Structure):
                 ("n_slots", u64), ("hash_bits", i32),
                 ("sentinel", u32), ("domain", u64), ("n_payloads", i32),
                 ("payload_min", i32 * MAX_PAYLOADS), ("payload_radix", u32 * MAX_PAYLOADS),
-                ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp), ("bits", vp)]
+                ("payload_div", u64 * MAX_PAYLOADS), ("map", vp), ("stats", vp), ("bits", vp),
+                ("filter", vp), ("filter_bits", u64), ("filter_kind", i32), ("reserved_", i32)]
 
 
 class SdbDimSummary(C.Structure):
@@ -71,7 +74,7 @@ class SdbDimSummary(C.Structure):
                 ("pass_keys_contiguous", i32), ("n_payloads", i32), ("n_slots", u64), ("table_bytes", u64),
                 ("occupancy", C.c_double), ("payload_min", i32 * MAX_PAYLOADS),
                 ("payload_max", i32 * MAX_PAYLOADS), ("payload_radix", u32 * MAX_PAYLOADS),
-                ("reserved_", i32), ("domain", u64)]
+                ("filter_kind", i32), ("domain", u64), ("filter_bytes", u64)]
 
 
 class SdbJoin(C.Structure):
@@ -96,7 +99,7 @@ class SdbQuery(C.Structure):
                 ("force_lds", i32), ("force_xcd", i32), ("force_eager", i32),
                 ("force_block", i32), ("force_range", i32), ("force_coarse", i32),
                 ("force_slice", i32), ("force_unroll", i32), ("force_window", i32), ("force_segments", i32),
-                ("reserved_", i32)]
+                ("force_prefilter", i32)]
 
 
 class SdbPlan(C.Structure):
@@ -113,7 +116,8 @@ class SdbPlan(C.Structure):
                 ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
                 ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64),
-                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("unroll", i32),
+                ("slice_bits", i32), ("slice_stage", i32), ("slice_grid", i32), ("slice_prefilter", i32),
+                ("unroll", i32),
                 ("n_segments", i32), ("segment_order", (i32 * MAX_STAGES) * MAX_SEGMENTS),
                 ("segment_start", i64 * (MAX_SEGMENTS + 1))]
 
@@ -302,7 +306,8 @@ def dim_info(table) -> dict:
             "pass_key_max": o.pass_key_max, "pass_keys_contiguous": bool(o.pass_keys_contiguous),
             "n_slots": int(o.n_slots), "table_bytes": int(o.table_bytes), "occupancy": o.occupancy,
             "payload_min": list(o.payload_min[:k]), "payload_max": list(o.payload_max[:k]),
-            "payload_radix": [int(x) for x in o.payload_radix[:k]], "domain": int(o.domain)}
+            "payload_radix": [int(x) for x in o.payload_radix[:k]], "domain": int(o.domain),
+            "filter": FILTER_NAMES.get(o.filter_kind, o.filter_kind), "filter_bytes": int(o.filter_bytes)}
 
 
 def _join_inputs(dims: dict, dim_keys: dict, jd: dict):
@@ -435,6 +440,7 @@ class StarQuery:
         q.force_unroll = int(force.get("unroll", 0))
         q.force_window = int(force.get("window", 0))
         q.force_segments = int(force.get("segments", 0))
+        q.force_prefilter = int(force.get("prefilter", 0))
         self.q = q
         self.query = query
         self.tables = tables
@@ -581,6 +587,8 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
                 st["deferred_gather"] = True
             if plan.slice_bits and s == plan.slice_stage:
                 st["table_slices"] = 1 << plan.slice_bits
+                if plan.slice_prefilter:
+                    st["prefilter"] = True
         stages.append(st)
     return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
             "ipt": plan.ipt, "vector": plan.vector, "eager": plan.eager, "block": plan.block, "grid": plan.grid,

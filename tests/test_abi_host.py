@@ -40,7 +40,7 @@ def test_struct_layout_matches_binding():
     assert L.sdb_struct_sizes(sizes, 9) == 0
     assert [C.sizeof(s) for s in sdb.STRUCTS] == list(sizes)
     assert L.sdb_struct_sizes(sizes, 10) == 1
-    assert L.sdb_abi_version() == 9
+    assert L.sdb_abi_version() == 10
 
 
 def test_status_strings():
@@ -67,11 +67,12 @@ def test_required_bytes_bounds():
     # stats + 2000 slots x 4 B + pass bitmap
     assert dense == 256 + 8192 + 256
     h = sdb.dim_required_bytes(_desc(1000, "hash"))
-    assert h == 256 + 2048 * 8
+    assert h == 256 + 2048 * 8 + 1024            # slots, then a pass filter of 8 bits per row (1024 bytes)
     a = sdb.dim_required_bytes(_desc(1000, "auto"))
     assert a == max(dense, h)
     big = sdb.dim_required_bytes(_desc(1 << 24, "hash", lf=0.5))
-    assert big == 256 + (1 << 25) * 8            # 256 MiB table at load factor 0.5
+    assert big == 256 + (1 << 25) * 8 + sdb.MAX_FILTER_BYTES   # 256 MiB table at load factor 0.5, 4 MiB filter
+    assert sdb.dim_required_bytes(_desc(10, "hash")) == 256 + 256 + 256      # 32 slots padded, 256-byte filter
     budget = _desc(1000, "auto")
     budget.dense_budget_bytes = 1 << 20
     assert sdb.dim_required_bytes(budget) == 256 + (1 << 20) + 512      # room for a dense table of the budget
@@ -609,7 +610,7 @@ def test_segment_validation():
         bad = sdb.SdbPlan.from_buffer_copy(good)
         mutate(bad)
         assert status(bad) == 1
-    for field, value in [("force_segments", 2), ("force_segments", -2), ("reserved_", 1)]:
+    for field, value in [("force_segments", 2), ("force_segments", -2), ("force_prefilter", 2), ("force_prefilter", -2)]:
         qb = sdb.SdbQuery.from_buffer_copy(q)
         setattr(qb, field, value)
         assert L.sdb_plan_star_query(C.byref(qb), None, 0, None, C.byref(sdb.SdbPlan())) == 1

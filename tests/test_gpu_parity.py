@@ -230,6 +230,143 @@ def test_sliced_probe_at_every_slice_count():
     assert seen == {1, 2, 3, 5, 8}, seen
 
 
+def _filter_words(table):
+    """The pass filter of a built hash table, copied from its workspace."""
+    import torch
+    from paper_2607_07632_amd import sdb
+    nbytes = sdb.dim_info(table)["filter_bytes"]
+    off = table.handle.filter - table.workspace.data_ptr()
+    return table.workspace[off:off + nbytes].view(torch.int32).cpu().numpy().view(np.uint32)
+
+
+def _bitmap_words(keys, key_min, n_bits):
+    bits = np.zeros((n_bits + 31) // 32 * 32, dtype=bool)
+    bits[keys.astype(np.int64) - key_min] = True
+    return np.packbits(bits, bitorder="little").view(np.uint32)
+
+
+def _bloom_words(keys, n_words):
+    """The blocked Bloom filter the header documents, written out in numpy:
+    word m mod n_words of m = mix(key) holds three bits picked by
+    t = rotl(m, 16) * 0x9E3779B1."""
+    m = keys.astype(np.int32).view(np.uint32).copy()
+    m = (m ^ (m >> np.uint32(16))) * np.uint32(0x85EBCA6B)
+    m ^= m >> np.uint32(13)
+    m *= np.uint32(0xC2B2AE35)
+    m ^= m >> np.uint32(16)
+    t = ((m << np.uint32(16)) | (m >> np.uint32(16))) * np.uint32(0x9E3779B1)
+    one = np.uint32(1)
+    mask = (np.left_shift(one, t >> np.uint32(27)) | np.left_shift(one, (t >> np.uint32(22)) & np.uint32(31)) |
+            np.left_shift(one, (t >> np.uint32(17)) & np.uint32(31)))
+    out = np.zeros(n_words, dtype=np.uint32)
+    np.bitwise_or.at(out, m & np.uint32(n_words - 1), mask)
+    return out
+
+
+def _one_hash_join(m, n, key_span, seed, lf=0.5):
+    """One hash join over m dimension rows whose distinct keys are drawn from
+    key_span values around 0 (half of the rows filtered out), n fact rows
+    with 80% hits, a fact predicate, SUM(value) by one payload."""
+    rng = np.random.default_rng([2607, 7632, 71, seed])
+    keys = (rng.choice(key_span, m, replace=False) - key_span // 2).astype(np.int32)
+    dims = {"big": {"key": keys, "flag": rng.integers(0, 2, m, dtype=np.int32),
+                    "attr": rng.integers(0, 700, m, dtype=np.int32)}}
+    hit = keys[rng.integers(0, m, n)]
+    miss = rng.integers(-key_span // 2 - 10, key_span // 2 + 10, n).astype(np.int32)
+    fact = {"key": np.where(rng.random(n) < 0.8, hit, miss).astype(np.int32),
+            "value": rng.integers(-10**6, 10**6, n, dtype=np.int32)}
+    query = {"fact_preds": [{"col": "value", "op": "ge", "lo": -900_000, "hi": None}],
+             "joins": [{"fact_key": "key", "dim": "big", "preds": [{"col": "flag", "op": "eq", "lo": 1, "hi": None}],
+                        "payloads": ["attr"], "kind": "hash", "load_factor": lf}],
+             "group_by": [["big", "attr"]], "agg": {"kind": "col", "a": "value", "b": None}}
+    return datagen.Workload(f"one hash join, {m} rows over {key_span} keys", n, fact, dims, {"big": "key"}, query)
+
+
+def test_hash_pass_filter_words():
+    """A hash table's pass filter holds exactly its passing keys: c5's table
+    and a permuted key range as a bitmap over the key range, keys spread over
+    2^31 values as the documented Bloom filter (word for word)."""
+    from paper_2607_07632_amd import sdb
+    w = workload("c5_hash_stress")
+    _, dims = upload(datagen.Workload(w.name, 0, {k: v[:0] for k, v in w.fact.items()}, w.dims, w.dim_keys,
+                                      w.query))
+    t = sdb.build_dims(dims, w.dim_keys, w.query)[0]
+    info = sdb.dim_info(t)
+    assert info["kind"] == "hash" and info["filter"] == "bitmap" and info["filter_bytes"] == 2 << 20
+    big = w.dims["big"]
+    want = _bitmap_words(big["key"][big["flag"] == 1], info["key_min"], info["key_max"] - info["key_min"] + 1)
+    assert np.array_equal(_filter_words(t), want)
+    for m, span, kind in ((3000, 7000, "bitmap"), (5000, 1 << 31, "bloom"), (1, 1, "bitmap")):
+        wj = _one_hash_join(m, 0, span, seed=m)
+        _, dj = upload(wj)
+        tj = sdb.build_dims(dj, wj.dim_keys, wj.query)[0]
+        ij = sdb.dim_info(tj)
+        assert ij["filter"] == kind, (m, span, ij)
+        passing = wj.dims["big"]["key"][wj.dims["big"]["flag"] == 1]
+        if kind == "bitmap":
+            want = _bitmap_words(passing, ij["key_min"], ij["key_max"] - ij["key_min"] + 1)
+        else:
+            assert ij["filter_bytes"] == 8192                     # 8 bits per row, a power of two
+            want = _bloom_words(passing, ij["filter_bytes"] // 4)
+        assert np.array_equal(_filter_words(tj), want), (m, span)
+
+
+@pytest.mark.parametrize("n", [1, 16_385, 300_007])
+@pytest.mark.parametrize("span", [7000, 1 << 31])
+def test_prefilter_agrees_with_the_oracle(n, span):
+    """The sliced probe with its pre-filter (bitmap or Bloom filter) and
+    without, every terminal shape and a two-column aggregate, against the
+    oracle."""
+    w = _one_hash_join(3000, n, span, seed=n + span)
+    want = oracle_rows(w)
+    for force in ({"slice": 1, "prefilter": 1}, {"slice": 1, "prefilter": 1, "terminal": "global"},
+                  {"slice": 1, "prefilter": 1, "terminal": "part"}, {"slice": 1, "prefilter": -1}):
+        got, q = run_gpu(w, force=force)
+        assert q.plan_obj.slice_bits > 0 and q.plan_obj.slice_prefilter == (force["prefilter"] == 1)
+        assert_same(got.as_rows(), want, f"{w.name}, {n} rows, {force}")
+    w2 = datagen.Workload(w.name, w.n_fact, w.fact, w.dims, w.dim_keys,
+                          {**w.query, "agg": {"kind": "sub", "a": "value", "b": "key"}})
+    got, q = run_gpu(w2, force={"slice": 1, "prefilter": 1})
+    assert q.plan_obj.slice_prefilter == 1
+    assert_same(got.as_rows(), oracle_rows(w2), f"{w.name}, {n} rows, value - key")
+
+
+@pytest.mark.parametrize("n", [0, 5, 16_383, 16_384, 70_001])
+def test_prefilter_on_random_tiny_schemas(n):
+    """Forced pre-filters over random one-join schemas (fact predicates,
+    misses, filtered rows, every aggregate kind) at row counts around the
+    passes' chunks: the oracle's groups, sums and counts exactly."""
+    done = 0
+    for seed in range(60):
+        w0 = random_tiny_workload(5000 + seed, n_fact=n, max_dim_rows=3000)
+        if not w0.query["joins"]:
+            continue
+        w = _sliceable(w0, load_factor=(0.5, 0.25, 0.9)[seed % 3], keep_agg=seed % 2 == 1)
+        for force in ({"slice": 1, "prefilter": 1}, {"slice": 1, "prefilter": 1, "order": True}):
+            got, q = run_gpu(w, force=force)
+            assert q.plan_obj.slice_prefilter == (1 if n else 0), (seed, force)
+            assert_same(got.as_rows(), oracle_rows(w), f"seed {seed} n {n} {force}")
+        done += 1
+        if done == 3:
+            break
+    assert done == 3
+
+
+def test_c5_prefilter_is_the_planners_choice():
+    """c5 (half of the table's rows filtered out): the planner takes the
+    pre-filter; with it and without, the oracle's result."""
+    w = workload("c5_hash_stress")
+    want = want_rows("c5_hash_stress")
+    got, q = run_gpu(w, force={"slice": 1})
+    assert q.plan_obj.slice_prefilter == 1
+    from paper_2607_07632_amd import sdb
+    assert sdb.plan_summary(q.plan_obj, w.query)["stages"][-1].get("prefilter") is True
+    assert_same(got.as_rows(), want, "c5 pre-filtered")
+    got, q = run_gpu(w, force={"slice": 1, "prefilter": -1})
+    assert q.plan_obj.slice_prefilter == 0
+    assert_same(got.as_rows(), want, "c5 without the pre-filter")
+
+
 def test_c1_forced_plans_agree():
     w = workload("c1_scalar_scan")
     want = want_rows("c1_scalar_scan")

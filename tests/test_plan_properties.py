@@ -56,6 +56,11 @@ def dims(draw):
         h.sentinel = 0xFFFFFFFE
     h.key_min = draw(st.integers(-5000, 5000))
     h.key_max = h.key_min + (h.n_slots - 1 if kind == 1 else n_rows * 2)
+    if kind == 2:
+        h.filter_kind = draw(st.sampled_from([0, 1, 2]))      # none, a bitmap over the key range, Bloom
+        if h.filter_kind:
+            h.filter = 0x800000
+            h.filter_bits = (h.key_max - h.key_min + 1) if h.filter_kind == 1 else 32 << draw(st.integers(0, 20))
     if n_pass and draw(st.booleans()):                      # passing keys one contiguous range
         lo = draw(st.integers(h.key_min, h.key_min + 1000))
         h.pass_key_min, h.pass_key_max = lo, lo + n_pass - 1
@@ -101,6 +106,7 @@ def queries(draw):
     q.force_slice = draw(st.sampled_from([-1, 0, 1, 1]))
     q.force_unroll = draw(st.sampled_from([-1, 0, 0]))
     q.force_window = draw(st.sampled_from([-1, 0, 0, 1, 2, 7]))
+    q.force_prefilter = draw(st.sampled_from([-1, 0, 1]))
     return q, ds
 
 
@@ -173,8 +179,17 @@ def check_plan(q, p):
         # partition counts and offsets, and one key and value (two for a two-column aggregate) per fact row
         per_row = 12 if q.agg.kind else 8
         assert p.run_scratch_bytes >= per_row * q.n_fact + 4 * p.slice_grid * (1 << p.slice_bits)
+        # the pre-filter: only into a table with a pass filter, always when forced, never when refused
+        assert p.slice_prefilter in (0, 1)
+        if d.filter_kind == 0 or q.force_prefilter == -1:
+            assert p.slice_prefilter == 0
+        elif q.force_prefilter == 1:
+            assert p.slice_prefilter == 1
+        if p.slice_prefilter:
+            assert p.run_scratch_bytes >= per_row * q.n_fact + q.n_fact // 4
     else:
         assert not (sliceable and q.force_slice == 1)
+        assert p.slice_prefilter == 0
     # the unrolled stage loop: exactly where its instance exists and no hash
     # table is probed, unless turned off
     hash_probe = any(q.joins[p.stage_index[s]].dim.contents.kind == 2 for s in join_probe)
@@ -246,13 +261,17 @@ def test_rank_and_deferred_placements_pass_run_validation(force_lds, force_block
     assert status in (OK, HIP_ERROR), (status, sdb.lib().sdb_last_error())
 
 
-def _c5_like(n_fact, hash_bits=25, n_preds=1, agg_kind=0, aligned=True):
+def _c5_like(n_fact, hash_bits=25, n_preds=1, agg_kind=0, aligned=True, filt=None, pass_frac=0.5):
     """One hash join with its payload as the group key (a 2^hash_bits-slot
-    table), an optional fact predicate, SUM of one column."""
+    table, `pass_frac` of its rows passing, with a pass filter `filt`: None,
+    "bitmap" or "bloom"), an optional fact predicate, SUM of one column."""
     d = sdb.SdbDim()
     d.kind, d.width, d.n_rows = 2, 8, 1 << (hash_bits - 1)
-    d.n_pass, d.hash_bits, d.n_slots, d.sentinel = 1 << (hash_bits - 2), hash_bits, 1 << hash_bits, 0xFFFFFFFE
+    d.n_pass, d.hash_bits, d.n_slots, d.sentinel = int(pass_frac * d.n_rows), hash_bits, 1 << hash_bits, 0xFFFFFFFE
     d.key_min, d.key_max = 0, (1 << (hash_bits - 1)) - 1
+    if filt:
+        d.filter, d.filter_kind = 0x800000, {"bitmap": 1, "bloom": 2}[filt]
+        d.filter_bits = d.key_max + 1 if filt == "bitmap" else min(8 * d.n_rows, sdb.MAX_FILTER_BYTES * 8)
     d.pass_key_min, d.pass_key_max = 0, 5                  # passing keys are not one range
     d.n_payloads, d.payload_radix[0], d.payload_div[0], d.domain = 1, 65536, 1, 65536
     d.map = 0x400000
@@ -326,3 +345,82 @@ def test_sliced_plan_validation():
     short = sdb.lib().sdb_run_star_query(C.byref(q), C.byref(p), 0x20000000, 0x30000000, int(p.n_groups),
                                          0x10000000, int(p.run_scratch_bytes) - 256, None)
     assert short == 4                                       # SDB_WORKSPACE_TOO_SMALL
+
+
+def _bloom_false_positive(bits, n_keys):
+    """Blocked Bloom filter, 3 bits of one 32-bit word per key: the chance
+    that all 3 bits of a key not in the set are set, a word holding
+    Poisson(n_keys / words) keys."""
+    import math
+    lam = n_keys / (bits // 32)
+    fp, pmf = 0.0, math.exp(-lam)
+    for j in range(int(lam + 12 * math.sqrt(lam + 1) + 24) + 1):
+        fp += pmf * (1 - (31 / 32) ** (3 * j)) ** 3
+        pmf *= lam / (j + 1)
+    return fp
+
+
+@pytest.mark.parametrize("filt,pass_frac,force,want", [
+    ("bitmap", 0.5, 0, 1),       # c5: half the rows cannot pass the join
+    ("bitmap", 0.9, 0, 0),       # too few rows dropped to pay for a filter read per row
+    ("bitmap", 0.9, 1, 1),
+    ("bitmap", 0.5, -1, 0),
+    (None, 0.5, 1, 0),           # no filter to test against
+    ("bloom", 0.05, 0, 1),       # few keys: few false positives
+    ("bloom", 0.7, 0, 0),        # a crowded filter lets most of the rest through
+])
+def test_prefilter_choice(filt, pass_frac, force, want):
+    q, _d = _c5_like(600_000_000, filt=filt, pass_frac=pass_frac)
+    q.force_prefilter = force
+    p = sdb.SdbPlan()
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p)) == OK, sdb.lib().sdb_last_error()
+    check_plan(q, p)
+    assert p.slice_bits and p.slice_prefilter == want
+    if filt == "bloom" and force == 0:
+        d = _d
+        kept = pass_frac + (1 - pass_frac) * _bloom_false_positive(d.filter_bits, d.n_pass)
+        assert (kept <= 0.7) == bool(want)
+    if want:
+        q0, _d0 = _c5_like(600_000_000, filt=filt, pass_frac=pass_frac)
+        q0.force_prefilter = -1
+        p0 = sdb.SdbPlan()
+        assert sdb.lib().sdb_plan_star_query(C.byref(q0), None, 0, None, C.byref(p0)) == OK
+        assert p.run_scratch_bytes - p0.run_scratch_bytes >= 600_000_000 // 4     # a byte per 4 rows
+    if not GPU_PRESENT:
+        assert _run_status(q, p) in (OK, HIP_ERROR), sdb.lib().sdb_last_error()
+
+
+def test_prefilter_plan_validation():
+    q, _d = _c5_like(600_000_000, filt="bitmap")
+    p = sdb.SdbPlan()
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p)) == OK
+    assert p.slice_prefilter == 1
+    for value in (2, -1):
+        bad = sdb.SdbPlan.from_buffer_copy(p)
+        bad.slice_prefilter = value
+        assert _run_status(q, bad) == INVALID_ARG
+    # a table without a pass filter cannot serve the plan
+    q2, _d2 = _c5_like(600_000_000)
+    assert _run_status(q2, sdb.SdbPlan.from_buffer_copy(p)) == INVALID_ARG
+    # nor a plan without the sliced probe
+    unsliced = sdb.SdbPlan.from_buffer_copy(p)
+    unsliced.slice_bits = 0
+    assert _run_status(q, unsliced) == INVALID_ARG
+
+
+@pytest.mark.parametrize("mutate", [
+    lambda d: setattr(d, "filter_bits", d.filter_bits - 1),     # a bitmap covers exactly the key range
+    lambda d: setattr(d, "filter", None),
+    lambda d: setattr(d, "filter_kind", 3),
+    lambda d: (setattr(d, "filter_kind", 2), setattr(d, "filter_bits", 96)),   # Bloom: 32 x a power of two
+    lambda d: (setattr(d, "filter_kind", 2), setattr(d, "filter_bits", 64 << 20)),   # above 4 MiB
+    lambda d: setattr(d, "reserved_", 1),
+])
+def test_filter_fields_are_checked(mutate):
+    q, d = _c5_like(600_000_000, filt="bitmap")
+    p = sdb.SdbPlan()
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(p)) == OK
+    mutate(d)
+    assert sdb.lib().sdb_plan_star_query(C.byref(q), None, 0, None, C.byref(sdb.SdbPlan())) == INVALID_ARG
+    msg = sdb.lib().sdb_last_error().decode()
+    assert "filter" in msg or "reserved" in msg, msg
