@@ -21,9 +21,10 @@ its launch; `frac_b_dense` rates it on all fact-column bytes, and
 `frac_run_window` rates the whole run (output fill, fused kernel, terminal
 passes). `cpu_baseline` times the CPU oracle over the whole fact table on one
 worker process per host core (at most 16), and the full GPU result is compared
-with it group by group. `configs` holds a compact record of each other
-workload (run and kernel times, roofline fractions, oracle parity over its
-whole fact table).
+with it group by group; `cpu_oracle_one_core` times it in one process on the
+first rows (c1 whole, c2 and c3 8M rows). `configs` holds a compact record of
+each other workload (run and kernel times, roofline fractions, oracle parity
+over its first 2^27 fact rows, the whole table for c1 and c2).
 """
 
 from __future__ import annotations
