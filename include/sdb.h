@@ -394,7 +394,9 @@ typedef struct sdb_plan {
     int32_t lds_bytes;                    /* dynamic LDS per block */
     int32_t part_shift;                   /* PART: partition of group g is g >> part_shift */
     int32_t n_parts;
-    int64_t part_cap;                     /* PART: records per fused-kernel block */
+    int32_t part_subs;                    /* PART: record regions per fused-kernel block (1 .. 4): wave
+                                             w appends to region w mod part_subs of its block */
+    int64_t part_cap;                     /* PART: records per region */
     int32_t n_group_keys;
     int32_t key_min[SDB_MAX_GROUP_KEYS];
     uint32_t radix[SDB_MAX_GROUP_KEYS];

@@ -781,7 +781,8 @@ void place_lds(const sdb_query* q, sdb_plan* plan, uint64_t budget) {
 uint32_t lds_layout(const sdb_query* q, const sdb_plan* plan, FusedParams* p) {
     uint64_t off = 0;
     if (plan->terminal == TERM_LDS) off = plan->n_groups * 16;
-    if (plan->terminal == TERM_PART) off = align_up((1 + (uint64_t)plan->n_parts) * 4, 16);
+    // (room for the most record regions a block may have, whatever part_subs)
+    if (plan->terminal == TERM_PART) off = align_up((uint64_t)kPartSubRegions * (1 + (uint64_t)plan->n_parts) * 4, 16);
     if (p) p->term_lds_bytes = (uint32_t)off;
     for (int s = 0; s < plan->n_stages; ++s) {
         if (plan->stage_lds[s] == LDS_GLOBAL) continue;
@@ -885,6 +886,8 @@ constexpr bool kAutoEager = false;
 constexpr double kEagerMinLive = 0.02;
 // the partitioned terminal: at least a million survivors, and this many per group
 constexpr double kPartMinPerGroup = 16.0;
+// ... and about this many record regions per launch (sdb_plan.part_subs)
+constexpr int64_t kPartRegions = 1024;
 
 // Partitioned-terminal records carry 64-bit values only when the aggregate
 // combines two columns; a single int32 column's values fit 32 bits.
@@ -896,10 +899,15 @@ struct PartLayout {
         sorted_val, item_sum, item_cnt, total;
 };
 
+// Record regions of a partitioned plan: part_subs per block of every launch
+// (a segmented plan launches once per segment).
+uint64_t part_regions(const sdb_plan* plan) {
+    return (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments) * (uint64_t)plan->part_subs;
+}
+
 PartLayout part_layout(const sdb_query* q, const sdb_plan* plan) {
     PartLayout L;
-    // one region per block of every launch (a segmented plan launches once per segment)
-    const uint64_t grid = (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments), P = (uint64_t)plan->n_parts;
+    const uint64_t grid = part_regions(plan), P = (uint64_t)plan->n_parts;
     const uint64_t recs = grid * (uint64_t)plan->part_cap;
     const uint64_t vbytes = records_wide(q) ? 8 : 4;
     // aggregation work items: at most one partial chunk per partition plus full chunks
@@ -1788,6 +1796,11 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             if (st != SDB_OK) return st;
             plan->grid = grid;
         }
+        // record regions per block: about kPartRegions in all, so the scatter
+        // pass runs several blocks per CU (measured on c3, grid 256: the pass
+        // takes 92 against 167 us with 4 regions per block instead of 1)
+        plan->part_subs = (int32_t)std::max<int64_t>(
+            1, std::min<int64_t>(kPartSubRegions, kPartRegions / std::max(1, plan->grid)));
         // records per block: 1.5 x the survivors the busiest launch (segment) expects
         double seg_rows = (double)q->n_fact, seg_surv = survivors;
         if (plan->n_segments > 1) {
@@ -1798,10 +1811,13 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
                 seg_surv = std::max(seg_surv, seg_survivors[g]);
             }
         }
-        const double cap_total = std::min(seg_rows, 1.5 * seg_surv + 256.0 * plan->grid);
-        plan->part_cap = (int64_t)std::ceil(cap_total / plan->grid);
+        // (records per region: each of a block's part_subs regions takes the
+        // records of its share of the block's waves)
+        const double launch_regions = (double)plan->grid * plan->part_subs;
+        const double cap_total = std::min(seg_rows, 1.5 * seg_surv + 256.0 * launch_regions);
+        plan->part_cap = (int64_t)std::ceil(cap_total / launch_regions);
         plan->part_cap = (int64_t)align_up((uint64_t)std::max<int64_t>(plan->part_cap, 64), 64);
-        const uint64_t regions = (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments);
+        const uint64_t regions = part_regions(plan);
         if ((uint64_t)plan->part_cap * regions > 0xFFFFFFF0ull)
             plan->part_cap = (int64_t)(0xFFFFFFF0ull / regions) / 64 * 64;
         plan->run_scratch_bytes = (int64_t)stage_bytes + (int64_t)part_layout(q, plan).total;
@@ -1838,8 +1854,8 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         if (plan->grid <= 0 || plan->part_cap <= 0 || plan->part_shift < 0 || plan->part_shift > kPartMaxShift ||
             plan->n_parts <= 0 || plan->n_parts > kPartMaxParts ||
             (uint64_t)plan->n_parts != ((plan->n_groups + (1ull << plan->part_shift) - 1) >> plan->part_shift) ||
-            (uint64_t)plan->part_cap * (uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments) >
-                0xFFFFFFFFull)
+            plan->part_subs < 1 || plan->part_subs > kPartSubRegions ||
+            (uint64_t)plan->part_cap * part_regions(plan) > 0xFFFFFFFFull)
             return fail(SDB_INVALID_ARG, "bad partitioned-terminal plan");
     }
     if (plan->n_segments < 0 || plan->n_segments > SDB_MAX_SEGMENTS)
@@ -2047,10 +2063,11 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         p.part_cap = (uint32_t)plan->part_cap;
         p.part_shift = plan->part_shift;
         p.n_parts = (uint32_t)plan->n_parts;
+        p.part_subs = (uint32_t)plan->part_subs;
         pp.n_groups = plan->n_groups;
         pp.part_shift = plan->part_shift;
         pp.n_parts = (uint32_t)plan->n_parts;
-        pp.n_regions = (uint32_t)((uint64_t)plan->grid * (uint64_t)std::max(1, plan->n_segments));
+        pp.n_regions = (uint32_t)part_regions(plan);
         pp.part_cap = (uint32_t)plan->part_cap;
         pp.region_count = p.region_count;
         pp.rec_gid = p.rec_gid;
@@ -2077,7 +2094,7 @@ SDB_API sdb_status sdb_run_star_query(const sdb_query* q, const sdb_plan* plan, 
         if (timed) SDB_HIP(hipEventRecord(g_fused_start, s), "event record");
         if (sliced) SDB_HIP(launch_slice_partition(sp, plan->slice_grid, s), "slice passes launch");
         const int segs = std::max(1, plan->n_segments);
-        p.n_regions = (uint32_t)((uint64_t)grid * (uint64_t)segs);
+        p.n_regions = (uint32_t)((uint64_t)grid * (uint64_t)segs * (uint64_t)plan->part_subs);
         for (int g = 0; g < segs; ++g) {
             // segment g: its rows, its stage order, its own block regions
             FusedParams pg = p;

@@ -508,17 +508,21 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
             ts.xt = p.xtab + 2ull * p.n_groups * (xcc_id() & (uint32_t)(p.xcd_copies - 1));
     }
     if constexpr (TERM == TERM_PART) {
-        ts.lfill = reinterpret_cast<uint32_t*>(lds);
-        ts.lhist = ts.lfill + 1;
-        for (uint32_t i = threadIdx.x; i < 1u + p.n_parts; i += blockDim.x) ts.lfill[i] = 0u;
+        // the block's part_subs fill counters, then a histogram each
+        uint32_t* fills = reinterpret_cast<uint32_t*>(lds);
+        for (uint32_t i = threadIdx.x; i < p.part_subs * (1u + p.n_parts); i += blockDim.x) fills[i] = 0u;
         // rings: every wave's 8-byte entries (values, or {group id, value}),
         // then (64-bit values) every wave's group ids
         const uint32_t wave = threadIdx.x >> 6;
+        const uint32_t sub = wave % p.part_subs;
+        ts.lfill = fills + sub;
+        ts.lhist = fills + p.part_subs + sub * p.n_parts;
         const uint32_t vbytes = p.rec_wide ? 8u : 4u;
         ts.ring_val = lds + p.ring_off + (size_t)wave * kRing * 8u;
         ts.ring_gid = reinterpret_cast<uint32_t*>(lds + p.ring_off + (blockDim.x >> 6) * kRing * 8u) +
                       (size_t)wave * kRing;
-        const uint64_t region = (uint64_t)p.region_base + blockIdx.x;   // launches of a segmented plan
+        // launches of a segmented plan start at region_base
+        const uint64_t region = ((uint64_t)p.region_base + blockIdx.x) * p.part_subs + sub;
         ts.rgid = p.rec_gid + region * p.part_cap;
         ts.rval = static_cast<unsigned char*>(p.rec_val) + region * p.part_cap * vbytes;
     }
@@ -603,11 +607,14 @@ __global__ void __launch_bounds__(LB) star_fused_kernel(FusedParams kernel_args)
     } else if constexpr (TERM == TERM_PART) {
         if (ts.pend) part_flush(p, ts, ts.pend);
         __syncthreads();
-        const uint32_t region = p.region_base + blockIdx.x;
-        if (threadIdx.x == 0) p.region_count[region] = min(*ts.lfill, p.part_cap);
-        // this block's column of the partition x block histogram
-        for (uint32_t q = threadIdx.x; q < p.n_parts; q += blockDim.x)
-            p.part_hist[(uint64_t)q * p.n_regions + region] = ts.lhist[q];
+        const uint32_t* fills = reinterpret_cast<const uint32_t*>(lds);
+        const uint32_t region0 = (p.region_base + blockIdx.x) * p.part_subs;
+        if (threadIdx.x < p.part_subs) p.region_count[region0 + threadIdx.x] = min(fills[threadIdx.x], p.part_cap);
+        // this block's columns of the partition x region histogram
+        for (uint32_t i = threadIdx.x; i < p.part_subs * p.n_parts; i += blockDim.x) {
+            const uint32_t sub = i / p.n_parts, q = i - sub * p.n_parts;
+            p.part_hist[(uint64_t)q * p.n_regions + region0 + sub] = fills[p.part_subs + i];
+        }
     }
 }
 

@@ -16,6 +16,11 @@ constexpr int kBlock = 256;              // default threads per block of the fus
 constexpr int kMaxBlock = 512;           // launch bound of the fused kernel
 constexpr int kBigBlock = 1024;          // launch bound of its big-block instances (4-row items, IPT 1 or 2)
 constexpr int kUnrollStages = 4;         // stage copies of the fused kernel's unrolled instances
+// partitioned terminal: at most this many record regions per fused-kernel
+// block (sdb_plan.part_subs; wave w writes region w mod part_subs of its
+// block), so that the partition scatter pass, one block per region, runs
+// several blocks per CU
+constexpr int kPartSubRegions = 4;
 constexpr int kLdsGroupLimit = 2048;     // LDS terminal: sums + counts of G <= 2048 groups (32 KB)
 constexpr int kLdsStageBudget = 32768;   // LDS bytes per block for staged dimension tables
 constexpr int kXcdCopies = 8;            // XCDs of an MI355X: private group-table copies
@@ -173,7 +178,8 @@ struct FusedParams {
     unsigned long long* sums;
     unsigned long long* counts;
     unsigned long long* xtab;  // interleaved {sum, count} x n_groups x xcd_copies
-    // TERM_PART: block b appends survivors to records [b * part_cap, (b+1) * part_cap)
+    // TERM_PART: region r = (region_base + block) * part_subs + (wave mod
+    // part_subs) appends survivors to records [r * part_cap, (r + 1) * part_cap)
     uint32_t* region_count;    // records each block wrote
     uint32_t* rec_gid;
     void* rec_val;             // int64 values if rec_wide, else int32
@@ -183,6 +189,7 @@ struct FusedParams {
     uint32_t part_cap;
     int32_t part_shift;
     uint32_t n_parts;
+    uint32_t part_subs;        // record regions per block (1 .. kPartSubRegions)
     uint32_t ring_off;         // byte offset of the per-wave record rings in dynamic LDS
     int32_t rec_wide;          // 1: record values need 64 bits (aggregate of two columns)
     // eager columns (4-row items): slot k holds cols[eg_col[k]] for the current items

@@ -112,7 +112,7 @@ class SdbPlan(C.Structure):
                 ("stage_window_cover", C.c_double * MAX_STAGES),
                 ("sampled_rows", i64), ("est_cost", C.c_double), ("terminal", i32), ("ipt", i32),
                 ("vector", i32), ("eager", i32), ("block", i32), ("grid", i32), ("xcd_copies", i32),
-                ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_cap", i64),
+                ("lds_bytes", i32), ("part_shift", i32), ("n_parts", i32), ("part_subs", i32), ("part_cap", i64),
                 ("n_group_keys", i32),
                 ("key_min", i32 * MAX_GROUP_KEYS), ("radix", u32 * MAX_GROUP_KEYS),
                 ("stride", u64 * MAX_GROUP_KEYS), ("n_groups", u64), ("run_scratch_bytes", i64),
@@ -593,7 +593,7 @@ def plan_summary(plan: SdbPlan, query: dict | None = None) -> dict:
     return {"stages": stages, "terminal": TERMINAL_NAMES.get(plan.terminal, plan.terminal),
             "ipt": plan.ipt, "vector": plan.vector, "eager": plan.eager, "block": plan.block, "grid": plan.grid,
             "xcd_copies": plan.xcd_copies, "lds_bytes": plan.lds_bytes,
-            "n_parts": plan.n_parts, "part_cap": int(plan.part_cap),
+            "n_parts": plan.n_parts, "part_subs": plan.part_subs, "part_cap": int(plan.part_cap),
             "slice_bits": plan.slice_bits, "slice_grid": plan.slice_grid, "unroll": plan.unroll,
             "segments": [{"rows": [int(plan.segment_start[g]), int(plan.segment_start[g + 1])],
                           "order": [int(plan.segment_order[g][i]) for i in range(plan.n_stages)]}
