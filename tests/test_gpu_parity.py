@@ -825,6 +825,28 @@ def test_partitioned_terminal_region_overflow(cap):
     assert_same(rows, want_rows("c3_star3"), f"overflow cap {cap}")
 
 
+@pytest.mark.parametrize("groups", [1, 3])
+@pytest.mark.parametrize("values", ["max", "min", "mixed"])
+def test_partitioned_sums_at_the_int32_limits(values, groups):
+    """All records in one group (or three), values at the int32 limits: each
+    aggregation work item sums one group to about 2^47 in magnitude, and the
+    partition's several work items are merged; the sums and counts stay
+    exact."""
+    rng = np.random.default_rng([2607, 7632, 83])
+    n = 200_003
+    vals = {"max": np.full(n, 2**31 - 1, np.int32), "min": np.full(n, -2**31, np.int32),
+            "mixed": np.where(rng.random(n) < 0.5, 2**31 - 1, -2**31).astype(np.int32)}[values]
+    g = np.zeros(4, np.int32) if groups == 1 else np.array([0, 0, 1, 2], np.int32)
+    dims = {"d": {"k": np.arange(4, dtype=np.int32), "g": g}}
+    fact = {"fk": rng.choice(np.array([0, 0, 0, 1, 2, 3], np.int32), n), "v": vals}
+    query = {"fact_preds": [], "joins": [{"fact_key": "fk", "dim": "d", "preds": [], "payloads": ["g"]}],
+             "group_by": [["d", "g"]], "agg": {"kind": "col", "a": "v", "b": None}}
+    w = datagen.Workload(f"int32 limits {values}", n, fact, dims, {"d": "k"}, query)
+    got, q = run_gpu(w, force={"terminal": "part"})
+    assert q.plan_obj.terminal == 4
+    assert_same(got.as_rows(), oracle_rows(w), f"int32 limits {values}, {groups} groups")
+
+
 @pytest.mark.parametrize("seed", [3, 11, 29, 41])
 def test_random_tiny_schemas_partitioned(seed):
     w = random_tiny_workload(seed + 2000, max_fact=6000, max_dim_rows=500, n_fact=5003)
