@@ -886,8 +886,10 @@ constexpr bool kAutoEager = false;
 constexpr double kEagerMinLive = 0.02;
 // the partitioned terminal: at least a million survivors, and this many per group
 constexpr double kPartMinPerGroup = 16.0;
-// ... and about this many record regions per launch (sdb_plan.part_subs)
+// ... and about this many record regions per launch (sdb_plan.part_subs),
+// for blocks expecting fewer than kPartSplitMaxRecords records
 constexpr int64_t kPartRegions = 1024;
+constexpr double kPartSplitMaxRecords = 262144.0;
 
 // Partitioned-terminal records carry 64-bit values only when the aggregate
 // combines two columns; a single int32 column's values fit 32 bits.
@@ -1796,11 +1798,16 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             if (st != SDB_OK) return st;
             plan->grid = grid;
         }
-        // record regions per block: about kPartRegions in all, so the scatter
-        // pass runs several blocks per CU (measured on c3, grid 256: the pass
-        // takes 92 against 167 us with 4 regions per block instead of 1)
-        plan->part_subs = (int32_t)std::max<int64_t>(
-            1, std::min<int64_t>(kPartSubRegions, kPartRegions / std::max(1, plan->grid)));
+        // record regions per block: about kPartRegions in all, so that the
+        // scatter pass runs several blocks per CU, where its blocks have few
+        // records each and wait on latency (measured on c3, grid 256, 80K
+        // records per block: 92 against 167 us with 4 regions per block);
+        // blocks with many records already keep it near bandwidth (c5, 586K
+        // per block: 1.10 ms with one region, 1.16 ms with 2 or 4)
+        plan->part_subs = survivors / std::max(1, plan->grid) >= kPartSplitMaxRecords
+                              ? 1
+                              : (int32_t)std::max<int64_t>(
+                                    1, std::min<int64_t>(kPartSubRegions, kPartRegions / std::max(1, plan->grid)));
         // records per block: 1.5 x the survivors the busiest launch (segment) expects
         double seg_rows = (double)q->n_fact, seg_surv = survivors;
         if (plan->n_segments > 1) {
