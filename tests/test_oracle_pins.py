@@ -236,6 +236,52 @@ def test_c2_closed_form_group_counts():
             assert abs(c - mean) < 6 * sd + 3, (nation, year, c, mean)
 
 
+def test_c3_closed_form_survivors():
+    """c3's fact keys are uniform over the dimension keys, so a row survives
+    with the product of the three dimensions' pass fractions (customer and
+    supplier region 2, about 1/5 each; 1992-1997, 2190 of 2556 days): about
+    3.43% of the rows, 20.56M of 600M. The oracle's total count and sum on a
+    2M-row head agree within 6 standard deviations, and every group key lies
+    in the payload domains (250 cities, six years)."""
+    n = 2_000_000
+    w = datagen.make_workload("c3_star3", n_fact=n)
+    res = oracle.star_query(w.fact, w.dims, w.dim_keys, w.query)
+    p_c = float(np.mean(w.dims["customer"]["region"] == 2))
+    p_s = float(np.mean(w.dims["supplier"]["region"] == 2))
+    p_d = 6 * 365 / 2556
+    p = p_c * p_s * p_d
+    assert abs(p - 0.0343) < 0.001
+    mean, sd = n * p, math.sqrt(n * p * (1 - p))
+    total = int(np.sum(res.counts))
+    assert abs(total - mean) < 6 * sd, (total, mean)
+    # revenue ~ U[1, 10^6] independent of the keys
+    e_v, var_v = (1 + 1_000_000) / 2, (1_000_000 ** 2 - 1) / 12
+    sd_sum = math.sqrt(n * (p * (var_v + e_v ** 2) - (p * e_v) ** 2))
+    assert abs(int(np.sum(res.sums)) - n * p * e_v) < 6 * sd_sum
+    keys = np.array(res.keys)
+    assert keys[:, 0].min() >= 0 and keys[:, 0].max() <= 249 and keys[:, 1].max() <= 249
+    assert set(keys[:, 2].tolist()) == set(range(1992, 1998))
+
+
+def test_c5_closed_form_survivors():
+    """Every c5 fact key exists in the dimension (its keys are a permutation of
+    0..2^24-1) and half of the dimension rows pass: about half of the fact
+    rows survive, 300M of 600M, about 4,578 per group of 65,536; the oracle's
+    totals on a 2M-row head agree within 6 standard deviations."""
+    n = 2_000_000
+    w = datagen.make_workload("c5_hash_stress", n_fact=n)
+    res = oracle.star_query(w.fact, w.dims, w.dim_keys, w.query)
+    p = float(np.mean(w.dims["big"]["flag"] == 1))
+    mean, sd = n * p, math.sqrt(n * p * (1 - p))
+    total = int(np.sum(res.counts))
+    assert abs(total - mean) < 6 * sd, (total, mean)
+    assert abs(600_000_000 * p / 65536 - 4578) < 10
+    e_v, var_v = (1 + 1_000_000) / 2, (1_000_000 ** 2 - 1) / 12
+    sd_sum = math.sqrt(n * (p * (var_v + e_v ** 2) - (p * e_v) ** 2))
+    assert abs(int(np.sum(res.sums)) - n * p * e_v) < 6 * sd_sum
+    assert len(res.counts) <= 65536 and np.array(res.keys)[:, 0].max() <= 65535
+
+
 def test_c4_zipf_head_mass():
     cdf = datagen.zipf_cdf(1_400_000, 1.1)
     h = np.sum(np.arange(1, 1_400_001, dtype=np.float64) ** -1.1)
