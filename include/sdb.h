@@ -489,12 +489,14 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
                                   const int64_t* workspace_bytes, void* stream, sdb_dim* outs);
 
 /* Host only. Describes the table `dim` (a handle sdb_build_dim or
- * sdb_build_dims filled) in `out` (host): its layout, key ranges, pass count
- * and payload domains, without touching the device (Sections 3.3 and 4.3:
- * the direct-mapped or hash layout a build chose, and the domains the group
- * table is sized from). Errors: INVALID_ARG (null pointer, or a handle whose
- * fields contradict each other: unknown kind, a width or slot count the
- * kind does not allow, a pass count above the row count, a missing map). */
+ * sdb_build_dims filled) in `out` (host): its layout, key ranges, pass count,
+ * payload domains and pass filter, without touching the device (Sections 3.3
+ * and 4.3: the direct-mapped or hash layout a build chose, and the domains
+ * the group table is sized from). Errors: INVALID_ARG (null pointer, or a
+ * handle whose fields contradict each other: unknown kind, a width or slot
+ * count the kind does not allow, a pass count above the row count, a missing
+ * map, a pass filter on a dense table, without its words, or of a size its
+ * kind does not allow). */
 SDB_API sdb_status sdb_dim_info(const sdb_dim* dim, sdb_dim_summary* out);
 
 /* ---- planning ----------------------------------------------------------- */
