@@ -153,6 +153,34 @@ def test_dim_info_reports_the_handle():
     assert h["occupancy"] == 0.5 and h["payload_max"] == [65535]
 
 
+def test_dim_info_reports_and_checks_the_pass_filter():
+    """A hash table's pass filter through sdb_dim_info: its kind and bytes,
+    and the handles whose filter fields contradict the table are refused."""
+    h = _fake_dim(kind=2, width=8, n_rows=1 << 24, n_pass=1 << 23, bits=25, radices=(65536,),
+                  n_slots=1 << 24)
+    assert sdb.dim_info(h)["filter"] is None and sdb.dim_info(h)["filter_bytes"] == 0
+    h.filter, h.filter_kind, h.filter_bits = 0x900000, 1, 1 << 24     # a bitmap over the 2^24 keys
+    info = sdb.dim_info(h)
+    assert info["filter"] == "bitmap" and info["filter_bytes"] == 2 << 20
+    h.filter_kind, h.filter_bits = 2, 1 << 25                       # a 4 MiB Bloom filter
+    assert sdb.dim_info(h)["filter"] == "bloom" and sdb.dim_info(h)["filter_bytes"] == 4 << 20
+    for field, value in [("filter_bits", 3 << 20), ("filter_bits", 16), ("filter_bits", 1 << 26), ("filter", None),
+                         ("filter_kind", 7), ("reserved_", 2)]:
+        bad = sdb.SdbDim.from_buffer_copy(h)
+        setattr(bad, field, value)
+        with pytest.raises(sdb.SdbError) as e:
+            sdb.dim_info(bad)
+        assert e.value.name == "SDB_INVALID_ARG", (field, value)
+    bad = sdb.SdbDim.from_buffer_copy(h)
+    bad.filter_kind, bad.filter_bits = 1, (1 << 24) - 1               # a bitmap must cover the key range
+    with pytest.raises(sdb.SdbError):
+        sdb.dim_info(bad)
+    dense = _fake_dim(with_bitmap=True)
+    dense.filter, dense.filter_kind, dense.filter_bits = 0x900000, 1, 200_000
+    with pytest.raises(sdb.SdbError):
+        sdb.dim_info(dense)                                          # only hash tables carry one
+
+
 @pytest.mark.parametrize("field,value", [("kind", 0), ("kind", 3), ("width", 3), ("n_pass", 200_001),
                                          ("n_rows", -1), ("n_payloads", 4), ("n_slots", 7), ("map", None),
                                          ("bits", None)])
