@@ -1126,7 +1126,8 @@ def test_random_override_combinations(seed):
         "terminal": ["auto", "scalar", "lds", "global", "part"], "ipt": [0, 1, 2, 4], "vector": [0, 1, -1],
         "order": [False, True], "grid": [0, 0, 1, 3, 17], "lds": [-1, 0, 2, 3], "xcd": [-1, 0, 1],
         "eager": [-1, 0, 1, 2, 4], "block": [0, 64, 128, 256, 512, 1024], "range": [-1, 0, 1],
-        "coarse": [-1, 0, 1, 2, 5], "slice": [-1, 0, 1],
+        "coarse": [-1, 0, 1, 2, 5], "slice": [-1, 0, 1], "prefilter": [-1, 0, 1], "segments": [-1, 0, 1],
+        "unroll": [-1, 0], "window": [-1, 0, 1, 3],
     }
     refused = ran = 0
     for case in range(4):
