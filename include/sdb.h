@@ -468,7 +468,9 @@ SDB_API sdb_status sdb_dim_required_bytes(const sdb_dim_desc* desc, int64_t* byt
  * per key, the sentinel for a filtered row, all ones for an absent key; 1, 2
  * or 4 bytes by payload domain) and its pass bitmap, or the open-addressing
  * table (64-bit compare-and-swap inserts) and its pass filter (a bitmap over
- * the key range when that fits the filter's bytes, else the Bloom filter).
+ * the key range when that fits the filter's bytes, set through one byte per
+ * key in the slot region before the slots are filled; else the Bloom filter,
+ * set with atomics by the inserts).
  * Synchronizes the stream twice (to
  * read the statistics, then the duplicate-key check: a dense map must end
  * with one occupied slot per row).

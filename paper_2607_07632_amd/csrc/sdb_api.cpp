@@ -1417,7 +1417,11 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
             bp[d].filt = filt;
             bp[d].filt_kind = out->filter_kind;
             bp[d].filt_bits = out->filter_bits;
-            bp[d].fill_words = (slot_bytes + fbytes) / 4;
+            // a bitmap goes through a byte per key in the slot region (no
+            // atomics) when the range's bytes, rounded to whole words, fit
+            // there; the slots are filled afterwards, the filter by the packing
+            bp[d].filt_via_bytes = bitmap && align_up(range, 32) <= slot_bytes ? 1 : 0;
+            bp[d].fill_words = (slot_bytes + (bp[d].filt_via_bytes ? 0 : fbytes)) / 4;
         }
     }
 

@@ -244,7 +244,9 @@ struct BuildParams {
     uint32_t* filt;            // hash: pass filter words (SDB_FILTER_*), or null
     uint64_t filt_bits;
     int32_t filt_kind;
-    int32_t pad2_;
+    int32_t filt_via_bytes;    // 1: a bitmap filter built through a byte per key in the slot
+                               // region before the slots are filled (no atomics); 0: the
+                               // inserts set its bits with atomics
 };
 
 // Every table of one sdb_build_dims call; kernels take table blockIdx.y.

@@ -368,7 +368,8 @@ __global__ void __launch_bounds__(256) hash_insert_kernel(BuildBatch kernel_args
         const uint32_t enc = dim_row_passes(bp, i) ? dim_row_code(bp, i) + 1u : 0xFFFFFFFFu;
         const unsigned long long slot = ((unsigned long long)enc << 32) | (uint32_t)k;
         uint32_t fw, fm;
-        if (bp.filt && enc != 0xFFFFFFFFu && filter_slot(bp.filt_kind, bp.filt_bits, bp.kmin, k, fw, fm))
+        if (bp.filt && !bp.filt_via_bytes && enc != 0xFFFFFFFFu &&
+            filter_slot(bp.filt_kind, bp.filt_bits, bp.kmin, k, fw, fm))
             atomicOr(&bp.filt[fw], fm);
         uint32_t h = ((uint32_t)k * 0x9E3779B1u) >> bp.hshift & bp.hmask;
         bool placed = false;
@@ -386,6 +387,52 @@ __global__ void __launch_bounds__(256) hash_insert_kernel(BuildBatch kernel_args
             h = (h + 1u) & bp.hmask;
         }
         if (!placed) atomicOr(&bp.stats->dup, 2u);
+    }
+}
+
+// A hash table's pass bitmap without atomics (filt_via_bytes): the slot
+// region, not yet filled, first holds one byte per key of the range, cleared,
+// then set by every passing row with a plain store; the bytes are then
+// packed 32 to a filter word. Each key has its own byte, so no two rows
+// write the same address unless they hold the same key (a duplicate, which
+// the inserts report).
+__global__ void __launch_bounds__(256) filter_clear_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    if (!bp.filt_via_bytes) return;
+    uint32_t* w = static_cast<uint32_t*>(bp.map);
+    const uint64_t n_words = (bp.filt_bits + 31u) / 32u * 8u;   // the bytes the packing reads
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_words; i += stride) w[i] = 0u;
+}
+
+__global__ void __launch_bounds__(256) filter_mark_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    if (!bp.filt_via_bytes) return;
+    uint8_t* b = static_cast<uint8_t*>(bp.map);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
+        const uint32_t idx = (uint32_t)bp.key[i] - (uint32_t)bp.kmin;
+        if ((uint64_t)idx < bp.filt_bits && dim_row_passes(bp, i)) b[idx] = 1u;
+    }
+}
+
+__global__ void __launch_bounds__(256) filter_pack_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    if (!bp.filt_via_bytes) return;
+    const v4u* b = static_cast<const v4u*>(bp.map);
+    const uint64_t n_words = (bp.filt_bits + 31u) / 32u;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t w = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; w < n_words; w += stride) {
+        const v4u lo = b[2 * w], hi = b[2 * w + 1];   // the 32 key bytes of word w
+        const uint32_t q[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        uint32_t out = 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if ((q[j] >> (8 * t)) & 0xFFu) out |= 1u << (4 * j + t);
+        if (32u * w + 32u > bp.filt_bits) out &= (1u << (uint32_t)(bp.filt_bits - 32u * w)) - 1u;   // past the range
+        bp.filt[w] = out;
     }
 }
 
@@ -413,8 +460,8 @@ hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s) {
 
 hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s) {
     if (bb.n <= 0) return hipSuccess;
-    uint64_t words = 0, n_words32 = 0;
-    int64_t n_dense = 0, n_hash = 0;
+    uint64_t words = 0, n_words32 = 0, filt_words = 0;
+    int64_t n_dense = 0, n_hash = 0, n_filt = 0;
     for (int d = 0; d < bb.n; ++d) {
         const BuildParams& bp = bb.bp[d];
         words = std::max<uint64_t>(words, bp.fill_words);
@@ -424,6 +471,23 @@ hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s) {
         } else {
             n_hash = std::max<int64_t>(n_hash, bp.n);
         }
+        if (bp.filt_via_bytes) {
+            n_filt = std::max<int64_t>(n_filt, bp.n);
+            filt_words = std::max<uint64_t>(filt_words, (bp.filt_bits + 31) / 32);
+        }
+    }
+    if (filt_words > 0) {   // before the fill: the bytes live in the slot region
+        hipLaunchKernelGGL(filter_clear_kernel, dim3(fill_grid(filt_words * 8), bb.n), dim3(256), 0, s, bb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        if (n_filt > 0) {
+            hipLaunchKernelGGL(filter_mark_kernel, dim3(build_grid(n_filt), bb.n), dim3(256), 0, s, bb);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(filter_pack_kernel, dim3(fill_grid(filt_words), bb.n), dim3(256), 0, s, bb);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
     if (words > 0) {
         hipLaunchKernelGGL(fill_table_kernel, dim3(fill_grid(words), bb.n), dim3(256), 0, s, bb);
