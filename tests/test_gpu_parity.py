@@ -284,8 +284,10 @@ def _one_hash_join(m, n, key_span, seed, lf=0.5):
 
 def test_hash_pass_filter_words():
     """A hash table's pass filter holds exactly its passing keys: c5's table
-    and a permuted key range as a bitmap over the key range, keys spread over
-    2^31 values as the documented Bloom filter (word for word)."""
+    and a permuted key range as a bitmap over the key range (built through a
+    byte per key, or with atomics where those bytes do not fit the slot
+    region), keys spread over 2^31 values as the documented Bloom filter
+    (word for word)."""
     from paper_2607_07632_amd import sdb
     w = workload("c5_hash_stress")
     _, dims = upload(datagen.Workload(w.name, 0, {k: v[:0] for k, v in w.fact.items()}, w.dims, w.dim_keys,
@@ -296,7 +298,9 @@ def test_hash_pass_filter_words():
     big = w.dims["big"]
     want = _bitmap_words(big["key"][big["flag"] == 1], info["key_min"], info["key_max"] - info["key_min"] + 1)
     assert np.array_equal(_filter_words(t), want)
-    for m, span, kind in ((3000, 7000, "bitmap"), (5000, 1 << 31, "bloom"), (1, 1, "bitmap")):
+    # (two rows over 1000 keys: a bitmap whose bytes do not fit the 4-slot
+    # table's region, so the inserts set its bits with atomics)
+    for m, span, kind in ((3000, 7000, "bitmap"), (5000, 1 << 31, "bloom"), (1, 1, "bitmap"), (2, 1000, "bitmap")):
         wj = _one_hash_join(m, 0, span, seed=m)
         _, dj = upload(wj)
         tj = sdb.build_dims(dj, wj.dim_keys, wj.query)[0]
