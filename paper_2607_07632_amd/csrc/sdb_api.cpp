@@ -149,6 +149,9 @@ sdb_status device_info(DeviceInfo* out) {
 // ---- dimension sizing -----------------------------------------------------
 
 constexpr uint64_t kStatsBytes = 256;
+// the smallest table region (a dense map of 1024 one-byte codes and its bitmap)
+// holds several blocks' partial statistics
+static_assert(sizeof(DimStats) * 4 <= 512, "statistics partials");
 
 // dense tables within a memory budget: key ranges up to 2^31 slots
 constexpr int64_t kMaxDenseBudget = 1ll << 36;
@@ -283,6 +286,13 @@ BuildParams build_params(const sdb_dim_desc* d, DimStats* stats) {
     bp.n_payloads = d->n_payloads;
     for (int p = 0; p < d->n_payloads; ++p) bp.payload_col[p] = d->payload_cols[p];
     bp.stats = stats;
+    // partial statistics go to the table region, which the build fills only after
+    // they have been combined; one block per 256 * kStatsRows rows, as many as the region holds
+    const uint64_t region = required_bytes(d) - kStatsBytes;
+    const int64_t by_rows = (d->n_rows + 256 * kStatsRows - 1) / (256 * kStatsRows);
+    const int64_t by_room = (int64_t)(region / sizeof(DimStats));
+    bp.stats_part = reinterpret_cast<DimStats*>(reinterpret_cast<uint8_t*>(stats) + kStatsBytes);
+    bp.stats_blocks = (int32_t)std::max<int64_t>(1, std::min<int64_t>({by_rows, by_room, (int64_t)kStatsMaxBlocks}));
     return bp;
 }
 

@@ -216,6 +216,12 @@ struct DimStats {
 static_assert(sizeof(DimStats) <= 256, "stats must fit the reserved 256 bytes");
 static_assert(sizeof(FusedParams) <= 4096, "kernel arguments must fit the 4 KB kernarg segment");
 
+// most statistics blocks per table: each writes its partial statistics (one
+// DimStats) to the table region, which the build fills only afterwards, and a
+// second kernel combines them, so no statistic is updated with atomics
+constexpr int kStatsMaxBlocks = 1024;
+constexpr int kStatsRows = 16;            // rows per thread of a 256-thread statistics block
+
 struct BuildParams {
     const int32_t* key;
     int64_t n;
@@ -228,6 +234,9 @@ struct BuildParams {
     int32_t pmin[SDB_MAX_PAYLOADS];
     uint32_t pdiv[SDB_MAX_PAYLOADS];
     DimStats* stats;
+    DimStats* stats_part;      // stats_blocks partial statistics (in the table region)
+    int32_t stats_blocks;
+    int32_t pad3_;
     void* map;                 // dense map or hash table
     uint32_t* pass_bits;       // dense pass bitmap
     int32_t width;

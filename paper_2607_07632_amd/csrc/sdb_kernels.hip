@@ -84,32 +84,13 @@ __device__ __forceinline__ bool dim_row_passes(const BuildParams& bp, int64_t i)
     const BuildParams& bp = bb.bp[blockIdx.y];                                              \
     (void)bb
 
-__global__ void stats_init_kernel(BuildBatch kernel_args) {
-    (void)kernel_args;
-    const BuildBatch& bb = *(const BuildBatch*)__builtin_amdgcn_kernarg_segment_ptr();
-    if (blockIdx.x == 0 && threadIdx.x < (uint32_t)bb.n) {
-        DimStats* st = bb.bp[threadIdx.x].stats;
-        st->kmin = INT_MAX;
-        st->kmax = INT_MIN;
-        st->npass = 0ull;
-        for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
-            st->pmin[p] = INT_MAX;
-            st->pmax[p] = INT_MIN;
-        }
-        st->dup = 0u;
-        st->occupied = 0ull;
-        st->pkmin = INT_MAX;
-        st->pkmax = INT_MIN;
-    }
-}
-
 // Key range over all rows; pass count and payload ranges over passing rows.
-constexpr int kStatsRows = 16;
-
-// Each block reduces in registers and LDS and then adds its result with one
-// set of atomics, so the atomics stay few however large the dimension.
+// Block b of a table's stats_blocks reduces its rows in registers and LDS and
+// writes its partial statistics to stats_part[b]; stats_reduce_kernel then
+// combines the partials (no atomics, however many blocks).
 __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) {
     SDB_BATCH_TABLE;
+    if ((int)blockIdx.x >= bp.stats_blocks) return;
     constexpr int kWaves = 256 / 64;
     __shared__ int32_t s_kmin[kWaves], s_kmax[kWaves], s_pkmin[kWaves], s_pkmax[kWaves];
     __shared__ unsigned long long s_np[kWaves];
@@ -123,7 +104,7 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
     }
     // kStatsRows rows per thread per step, each column's loads issued together
     constexpr int U = kStatsRows;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x * U;
+    const int64_t stride = (int64_t)bp.stats_blocks * blockDim.x * U;
     for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x * U + threadIdx.x; i0 < bp.n; i0 += stride) {
         bool ok[U], pass[U];
         int32_t x[U], key[U];
@@ -202,19 +183,72 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
                 pmax[p] = max(pmax[p], s_pmax[p][w]);
             }
         }
-        DimStats* st = bp.stats;
-        if (kmin != INT_MAX) atomicMin(&st->kmin, kmin);
-        if (kmax != INT_MIN) atomicMax(&st->kmax, kmax);
-        if (npass) {
-            atomicAdd(&st->npass, npass);
-            atomicMin(&st->pkmin, pkmin);
-            atomicMax(&st->pkmax, pkmax);
-            for (int p = 0; p < bp.n_payloads; ++p) {
-                atomicMin(&st->pmin[p], pmin[p]);
-                atomicMax(&st->pmax[p], pmax[p]);
-            }
+        DimStats part;
+        part.kmin = kmin;
+        part.kmax = kmax;
+        part.npass = npass;
+        for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+            part.pmin[p] = pmin[p];
+            part.pmax[p] = pmax[p];
+        }
+        part.dup = 0u;
+        part.pad_ = 0u;
+        part.occupied = 0ull;
+        part.pkmin = pkmin;
+        part.pkmax = pkmax;
+        bp.stats_part[blockIdx.x] = part;
+    }
+}
+
+// One block per table: the table's statistics from its blocks' partials
+// (and the duplicate and occupancy counters the build passes add to, zeroed).
+__global__ void __launch_bounds__(256) stats_reduce_kernel(BuildBatch kernel_args) {
+    SDB_BATCH_TABLE;
+    __shared__ DimStats red[256];
+    DimStats acc;
+    acc.kmin = INT_MAX;
+    acc.kmax = INT_MIN;
+    acc.npass = 0ull;
+    for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+        acc.pmin[p] = INT_MAX;
+        acc.pmax[p] = INT_MIN;
+    }
+    acc.dup = 0u;
+    acc.pad_ = 0u;
+    acc.occupied = 0ull;
+    acc.pkmin = INT_MAX;
+    acc.pkmax = INT_MIN;
+    for (int b = threadIdx.x; b < bp.stats_blocks; b += blockDim.x) {
+        const DimStats& s = bp.stats_part[b];
+        acc.kmin = min(acc.kmin, s.kmin);
+        acc.kmax = max(acc.kmax, s.kmax);
+        acc.npass += s.npass;
+        acc.pkmin = min(acc.pkmin, s.pkmin);
+        acc.pkmax = max(acc.pkmax, s.pkmax);
+        for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+            acc.pmin[p] = min(acc.pmin[p], s.pmin[p]);
+            acc.pmax[p] = max(acc.pmax[p], s.pmax[p]);
         }
     }
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (uint32_t half = blockDim.x / 2; half > 0; half >>= 1) {
+        if (threadIdx.x < half) {
+            DimStats& a = red[threadIdx.x];
+            const DimStats& s = red[threadIdx.x + half];
+            a.kmin = min(a.kmin, s.kmin);
+            a.kmax = max(a.kmax, s.kmax);
+            a.npass += s.npass;
+            a.pkmin = min(a.pkmin, s.pkmin);
+            a.pkmax = max(a.pkmax, s.pkmax);
+            for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+                a.pmin[p] = min(a.pmin[p], s.pmin[p]);
+                a.pmax[p] = max(a.pmax[p], s.pmax[p]);
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *bp.stats = red[0];
 }
 
 __device__ __forceinline__ uint32_t dim_row_code(const BuildParams& bp, int64_t i) {
@@ -445,16 +479,15 @@ static int build_grid(int64_t n) {
 
 hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s) {
     if (bb.n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(64), 0, s, bb);
+    int g = 1;
+    for (int d = 0; d < bb.n; ++d) {
+        if (bb.bp[d].stats_blocks < 1 || bb.bp[d].stats_blocks > kStatsMaxBlocks) return hipErrorInvalidValue;
+        g = std::max(g, bb.bp[d].stats_blocks);
+    }
+    hipLaunchKernelGGL(dim_stats_kernel, dim3(g, bb.n), dim3(256), 0, s, bb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    int64_t n_max = 0;
-    for (int d = 0; d < bb.n; ++d) n_max = std::max<int64_t>(n_max, bb.bp[d].n);
-    if (n_max == 0) return hipSuccess;
-    // few blocks per table: every block ends with one set of atomics on the same words
-    int g = build_grid((n_max + kStatsRows - 1) / kStatsRows);
-    if (g > 256) g = 256;
-    hipLaunchKernelGGL(dim_stats_kernel, dim3(g, bb.n), dim3(256), 0, s, bb);
+    hipLaunchKernelGGL(stats_reduce_kernel, dim3(1, bb.n), dim3(256), 0, s, bb);
     return hipGetLastError();
 }
 
