@@ -654,9 +654,11 @@ def main(argv=None) -> int:
             build_ms.append(1000.0 * (time.perf_counter() - t0))
             q = sdb.StarQuery(fact, tabs, query, force)
             plan = q.plan(stream=bs)
-        planned = torch.cuda.Event()
-        planned.record(bs)
-        stream.wait_event(planned)
+        # no event from the build stream to the run stream: sdb_build_dims ends
+        # with a synchronization of the build stream and sdb_plan_star_query
+        # either synchronizes it or makes no GPU call, so the tables and the
+        # plan are complete here (an event record and wait cost about 25 us of
+        # the critical path from one fused kernel to the next)
         # ev[0..1]: the fused kernel alone (recorded by the library around its
         # launch); ev[2..3]: the whole run (fill, fused kernel, terminal passes)
         sdb.set_fused_events(ev[0], ev[1])

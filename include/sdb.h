@@ -16,10 +16,11 @@
  *    stay valid until the work queued on the stream has finished. The library
  *    allocates no device memory and keeps no global mutable state besides a
  *    per-thread error string, the per-thread measurement events of
- *    sdb_set_fused_events, a per-device properties cache and a 96 KB pinned
- *    host buffer per calling thread (allocated on the first build or sampled
- *    plan, kept while the thread lives) for the small reads those calls
- *    synchronize on; calls on different streams may run concurrently.
+ *    sdb_set_fused_events, a per-device properties cache and a 96 KB pinned,
+ *    coherent host buffer per calling thread (allocated on the first build or
+ *    sampled plan, kept while the thread lives) for the small reads those
+ *    calls synchronize on, which kernels write directly; calls on different
+ *    streams may run concurrently.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *  - Every call returns an sdb_status; nothing throws across the ABI.
  *    sdb_last_error() returns a message for the last failing call on the

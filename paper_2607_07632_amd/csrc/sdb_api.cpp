@@ -65,17 +65,29 @@ static_assert(sizeof(DimStats) * SDB_MAX_JOINS <= kStagingBytes, "statistics sta
 static_assert(kPatternBytes + kKeyHistBytes <= kStagingBytes, "sample staging");
 static_assert(kPatternBytes + kKeyHistBytes <= SDB_PLAN_SCRATCH_BYTES, "planner scratch");
 thread_local void* t_staging = nullptr;
+thread_local void* t_staging_dev = nullptr;
 thread_local bool t_staging_failed = false;
 
+// Pinned, coherent host buffer for the small reads the builds and the planner
+// wait for; kernels write it directly (through its device address), so a read
+// costs one small kernel rather than one copy per block read.
 void* host_staging() {
     if (!t_staging && !t_staging_failed) {
-        if (hipHostMalloc(&t_staging, kStagingBytes, hipHostMallocDefault) != hipSuccess) {
+        if (hipHostMalloc(&t_staging, kStagingBytes, hipHostMallocCoherent) != hipSuccess) {
             t_staging = nullptr;
             t_staging_failed = true;
+            (void)hipGetLastError();
+        } else if (hipHostGetDevicePointer(&t_staging_dev, t_staging, 0) != hipSuccess || !t_staging_dev) {
+            t_staging_dev = nullptr;   // the buffer still serves copies
             (void)hipGetLastError();
         }
     }
     return t_staging;
+}
+
+// The staging buffer's device address, or null (then reads go through copies).
+void* host_staging_device() {
+    return host_staging() ? t_staging_dev : nullptr;
 }
 
 inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
@@ -1324,10 +1336,13 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
 
     // pass 1 for every table: statistics, read back with one synchronization
     for (int d = 0; d < n_dims; ++d) bp[d] = build_params(&descs[d], (DimStats*)workspaces[d]);
-    SDB_HIP(launch_build_stats(bb, s), "dimension statistics launch");
     if (void* pinned = host_staging()) hs = static_cast<DimStats*>(pinned);
-    for (int d = 0; d < n_dims; ++d)
-        SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "statistics copy");
+    // the statistics kernels write the staging buffer themselves where it has a device address
+    bb.host_stats = static_cast<DimStats*>(host_staging_device());
+    SDB_HIP(launch_build_stats(bb, s), "dimension statistics launch");
+    if (!bb.host_stats)
+        for (int d = 0; d < n_dims; ++d)
+            SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "statistics copy");
     if (n_dims > 0) SDB_HIP(hipStreamSynchronize(s), "statistics sync");
 
     // pass 2 for every table: layout from the statistics, then the map or hash table
@@ -1438,8 +1453,11 @@ SDB_API sdb_status sdb_build_dims(int32_t n_dims, const sdb_dim_desc* descs, voi
     SDB_HIP(launch_build_tables(bb, s), "table build launch");
 
     // duplicate-key checks of every table, with one synchronization
-    for (int d = 0; d < n_dims; ++d)
-        SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "flag copy");
+    if (bb.host_stats)
+        SDB_HIP(launch_export_stats(bb, s), "flag export launch");
+    else
+        for (int d = 0; d < n_dims; ++d)
+            SDB_HIP(hipMemcpyAsync(&hs[d], workspaces[d], sizeof(DimStats), hipMemcpyDeviceToHost, s), "flag copy");
     if (n_dims > 0) SDB_HIP(hipStreamSynchronize(s), "build sync");
     for (int d = 0; d < n_dims; ++d) {
         const DimStats& fin = hs[d];
@@ -1602,9 +1620,15 @@ SDB_API sdb_status sdb_plan_star_query(const sdb_query* q, void* scratch, int64_
             host = fallback.data();
         }
         const size_t pattern_bytes = (sizeof(uint32_t) << n) * (size_t)n_ranges;
-        SDB_HIP(hipMemcpyAsync(host, dpattern, pattern_bytes, hipMemcpyDeviceToHost, s), "sample copy");
-        SDB_HIP(hipMemcpyAsync(host + kPatternBytes, dkeys, sizeof(uint32_t) * kKeyBuckets * (size_t)n,
-                               hipMemcpyDeviceToHost, s), "sample copy");
+        const size_t key_bytes = sizeof(uint32_t) * kKeyBuckets * (size_t)n;
+        if (void* hdev = fallback.empty() ? host_staging_device() : nullptr) {
+            // one kernel writes both histograms where the copies would put them
+            SDB_HIP(launch_copy_out(dpattern, (uint32_t)(kPatternBytes / 4), dkeys, (uint32_t)(key_bytes / 4),
+                                    static_cast<uint32_t*>(hdev), s), "sample export launch");
+        } else {
+            SDB_HIP(hipMemcpyAsync(host, dpattern, pattern_bytes, hipMemcpyDeviceToHost, s), "sample copy");
+            SDB_HIP(hipMemcpyAsync(host + kPatternBytes, dkeys, key_bytes, hipMemcpyDeviceToHost, s), "sample copy");
+        }
         SDB_HIP(hipStreamSynchronize(s), "sample sync");
         const uint32_t* ph = reinterpret_cast<const uint32_t*>(host);
         std::vector<uint32_t> whole((size_t)1 << n, 0u);

@@ -262,6 +262,7 @@ struct BuildParams {
 struct BuildBatch {
     int32_t n;
     int32_t pad_;
+    DimStats* host_stats;      // n statistics blocks in pinned host memory (device address), or null
     BuildParams bp[SDB_MAX_JOINS];
 };
 
@@ -346,13 +347,21 @@ struct SliceParams {
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n_words, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, uint64_t n, hipStream_t s);
 hipError_t launch_zero_pair(unsigned long long* a, unsigned long long* b, uint64_t n, hipStream_t s);
-// statistics pass of every table (their stats blocks are reset first)
+// statistics pass of every table: per-block partials, then the combined
+// statistics block of each table (also copied to bb.host_stats when set)
 hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s);
 // table fill, then dense scatter + pass bitmap or hash inserts, of every table
 hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s);
+// copies every table's statistics block to bb.host_stats (one launch)
+hipError_t launch_export_stats(const BuildBatch& bb, hipStream_t s);
+// copies words0 words from src0, then words1 from src1, to dst (pinned host
+// memory, device address) in one launch
+hipError_t launch_copy_out(const uint32_t* src0, uint32_t words0, const uint32_t* src1, uint32_t words1,
+                           uint32_t* dst, hipStream_t s);
 // Planner sampling: pass-pattern histograms (n_ranges x 2^nstages uint32: the
 // sampled rows split into n_ranges equal runs) and per-stage key histograms
-// (kMaxStages x kKeyBuckets uint32), both zeroed first.
+// (kMaxStages x kKeyBuckets uint32), both zeroed first (by one fill where the
+// key histograms follow the pattern histograms' 2^kMaxStages words).
 hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, int32_t n_ranges,
                          uint32_t* pattern_hist, uint32_t* key_hist, hipStream_t s);
 // Returns the kernel's occupancy (blocks per CU) for the given instance, or <= 0 if

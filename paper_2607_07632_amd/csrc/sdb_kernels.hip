@@ -248,7 +248,28 @@ __global__ void __launch_bounds__(256) stats_reduce_kernel(BuildBatch kernel_arg
         }
         __syncthreads();
     }
-    if (threadIdx.x == 0) *bp.stats = red[0];
+    if (threadIdx.x == 0) {
+        *bp.stats = red[0];
+        if (bb.host_stats) bb.host_stats[blockIdx.y] = red[0];
+    }
+}
+
+// One block: every table's statistics block, word by word, to pinned host memory.
+__global__ void __launch_bounds__(256) export_stats_kernel(BuildBatch kernel_args) {
+    (void)kernel_args;
+    const BuildBatch& bb = *(const BuildBatch*)__builtin_amdgcn_kernarg_segment_ptr();
+    constexpr int kWords = sizeof(DimStats) / 4;
+    for (int i = threadIdx.x; i < bb.n * kWords; i += blockDim.x) {
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(bb.bp[i / kWords].stats);
+        reinterpret_cast<uint32_t*>(bb.host_stats + i / kWords)[i % kWords] = src[i % kWords];
+    }
+}
+
+__global__ void __launch_bounds__(256) copy_out_kernel(const uint32_t* src0, uint32_t words0, const uint32_t* src1,
+                                                       uint32_t words1, uint32_t* dst) {
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < words0 + words1; i += stride)
+        dst[i] = i < words0 ? src0[i] : src1[i - words0];
 }
 
 __device__ __forceinline__ uint32_t dim_row_code(const BuildParams& bp, int64_t i) {
@@ -491,6 +512,24 @@ hipError_t launch_build_stats(const BuildBatch& bb, hipStream_t s) {
     return hipGetLastError();
 }
 
+hipError_t launch_export_stats(const BuildBatch& bb, hipStream_t s) {
+    if (bb.n <= 0) return hipSuccess;
+    if (!bb.host_stats || bb.n > SDB_MAX_JOINS) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(export_stats_kernel, dim3(1), dim3(256), 0, s, bb);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_out(const uint32_t* src0, uint32_t words0, const uint32_t* src1, uint32_t words1,
+                           uint32_t* dst, hipStream_t s) {
+    const uint64_t total = (uint64_t)words0 + words1;
+    if (total == 0) return hipSuccess;
+    if (!dst || (words0 && !src0) || (words1 && !src1) || total > (1ull << 30)) return hipErrorInvalidValue;
+    uint64_t g = (total + 255) / 256;
+    if (g > 64) g = 64;
+    hipLaunchKernelGGL(copy_out_kernel, dim3((uint32_t)g), dim3(256), 0, s, src0, words0, src1, words1, dst);
+    return hipGetLastError();
+}
+
 hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s) {
     if (bb.n <= 0) return hipSuccess;
     uint64_t words = 0, n_words32 = 0, filt_words = 0;
@@ -696,9 +735,14 @@ hipError_t launch_sample(const FusedParams& p, int64_t step, int64_t n_sample, i
                          uint32_t* pattern_hist, uint32_t* key_hist, hipStream_t s) {
     if (p.nstages < 0 || p.nstages > kMaxStages || n_ranges < 1 || ((uint64_t)n_ranges << p.nstages) > (1ull << kMaxStages))
         return hipErrorInvalidValue;
-    hipError_t e = launch_fill_u32(pattern_hist, (uint64_t)n_ranges << p.nstages, 0u, s);
-    if (e != hipSuccess) return e;
-    e = launch_fill_u32(key_hist, (uint64_t)kMaxStages * kKeyBuckets, 0u, s);
+    hipError_t e;
+    if (key_hist == pattern_hist + (1u << kMaxStages)) {
+        e = launch_fill_u32(pattern_hist, (1u << kMaxStages) + (uint64_t)kMaxStages * kKeyBuckets, 0u, s);
+    } else {
+        e = launch_fill_u32(pattern_hist, (uint64_t)n_ranges << p.nstages, 0u, s);
+        if (e != hipSuccess) return e;
+        e = launch_fill_u32(key_hist, (uint64_t)kMaxStages * kKeyBuckets, 0u, s);
+    }
     if (e != hipSuccess || n_sample == 0 || p.nstages == 0) return e;
     int64_t g = (n_sample + 255) / 256;
     if (g > 256) g = 256;
