@@ -541,6 +541,41 @@ def test_build_statistics_match_numpy():
     assert np.array_equal(unpacked, ok)
 
 
+@pytest.mark.parametrize("n,kind,npass", [(1, "dense", "some"), (4095, "dense", "some"), (4097, "hash", "some"),
+                                           (10_000, "dense", "none"), (5_000_001, "dense", "some"),
+                                           (5_000_001, "hash", "all")])
+def test_build_statistics_over_many_blocks(n, kind, npass):
+    """Key range, pass count and payload ranges from the per-block partials
+    (one block per 4,096 rows, at most 1,024, so 5M rows loop) against numpy,
+    with keys and payloads at the int32 extremes."""
+    import torch
+    from paper_2607_07632_amd import sdb
+    rng = np.random.default_rng(n + len(kind))
+    step = 1 if kind == "dense" else 3
+    key = (rng.permutation(n).astype(np.int64) * step + np.iinfo(np.int32).min + 7).astype(np.int32)
+    f = rng.integers(0, 10, n).astype(np.int32)
+    a = rng.integers(-5, 41, n).astype(np.int32)
+    b = rng.integers(1000, 1100, n).astype(np.int32)
+    c = (np.iinfo(np.int32).min + rng.integers(0, 51, n)).astype(np.int32)
+    bound = {"some": 3, "none": 0, "all": 10}[npass]
+    ok = f < bound
+    dev = lambda x: torch.from_numpy(x).cuda()
+    t = sdb.build_dim(dev(key), {"f": dev(f), "a": dev(a), "b": dev(b), "c": dev(c)},
+                      [{"col": "f", "op": "lt", "lo": bound, "hi": None}], ["a", "b", "c"], kind)
+    info = sdb.dim_info(t)
+    assert info["kind"] == kind
+    assert info["n_rows"] == n and info["n_pass"] == int(ok.sum())
+    assert (info["key_min"], info["key_max"]) == (int(key.min()), int(key.max()))
+    if ok.any():
+        assert (info["pass_key_min"], info["pass_key_max"]) == (int(key[ok].min()), int(key[ok].max()))
+        for i, col in enumerate((a, b, c)):
+            assert info["payload_min"][i] == int(col[ok].min())
+            assert info["payload_max"][i] == int(col[ok].max())
+            assert info["payload_radix"][i] == int(col[ok].max()) - int(col[ok].min()) + 1
+    else:
+        assert info["payload_radix"] == [1, 1, 1]
+
+
 def _stage_masks(w, rows):
     """Pass mask of every stage (query order: predicates, then joins) on the
     given fact rows, by direct indexing (dimension keys are row numbers here)."""
