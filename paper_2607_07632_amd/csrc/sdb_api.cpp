@@ -73,7 +73,7 @@ thread_local bool t_staging_failed = false;
 // costs one small kernel rather than one copy per block read.
 void* host_staging() {
     if (!t_staging && !t_staging_failed) {
-        if (hipHostMalloc(&t_staging, kStagingBytes, hipHostMallocCoherent) != hipSuccess) {
+        if (hipHostMalloc(&t_staging, kStagingBytes, hipHostMallocCoherent | hipHostMallocPortable) != hipSuccess) {
             t_staging = nullptr;
             t_staging_failed = true;
             (void)hipGetLastError();

@@ -455,6 +455,43 @@ def test_repeat_runs_are_identical():
         assert again.as_rows() == first.as_rows()
 
 
+def test_two_host_threads_on_streams_of_their_own():
+    """Builds, plans, runs and compactions from two host threads at once, each
+    on a stream of its own: the library's per-thread state (error string,
+    pinned staging) keeps them apart; every result against the oracle."""
+    import threading
+    import torch
+    from paper_2607_07632_amd import sdb
+    works = [datagen.make_workload("c3_star3", n_fact=400_003),
+             datagen.make_workload("c5_hash_stress", n_fact=300_001)]
+    wants = [oracle_rows(w) for w in works]
+    devs = [upload(w) for w in works]
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream()
+            w = works[i]
+            fact, dims = devs[i]
+            with torch.cuda.stream(s):
+                for it in range(4):
+                    tables = sdb.build_dims(dims, w.dim_keys, w.query, stream=s)
+                    got = sdb.StarQuery(fact, tables, w.query).execute(stream=s)
+                    if got.as_rows() != wants[i]:
+                        errors.append(f"thread {i}, iteration {it}: result differs from the oracle")
+        except Exception as e:  # reported by the main thread
+            errors.append(f"thread {i}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=100)
+    assert not any(t.is_alive() for t in threads), "a worker thread did not finish"
+    assert not errors, errors
+
+
 def test_all_pass_and_all_fail():
     w = datagen.make_workload("c2_join_group", n_fact=200_000)
     q = dict(w.query)
