@@ -299,9 +299,9 @@ BuildParams build_params(const sdb_dim_desc* d, DimStats* stats) {
     for (int p = 0; p < d->n_payloads; ++p) bp.payload_col[p] = d->payload_cols[p];
     bp.stats = stats;
     // partial statistics go to the table region, which the build fills only after
-    // they have been combined; one block per 256 * kStatsRows rows, as many as the region holds
+    // they have been combined; one block per 256 * kBuildRows rows, as many as the region holds
     const uint64_t region = required_bytes(d) - kStatsBytes;
-    const int64_t by_rows = (d->n_rows + 256 * kStatsRows - 1) / (256 * kStatsRows);
+    const int64_t by_rows = (d->n_rows + 256 * kBuildRows - 1) / (256 * kBuildRows);
     const int64_t by_room = (int64_t)(region / sizeof(DimStats));
     bp.stats_part = reinterpret_cast<DimStats*>(reinterpret_cast<uint8_t*>(stats) + kStatsBytes);
     bp.stats_blocks = (int32_t)std::max<int64_t>(1, std::min<int64_t>({by_rows, by_room, (int64_t)kStatsMaxBlocks}));

@@ -220,7 +220,7 @@ static_assert(sizeof(FusedParams) <= 4096, "kernel arguments must fit the 4 KB k
 // DimStats) to the table region, which the build fills only afterwards, and a
 // second kernel combines them, so no statistic is updated with atomics
 constexpr int kStatsMaxBlocks = 1024;
-constexpr int kStatsRows = 16;            // rows per thread of a 256-thread statistics block
+constexpr int kBuildRows = 16;            // rows per thread and step of a 256-thread statistics or dense-scatter block
 
 struct BuildParams {
     const int32_t* key;

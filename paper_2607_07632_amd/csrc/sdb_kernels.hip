@@ -102,8 +102,8 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
         pmin[p] = INT_MAX;
         pmax[p] = INT_MIN;
     }
-    // kStatsRows rows per thread per step, each column's loads issued together
-    constexpr int U = kStatsRows;
+    // kBuildRows rows per thread per step, each column's loads issued together
+    constexpr int U = kBuildRows;
     const int64_t stride = (int64_t)bp.stats_blocks * blockDim.x * U;
     for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x * U + threadIdx.x; i0 < bp.n; i0 += stride) {
         bool ok[U], pass[U];
@@ -294,17 +294,52 @@ __global__ void __launch_bounds__(256) fill_table_kernel(BuildBatch kernel_args)
 __global__ void __launch_bounds__(256) dense_scatter_kernel(BuildBatch kernel_args) {
     SDB_BATCH_TABLE;
     if (!bp.dense) return;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < bp.n; i += stride) {
-        const uint32_t idx = (uint32_t)(bp.key[i] - bp.kmin);
-        if ((uint64_t)idx >= bp.nslots) {          // cannot happen: kmin/kmax cover all keys
-            atomicOr(&bp.stats->dup, 4u);
-            continue;
+    // kBuildRows rows per thread per step, each column's loads issued together
+    // (a row at a time, the key, predicate and payload loads form one chain)
+    constexpr int U = kBuildRows;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x * U;
+    for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x * U + threadIdx.x; i0 < bp.n; i0 += stride) {
+        bool ok[U], pass[U];
+        int32_t x[U];
+        uint32_t idx[U], code[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + (int64_t)u * blockDim.x;
+            ok[u] = i < bp.n;
+            x[u] = ok[u] ? bp.key[i] : 0;
         }
-        const uint32_t c = dim_row_passes(bp, i) ? dim_row_code(bp, i) : bp.sentinel;
-        if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx] = (uint8_t)c;
-        else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx] = (uint16_t)c;
-        else static_cast<uint32_t*>(bp.map)[idx] = c;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            idx[u] = (uint32_t)((int64_t)x[u] - (int64_t)bp.kmin);
+            pass[u] = ok[u];
+            code[u] = 0u;
+        }
+        for (int q = 0; q < bp.n_preds; ++q) {
+            const int32_t* col = bp.cols[bp.pred_col[q]];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = ok[u] ? col[i0 + (int64_t)u * blockDim.x] : 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) pass[u] = pass[u] && range_pass(bp.pred[q], x[u]);
+        }
+        for (int p = 0; p < bp.n_payloads; ++p) {
+            const int32_t* col = bp.cols[bp.payload_col[p]];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = pass[u] ? col[i0 + (int64_t)u * blockDim.x] : 0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) code[u] += (uint32_t)((int64_t)x[u] - (int64_t)bp.pmin[p]) * bp.pdiv[p];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!ok[u]) continue;
+            if ((uint64_t)idx[u] >= bp.nslots) {          // cannot happen: kmin/kmax cover all keys
+                atomicOr(&bp.stats->dup, 4u);
+                continue;
+            }
+            const uint32_t c = pass[u] ? code[u] : bp.sentinel;
+            if (bp.width == 1) static_cast<uint8_t*>(bp.map)[idx[u]] = (uint8_t)c;
+            else if (bp.width == 2) static_cast<uint16_t*>(bp.map)[idx[u]] = (uint16_t)c;
+            else static_cast<uint32_t*>(bp.map)[idx[u]] = c;
+        }
     }
 }
 
@@ -567,7 +602,8 @@ hipError_t launch_build_tables(const BuildBatch& bb, hipStream_t s) {
         if (e != hipSuccess) return e;
     }
     if (n_dense > 0) {
-        hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid(n_dense), bb.n), dim3(256), 0, s, bb);
+        hipLaunchKernelGGL(dense_scatter_kernel, dim3(build_grid((n_dense + kBuildRows - 1) / kBuildRows), bb.n),
+                           dim3(256), 0, s, bb);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
