@@ -319,32 +319,48 @@ def _join_inputs(dims: dict, dim_keys: dict, jd: dict):
             jd.get("kind", "auto"), jd.get("load_factor", 0.0), jd.get("dense_budget_bytes", 0))
 
 
+class PreparedDims:
+    """The batched build of a query's dimension tables with its arguments
+    marshalled once. Every :meth:`build` runs sdb_build_dims again (all of its
+    work and both stream synchronizations) on the same descriptors and
+    workspaces and refills the same handles in place, so a StarQuery made
+    from :attr:`tables` stays valid from one build to the next."""
+
+    def __init__(self, dims: dict, dim_keys: dict, query: dict, workspaces=None):
+        import torch
+        joins = query.get("joins", [])
+        self.n = len(joins)
+        inputs = [_join_inputs(dims, dim_keys, jd) for jd in joins]
+        self.descs = (SdbDimDesc * max(self.n, 1))()
+        for i, args in enumerate(inputs):
+            self.descs[i] = dim_desc(*args)
+        if workspaces is None:
+            workspaces = [torch.empty(dim_required_bytes(self.descs[i]), dtype=torch.uint8,
+                                      device=inputs[i][0].device) for i in range(self.n)]
+        if len(workspaces) != self.n:
+            raise ValueError(f"{len(workspaces)} workspaces for {self.n} joins")
+        for i, w in enumerate(workspaces):
+            check_column(w, f"workspace of join {i}", device=inputs[i][0].device, dtype="uint8")
+        self.ws_ptrs = (C.c_void_p * max(self.n, 1))(*[_ptr(w) for w in workspaces])
+        self.ws_bytes = (C.c_int64 * max(self.n, 1))(*[w.numel() for w in workspaces])
+        self.outs = (SdbDim * max(self.n, 1))()
+        # each table's handle is a view of self.outs, which every build refills
+        self.tables = [DimTable(self.outs[i], self.descs[i], workspaces[i],
+                                [inputs[i][0]] + list(inputs[i][1].values())) for i in range(self.n)]
+
+    def build(self, stream=None) -> list:
+        if self.n:
+            _check(lib().sdb_build_dims(self.n, self.descs, self.ws_ptrs, self.ws_bytes, _stream_handle(stream),
+                                        self.outs))
+        return self.tables
+
+
 def build_dims(dims: dict, dim_keys: dict, query: dict, stream=None, workspaces=None) -> list:
     """One DimTable per join of ``query`` (dims: name -> {column: int32 device
     tensor}), built by one batched call (two stream synchronizations in all).
     ``workspaces`` (one uint8 device tensor per join, large enough) are reused
     when given."""
-    import torch
-    joins = query.get("joins", [])
-    if not joins:
-        return []
-    inputs = [_join_inputs(dims, dim_keys, jd) for jd in joins]
-    descs = (SdbDimDesc * len(joins))()
-    for i, args in enumerate(inputs):
-        descs[i] = dim_desc(*args)
-    if workspaces is None:
-        workspaces = [torch.empty(dim_required_bytes(descs[i]), dtype=torch.uint8, device=inputs[i][0].device)
-                      for i in range(len(joins))]
-    if len(workspaces) != len(joins):
-        raise ValueError(f"{len(workspaces)} workspaces for {len(joins)} joins")
-    for i, w in enumerate(workspaces):
-        check_column(w, f"workspace of join {i}", device=inputs[i][0].device, dtype="uint8")
-    ws_ptrs = (C.c_void_p * len(joins))(*[_ptr(w) for w in workspaces])
-    ws_bytes = (C.c_int64 * len(joins))(*[w.numel() for w in workspaces])
-    outs = (SdbDim * len(joins))()
-    _check(lib().sdb_build_dims(len(joins), descs, ws_ptrs, ws_bytes, _stream_handle(stream), outs))
-    return [DimTable(outs[i], descs[i], workspaces[i], [inputs[i][0]] + list(inputs[i][1].values()))
-            for i in range(len(joins))]
+    return PreparedDims(dims, dim_keys, query, workspaces).build(stream)
 
 
 # ---------------------------------------------------------------------------
