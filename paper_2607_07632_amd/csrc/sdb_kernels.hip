@@ -204,7 +204,7 @@ __global__ void __launch_bounds__(256) dim_stats_kernel(BuildBatch kernel_args) 
 // (and the duplicate and occupancy counters the build passes add to, zeroed).
 __global__ void __launch_bounds__(256) stats_reduce_kernel(BuildBatch kernel_args) {
     SDB_BATCH_TABLE;
-    __shared__ DimStats red[256];
+    __shared__ DimStats red[256 / 64];
     DimStats acc;
     acc.kmin = INT_MAX;
     acc.kmax = INT_MIN;
@@ -218,8 +218,21 @@ __global__ void __launch_bounds__(256) stats_reduce_kernel(BuildBatch kernel_arg
     acc.occupied = 0ull;
     acc.pkmin = INT_MAX;
     acc.pkmax = INT_MIN;
-    for (int b = threadIdx.x; b < bp.stats_blocks; b += blockDim.x) {
-        const DimStats& s = bp.stats_part[b];
+    // up to kStatsMaxBlocks / 256 partials per thread, loaded together
+    constexpr int kPer = kStatsMaxBlocks / 256;
+    static_assert(kPer * 256 == kStatsMaxBlocks, "whole partials per thread");
+    DimStats part[kPer];
+    bool have[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+        const int b = (int)threadIdx.x + u * 256;
+        have[u] = b < bp.stats_blocks;
+        if (have[u]) part[u] = bp.stats_part[b];
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+        if (!have[u]) continue;
+        const DimStats& s = part[u];
         acc.kmin = min(acc.kmin, s.kmin);
         acc.kmax = max(acc.kmax, s.kmax);
         acc.npass += s.npass;
@@ -230,12 +243,22 @@ __global__ void __launch_bounds__(256) stats_reduce_kernel(BuildBatch kernel_arg
             acc.pmax[p] = max(acc.pmax[p], s.pmax[p]);
         }
     }
-    red[threadIdx.x] = acc;
+    // wave reductions, then the 4 waves' results in LDS
+    acc.kmin = wave_min_i32(acc.kmin);
+    acc.kmax = wave_max_i32(acc.kmax);
+    acc.npass = wave_sum_u64(acc.npass);
+    acc.pkmin = wave_min_i32(acc.pkmin);
+    acc.pkmax = wave_max_i32(acc.pkmax);
+    for (int p = 0; p < SDB_MAX_PAYLOADS; ++p) {
+        acc.pmin[p] = wave_min_i32(acc.pmin[p]);
+        acc.pmax[p] = wave_max_i32(acc.pmax[p]);
+    }
+    if ((threadIdx.x & 63u) == 0u) red[threadIdx.x >> 6] = acc;
     __syncthreads();
-    for (uint32_t half = blockDim.x / 2; half > 0; half >>= 1) {
-        if (threadIdx.x < half) {
-            DimStats& a = red[threadIdx.x];
-            const DimStats& s = red[threadIdx.x + half];
+    if (threadIdx.x == 0) {
+        DimStats a = red[0];
+        for (uint32_t w = 1; w < blockDim.x / 64u; ++w) {
+            const DimStats& s = red[w];
             a.kmin = min(a.kmin, s.kmin);
             a.kmax = max(a.kmax, s.kmax);
             a.npass += s.npass;
@@ -246,11 +269,8 @@ __global__ void __launch_bounds__(256) stats_reduce_kernel(BuildBatch kernel_arg
                 a.pmax[p] = max(a.pmax[p], s.pmax[p]);
             }
         }
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        *bp.stats = red[0];
-        if (bb.host_stats) bb.host_stats[blockIdx.y] = red[0];
+        *bp.stats = a;
+        if (bb.host_stats) bb.host_stats[blockIdx.y] = a;
     }
 }
 
