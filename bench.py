@@ -571,8 +571,9 @@ def main(argv=None) -> int:
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the path needs no collective, and --gpus {args.gpus} "
-              "is not supported (see the sharding plan in the design notes)", file=sys.stderr)
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (sharding the fact rows "
+              "over GPUs would need one all-reduce of the group table per query, which is not built)",
+              file=sys.stderr)
         return 2
 
     if not args.no_cpu:
